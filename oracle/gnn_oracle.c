@@ -1,0 +1,325 @@
+/*
+ * CPU oracle for GraphSAGE feature propagation on a sampled subgraph.
+ * TEST INFRASTRUCTURE ONLY -- see gnn_oracle.h.  Plain loops, double
+ * precision throughout, fixed summation order, OpenMP only over independent
+ * outputs.  Shares nothing with the GPU library.
+ */
+#include "gnn_oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+int32_t oracle_num_threads(void) {
+#ifdef _OPENMP
+  return (int32_t)omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------ SpMM */
+
+/* Feature aggregation A_s . X (Section 2.1; Section 5.3 for the operation
+ * itself): row v of the output is the values-weighted sum of the input rows
+ * of v's neighbours, taken in CSR order. */
+void oracle_spmm(int32_t n, const int32_t* indptr, const int32_t* indices,
+                 const double* values, int32_t w, const double* in,
+                 double* out) {
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int32_t v = 0; v < n; ++v) {
+    double* o = out + (int64_t)v * w;
+    for (int32_t c = 0; c < w; ++c) o[c] = 0.0;
+    for (int32_t j = indptr[v]; j < indptr[v + 1]; ++j) {
+      const double a = values[j];
+      const double* x = in + (int64_t)indices[j] * w;
+      for (int32_t c = 0; c < w; ++c) o[c] += a * x[c];
+    }
+  }
+}
+
+/* Transposed aggregation (A_s)^T . in used by the input gradient (Section
+ * 5.1).  Entry (v,u) of A_s is entry (u,v) of the transpose, so every stored
+ * (v,u) adds A_s[v,u] * in[v,:] into out[u,:].  Each thread owns a range of
+ * feature columns (all rows), so every output element is summed by one
+ * thread in ascending v. */
+void oracle_spmm_transpose(int32_t n, const int32_t* indptr,
+                           const int32_t* indices, const double* values,
+                           int32_t w, const double* in, double* out) {
+  memset(out, 0, sizeof(double) * (size_t)n * (size_t)w);
+#pragma omp parallel
+  {
+    int nt = 1, t = 0;
+#ifdef _OPENMP
+    nt = omp_get_num_threads();
+    t = omp_get_thread_num();
+#endif
+    const int32_t c0 = (int32_t)((int64_t)w * t / nt);
+    const int32_t c1 = (int32_t)((int64_t)w * (t + 1) / nt);
+    for (int32_t v = 0; v < n; ++v) {
+      const double* x = in + (int64_t)v * w;
+      for (int32_t j = indptr[v]; j < indptr[v + 1]; ++j) {
+        const double a = values[j];
+        double* o = out + (int64_t)indices[j] * w;
+        for (int32_t c = c0; c < c1; ++c) o[c] += a * x[c];
+      }
+    }
+  }
+}
+
+/* Algorithm 6 (Section 5.2).  Walk rows v in order; the value of stored
+ * entry (v,u) is appended to row u of the transposed data array at that
+ * row's cursor.  With ascending indices, the entries of row u of the
+ * transpose arrive in ascending v, i.e. in the order row u stores them. */
+int32_t oracle_transpose_values(int32_t n, const int32_t* indptr,
+                                const int32_t* indices, const double* values,
+                                double* values_t) {
+  int32_t* cursor = (int32_t*)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+  if (!cursor) return -1;
+  for (int32_t u = 0; u < n; ++u) cursor[u] = indptr[u];
+  int32_t status = 0;
+  for (int32_t v = 0; v < n && status == 0; ++v) {
+    for (int32_t j = indptr[v]; j < indptr[v + 1]; ++j) { /* half-open */
+      const int32_t u = indices[j];
+      if (cursor[u] >= indptr[u + 1]) { status = -1; break; }
+      values_t[cursor[u]] = values[j];
+      cursor[u] += 1;
+    }
+  }
+  free(cursor);
+  return status;
+}
+
+/* Section 6.1: order 1 costs delta n^2 f1 + n f1 f2 MACs, order 2 costs
+ * delta n^2 f2 + n f1 f2; the shared term cancels, so order 1 wins when
+ * f1 < f2.  A tie costs the same either way and is given to order 1. */
+int32_t oracle_choose_order(int64_t f1, int64_t f2) {
+  return f1 <= f2 ? 1 : 2;
+}
+
+/* ---------------------------------------------------------- dense products */
+
+void oracle_mm_nn(int32_t M, int32_t N, int32_t K, const double* A,
+                  const double* B, double* C) {
+#pragma omp parallel for schedule(static)
+  for (int32_t i = 0; i < M; ++i) {
+    double* c = C + (int64_t)i * N;
+    for (int32_t j = 0; j < N; ++j) c[j] = 0.0;
+    for (int32_t k = 0; k < K; ++k) {
+      const double a = A[(int64_t)i * K + k];
+      const double* b = B + (int64_t)k * N;
+      for (int32_t j = 0; j < N; ++j) c[j] += a * b[j];
+    }
+  }
+}
+
+void oracle_mm_tn(int32_t M, int32_t N, int32_t K, const double* A,
+                  const double* B, double* C) {
+#pragma omp parallel for schedule(static)
+  for (int32_t i = 0; i < M; ++i) {
+    double* c = C + (int64_t)i * N;
+    for (int32_t j = 0; j < N; ++j) c[j] = 0.0;
+    for (int32_t k = 0; k < K; ++k) {
+      const double a = A[(int64_t)k * M + i];
+      const double* b = B + (int64_t)k * N;
+      for (int32_t j = 0; j < N; ++j) c[j] += a * b[j];
+    }
+  }
+}
+
+void oracle_mm_nt(int32_t M, int32_t N, int32_t K, const double* A,
+                  const double* B, double* C) {
+#pragma omp parallel for schedule(static)
+  for (int32_t i = 0; i < M; ++i) {
+    const double* a = A + (int64_t)i * K;
+    for (int32_t j = 0; j < N; ++j) {
+      const double* b = B + (int64_t)j * K;
+      double s = 0.0;
+      for (int32_t k = 0; k < K; ++k) s += a[k] * b[k];
+      C[(int64_t)i * N + j] = s;
+    }
+  }
+}
+
+/* ------------------------------------------------------------- one layer */
+
+static double relu(double z) { return z > 0.0 ? z : 0.0; }
+
+/* Eq. "graphsage forward": X_out = ReLU( X W_self || (A_s X) W_neigh ),
+ * with the self half in columns [0,h) (the column split the gradient
+ * equations of Section 5.1 use) and an optional per-half bias added
+ * before the activation. */
+void oracle_sage_fwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                     const double* values, int32_t f_in, int32_t h,
+                     const double* X, const double* W_self,
+                     const double* W_neigh, const double* b_self,
+                     const double* b_neigh, double* Y, double* S_out) {
+  const size_t nf = (size_t)n * (size_t)f_in, nh = (size_t)n * (size_t)h;
+  double* S = S_out ? S_out : (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  double* Zs = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  double* Zn = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  oracle_spmm(n, indptr, indices, values, f_in, X, S); /* A_s X */
+  oracle_mm_nn(n, h, f_in, X, W_self, Zs);              /* X W_self */
+  oracle_mm_nn(n, h, f_in, S, W_neigh, Zn);             /* (A_s X) W_neigh */
+#pragma omp parallel for schedule(static)
+  for (int32_t v = 0; v < n; ++v) {
+    double* y = Y + (int64_t)v * 2 * h;
+    for (int32_t c = 0; c < h; ++c) {
+      const double zs = Zs[(int64_t)v * h + c] + (b_self ? b_self[c] : 0.0);
+      const double zn = Zn[(int64_t)v * h + c] + (b_neigh ? b_neigh[c] : 0.0);
+      y[c] = relu(zs);
+      y[h + c] = relu(zn);
+    }
+  }
+  free(Zs);
+  free(Zn);
+  if (!S_out) free(S);
+}
+
+/* mask(): the derivative of the layer's own ReLU, 1 where the output is
+ * positive and 0 elsewhere (0 is taken at the kink). */
+static void masked_grad(int32_t n, int32_t h, const double* Y,
+                        const double* dY, double* Gs, double* Gn) {
+#pragma omp parallel for schedule(static)
+  for (int32_t v = 0; v < n; ++v) {
+    for (int32_t c = 0; c < h; ++c) {
+      const int64_t a = (int64_t)v * 2 * h + c, b = a + h;
+      Gs[(int64_t)v * h + c] = Y[a] > 0.0 ? dY[a] : 0.0;
+      Gn[(int64_t)v * h + c] = Y[b] > 0.0 ? dY[b] : 0.0;
+    }
+  }
+}
+
+/* Section 5.1, Eq. "gcn backward" (stated there for GraphSAGE). */
+void oracle_sage_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                     const double* values, int32_t f_in, int32_t h,
+                     const double* X, const double* W_self,
+                     const double* W_neigh, const double* Y, const double* dY,
+                     double* dX, double* dW_self, double* dW_neigh,
+                     double* db_self, double* db_neigh) {
+  const size_t nf = (size_t)n * (size_t)f_in, nh = (size_t)n * (size_t)h;
+  double* Gs = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  double* Gn = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  double* S = (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  masked_grad(n, h, Y, dY, Gs, Gn);
+
+  oracle_mm_tn(f_in, h, n, X, Gs, dW_self);            /* X^T G_s */
+  oracle_spmm(n, indptr, indices, values, f_in, X, S);  /* A_s X */
+  oracle_mm_tn(f_in, h, n, S, Gn, dW_neigh);           /* (A_s X)^T G_n */
+
+  if (db_self || db_neigh) {
+    for (int32_t c = 0; c < h; ++c) {
+      double ss = 0.0, sn = 0.0;
+      for (int32_t v = 0; v < n; ++v) {
+        ss += Gs[(int64_t)v * h + c];
+        sn += Gn[(int64_t)v * h + c];
+      }
+      if (db_self) db_self[c] = ss;
+      if (db_neigh) db_neigh[c] = sn;
+    }
+  }
+
+  if (dX) {
+    double* T = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+    double* R = (double*)malloc(sizeof(double) * (nf ? nf : 1));
+    oracle_spmm_transpose(n, indptr, indices, values, h, Gn, T); /* A^T G_n */
+    oracle_mm_nt(n, f_in, h, Gs, W_self, dX);                     /* G_s W_s^T */
+    oracle_mm_nt(n, f_in, h, T, W_neigh, R);            /* (A^T G_n) W_n^T */
+    for (size_t i = 0; i < nf; ++i) dX[i] += R[i];
+    free(T);
+    free(R);
+  }
+  free(Gs);
+  free(Gn);
+  free(S);
+}
+
+/* ---------------------------------------------- per-output spot evaluation */
+
+void oracle_sage_fwd_rows(int32_t n, const int32_t* indptr,
+                          const int32_t* indices, const double* values,
+                          int32_t f_in, int32_t h, const double* X,
+                          const double* W_self, const double* W_neigh,
+                          const double* b_self, const double* b_neigh,
+                          int32_t nrows, const int32_t* rows, double* Y_rows) {
+  (void)n;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int32_t r = 0; r < nrows; ++r) {
+    const int32_t v = rows[r];
+    double* s = (double*)malloc(sizeof(double) * (size_t)(f_in > 0 ? f_in : 1));
+    for (int32_t k = 0; k < f_in; ++k) s[k] = 0.0;
+    for (int32_t j = indptr[v]; j < indptr[v + 1]; ++j)
+      for (int32_t k = 0; k < f_in; ++k)
+        s[k] += values[j] * X[(int64_t)indices[j] * f_in + k];
+    for (int32_t c = 0; c < h; ++c) {
+      double zs = 0.0, zn = 0.0;
+      for (int32_t k = 0; k < f_in; ++k) {
+        zs += X[(int64_t)v * f_in + k] * W_self[(int64_t)k * h + c];
+        zn += s[k] * W_neigh[(int64_t)k * h + c];
+      }
+      if (b_self) zs += b_self[c];
+      if (b_neigh) zn += b_neigh[c];
+      Y_rows[(int64_t)r * 2 * h + c] = relu(zs);
+      Y_rows[(int64_t)r * 2 * h + h + c] = relu(zn);
+    }
+    free(s);
+  }
+}
+
+void oracle_sage_bwd_dx_rows(int32_t n, const int32_t* indptr,
+                             const int32_t* indices, const double* values,
+                             int32_t f_in, int32_t h, const double* W_self,
+                             const double* W_neigh, const double* Y,
+                             const double* dY, int32_t nrows,
+                             const int32_t* rows, double* dX_rows) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int32_t r = 0; r < nrows; ++r) {
+    const int32_t u = rows[r];
+    /* t = row u of (A_s)^T G_n: every stored (v,u), v ascending. */
+    double* t = (double*)malloc(sizeof(double) * (size_t)(h > 0 ? h : 1));
+    for (int32_t c = 0; c < h; ++c) t[c] = 0.0;
+    for (int32_t v = 0; v < n; ++v)
+      for (int32_t j = indptr[v]; j < indptr[v + 1]; ++j)
+        if (indices[j] == u)
+          for (int32_t c = 0; c < h; ++c) {
+            const int64_t b = (int64_t)v * 2 * h + h + c;
+            t[c] += values[j] * (Y[b] > 0.0 ? dY[b] : 0.0);
+          }
+    for (int32_t k = 0; k < f_in; ++k) {
+      double a = 0.0, b = 0.0;
+      for (int32_t c = 0; c < h; ++c) {
+        const int64_t s = (int64_t)u * 2 * h + c;
+        a += (Y[s] > 0.0 ? dY[s] : 0.0) * W_self[(int64_t)k * h + c];
+        b += t[c] * W_neigh[(int64_t)k * h + c];
+      }
+      dX_rows[(int64_t)r * f_in + k] = a + b;
+    }
+    free(t);
+  }
+}
+
+void oracle_sage_bwd_dw_entries(int32_t n, const int32_t* indptr,
+                                const int32_t* indices, const double* values,
+                                int32_t f_in, int32_t h, const double* X,
+                                const double* Y, const double* dY,
+                                int32_t nent, const int32_t* ei,
+                                const int32_t* ej, double* dWs_ent,
+                                double* dWn_ent) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int32_t e = 0; e < nent; ++e) {
+    const int32_t i = ei[e], c = ej[e];
+    double ws = 0.0, wn = 0.0;
+    for (int32_t v = 0; v < n; ++v) {
+      const int64_t a = (int64_t)v * 2 * h + c, b = a + h;
+      double s = 0.0; /* (A_s X)[v, i] */
+      for (int32_t j = indptr[v]; j < indptr[v + 1]; ++j)
+        s += values[j] * X[(int64_t)indices[j] * f_in + i];
+      ws += X[(int64_t)v * f_in + i] * (Y[a] > 0.0 ? dY[a] : 0.0);
+      wn += s * (Y[b] > 0.0 ? dY[b] : 0.0);
+    }
+    dWs_ent[e] = ws;
+    dWn_ent[e] = wn;
+  }
+}

@@ -1,0 +1,120 @@
+/*
+ * CPU oracle for one GraphSAGE layer's feature propagation, forward and
+ * backward, on a sampled subgraph ("Accurate, Efficient and Scalable
+ * Training of Graph Neural Networks", Zeng et al.).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library is the slow, obviously-correct
+ * reference that the GPU path is checked against.  Only the test suite, the
+ * smoke check and the benchmark's CPU-baseline leg may load it.  It shares no
+ * source, header, table or helper with the GPU library.
+ *
+ * Conventions
+ *   - every floating-point input and output is double (the paper trains in
+ *     double precision, Section 5.3 footnote); all sums accumulate in double
+ *     in a fixed order, so results do not depend on the thread count;
+ *   - dense matrices are row-major and contiguous (leading dimension = width);
+ *   - the subgraph adjacency is CSR: indptr[n+1], indices[nnz] (column ids,
+ *     ascending within a row), values[nnz];
+ *   - a layer's output is [self half | neighbour half], each h wide.
+ */
+#ifndef GNN_ORACLE_H
+#define GNN_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Section 2.1, Eq. "graphsage forward": out = A_s . in  (CSR order sum). */
+void oracle_spmm(int32_t n, const int32_t* indptr, const int32_t* indices,
+                 const double* values, int32_t w, const double* in,
+                 double* out);
+
+/* out = (A_s)^T . in, applied as a scatter over the CSR of A_s:
+ * out[u,:] = sum over stored (v,u) of A_s[v,u] * in[v,:], v ascending.
+ * Independent of Algorithm 6 and of any symmetry of the pattern. */
+void oracle_spmm_transpose(int32_t n, const int32_t* indptr,
+                           const int32_t* indices, const double* values,
+                           int32_t w, const double* in, double* out);
+
+/* Section 5.2, Algorithm 6: values of (A_s)^T on the same indptr/indices,
+ * by one pass with per-row append cursors.  Requires a symmetric pattern and
+ * ascending indices within each row.  Returns 0, or -1 if a cursor would run
+ * past its row (pattern not symmetric). */
+int32_t oracle_transpose_values(int32_t n, const int32_t* indptr,
+                                const int32_t* indices, const double* values,
+                                double* values_t);
+
+/* Section 6.1: computation order of A.W1.W2 (A n-by-n sparse, W1 n-by-f1,
+ * W2 f1-by-f2).  Returns 1 for (A W1) W2, 2 for A (W1 W2). */
+int32_t oracle_choose_order(int64_t f1, int64_t f2);
+
+/* Dense products, ascending-k sums.  C is M x N.
+ *   nn: C = A B      A: M x K, B: K x N
+ *   tn: C = A^T B    A: K x M, B: K x N
+ *   nt: C = A B^T    A: M x K, B: N x K                                    */
+void oracle_mm_nn(int32_t M, int32_t N, int32_t K, const double* A,
+                  const double* B, double* C);
+void oracle_mm_tn(int32_t M, int32_t N, int32_t K, const double* A,
+                  const double* B, double* C);
+void oracle_mm_nt(int32_t M, int32_t N, int32_t K, const double* A,
+                  const double* B, double* C);
+
+/* Forward of one layer (Eq. "graphsage forward", self half first):
+ *   S = A_s X                                  (n x f_in, may be NULL)
+ *   Y = ReLU([X W_self + b_self || S W_neigh + b_neigh])   (n x 2h)
+ * b_self / b_neigh may be NULL (no bias, the paper's form). */
+void oracle_sage_fwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                     const double* values, int32_t f_in, int32_t h,
+                     const double* X, const double* W_self,
+                     const double* W_neigh, const double* b_self,
+                     const double* b_neigh, double* Y, double* S);
+
+/* Backward of one layer (Section 5.1, Eq. "gcn backward"), given the
+ * layer output Y (its sign pattern is the ReLU mask) and dY = dL/dY:
+ *   G       = dY * 1[Y > 0]            G_s = G[:, :h], G_n = G[:, h:]
+ *   dW_self = X^T G_s
+ *   dW_neigh= (A_s X)^T G_n
+ *   dX      = G_s W_self^T + ((A_s)^T G_n) W_neigh^T
+ *   db_*    = column sums of G_*  (db pointers may be NULL)
+ * dX may be NULL (skipped). */
+void oracle_sage_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                     const double* values, int32_t f_in, int32_t h,
+                     const double* X, const double* W_self,
+                     const double* W_neigh, const double* Y, const double* dY,
+                     double* dX, double* dW_self, double* dW_neigh,
+                     double* db_self, double* db_neigh);
+
+/* The same definitions evaluated one output at a time, for spot checks of
+ * large cases.  rows[] lists node ids; outputs are packed per listed row. */
+void oracle_sage_fwd_rows(int32_t n, const int32_t* indptr,
+                          const int32_t* indices, const double* values,
+                          int32_t f_in, int32_t h, const double* X,
+                          const double* W_self, const double* W_neigh,
+                          const double* b_self, const double* b_neigh,
+                          int32_t nrows, const int32_t* rows, double* Y_rows);
+
+void oracle_sage_bwd_dx_rows(int32_t n, const int32_t* indptr,
+                             const int32_t* indices, const double* values,
+                             int32_t f_in, int32_t h, const double* W_self,
+                             const double* W_neigh, const double* Y,
+                             const double* dY, int32_t nrows,
+                             const int32_t* rows, double* dX_rows);
+
+/* Entries (ei[k], ej[k]) of dW_self and dW_neigh. */
+void oracle_sage_bwd_dw_entries(int32_t n, const int32_t* indptr,
+                                const int32_t* indices, const double* values,
+                                int32_t f_in, int32_t h, const double* X,
+                                const double* Y, const double* dY,
+                                int32_t nent, const int32_t* ei,
+                                const int32_t* ej, double* dWs_ent,
+                                double* dWn_ent);
+
+/* Number of OpenMP threads the oracle runs with. */
+int32_t oracle_num_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

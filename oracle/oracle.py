@@ -1,0 +1,256 @@
+"""Python face of the CPU oracle (test infrastructure only).
+
+The oracle is plain C in double precision (gnn_oracle.c); this module
+compiles it with gcc on first use, loads it with ctypes and converts numpy
+arrays.  Only the tests, the smoke check and the benchmark's CPU-baseline
+leg use it; the GPU library never does.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+from typing import Optional, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gnn_oracle.c")
+_LIB = os.path.join(_HERE, "libgnn_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+_I32P = ctypes.POINTER(ctypes.c_int32)
+_F64P = ctypes.POINTER(ctypes.c_double)
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle into oracle/libgnn_oracle.so (gcc, OpenMP)."""
+    if not force and os.path.exists(_LIB):
+        return _LIB
+    tmp = _LIB + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O3", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+           "-shared", "-fPIC", "-std=c99", "-Wall", "-o", tmp, _SRC]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def lib():
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_LIB) or \
+                    os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build()
+            L = ctypes.CDLL(_LIB)
+            i32, i64 = ctypes.c_int32, ctypes.c_int64
+            sigs = {
+                "oracle_spmm": [i32, _I32P, _I32P, _F64P, i32, _F64P, _F64P],
+                "oracle_spmm_transpose": [i32, _I32P, _I32P, _F64P, i32, _F64P,
+                                          _F64P],
+                "oracle_transpose_values": [i32, _I32P, _I32P, _F64P, _F64P],
+                "oracle_choose_order": [i64, i64],
+                "oracle_mm_nn": [i32, i32, i32, _F64P, _F64P, _F64P],
+                "oracle_mm_tn": [i32, i32, i32, _F64P, _F64P, _F64P],
+                "oracle_mm_nt": [i32, i32, i32, _F64P, _F64P, _F64P],
+                "oracle_sage_fwd": [i32, _I32P, _I32P, _F64P, i32, i32, _F64P,
+                                    _F64P, _F64P, _F64P, _F64P, _F64P, _F64P],
+                "oracle_sage_bwd": [i32, _I32P, _I32P, _F64P, i32, i32, _F64P,
+                                    _F64P, _F64P, _F64P, _F64P, _F64P, _F64P,
+                                    _F64P, _F64P, _F64P],
+                "oracle_sage_fwd_rows": [i32, _I32P, _I32P, _F64P, i32, i32,
+                                         _F64P, _F64P, _F64P, _F64P, _F64P,
+                                         i32, _I32P, _F64P],
+                "oracle_sage_bwd_dx_rows": [i32, _I32P, _I32P, _F64P, i32, i32,
+                                            _F64P, _F64P, _F64P, _F64P, i32,
+                                            _I32P, _F64P],
+                "oracle_sage_bwd_dw_entries": [i32, _I32P, _I32P, _F64P, i32,
+                                               i32, _F64P, _F64P, _F64P, i32,
+                                               _I32P, _I32P, _F64P, _F64P],
+                "oracle_num_threads": [],
+            }
+            for name, args in sigs.items():
+                fn = getattr(L, name)
+                fn.argtypes = args
+                fn.restype = ctypes.c_int32 if name in (
+                    "oracle_transpose_values", "oracle_choose_order",
+                    "oracle_num_threads") else None
+            _lib = L
+        return _lib
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _p(a: Optional[np.ndarray], t):
+    if a is None:
+        return None
+    return a.ctypes.data_as(t)
+
+
+def _csr(g) -> Tuple[int, np.ndarray, np.ndarray, np.ndarray]:
+    return g.n, _i32(g.indptr), _i32(g.indices), _f64(g.values)
+
+
+def num_threads() -> int:
+    return int(lib().oracle_num_threads())
+
+
+def spmm(g, x: np.ndarray) -> np.ndarray:
+    n, ip, ix, v = _csr(g)
+    x = _f64(x)
+    w = x.shape[1]
+    out = np.empty((n, w), np.float64)
+    lib().oracle_spmm(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P), w,
+                      _p(x, _F64P), _p(out, _F64P))
+    return out
+
+
+def spmm_transpose(g, u: np.ndarray) -> np.ndarray:
+    n, ip, ix, v = _csr(g)
+    u = _f64(u)
+    w = u.shape[1]
+    out = np.empty((n, w), np.float64)
+    lib().oracle_spmm_transpose(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P),
+                                w, _p(u, _F64P), _p(out, _F64P))
+    return out
+
+
+def transpose_values(g) -> np.ndarray:
+    n, ip, ix, v = _csr(g)
+    vt = np.full(v.shape, np.nan, np.float64)
+    rc = lib().oracle_transpose_values(n, _p(ip, _I32P), _p(ix, _I32P),
+                                       _p(v, _F64P), _p(vt, _F64P))
+    if rc != 0:
+        raise ValueError("pattern is not symmetric")
+    return vt
+
+
+def choose_order(f1: int, f2: int) -> int:
+    return int(lib().oracle_choose_order(int(f1), int(f2)))
+
+
+def _mm(name, M, N, K, a, b):
+    a, b = _f64(a), _f64(b)
+    c = np.empty((M, N), np.float64)
+    getattr(lib(), name)(M, N, K, _p(a, _F64P), _p(b, _F64P), _p(c, _F64P))
+    return c
+
+
+def mm_nn(a, b):
+    return _mm("oracle_mm_nn", a.shape[0], b.shape[1], a.shape[1], a, b)
+
+
+def mm_tn(a, b):
+    return _mm("oracle_mm_tn", a.shape[1], b.shape[1], a.shape[0], a, b)
+
+
+def mm_nt(a, b):
+    return _mm("oracle_mm_nt", a.shape[0], b.shape[0], a.shape[1], a, b)
+
+
+def sage_fwd(g, x, w_self, w_neigh, b_self=None, b_neigh=None,
+             want_s: bool = False):
+    """Returns Y (n x 2h) [and S = A_s X]."""
+    n, ip, ix, v = _csr(g)
+    x, ws, wn = _f64(x), _f64(w_self), _f64(w_neigh)
+    f_in, h = ws.shape
+    assert x.shape == (n, f_in) and wn.shape == (f_in, h)
+    bs = None if b_self is None else _f64(b_self)
+    bn = None if b_neigh is None else _f64(b_neigh)
+    y = np.empty((n, 2 * h), np.float64)
+    s = np.empty((n, f_in), np.float64) if want_s else None
+    lib().oracle_sage_fwd(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P), f_in,
+                          h, _p(x, _F64P), _p(ws, _F64P), _p(wn, _F64P),
+                          _p(bs, _F64P), _p(bn, _F64P), _p(y, _F64P),
+                          _p(s, _F64P))
+    return (y, s) if want_s else y
+
+
+def sage_bwd(g, x, w_self, w_neigh, y, dy, want_dx: bool = True,
+             want_db: bool = False) -> dict:
+    n, ip, ix, v = _csr(g)
+    x, ws, wn, y, dy = _f64(x), _f64(w_self), _f64(w_neigh), _f64(y), _f64(dy)
+    f_in, h = ws.shape
+    assert x.shape == (n, f_in) and y.shape == (n, 2 * h) == dy.shape
+    out = {"dW_self": np.empty((f_in, h)), "dW_neigh": np.empty((f_in, h))}
+    out["dX"] = np.empty((n, f_in)) if want_dx else None
+    out["db_self"] = np.empty(h) if want_db else None
+    out["db_neigh"] = np.empty(h) if want_db else None
+    lib().oracle_sage_bwd(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P), f_in,
+                          h, _p(x, _F64P), _p(ws, _F64P), _p(wn, _F64P),
+                          _p(y, _F64P), _p(dy, _F64P), _p(out["dX"], _F64P),
+                          _p(out["dW_self"], _F64P), _p(out["dW_neigh"], _F64P),
+                          _p(out["db_self"], _F64P), _p(out["db_neigh"], _F64P))
+    return out
+
+
+def sage_fwd_rows(g, x, w_self, w_neigh, rows, b_self=None, b_neigh=None):
+    n, ip, ix, v = _csr(g)
+    x, ws, wn = _f64(x), _f64(w_self), _f64(w_neigh)
+    f_in, h = ws.shape
+    rows = _i32(rows)
+    bs = None if b_self is None else _f64(b_self)
+    bn = None if b_neigh is None else _f64(b_neigh)
+    y = np.empty((rows.size, 2 * h), np.float64)
+    lib().oracle_sage_fwd_rows(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P),
+                               f_in, h, _p(x, _F64P), _p(ws, _F64P),
+                               _p(wn, _F64P), _p(bs, _F64P), _p(bn, _F64P),
+                               rows.size, _p(rows, _I32P), _p(y, _F64P))
+    return y
+
+
+def sage_bwd_dx_rows(g, w_self, w_neigh, y, dy, rows):
+    n, ip, ix, v = _csr(g)
+    ws, wn, y, dy = _f64(w_self), _f64(w_neigh), _f64(y), _f64(dy)
+    f_in, h = ws.shape
+    rows = _i32(rows)
+    out = np.empty((rows.size, f_in), np.float64)
+    lib().oracle_sage_bwd_dx_rows(n, _p(ip, _I32P), _p(ix, _I32P),
+                                  _p(v, _F64P), f_in, h, _p(ws, _F64P),
+                                  _p(wn, _F64P), _p(y, _F64P), _p(dy, _F64P),
+                                  rows.size, _p(rows, _I32P), _p(out, _F64P))
+    return out
+
+
+def sage_bwd_dw_entries(g, x, y, dy, h, ei, ej):
+    n, ip, ix, v = _csr(g)
+    x, y, dy = _f64(x), _f64(y), _f64(dy)
+    f_in = x.shape[1]
+    ei, ej = _i32(ei), _i32(ej)
+    ws = np.empty(ei.size, np.float64)
+    wn = np.empty(ei.size, np.float64)
+    lib().oracle_sage_bwd_dw_entries(n, _p(ip, _I32P), _p(ix, _I32P),
+                                     _p(v, _F64P), f_in, h, _p(x, _F64P),
+                                     _p(y, _F64P), _p(dy, _F64P), ei.size,
+                                     _p(ei, _I32P), _p(ej, _I32P),
+                                     _p(ws, _F64P), _p(wn, _F64P))
+    return ws, wn
+
+
+def sage_stack(g, x, params, dy_top, want_dx_first: bool = True):
+    """L layers forward then backward (Algorithm 1's layer loop with a given
+    top gradient in place of the classifier and loss).  Every layer's input
+    is the previous layer's double-precision output."""
+    acts, ys = [_f64(x)], []
+    for p in params:
+        y = sage_fwd(g, acts[-1], p.w_self, p.w_neigh, p.b_self, p.b_neigh)
+        ys.append(y)
+        acts.append(y)
+    grads = [None] * len(params)
+    dy = _f64(dy_top)
+    for l in reversed(range(len(params))):
+        p = params[l]
+        need_dx = l > 0 or want_dx_first
+        r = sage_bwd(g, acts[l], p.w_self, p.w_neigh, ys[l], dy,
+                     want_dx=need_dx, want_db=p.b_self is not None)
+        grads[l] = r
+        dy = r["dX"]
+    return {"acts": acts, "ys": ys, "grads": grads}

@@ -1,0 +1,396 @@
+"""Pins of the CPU oracle to facts other than itself.
+
+Each check ties the oracle to something the paper or plain mathematics fixes:
+a hand-worked example (tests/golden), brute force against dense matrices,
+closed forms on star / complete / identity graphs, invariants (row sums of a
+row-normalised adjacency, the adjoint identity), the order rule's MAC counts,
+and central finite differences of the backward pass.  No GPU is used.
+"""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2010_03166_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def dense(g, vals=None):
+    """Dense matrix of a CSR (test-side brute force)."""
+    vals = g.values if vals is None else vals
+    a = np.zeros((g.n, g.n), np.float64)
+    for v in range(g.n):
+        for j in range(g.indptr[v], g.indptr[v + 1]):
+            a[v, g.indices[j]] += float(vals[j])
+    return a
+
+
+def fr(a):
+    return np.array([[float(Fraction(x)) for x in row] for row in a]) \
+        if isinstance(a[0], list) else np.array([float(Fraction(x)) for x in a])
+
+
+def rel(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    s = max(np.abs(b).max(), 1e-300) if b.size else 1.0
+    return float(np.abs(a - b).max() / s) if b.size else 0.0
+
+
+# ------------------------------------------------------------------ golden
+
+@pytest.fixture(scope="module")
+def path4():
+    d = json.load(open(os.path.join(GOLDEN, "sage_path4.json")))
+    g = synth.symmetric_csr(4, np.array(d["edges"]), self_loops=True)
+    assert g.indptr.tolist() == d["csr"]["indptr"]
+    assert g.indices.tolist() == d["csr"]["indices"]
+    np.testing.assert_allclose(g.values, fr(d["csr"]["values"]), rtol=1e-7)
+    # use the exact fractions as double values
+    g.values = fr(d["csr"]["values"])
+    return g, d
+
+
+def test_golden_transpose_values(path4):
+    g, d = path4
+    np.testing.assert_array_equal(O.transpose_values(g), fr(d["values_t"]))
+
+
+def test_golden_aggregation(path4):
+    g, d = path4
+    x = fr(d["X"])
+    np.testing.assert_allclose(O.spmm(g, x), fr(d["AX"]), rtol=0, atol=1e-15)
+    np.testing.assert_allclose(O.spmm_transpose(g, x), fr(d["ATX"]),
+                               rtol=0, atol=1e-15)
+
+
+def test_golden_layer(path4):
+    g, d = path4
+    x, ws, wn = fr(d["X"]), fr(d["W_self"]), fr(d["W_neigh"])
+    y = O.sage_fwd(g, x, ws, wn)
+    np.testing.assert_allclose(y, fr(d["Y"]), rtol=0, atol=1e-15)
+    r = O.sage_bwd(g, x, ws, wn, fr(d["Y"]), fr(d["dY"]), want_db=True)
+    for k in ("dW_self", "dW_neigh", "dX"):
+        np.testing.assert_allclose(r[k], fr(d[k]), rtol=0, atol=1e-14, err_msg=k)
+    np.testing.assert_allclose(r["db_self"], fr(d["db_self"]), atol=1e-15)
+    np.testing.assert_allclose(r["db_neigh"], fr(d["db_neigh"]), atol=1e-15)
+
+
+# --------------------------------------------------------------- aggregation
+
+@pytest.mark.parametrize("seed,self_loops,values", [
+    (0, True, "row-normalized"), (1, False, "row-normalized"),
+    (2, True, "random"), (3, False, "random")])
+def test_spmm_brute_force(seed, self_loops, values):
+    g = synth.random_graph(40, 4.0, seed, self_loops=self_loops, values=values)
+    x = np.random.default_rng(seed).standard_normal((g.n, 7))
+    a = dense(g)
+    assert rel(O.spmm(g, x), a @ x) < 1e-13
+    assert rel(O.spmm_transpose(g, x), a.T @ x) < 1e-13
+
+
+def test_spmm_empty_rows_give_zero():
+    # isolated nodes without self loops have empty rows
+    g = synth.symmetric_csr(5, np.array([[0, 1]]), self_loops=False)
+    assert g.degrees().tolist() == [1, 1, 0, 0, 0]
+    x = np.arange(15, dtype=np.float64).reshape(5, 3) + 1
+    out = O.spmm(g, x)
+    np.testing.assert_array_equal(out[2:], 0.0)
+    np.testing.assert_array_equal(out[0], x[1])
+
+
+def exact_row_norm(g):
+    """The same graph with D^-1 values held in double (not rounded to f32)."""
+    d = g.degrees()
+    g.values = 1.0 / np.repeat(d, d).astype(np.float64)
+    return g
+
+
+def test_row_sum_invariant():
+    g = exact_row_norm(synth.power_law_graph(300, 2.1, 8.0, seed=5))
+    ones = np.ones((g.n, 3))
+    np.testing.assert_allclose(O.spmm(g, ones), 1.0, rtol=0, atol=1e-13)
+    c = np.tile(np.array([[2.5, -1.0, 7.0]]), (g.n, 1))
+    np.testing.assert_allclose(O.spmm(g, c), c, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("k", [1, 3, 17])
+def test_star_closed_form(k):
+    g = exact_row_norm(synth.star_graph(k))
+    x = np.random.default_rng(k).standard_normal((k + 1, 5))
+    out = O.spmm(g, x)
+    np.testing.assert_allclose(out[0], x.sum(0) / (k + 1), atol=1e-13)
+    np.testing.assert_allclose(out[1:], (x[1:] + x[0]) / 2, atol=1e-13)
+    t = O.spmm_transpose(g, x)
+    np.testing.assert_allclose(t[0], x[0] / (k + 1) + x[1:].sum(0) / 2,
+                               atol=1e-13)
+    np.testing.assert_allclose(t[1:], x[0] / (k + 1) + x[1:] / 2, atol=1e-13)
+    # column sums of A: centre 1/(k+1) + k/2, leaf 1/(k+1) + 1/2, total n
+    cs = O.spmm_transpose(g, np.ones((k + 1, 1)))[:, 0]
+    np.testing.assert_allclose(cs[0], 1 / (k + 1) + k / 2, atol=1e-14)
+    np.testing.assert_allclose(cs[1:], 1 / (k + 1) + 0.5, atol=1e-14)
+    np.testing.assert_allclose(cs.sum(), k + 1, atol=1e-12)
+
+
+def test_complete_graph_closed_form():
+    n = 9
+    x = np.random.default_rng(1).standard_normal((n, 4))
+    out = O.spmm(exact_row_norm(synth.complete_graph(n, True)), x)
+    np.testing.assert_allclose(out, np.tile(x.mean(0), (n, 1)), atol=1e-13)
+    out = O.spmm(exact_row_norm(synth.complete_graph(n, False)), x)
+    np.testing.assert_allclose(out, (x.sum(0) - x) / (n - 1), atol=1e-13)
+
+
+def test_identity_graph():
+    x = np.random.default_rng(2).standard_normal((6, 3))
+    g = synth.identity_graph(6)
+    np.testing.assert_array_equal(O.spmm(g, x), x)
+    np.testing.assert_array_equal(O.spmm_transpose(g, x), x)
+
+
+def test_adjoint_identity():
+    g = synth.random_graph(60, 5.0, 7, values="random")
+    r = np.random.default_rng(7)
+    x, u = r.standard_normal((60, 6)), r.standard_normal((60, 6))
+    lhs = np.sum(O.spmm(g, x) * u)
+    rhs = np.sum(x * O.spmm_transpose(g, u))
+    assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs))
+
+
+# ------------------------------------------------------------- Algorithm 6
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_transpose_values_is_dense_transpose(seed):
+    g = synth.random_graph(50, 6.0, seed, values="random")
+    vt = O.transpose_values(g)
+    # exact: a pure permutation of the stored values
+    np.testing.assert_array_equal(dense(g, vt), dense(g).T)
+    np.testing.assert_array_equal(np.sort(vt), np.sort(g.values.astype(float)))
+
+
+def test_transpose_values_regular_graph_unchanged():
+    n = 12  # cycle + self loops: every degree is 3, so A is symmetric
+    e = np.stack([np.arange(n), (np.arange(n) + 1) % n], 1)
+    g = synth.symmetric_csr(n, e)
+    np.testing.assert_array_equal(O.transpose_values(g),
+                                  g.values.astype(np.float64))
+
+
+def test_transpose_values_rejects_asymmetric_pattern():
+    g = synth.csr_from_pairs(3, np.array([0, 0, 1, 2]), np.array([0, 1, 1, 2]))
+    with pytest.raises(ValueError):
+        O.transpose_values(g)
+
+
+# ------------------------------------------------------------ order choice
+
+@pytest.mark.parametrize("f1,f2", [(50, 128), (602, 512), (300, 512),
+                                   (512, 512), (1024, 512), (256, 1024),
+                                   (2048, 1024), (1, 1000)])
+def test_order_rule_matches_mac_counts(f1, f2):
+    n, delta = 8000, 16 / 8000
+    mac1 = delta * n * n * f1 + n * f1 * f2   # (A W1) W2
+    mac2 = delta * n * n * f2 + n * f1 * f2   # A (W1 W2)
+    assert O.choose_order(f1, f2) == (1 if mac1 <= mac2 else 2)
+
+
+def test_orders_agree():
+    g = synth.power_law_graph(200, 2.1, 6.0, seed=3)
+    r = np.random.default_rng(3)
+    x, w = r.standard_normal((200, 9)), r.standard_normal((9, 5))
+    o1 = O.mm_nn(O.spmm(g, x), w)
+    o2 = O.spmm(g, O.mm_nn(x, w))
+    assert rel(o1, o2) < 1e-13
+
+
+# ----------------------------------------------------------- dense products
+
+def test_dense_products_vs_numpy():
+    r = np.random.default_rng(4)
+    a, b = r.standard_normal((13, 7)), r.standard_normal((7, 11))
+    assert rel(O.mm_nn(a, b), a @ b) < 1e-14
+    assert rel(O.mm_tn(a.T.copy(), b), a @ b) < 1e-14
+    assert rel(O.mm_nt(a, b.T.copy()), a @ b) < 1e-14
+
+
+# -------------------------------------------------------------- whole layer
+
+def layer_case(seed, n=30, f_in=6, h=4, bias=False, graph="random"):
+    r = np.random.default_rng(seed)
+    if graph == "random":
+        g = synth.random_graph(n, 4.0, seed)
+    elif graph == "identity":
+        g = synth.identity_graph(n)
+    else:
+        g = exact_row_norm(synth.complete_graph(n))
+    x = r.standard_normal((n, f_in))
+    ws, wn = r.standard_normal((f_in, h)), r.standard_normal((f_in, h))
+    bs = r.standard_normal(h) if bias else None
+    bn = r.standard_normal(h) if bias else None
+    return g, x, ws, wn, bs, bn
+
+
+def test_layer_identity_graph_is_two_path_mlp():
+    g, x, ws, wn, _, _ = layer_case(0, graph="identity")
+    y = O.sage_fwd(g, x, ws, wn)
+    np.testing.assert_allclose(y, np.maximum(np.hstack([x @ ws, x @ wn]), 0),
+                               atol=1e-13)
+
+
+def test_layer_dense_brute_force_with_bias():
+    g, x, ws, wn, bs, bn = layer_case(1, bias=True)
+    a = dense(g)
+    z = np.hstack([x @ ws + bs, (a @ x) @ wn + bn])
+    y, s = O.sage_fwd(g, x, ws, wn, bs, bn, want_s=True)
+    assert rel(y, np.maximum(z, 0)) < 1e-13
+    assert rel(s, a @ x) < 1e-13
+
+
+def test_layer_zero_weights():
+    g, x, ws, wn, _, _ = layer_case(2)
+    y = O.sage_fwd(g, x, ws, np.zeros_like(wn))
+    np.testing.assert_array_equal(y[:, 4:], 0.0)
+    y = O.sage_fwd(g, x, np.zeros_like(ws), wn)
+    np.testing.assert_array_equal(y[:, :4], 0.0)
+
+
+def test_layer_complete_graph_neighbour_half_rows_equal():
+    g, x, ws, wn, _, _ = layer_case(3, n=12, graph="complete")
+    y = O.sage_fwd(g, x, ws, wn)
+    np.testing.assert_allclose(y[:, 4:], np.tile(y[0, 4:], (12, 1)), atol=1e-13)
+    dy = np.random.default_rng(3).standard_normal(y.shape)
+    r = O.sage_bwd(g, x, ws, wn, y, dy)
+    # dW_neigh = mu^T (1^T G_n): rank one, mu = column mean of X
+    gn = dy[:, 4:] * (y[:, 4:] > 0)
+    np.testing.assert_allclose(r["dW_neigh"], np.outer(x.mean(0), gn.sum(0)),
+                               atol=1e-12)
+
+
+def _loss(g, x, ws, wn, bs, bn, dy):
+    return float(np.sum(dy * O.sage_fwd(g, x, ws, wn, bs, bn)))
+
+
+def _preact(g, x, ws, wn, bs, bn):
+    a = dense(g)
+    z = np.hstack([x @ ws, (a @ x) @ wn])
+    if bs is not None:
+        z = z + np.concatenate([bs, bn])
+    return z
+
+
+@pytest.mark.parametrize("seed,bias", [(10, False), (11, True), (12, False)])
+def test_backward_finite_differences(seed, bias):
+    # central differences of L = <dY, Y> in double; the layer is piecewise
+    # linear, so away from ReLU kinks the difference quotient is exact up to
+    # rounding.  Cases whose pre-activations come near 0 are re-drawn.
+    for s in range(seed, seed + 50):
+        g, x, ws, wn, bs, bn = layer_case(s, n=10, f_in=4, h=3, bias=bias)
+        if np.abs(_preact(g, x, ws, wn, bs, bn)).min() > 1e-3:
+            break
+    dy = np.random.default_rng(seed + 100).standard_normal((10, 6))
+    y = O.sage_fwd(g, x, ws, wn, bs, bn)
+    r = O.sage_bwd(g, x, ws, wn, y, dy, want_db=bias)
+    eps = 1e-6
+
+    def fd(arr):
+        out = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            old = arr[idx]
+            arr[idx] = old + eps
+            lp = _loss(g, x, ws, wn, bs, bn, dy)
+            arr[idx] = old - eps
+            lm = _loss(g, x, ws, wn, bs, bn, dy)
+            arr[idx] = old
+            out[idx] = (lp - lm) / (2 * eps)
+        return out
+
+    assert rel(r["dX"], fd(x)) < 1e-6
+    assert rel(r["dW_self"], fd(ws)) < 1e-6
+    assert rel(r["dW_neigh"], fd(wn)) < 1e-6
+    if bias:
+        assert rel(r["db_self"], fd(bs)) < 1e-6
+        assert rel(r["db_neigh"], fd(bn)) < 1e-6
+
+
+def test_two_layer_stack_finite_differences():
+    for s in range(50):
+        r = np.random.default_rng(s)
+        g = synth.random_graph(8, 3.0, s)
+        x = r.standard_normal((8, 3))
+        p1 = synth.LayerParams(r.standard_normal((3, 2)), r.standard_normal((3, 2)))
+        p2 = synth.LayerParams(r.standard_normal((4, 2)), r.standard_normal((4, 2)))
+        y1 = O.sage_fwd(g, x, p1.w_self, p1.w_neigh)
+        z1 = _preact(g, x, p1.w_self, p1.w_neigh, None, None)
+        z2 = _preact(g, y1, p2.w_self, p2.w_neigh, None, None)
+        if min(np.abs(z1).min(), np.abs(z2).min()) > 1e-3:
+            break
+    dy = np.random.default_rng(99).standard_normal((8, 4))
+    res = O.sage_stack(g, x, [p1, p2], dy)
+
+    def loss():
+        y1 = O.sage_fwd(g, x, p1.w_self, p1.w_neigh)
+        return float(np.sum(dy * O.sage_fwd(g, y1, p2.w_self, p2.w_neigh)))
+
+    eps = 1e-6
+    for arr, got in [(x, res["grads"][0]["dX"]),
+                     (p1.w_neigh, res["grads"][0]["dW_neigh"]),
+                     (p2.w_self, res["grads"][1]["dW_self"])]:
+        num = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            old = arr[idx]
+            arr[idx] = old + eps
+            lp = loss()
+            arr[idx] = old - eps
+            lm = loss()
+            arr[idx] = old
+            num[idx] = (lp - lm) / (2 * eps)
+        assert rel(got, num) < 1e-6
+
+
+# ------------------------------------------------------ per-output spot evals
+
+def test_spot_evaluations_match_full_layer():
+    g = synth.power_law_graph(120, 2.1, 6.0, seed=9)
+    r = np.random.default_rng(9)
+    f_in, h = 7, 5
+    x = r.standard_normal((120, f_in))
+    ws, wn = r.standard_normal((f_in, h)), r.standard_normal((f_in, h))
+    bs, bn = r.standard_normal(h), r.standard_normal(h)
+    y = O.sage_fwd(g, x, ws, wn, bs, bn)
+    rows = np.array([0, 5, 119, 64, 5])
+    assert rel(O.sage_fwd_rows(g, x, ws, wn, rows, bs, bn), y[rows]) < 1e-14
+    ysyn = r.standard_normal((120, 2 * h))  # any sign pattern is a valid mask
+    dy = r.standard_normal((120, 2 * h))
+    full = O.sage_bwd(g, x, ws, wn, ysyn, dy)
+    assert rel(O.sage_bwd_dx_rows(g, ws, wn, ysyn, dy, rows), full["dX"][rows]) \
+        < 1e-13
+    ei, ej = np.array([0, 6, 3, 2]), np.array([4, 0, 2, 2])
+    a, b = O.sage_bwd_dw_entries(g, x, ysyn, dy, h, ei, ej)
+    assert rel(a, full["dW_self"][ei, ej]) < 1e-13
+    assert rel(b, full["dW_neigh"][ei, ej]) < 1e-13
+
+
+def test_result_independent_of_thread_count(monkeypatch):
+    # fixed summation order: the same bits with any OpenMP thread count
+    import subprocess
+    import sys
+    code = ("import numpy as np,sys;sys.path.insert(0,%r);"
+            "from oracle import oracle as O;from paper_2010_03166_amd import synth;"
+            "g=synth.power_law_graph(500,2.1,8.0,seed=1);"
+            "x=np.random.default_rng(0).standard_normal((500,33));"
+            "w=np.random.default_rng(1).standard_normal((33,8));"
+            "y=O.sage_fwd(g,x,w,w);r=O.sage_bwd(g,x,w,w,y,y);"
+            "sys.stdout.write(str(hash(y.tobytes()+r['dX'].tobytes()+r['dW_neigh'].tobytes()"
+            "+O.spmm_transpose(g,x).tobytes())))") % os.path.dirname(GOLDEN + "/..")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = code.replace(repr(os.path.dirname(GOLDEN + "/..")), repr(root))
+    outs = []
+    for t in ("1", "3", "8"):
+        env = dict(os.environ, OMP_NUM_THREADS=t, PYTHONHASHSEED="0")
+        outs.append(subprocess.run([sys.executable, "-c", code], env=env,
+                                   capture_output=True, text=True,
+                                   check=True).stdout)
+    assert outs[0] == outs[1] == outs[2]
