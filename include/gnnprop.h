@@ -1,0 +1,237 @@
+/*
+ * gnnprop -- GraphSAGE feature propagation on a sampled subgraph, forward
+ * and backward, on AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow "Accurate, Efficient and Scalable Training of Graph
+ * Neural Networks" (Zeng, Zhou, Srivastava, Kannan, Prasanna):
+ *   - one layer's forward, Section 2.1, Eq. "graphsage forward":
+ *       Y = ReLU( X W_self || A_s X W_neigh )      (self half first)
+ *     with A_s the subgraph's normalised adjacency (D^-1 A for GraphSAGE);
+ *   - its backward, Section 5.1, Eq. "gcn backward";
+ *   - the three kernels Section 5.1 names: sparse feature / gradient
+ *     propagation (CSR SpMM), dense weight transformation (GEMM on the
+ *     matrix cores), and the sparse adjacency transpose (Section 5.2,
+ *     Algorithm 6);
+ *   - the computation-order choice of Section 6.1.
+ *
+ * Conventions for every entry point
+ *   - Pointers named as device pointers must point to memory of the current
+ *     HIP device; the library never takes ownership and never frees them.
+ *   - Dense matrices are row-major fp32 with an explicit leading dimension
+ *     (row stride, in elements, >= the row width).  Any 4-byte-aligned
+ *     pointer and any stride is accepted; 16-byte alignment of the base and a
+ *     stride that is a multiple of 4 enable the vector paths.
+ *   - Work is enqueued on `stream` (NULL = the null stream) and is complete
+ *     once the stream is synchronised.  Only gnn_csr_validate synchronises.
+ *   - Argument errors are reported synchronously, before anything is
+ *     enqueued; a failed launch returns GNN_ERR_HIP.  Nothing is printed and
+ *     no C++ exception crosses this interface.
+ *   - Outputs are overwritten, never accumulated into.  Inputs and outputs
+ *     must not overlap unless an entry point says otherwise.
+ *   - gnn_prop_fwd / gnn_prop_bwd / gnn_spmm / gnn_gemm allocate no device
+ *     memory: scratch comes from the caller's `workspace`.
+ */
+#ifndef GNNPROP_H
+#define GNNPROP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gnn_status {
+  GNN_OK = 0,
+  GNN_ERR_NULL = -1,        /* a required pointer is NULL */
+  GNN_ERR_SHAPE = -2,       /* a size or leading dimension is invalid */
+  GNN_ERR_CSR = -3,         /* gnn_csr_validate found an invalid CSR */
+  GNN_ERR_UNSUPPORTED = -4, /* option not supported */
+  GNN_ERR_WORKSPACE = -5,   /* workspace or plan buffer too small */
+  GNN_ERR_HIP = -6,         /* a HIP runtime call or launch failed */
+  GNN_ERR_ALIAS = -7        /* outputs overlap inputs where forbidden */
+} gnn_status;
+
+/* Layer flags. */
+#define GNN_FLAG_BF16 0x1u /* GEMM operands rounded to bf16 (round to nearest
+                              even), fp32 accumulation; aggregation stays fp32 */
+
+/* The sampled subgraph's adjacency A_s in CSR (Section 5.2: Indptr,
+ * Indices, Data).  All arrays are device memory.
+ *   indptr  [n+1]  indptr[0] = 0, non-decreasing, indptr[n] = nnz
+ *   indices [nnz]  column ids in [0,n), ascending within each row
+ *   values  [nnz]  A_s entries (any values; D^-1 A for GraphSAGE)
+ *   values_t[nnz]  entries of (A_s)^T on the same indptr/indices, from
+ *                  gnn_csr_transpose_values; needed by the backward pass
+ *                  and by gnn_spmm with transpose = 1.  The transpose reuses
+ *                  indptr/indices, so the pattern must be symmetric
+ *                  (undirected subgraph, Section 5.2).
+ *   plan           device buffer written by gnn_csr_build_plan: the
+ *                  degree-binned work list of the aggregation kernel. */
+typedef struct gnn_csr {
+  int32_t n;
+  int64_t nnz;
+  const int32_t* indptr;
+  const int32_t* indices;
+  const float* values;
+  const float* values_t;
+  const void* plan;
+} gnn_csr;
+
+/* One layer's shape.  X is n x f_in (stride ld_x); Y and dY are n x 2h
+ * (stride ld_y), self half in columns [0,h), neighbour half in [h,2h);
+ * dX is n x f_in (stride ld_dx); W_self and W_neigh are f_in x h, dense
+ * row-major (stride h); biases are [h].
+ *   order: 0 = choose by gnn_choose_order, 1 = (A_s X) W_neigh,
+ *          2 = A_s (X W_neigh).  Both orders compute the same values. */
+typedef struct gnn_layer {
+  int32_t f_in;
+  int32_t h;
+  int64_t ld_x;
+  int64_t ld_y;
+  int64_t ld_dx;
+  int32_t order;
+  uint32_t flags;
+} gnn_layer;
+
+/* Human-readable name of a status code (static storage). */
+const char* gnn_status_string(gnn_status s);
+
+/* Section 6.1: for A (sparse n x n) . W1 (n x f1) . W2 (f1 x f2), order 1
+ * (A W1) W2 costs delta n^2 f1 + n f1 f2 multiply-adds and order 2
+ * A (W1 W2) costs delta n^2 f2 + n f1 f2.  Returns 1 when f1 <= f2 (ties go
+ * to order 1), else 2.  For a layer, f1 = f_in and f2 = h. */
+int32_t gnn_choose_order(int32_t f_in, int32_t h);
+
+/* ---------------------------------------------------- per-subgraph prep */
+
+/* Section 5.2, Algorithm 6: values of (A_s)^T on the pattern of A_s.  For
+ * each stored (v,u), writes values[pos(v,u)] to values_t[pos(u,v)]; a pure
+ * permutation, bit-exact.  Requires csr->indptr/indices/values; the pattern
+ * must be symmetric with ascending indices per row (check with
+ * gnn_csr_validate).  values_t is device memory of nnz floats. */
+gnn_status gnn_csr_transpose_values(const gnn_csr* csr, float* values_t,
+                                    hipStream_t stream);
+
+/* Bytes of the aggregation work plan for a graph of n rows and nnz entries. */
+size_t gnn_plan_bytes(int32_t n, int64_t nnz);
+
+/* Builds the aggregation work plan into `plan` (device memory of at least
+ * gnn_plan_bytes(n, nnz) bytes): rows are binned by degree; a row with more
+ * stored entries than the plan's chunk length is split into chunks whose
+ * partial sums are combined in a fixed order, so results are deterministic.
+ * Reads only csr->n, nnz and indptr. */
+gnn_status gnn_csr_build_plan(const gnn_csr* csr, void* plan,
+                              size_t plan_bytes, hipStream_t stream);
+
+/* Checks the CSR on the device and synchronises `stream`: indptr
+ * monotone with indptr[0] = 0 and indptr[n] = nnz, indices in range and
+ * strictly ascending per row, and, if require_symmetric, that every stored
+ * (v,u) has a stored (u,v).  Returns GNN_OK or GNN_ERR_CSR.  May allocate a
+ * few bytes of device memory. */
+gnn_status gnn_csr_validate(const gnn_csr* csr, int32_t require_symmetric,
+                            hipStream_t stream);
+
+/* ------------------------------------------------------------ one layer */
+
+/* Device bytes the forward pass saves for the backward pass (order 1 keeps
+ * A_s X, n x f_in floats; order 2 keeps nothing), and the scratch bytes
+ * forward and backward need.  Both depend only on csr->n, csr->nnz and the
+ * layer shape. */
+size_t gnn_prop_saved_bytes(const gnn_csr* csr, const gnn_layer* layer);
+size_t gnn_prop_workspace_bytes(const gnn_csr* csr, const gnn_layer* layer);
+
+/* Forward of one layer, Section 2.1 Eq. "graphsage forward":
+ *   Y[:, 0:h]  = ReLU(X W_self + b_self)
+ *   Y[:, h:2h] = ReLU(A_s X W_neigh + b_neigh)
+ * b_self / b_neigh may be NULL (no bias: the paper's form).  Needs
+ * csr->values and csr->plan.  `saved` (gnn_prop_saved_bytes, may be NULL
+ * when that is 0) receives what gnn_prop_bwd needs and must be passed to it
+ * unchanged.  Y must not overlap X. */
+gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
+                        const float* X, const float* W_self,
+                        const float* W_neigh, const float* b_self,
+                        const float* b_neigh, float* Y, void* saved,
+                        void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
+/* Backward of one layer, Section 5.1 Eq. "gcn backward", given the forward
+ * output Y (its sign pattern is the ReLU mask: G = dY * 1[Y > 0], 0 at the
+ * kink) and dY = dL/dY:
+ *   dW_self  = X^T G[:, 0:h]
+ *   dW_neigh = (A_s X)^T G[:, h:2h]
+ *   dX       = G[:, 0:h] W_self^T + (A_s)^T G[:, h:2h] W_neigh^T
+ *   db_self, db_neigh = column sums of the two halves of G
+ * dX may be NULL (not computed; e.g. the first layer).  db_* may be NULL.
+ * Needs csr->values, csr->values_t and csr->plan, and the `saved` buffer of
+ * the matching gnn_prop_fwd call with the same layer (same order).  Outputs
+ * must not overlap inputs. */
+gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
+                        const float* X, const float* W_self,
+                        const float* W_neigh, const float* Y, const float* dY,
+                        const void* saved, float* dX, float* dW_self,
+                        float* dW_neigh, float* db_self, float* db_neigh,
+                        void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
+/* ------------------------------------------------------------- kernels */
+
+/* Feature / gradient propagation alone (Section 5.1's first kernel, the
+ * per-slice product of Section 5.3, Algorithm 7):
+ *   out = A_s . in        (transpose = 0, uses csr->values)
+ *   out = (A_s)^T . in    (transpose = 1, uses csr->values_t)
+ * in and out are n x w with strides ld_in, ld_out; needs csr->plan;
+ * `workspace` of gnn_spmm_workspace_bytes(csr, w) bytes (may be NULL if 0).
+ * out must not overlap in. */
+size_t gnn_spmm_workspace_bytes(const gnn_csr* csr, int32_t w);
+gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
+                    const float* in, int64_t ld_in, float* out,
+                    int64_t ld_out, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream);
+
+/* Dense weight transformation alone (Section 5.1's second kernel):
+ *   C = op(A) op(B),  C is M x N (stride ldc),
+ *   op(A) = A (M x K, stride lda)  or A^T with A stored K x M (trans_a = 1),
+ *   op(B) = B (K x N, stride ldb)  or B^T with B stored N x K (trans_b = 1).
+ * flags: GNN_FLAG_BF16.  `workspace` of gnn_gemm_workspace_bytes bytes. */
+size_t gnn_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
+gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
+                    int32_t K, const float* A, int64_t lda, const float* B,
+                    int64_t ldb, float* C, int64_t ldc, uint32_t flags,
+                    void* workspace, size_t workspace_bytes,
+                    hipStream_t stream);
+
+/* ----------------------------------------------------- kernel timing */
+
+/* Kernels timed by the optional event timer. */
+#define GNN_K_SPMM 0          /* aggregation over work items */
+#define GNN_K_SPMM_REDUCE 1   /* chunk-partial reduction of long rows */
+#define GNN_K_GEMM_NN 2       /* C = A B            (forward transforms) */
+#define GNN_K_GEMM_TN 3       /* C = A^T B          (weight gradients) */
+#define GNN_K_GEMM_NT 4       /* C = A B^T          (input gradients) */
+#define GNN_K_GEMM_TT 5       /* C = A^T B^T */
+#define GNN_K_GEMM_REDUCE 6   /* split-K partial reduction */
+#define GNN_K_MASK 7          /* ReLU mask of the output gradient */
+#define GNN_K_COLSUM 8        /* bias-gradient column sums */
+#define GNN_K_PLAN 9          /* aggregation plan build */
+#define GNN_K_TRANSPOSE 10    /* transposed values (Algorithm 6) */
+#define GNN_K_COUNT 11
+
+/* When enabled, every kernel launch is bracketed by a pair of HIP events on
+ * its stream.  gnn_timer_read synchronises on the recorded events and
+ * returns, for one kernel id since the last reset, the summed milliseconds,
+ * the launch count and the summed algorithmic work of those launches:
+ * bytes for memory-bound kernels (aggregation: 4(n+1) + 8 nnz + 8 n w per
+ * call, counted on GNN_K_SPMM), flops for the GEMMs (2 M N K).  Host-side
+ * bookkeeping only; not thread safe. */
+gnn_status gnn_timer_enable(int32_t enable);
+gnn_status gnn_timer_reset(void);
+gnn_status gnn_timer_read(int32_t kernel, double* ms, int64_t* launches,
+                          double* work);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GNNPROP_H */

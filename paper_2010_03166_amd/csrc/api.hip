@@ -1,0 +1,593 @@
+// C-ABI of libgnnprop: argument checks, workspace carving and the launch
+// sequence of one GraphSAGE layer's forward and backward pass.
+//
+// Forward (Section 2.1, Eq. "graphsage forward"), with the Section 6.1
+// order choice for the neighbour path A_s X W_neigh:
+//   order 1:  S = A_s X (kept for the backward pass)
+//             [Y_self | Y_neigh] = ReLU([X W_self + b_s | S W_neigh + b_n])
+//             -- one aggregation, one two-problem matrix-core launch
+//   order 2:  [Y_self | P] = [ReLU(X W_self + b_s) | X W_neigh]
+//             Y_neigh = ReLU(A_s P + b_n)   (bias + ReLU fused into the
+//                                            aggregation's store)
+// Backward (Section 5.1, Eq. "gcn backward"), G = dY * 1[Y > 0]:
+//   order 2:  [G_s | G_n] <- mask;  T = (A_s)^T G_n
+//             dW_self = X^T G_s, dW_neigh = X^T T     ( = (A_s X)^T G_n )
+//             dX = G_s W_self^T + T W_neigh^T         (one launch, 2 K parts)
+//   order 1:  G <- mask;  dW_self = X^T G_s, dW_neigh = S^T G_n
+//             dX = G_s W_self^T;  V = G_n W_neigh^T;  dX += (A_s)^T V
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "internal.hpp"
+
+using namespace gnnprop;
+
+namespace {
+
+#define GNN_HIP(expr)                         \
+  do {                                        \
+    if ((expr) != hipSuccess) return GNN_ERR_HIP; \
+  } while (0)
+
+// ------------------------------------------------------------- timer
+
+struct TimerRec {
+  int kclass;
+  double work;
+  hipEvent_t a, b;
+};
+bool g_timer_on = false;
+std::vector<hipEvent_t> g_pool;
+size_t g_pool_used = 0;
+std::vector<TimerRec> g_recs;
+TimerRec g_cur;
+
+bool ranges_overlap(const void* a, size_t an, const void* b, size_t bn) {
+  if (!a || !b || an == 0 || bn == 0) return false;
+  const char* pa = static_cast<const char*>(a);
+  const char* pb = static_cast<const char*>(b);
+  return pa < pb + bn && pb < pa + an;
+}
+
+size_t mat_bytes(int64_t rows, int64_t cols, int64_t ld) {
+  if (rows <= 0 || cols <= 0) return 0;
+  return (size_t)(((rows - 1) * ld + cols) * 4);
+}
+
+// ------------------------------------------------------- layer layout
+
+struct LayerLayout {
+  int order;
+  int64_t ld_s, ld_p, ld_g, ld_gn, ld_v;
+  size_t off_buf0, off_buf1, off_spart, off_gemm, off_cs, total;
+};
+
+int resolve_order(const gnn_layer* L) {
+  return L->order ? L->order : gnn_choose_order(L->f_in, L->h);
+}
+
+GemmBatch fwd_batch(int order, int32_t n, int32_t f_in, int32_t h,
+                    const float* X, int64_t ld_x, const float* S, int64_t ld_s,
+                    const float* Ws, const float* Wn, const float* bs,
+                    const float* bn, float* Y, int64_t ld_y, float* P,
+                    int64_t ld_p) {
+  GemmBatch b;
+  memset(&b, 0, sizeof(b));
+  b.nprob = 2;
+  b.trans_a = 0;
+  b.trans_b = 0;
+  GemmProblem& p0 = b.p[0];
+  p0.nseg = 1;
+  p0.seg[0] = {X, Ws, ld_x, h, f_in};
+  p0.M = n;
+  p0.N = h;
+  p0.C = Y;
+  p0.ldc = ld_y;
+  p0.bias = bs;
+  p0.relu = 1;
+  GemmProblem& p1 = b.p[1];
+  p1.nseg = 1;
+  p1.M = n;
+  p1.N = h;
+  if (order == 1) {  // Y_neigh = ReLU(S W_neigh + b_n)
+    p1.seg[0] = {S, Wn, ld_s, h, f_in};
+    p1.C = Y ? Y + h : nullptr;
+    p1.ldc = ld_y;
+    p1.bias = bn;
+    p1.relu = 1;
+  } else {           // P = X W_neigh
+    p1.seg[0] = {X, Wn, ld_x, h, f_in};
+    p1.C = P;
+    p1.ldc = ld_p;
+    p1.bias = nullptr;
+    p1.relu = 0;
+  }
+  return b;
+}
+
+// dW_self = X^T G_s ; dW_neigh = (order 1: S, order 2: X)^T (G_n or T)
+GemmBatch dw_batch(int order, int32_t n, int32_t f_in, int32_t h,
+                   const float* X, int64_t ld_x, const float* S, int64_t ld_s,
+                   const float* Gs, const float* Gn, int64_t ld_g,
+                   float* dWs, float* dWn) {
+  GemmBatch b;
+  memset(&b, 0, sizeof(b));
+  b.nprob = 2;
+  b.trans_a = 1;
+  b.trans_b = 0;
+  for (int i = 0; i < 2; ++i) {
+    GemmProblem& p = b.p[i];
+    p.nseg = 1;
+    p.M = f_in;
+    p.N = h;
+    p.ldc = h;
+    p.relu = 0;
+    p.bias = nullptr;
+  }
+  b.p[0].seg[0] = {X, Gs, ld_x, ld_g, n};
+  b.p[0].C = dWs;
+  if (order == 1)
+    b.p[1].seg[0] = {S, Gn, ld_s, ld_g, n};
+  else
+    b.p[1].seg[0] = {X, Gn, ld_x, ld_g, n};
+  b.p[1].C = dWn;
+  return b;
+}
+
+// order 2: dX = G_s W_s^T + T W_n^T (one problem, two K parts)
+// order 1: dX = G_s W_s^T ; V = G_n W_n^T
+GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
+                   const float* Gs, const float* Gn, int64_t ld_g,
+                   const float* Ws, const float* Wn, float* dX, int64_t ld_dx,
+                   float* V, int64_t ld_v) {
+  GemmBatch b;
+  memset(&b, 0, sizeof(b));
+  b.trans_a = 0;
+  b.trans_b = 1;
+  if (order == 2) {
+    b.nprob = 1;
+    GemmProblem& p = b.p[0];
+    p.nseg = 2;
+    p.seg[0] = {Gs, Ws, ld_g, h, h};
+    p.seg[1] = {Gn, Wn, ld_g, h, h};
+    p.M = n;
+    p.N = f_in;
+    p.C = dX;
+    p.ldc = ld_dx;
+  } else {
+    b.nprob = 2;
+    for (int i = 0; i < 2; ++i) {
+      b.p[i].nseg = 1;
+      b.p[i].M = n;
+      b.p[i].N = f_in;
+    }
+    b.p[0].seg[0] = {Gs, Ws, ld_g, h, h};
+    b.p[0].C = dX;
+    b.p[0].ldc = ld_dx;
+    b.p[1].seg[0] = {Gn, Wn, ld_g, h, h};
+    b.p[1].C = V;
+    b.p[1].ldc = ld_v;
+  }
+  return b;
+}
+
+LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
+  LayerLayout o;
+  const int32_t n = csr->n, f_in = L->f_in, h = L->h;
+  o.order = resolve_order(L);
+  o.ld_s = round_up(f_in, 4);
+  o.ld_p = round_up(h, 4);
+  o.ld_g = round_up(2 * (int64_t)h, 4);
+  o.ld_gn = round_up(h, 4);
+  o.ld_v = round_up(f_in, 4);
+  size_t buf0, buf1;
+  if (o.order == 2) {
+    buf0 = std::max((size_t)n * o.ld_p, (size_t)n * o.ld_g) * 4;  // P | GT
+    buf1 = (size_t)n * o.ld_gn * 4;                               // G_n
+  } else {
+    buf0 = (size_t)n * o.ld_g * 4;  // G
+    buf1 = (size_t)n * o.ld_v * 4;  // V
+  }
+  const int32_t w = o.order == 1 ? f_in : h;
+  size_t gemm = 0;
+  gemm = std::max(gemm, gemm_workspace_bytes(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0)));
+  gemm = std::max(gemm, gemm_workspace_bytes(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 2 * h, 0, 0)));
+  gemm = std::max(gemm, gemm_workspace_bytes(dx_batch(o.order, n, f_in, h, 0, 0, 2 * h, 0, 0, 0, f_in, 0, f_in)));
+  o.off_buf0 = 0;
+  o.off_buf1 = round_up(buf0, 256);
+  o.off_spart = o.off_buf1 + round_up(buf1, 256);
+  o.off_gemm = o.off_spart + spmm_partials_bytes(n, csr->nnz, w);
+  o.off_cs = o.off_gemm + round_up(gemm, 256);
+  o.total = o.off_cs + colsum_partials_bytes(n, h);
+  return o;
+}
+
+gnn_status check_csr(const gnn_csr* c, bool need_vals, bool need_vals_t) {
+  if (!c) return GNN_ERR_NULL;
+  if (c->n < 0 || c->nnz < 0 || c->nnz > INT32_MAX) return GNN_ERR_SHAPE;
+  if (!c->indptr) return GNN_ERR_NULL;
+  if (c->nnz > 0 && !c->indices) return GNN_ERR_NULL;
+  if (need_vals && c->nnz > 0 && !c->values) return GNN_ERR_NULL;
+  if (need_vals_t && c->nnz > 0 && !c->values_t) return GNN_ERR_NULL;
+  return GNN_OK;
+}
+
+gnn_status check_layer(const gnn_layer* L) {
+  if (!L) return GNN_ERR_NULL;
+  if (L->f_in <= 0 || L->h <= 0) return GNN_ERR_SHAPE;
+  if (L->ld_x < L->f_in || L->ld_y < 2 * (int64_t)L->h) return GNN_ERR_SHAPE;
+  if (L->order < 0 || L->order > 2) return GNN_ERR_SHAPE;
+  if (L->flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  if (L->flags & GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  return GNN_OK;
+}
+
+SpmmCall spmm_call(const gnn_csr* c, bool transpose, int32_t w,
+                   const float* in, int64_t ld_in, float* out, int64_t ld_out,
+                   float* partials) {
+  SpmmCall s;
+  memset(&s, 0, sizeof(s));
+  s.n = c->n;
+  s.nnz = c->nnz;
+  s.indices = c->indices;
+  s.vals = transpose ? c->values_t : c->values;
+  s.plan = c->plan;
+  s.w = w;
+  s.in = in;
+  s.ld_in = ld_in;
+  s.out = out;
+  s.ld_out = ld_out;
+  s.epilogue = SPMM_STORE;
+  s.partials = partials;
+  return s;
+}
+
+
+}  // namespace
+
+namespace gnnprop {
+
+void timer_begin(int kclass, hipStream_t s) {
+  if (!g_timer_on) return;
+  while (g_pool_used + 2 > g_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    g_pool.push_back(e);
+  }
+  g_cur.kclass = kclass;
+  g_cur.a = g_pool[g_pool_used++];
+  g_cur.b = g_pool[g_pool_used++];
+  (void)hipEventRecord(g_cur.a, s);
+}
+
+void timer_end(int kclass, double work, hipStream_t s) {
+  if (!g_timer_on || g_cur.kclass != kclass) return;
+  (void)hipEventRecord(g_cur.b, s);
+  g_cur.work = work;
+  g_recs.push_back(g_cur);
+  g_cur.kclass = -1;
+}
+
+}  // namespace gnnprop
+
+extern "C" {
+
+const char* gnn_status_string(gnn_status s) {
+  switch (s) {
+    case GNN_OK: return "ok";
+    case GNN_ERR_NULL: return "required pointer is NULL";
+    case GNN_ERR_SHAPE: return "invalid size or leading dimension";
+    case GNN_ERR_CSR: return "invalid CSR";
+    case GNN_ERR_UNSUPPORTED: return "unsupported option";
+    case GNN_ERR_WORKSPACE: return "workspace or plan buffer too small";
+    case GNN_ERR_HIP: return "HIP runtime error";
+    case GNN_ERR_ALIAS: return "output overlaps an input";
+  }
+  return "unknown status";
+}
+
+int32_t gnn_choose_order(int32_t f_in, int32_t h) { return f_in <= h ? 1 : 2; }
+
+size_t gnn_plan_bytes(int32_t n, int64_t nnz) {
+  if (n < 0 || nnz < 0) return 0;
+  return plan_dims(n, nnz).bytes;
+}
+
+gnn_status gnn_csr_transpose_values(const gnn_csr* csr, float* values_t,
+                                    hipStream_t stream) {
+  gnn_status st = check_csr(csr, true, false);
+  if (st != GNN_OK) return st;
+  if (csr->nnz > 0 && !values_t) return GNN_ERR_NULL;
+  if (ranges_overlap(values_t, csr->nnz * 4, csr->values, csr->nnz * 4))
+    return GNN_ERR_ALIAS;
+  GNN_HIP(transpose_values_launch(csr->n, csr->indptr, csr->indices,
+                                  csr->values, values_t, stream));
+  return GNN_OK;
+}
+
+gnn_status gnn_csr_build_plan(const gnn_csr* csr, void* plan,
+                              size_t plan_bytes, hipStream_t stream) {
+  gnn_status st = check_csr(csr, false, false);
+  if (st != GNN_OK) return st;
+  if (!plan) return GNN_ERR_NULL;
+  if (plan_bytes < gnn_plan_bytes(csr->n, csr->nnz)) return GNN_ERR_WORKSPACE;
+  GNN_HIP(plan_build_launch(csr->n, csr->nnz, csr->indptr, plan, stream));
+  return GNN_OK;
+}
+
+gnn_status gnn_csr_validate(const gnn_csr* csr, int32_t require_symmetric,
+                            hipStream_t stream) {
+  gnn_status st = check_csr(csr, false, false);
+  if (st != GNN_OK) return st;
+  int32_t* bad = nullptr;
+  GNN_HIP(hipMalloc(&bad, sizeof(int32_t)));
+  int32_t h_bad = 0;
+  hipError_t e = hipMemcpyAsync(bad, &h_bad, sizeof(int32_t),
+                                hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess)
+    e = validate_csr(csr->n, csr->nnz, csr->indptr, csr->indices,
+                     require_symmetric, bad, stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(&h_bad, bad, sizeof(int32_t), hipMemcpyDeviceToHost,
+                       stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  (void)hipFree(bad);
+  if (e != hipSuccess) return GNN_ERR_HIP;
+  return h_bad ? GNN_ERR_CSR : GNN_OK;
+}
+
+size_t gnn_spmm_workspace_bytes(const gnn_csr* csr, int32_t w) {
+  if (!csr || csr->n < 0 || csr->nnz < 0 || w < 0) return 0;
+  return spmm_partials_bytes(csr->n, csr->nnz, w);
+}
+
+gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
+                    const float* in, int64_t ld_in, float* out,
+                    int64_t ld_out, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+  gnn_status st = check_csr(csr, !transpose, transpose != 0);
+  if (st != GNN_OK) return st;
+  if (w < 0 || ld_in < w || ld_out < w) return GNN_ERR_SHAPE;
+  if (csr->n == 0 || w == 0) return GNN_OK;
+  if (!in || !out || !csr->plan) return GNN_ERR_NULL;
+  const size_t need = spmm_partials_bytes(csr->n, csr->nnz, w);
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return GNN_ERR_WORKSPACE;
+  if (ranges_overlap(in, mat_bytes(csr->n, w, ld_in), out,
+                     mat_bytes(csr->n, w, ld_out)))
+    return GNN_ERR_ALIAS;
+  SpmmCall c = spmm_call(csr, transpose != 0, w, in, ld_in, out, ld_out,
+                         static_cast<float*>(workspace));
+  GNN_HIP(spmm_launch(c, stream));
+  return GNN_OK;
+}
+
+size_t gnn_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
+  if (M < 0 || N < 0 || K < 0) return 0;
+  GemmBatch b;
+  memset(&b, 0, sizeof(b));
+  b.nprob = 1;
+  b.p[0].nseg = 1;
+  b.p[0].M = M;
+  b.p[0].N = N;
+  b.p[0].seg[0].K = K;
+  return gemm_workspace_bytes(b);
+}
+
+gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
+                    int32_t K, const float* A, int64_t lda, const float* B,
+                    int64_t ldb, float* C, int64_t ldc, uint32_t flags,
+                    void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+  if (M < 0 || N < 0 || K < 0) return GNN_ERR_SHAPE;
+  if (flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  if (flags & GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  if (M == 0 || N == 0) return GNN_OK;
+  if (!C || (K > 0 && (!A || !B))) return GNN_ERR_NULL;
+  if (ldc < N) return GNN_ERR_SHAPE;
+  if (K > 0) {
+    if (trans_a ? lda < M : lda < K) return GNN_ERR_SHAPE;
+    if (trans_b ? ldb < K : ldb < N) return GNN_ERR_SHAPE;
+  }
+  GemmBatch b;
+  memset(&b, 0, sizeof(b));
+  b.nprob = 1;
+  b.trans_a = trans_a != 0;
+  b.trans_b = trans_b != 0;
+  b.p[0].nseg = 1;
+  b.p[0].seg[0] = {A, B, lda, ldb, K};
+  b.p[0].M = M;
+  b.p[0].N = N;
+  b.p[0].C = C;
+  b.p[0].ldc = ldc;
+  const size_t need = gemm_workspace_bytes(b);
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return GNN_ERR_WORKSPACE;
+  const size_t cb = mat_bytes(M, N, ldc);
+  if (K > 0 &&
+      (ranges_overlap(C, cb, A, trans_a ? mat_bytes(K, M, lda) : mat_bytes(M, K, lda)) ||
+       ranges_overlap(C, cb, B, trans_b ? mat_bytes(N, K, ldb) : mat_bytes(K, N, ldb))))
+    return GNN_ERR_ALIAS;
+  GNN_HIP(gemm_launch(b, workspace, workspace_bytes, stream));
+  return GNN_OK;
+}
+
+size_t gnn_prop_saved_bytes(const gnn_csr* csr, const gnn_layer* layer) {
+  if (!csr || !layer || csr->n < 0 || layer->f_in <= 0 || layer->h <= 0)
+    return 0;
+  if (resolve_order(layer) != 1) return 0;
+  return round_up((size_t)csr->n * round_up(layer->f_in, 4) * 4, 256);
+}
+
+size_t gnn_prop_workspace_bytes(const gnn_csr* csr, const gnn_layer* layer) {
+  if (!csr || !layer || csr->n < 0 || csr->nnz < 0 || layer->f_in <= 0 ||
+      layer->h <= 0)
+    return 0;
+  return layer_layout(csr, layer).total;
+}
+
+gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
+                        const float* X, const float* W_self,
+                        const float* W_neigh, const float* b_self,
+                        const float* b_neigh, float* Y, void* saved,
+                        void* workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+  gnn_status st = check_csr(csr, true, false);
+  if (st != GNN_OK) return st;
+  if ((st = check_layer(layer)) != GNN_OK) return st;
+  const int32_t n = csr->n, f_in = layer->f_in, h = layer->h;
+  if (n > 0 && (!X || !Y || !csr->plan)) return GNN_ERR_NULL;
+  if (!W_self || !W_neigh) return GNN_ERR_NULL;
+  const LayerLayout o = layer_layout(csr, layer);
+  if (o.order == 1 && n > 0 && !saved) return GNN_ERR_NULL;
+  if (workspace_bytes < o.total || (o.total > 0 && !workspace))
+    return GNN_ERR_WORKSPACE;
+  if (n == 0) return GNN_OK;
+  const size_t yb = mat_bytes(n, 2 * h, layer->ld_y);
+  if (ranges_overlap(Y, yb, X, mat_bytes(n, f_in, layer->ld_x)) ||
+      ranges_overlap(Y, yb, W_self, (size_t)f_in * h * 4) ||
+      ranges_overlap(Y, yb, W_neigh, (size_t)f_in * h * 4))
+    return GNN_ERR_ALIAS;
+
+  char* ws = static_cast<char*>(workspace);
+  float* spart = reinterpret_cast<float*>(ws + o.off_spart);
+  void* gws = ws + o.off_gemm;
+  const size_t gws_bytes = o.off_cs - o.off_gemm;
+  if (o.order == 1) {
+    float* S = static_cast<float*>(saved);
+    SpmmCall c = spmm_call(csr, false, f_in, X, layer->ld_x, S, o.ld_s, spart);
+    GNN_HIP(spmm_launch(c, stream));
+    GemmBatch b = fwd_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, W_self,
+                            W_neigh, b_self, b_neigh, Y, layer->ld_y, nullptr, 0);
+    GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
+  } else {
+    float* P = reinterpret_cast<float*>(ws + o.off_buf0);
+    GemmBatch b = fwd_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, W_self,
+                            W_neigh, b_self, nullptr, Y, layer->ld_y, P, o.ld_p);
+    GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
+    SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y, spart);
+    c.epilogue = SPMM_BIAS_RELU;
+    c.bias = b_neigh;
+    GNN_HIP(spmm_launch(c, stream));
+  }
+  return GNN_OK;
+}
+
+gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
+                        const float* X, const float* W_self,
+                        const float* W_neigh, const float* Y, const float* dY,
+                        const void* saved, float* dX, float* dW_self,
+                        float* dW_neigh, float* db_self, float* db_neigh,
+                        void* workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+  gnn_status st = check_csr(csr, true, true);
+  if (st != GNN_OK) return st;
+  if ((st = check_layer(layer)) != GNN_OK) return st;
+  const int32_t n = csr->n, f_in = layer->f_in, h = layer->h;
+  if (!W_self || !W_neigh || !dW_self || !dW_neigh) return GNN_ERR_NULL;
+  if (n > 0 && (!X || !Y || !dY || !csr->plan)) return GNN_ERR_NULL;
+  if (dX && layer->ld_dx < f_in) return GNN_ERR_SHAPE;
+  const LayerLayout o = layer_layout(csr, layer);
+  if (o.order == 1 && n > 0 && !saved) return GNN_ERR_NULL;
+  if (workspace_bytes < o.total || (o.total > 0 && !workspace))
+    return GNN_ERR_WORKSPACE;
+  {
+    const size_t wb = (size_t)f_in * h * 4;
+    const void* ins[] = {X, W_self, W_neigh, Y, dY};
+    const size_t inb[] = {mat_bytes(n, f_in, layer->ld_x), wb, wb,
+                          mat_bytes(n, 2 * h, layer->ld_y),
+                          mat_bytes(n, 2 * h, layer->ld_y)};
+    const void* outs[] = {dX, dW_self, dW_neigh, db_self, db_neigh};
+    const size_t outb[] = {dX ? mat_bytes(n, f_in, layer->ld_dx) : 0, wb, wb,
+                           (size_t)h * 4, (size_t)h * 4};
+    for (int i = 0; i < 5; ++i)
+      for (int k = 0; k < 5; ++k)
+        if (ranges_overlap(outs[i], outb[i], ins[k], inb[k])) return GNN_ERR_ALIAS;
+  }
+
+  char* ws = static_cast<char*>(workspace);
+  float* buf0 = reinterpret_cast<float*>(ws + o.off_buf0);
+  float* buf1 = reinterpret_cast<float*>(ws + o.off_buf1);
+  float* spart = reinterpret_cast<float*>(ws + o.off_spart);
+  void* gws = ws + o.off_gemm;
+  const size_t gws_bytes = o.off_cs - o.off_gemm;
+  float* cspart = reinterpret_cast<float*>(ws + o.off_cs);
+
+  if (o.order == 2) {
+    float* GT = buf0;  // [G_s | T], n x ld_g
+    float* Gn = buf1;  // G_n, n x ld_gn
+    GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, GT, o.ld_g, Gn, o.ld_gn, stream));
+    SpmmCall c = spmm_call(csr, true, h, Gn, o.ld_gn, GT + h, o.ld_g, spart);
+    GNN_HIP(spmm_launch(c, stream));
+    GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, GT,
+                            GT + h, o.ld_g, dW_self, dW_neigh);
+    GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
+    if (dX) {
+      GemmBatch bx = dx_batch(2, n, f_in, h, GT, GT + h, o.ld_g, W_self,
+                              W_neigh, dX, layer->ld_dx, nullptr, 0);
+      GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
+    }
+    if (db_self || db_neigh) {
+      if (db_self) GNN_HIP(colsum_launch(n, h, GT, o.ld_g, db_self, cspart, stream));
+      if (db_neigh) GNN_HIP(colsum_launch(n, h, Gn, o.ld_gn, db_neigh, cspart, stream));
+    }
+  } else {
+    float* G = buf0;  // [G_s | G_n], n x ld_g
+    float* V = buf1;  // G_n W_n^T, n x ld_v
+    const float* S = static_cast<const float*>(saved);
+    GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, G, o.ld_g, G + h, o.ld_g, stream));
+    GemmBatch bw = dw_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, G, G + h,
+                            o.ld_g, dW_self, dW_neigh);
+    GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
+    if (dX) {
+      GemmBatch bx = dx_batch(1, n, f_in, h, G, G + h, o.ld_g, W_self, W_neigh,
+                              dX, layer->ld_dx, V, o.ld_v);
+      GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
+      SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx, spart);
+      c.epilogue = SPMM_ADD;
+      c.res = dX;
+      c.ld_res = layer->ld_dx;
+      GNN_HIP(spmm_launch(c, stream));
+    }
+    if (db_self || db_neigh) {
+      if (db_self) GNN_HIP(colsum_launch(n, h, G, o.ld_g, db_self, cspart, stream));
+      if (db_neigh) GNN_HIP(colsum_launch(n, h, G + h, o.ld_g, db_neigh, cspart, stream));
+    }
+  }
+  return GNN_OK;
+}
+
+gnn_status gnn_timer_enable(int32_t enable) {
+  g_timer_on = enable != 0;
+  return GNN_OK;
+}
+
+gnn_status gnn_timer_reset(void) {
+  g_recs.clear();
+  g_pool_used = 0;
+  g_cur.kclass = -1;
+  return GNN_OK;
+}
+
+gnn_status gnn_timer_read(int32_t kernel, double* ms, int64_t* launches,
+                          double* work) {
+  if (kernel < 0 || kernel >= GNN_K_COUNT) return GNN_ERR_SHAPE;
+  double t = 0, wk = 0;
+  int64_t c = 0;
+  for (const TimerRec& r : g_recs) {
+    if (r.kclass != kernel) continue;
+    if (hipEventSynchronize(r.b) != hipSuccess) return GNN_ERR_HIP;
+    float e = 0.f;
+    if (hipEventElapsedTime(&e, r.a, r.b) != hipSuccess) return GNN_ERR_HIP;
+    t += e;
+    wk += r.work;
+    ++c;
+  }
+  if (ms) *ms = t;
+  if (launches) *launches = c;
+  if (work) *work = wk;
+  return GNN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,142 @@
+// Internal interfaces between the translation units of libgnnprop.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cstring>
+
+#include "gnnprop.h"
+
+namespace gnnprop {
+
+// --------------------------------------------------------------- helpers
+
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) {
+  return (a + b - 1) / b;
+}
+__host__ __device__ inline int64_t round_up(int64_t a, int64_t b) {
+  return ceil_div(a, b) * b;
+}
+inline bool aligned16(const void* p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+// Row-major matrix that may be read/written with float4 accesses.
+inline bool vec4_ok(const void* p, int64_t ld) {
+  return p != nullptr && aligned16(p) && (ld % 4) == 0;
+}
+
+// ------------------------------------------------------------ work plan
+
+// Layout of the aggregation plan buffer (device memory):
+//   PlanHeader, then int4 items[max_items], then int4 splits[max_splits].
+// item  = {row, begin, end, slot}: the stored entries [begin,end) of `row`;
+//         slot < 0 -> the item covers the whole row and writes the output
+//         row; slot >= 0 -> partial sum written to partial row `slot`.
+// split = {row, first_slot, n_slots, 0}: a row cut into n_slots chunks whose
+//         partials are summed in slot order by the reduction kernel.
+struct PlanHeader {
+  int32_t n_items;
+  int32_t n_splits;
+  int32_t chunk;
+  int32_t n_slots;
+  int32_t n;
+  int32_t pad[3];
+};
+
+struct PlanDims {
+  int32_t chunk;
+  int64_t max_items, max_splits, max_slots;
+  size_t items_offset, splits_offset, bytes;
+};
+PlanDims plan_dims(int32_t n, int64_t nnz);
+
+// ------------------------------------------------------- kernel timing
+
+struct Timer;
+// Records `start`/`stop` events around the launch when timing is enabled.
+void timer_begin(int kclass, hipStream_t s);
+void timer_end(int kclass, double work, hipStream_t s);
+
+// ------------------------------------------------------------ SpMM
+
+enum SpmmEpilogue : int32_t {
+  SPMM_STORE = 0,      // out = acc
+  SPMM_BIAS_RELU = 1,  // out = max(acc + bias[c], 0)   (bias may be null)
+  SPMM_ADD = 2,        // out = acc + res[row, c]         (res may alias out)
+};
+
+struct SpmmCall {
+  int32_t n;
+  int64_t nnz;
+  const int32_t* indices;
+  const float* vals;
+  const void* plan;
+  int32_t w;
+  const float* in;
+  int64_t ld_in;
+  float* out;
+  int64_t ld_out;
+  int32_t epilogue;
+  const float* bias;
+  const float* res;
+  int64_t ld_res;
+  float* partials;  // workspace: max_slots x round_up(w,4) floats
+};
+size_t spmm_partials_bytes(int32_t n, int64_t nnz, int32_t w);
+hipError_t spmm_launch(const SpmmCall& c, hipStream_t s);
+
+hipError_t plan_build_launch(int32_t n, int64_t nnz, const int32_t* indptr,
+                             void* plan, hipStream_t s);
+hipError_t transpose_values_launch(int32_t n, const int32_t* indptr,
+                                   const int32_t* indices, const float* vals,
+                                   float* vals_t, hipStream_t s);
+// Returns 0 if valid, else a nonzero code; synchronises.
+hipError_t validate_csr(int32_t n, int64_t nnz, const int32_t* indptr,
+                        const int32_t* indices, int32_t symmetric,
+                        int32_t* bad, hipStream_t s);
+
+// ------------------------------------------------------------ GEMM
+
+// C = sum over segments of op(A_s) op(B_s), then + bias[col], then ReLU.
+struct GemmSeg {
+  const float* A;
+  const float* B;
+  int64_t lda, ldb;
+  int32_t K;
+};
+struct GemmProblem {
+  GemmSeg seg[2];
+  int32_t nseg;
+  int32_t M, N;
+  float* C;
+  int64_t ldc;
+  const float* bias;
+  int32_t relu;
+};
+struct GemmBatch {
+  GemmProblem p[2];
+  int32_t nprob;
+  int32_t trans_a, trans_b;  // A stored K x M; B stored N x K
+  int32_t bf16;
+};
+size_t gemm_workspace_bytes(const GemmBatch& b);
+hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
+                       hipStream_t s);
+double gemm_flops(const GemmBatch& b);
+
+// ----------------------------------------------------- elementwise
+
+// G = dY * 1[Y > 0] over an n x 2h block; columns [0,h) -> dst0, [h,2h)
+// -> dst1.
+hipError_t mask_launch(int32_t n, int32_t h, const float* Y, const float* dY,
+                       int64_t ld_y, float* dst0, int64_t ld0, float* dst1,
+                       int64_t ld1, hipStream_t s);
+// out[c] = sum over rows of G[r, c], rows in ascending blocks of 256 summed
+// in a fixed order.  partials: colsum_partials_bytes.
+size_t colsum_partials_bytes(int32_t n, int32_t w);
+hipError_t colsum_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
+                         float* out, float* partials, hipStream_t s);
+
+}  // namespace gnnprop

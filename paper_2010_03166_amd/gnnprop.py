@@ -1,0 +1,244 @@
+"""Python binding of libgnnprop (ctypes).
+
+Argument marshalling only: every function here has the name of the C entry
+point it calls, takes torch tensors on the current HIP device (or plain
+integers), passes their data pointers and the current stream, and raises
+GnnError when the library returns an error status.  All computation happens
+in the HIP kernels of libgnnprop.so; if that library is missing this module
+raises instead of computing anything itself.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libgnnprop.so")
+
+GNN_OK = 0
+GNN_FLAG_BF16 = 0x1
+KERNELS = {"spmm": 0, "spmm_reduce": 1, "gemm_nn": 2, "gemm_tn": 3,
+           "gemm_nt": 4, "gemm_tt": 5, "gemm_reduce": 6, "mask": 7,
+           "colsum": 8, "plan": 9, "transpose": 10}
+
+_lib = None
+
+
+class GnnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (where, status_string(status), status))
+
+
+class gnn_csr(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("nnz", ctypes.c_int64),
+                ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p),
+                ("values", ctypes.c_void_p), ("values_t", ctypes.c_void_p),
+                ("plan", ctypes.c_void_p)]
+
+
+class gnn_layer(ctypes.Structure):
+    _fields_ = [("f_in", ctypes.c_int32), ("h", ctypes.c_int32),
+                ("ld_x", ctypes.c_int64), ("ld_y", ctypes.c_int64),
+                ("ld_dx", ctypes.c_int64), ("order", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
+
+
+EXPORTS = {
+    # name: (restype, argtypes)
+    "gnn_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
+    "gnn_choose_order": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_int32]),
+    "gnn_plan_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int64]),
+    "gnn_csr_transpose_values": (ctypes.c_int32, [ctypes.POINTER(gnn_csr),
+                                                  ctypes.c_void_p, ctypes.c_void_p]),
+    "gnn_csr_build_plan": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.c_void_p,
+                                            ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_csr_validate": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.c_int32,
+                                          ctypes.c_void_p]),
+    "gnn_prop_saved_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                               ctypes.POINTER(gnn_layer)]),
+    "gnn_prop_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                                   ctypes.POINTER(gnn_layer)]),
+    "gnn_prop_fwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer)]
+                     + [ctypes.c_void_p] * 8 + [ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_prop_bwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer)]
+                     + [ctypes.c_void_p] * 12 + [ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_spmm_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                                   ctypes.c_int32]),
+    "gnn_spmm": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                  ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t,
+                                  ctypes.c_void_p]),
+    "gnn_gemm_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32] * 3),
+    "gnn_gemm": (ctypes.c_int32, [ctypes.c_int32] * 5 + [
+        ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+        ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32, ctypes.c_void_p,
+        ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_timer_enable": (ctypes.c_int32, [ctypes.c_int32]),
+    "gnn_timer_reset": (ctypes.c_int32, []),
+    "gnn_timer_read": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int64),
+                                        ctypes.POINTER(ctypes.c_double)]),
+}
+
+
+def lib():
+    """The loaded libgnnprop.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                "libgnnprop.so is not built (expected at %s); run "
+                "`python -c 'import __graft_entry__ as g; g.build()'`" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in EXPORTS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_string(s: int) -> str:
+    return lib().gnn_status_string(int(s)).decode()
+
+
+def _check(st: int, where: str):
+    if st != GNN_OK:
+        raise GnnError(st, where)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ld(t) -> int:
+    return int(t.stride(0)) if t.dim() == 2 else int(t.shape[-1])
+
+
+# ------------------------------------------------------------ structures
+
+def make_csr(n: int, nnz: int, indptr, indices, values, values_t=None,
+             plan=None) -> gnn_csr:
+    return gnn_csr(int(n), int(nnz), _ptr(indptr), _ptr(indices), _ptr(values),
+                   _ptr(values_t), _ptr(plan))
+
+
+def make_layer(f_in: int, h: int, ld_x: int, ld_y: int, ld_dx: int = 0,
+               order: int = 0, flags: int = 0) -> gnn_layer:
+    return gnn_layer(int(f_in), int(h), int(ld_x), int(ld_y),
+                     int(ld_dx or ld_x), int(order), int(flags))
+
+
+# ------------------------------------------------------------ entry points
+
+def gnn_choose_order(f_in: int, h: int) -> int:
+    return int(lib().gnn_choose_order(int(f_in), int(h)))
+
+
+def gnn_plan_bytes(n: int, nnz: int) -> int:
+    return int(lib().gnn_plan_bytes(int(n), int(nnz)))
+
+
+def gnn_csr_transpose_values(csr: gnn_csr, values_t, stream=None):
+    _check(lib().gnn_csr_transpose_values(ctypes.byref(csr), _ptr(values_t),
+                                          _stream(stream)),
+           "gnn_csr_transpose_values")
+
+
+def gnn_csr_build_plan(csr: gnn_csr, plan, stream=None):
+    nbytes = plan.numel() * plan.element_size()
+    _check(lib().gnn_csr_build_plan(ctypes.byref(csr), _ptr(plan), nbytes,
+                                    _stream(stream)), "gnn_csr_build_plan")
+
+
+def gnn_csr_validate(csr: gnn_csr, require_symmetric: bool = True,
+                     stream=None) -> int:
+    """Returns the status (GNN_OK or an error code) without raising."""
+    return int(lib().gnn_csr_validate(ctypes.byref(csr), int(require_symmetric),
+                                      _stream(stream)))
+
+
+def gnn_prop_saved_bytes(csr: gnn_csr, layer: gnn_layer) -> int:
+    return int(lib().gnn_prop_saved_bytes(ctypes.byref(csr), ctypes.byref(layer)))
+
+
+def gnn_prop_workspace_bytes(csr: gnn_csr, layer: gnn_layer) -> int:
+    return int(lib().gnn_prop_workspace_bytes(ctypes.byref(csr), ctypes.byref(layer)))
+
+
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def gnn_prop_fwd(csr: gnn_csr, layer: gnn_layer, X, W_self, W_neigh, b_self,
+                 b_neigh, Y, saved, workspace, stream=None):
+    _check(lib().gnn_prop_fwd(ctypes.byref(csr), ctypes.byref(layer), _ptr(X),
+                              _ptr(W_self), _ptr(W_neigh), _ptr(b_self),
+                              _ptr(b_neigh), _ptr(Y), _ptr(saved),
+                              _ptr(workspace), _nbytes(workspace),
+                              _stream(stream)), "gnn_prop_fwd")
+
+
+def gnn_prop_bwd(csr: gnn_csr, layer: gnn_layer, X, W_self, W_neigh, Y, dY,
+                 saved, dX, dW_self, dW_neigh, db_self, db_neigh, workspace,
+                 stream=None):
+    _check(lib().gnn_prop_bwd(ctypes.byref(csr), ctypes.byref(layer), _ptr(X),
+                              _ptr(W_self), _ptr(W_neigh), _ptr(Y), _ptr(dY),
+                              _ptr(saved), _ptr(dX), _ptr(dW_self),
+                              _ptr(dW_neigh), _ptr(db_self), _ptr(db_neigh),
+                              _ptr(workspace), _nbytes(workspace),
+                              _stream(stream)), "gnn_prop_bwd")
+
+
+def gnn_spmm_workspace_bytes(csr: gnn_csr, w: int) -> int:
+    return int(lib().gnn_spmm_workspace_bytes(ctypes.byref(csr), int(w)))
+
+
+def gnn_spmm(csr: gnn_csr, transpose: bool, w: int, inp, ld_in: int, out,
+             ld_out: int, workspace, stream=None):
+    _check(lib().gnn_spmm(ctypes.byref(csr), int(transpose), int(w), _ptr(inp),
+                          int(ld_in), _ptr(out), int(ld_out), _ptr(workspace),
+                          _nbytes(workspace), _stream(stream)), "gnn_spmm")
+
+
+def gnn_gemm_workspace_bytes(M: int, N: int, K: int) -> int:
+    return int(lib().gnn_gemm_workspace_bytes(int(M), int(N), int(K)))
+
+
+def gnn_gemm(trans_a: bool, trans_b: bool, M: int, N: int, K: int, A, lda: int,
+             B, ldb: int, C, ldc: int, flags: int = 0, workspace=None,
+             stream=None):
+    _check(lib().gnn_gemm(int(trans_a), int(trans_b), int(M), int(N), int(K),
+                          _ptr(A), int(lda), _ptr(B), int(ldb), _ptr(C), int(ldc),
+                          int(flags), _ptr(workspace), _nbytes(workspace),
+                          _stream(stream)), "gnn_gemm")
+
+
+def gnn_timer_enable(enable: bool = True):
+    _check(lib().gnn_timer_enable(int(enable)), "gnn_timer_enable")
+
+
+def gnn_timer_reset():
+    _check(lib().gnn_timer_reset(), "gnn_timer_reset")
+
+
+def gnn_timer_read(kernel) -> tuple:
+    """(milliseconds, launches, algorithmic work) of one kernel."""
+    k = KERNELS[kernel] if isinstance(kernel, str) else int(kernel)
+    ms, n, w = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double()
+    _check(lib().gnn_timer_read(k, ctypes.byref(ms), ctypes.byref(n),
+                                ctypes.byref(w)), "gnn_timer_read")
+    return ms.value, n.value, w.value

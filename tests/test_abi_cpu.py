@@ -1,0 +1,151 @@
+"""Host-side checks of the C-ABI library; no GPU needed.
+
+The library must load, export every function include/gnnprop.h declares,
+and reject bad arguments synchronously, before anything is enqueued.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2010_03166_amd import gnnprop as G
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gnnprop.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"\b(gnn_[a-z_0-9]+)\s*\(", src)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(G.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return G.lib()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for must in ("gnn_prop_fwd", "gnn_prop_bwd", "gnn_csr_transpose_values",
+                 "gnn_csr_build_plan", "gnn_csr_validate", "gnn_spmm", "gnn_gemm",
+                 "gnn_choose_order", "gnn_status_string"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    # and the binding wraps every one of them by the same name
+    assert set(names) <= set(G.EXPORTS), set(names) - set(G.EXPORTS)
+
+
+def test_binding_has_same_names(lib):
+    for n in declared_functions():
+        if n == "gnn_status_string":
+            continue
+        assert callable(getattr(G, n)), n
+
+
+def test_status_strings(lib):
+    for s in range(0, -8, -1):
+        assert G.status_string(s)
+    assert G.status_string(-99) == "unknown status"
+
+
+@pytest.mark.parametrize("f_in,h", [(50, 128), (602, 512), (300, 512), (512, 512),
+                                    (1024, 512), (200, 512), (256, 1024),
+                                    (2048, 1024), (1, 1), (7, 3)])
+def test_order_rule_agrees_with_oracle(lib, f_in, h):
+    assert G.gnn_choose_order(f_in, h) == O.choose_order(f_in, h)
+
+
+def test_plan_bytes_monotone(lib):
+    a = G.gnn_plan_bytes(1000, 10000)
+    assert a > 0 and G.gnn_plan_bytes(2000, 10000) > a
+    assert G.gnn_plan_bytes(1000, 100000) > a
+    assert G.gnn_plan_bytes(0, 0) > 0
+    assert G.gnn_plan_bytes(-1, 0) == 0
+
+
+def _fake_csr(n=10, nnz=30):
+    # host addresses stand in for device pointers: these calls must fail
+    # before dereferencing or launching anything
+    return G.make_csr(n, nnz, 0x1000, 0x2000, 0x3000, 0x4000, 0x5000)
+
+
+def test_size_queries(lib):
+    c = _fake_csr(8000, 128000)
+    l1 = G.make_layer(602, 512, 604, 1024, 604, order=1)
+    l2 = G.make_layer(602, 512, 604, 1024, 604, order=2)
+    assert G.gnn_prop_saved_bytes(c, l1) >= 8000 * 604 * 4
+    assert G.gnn_prop_saved_bytes(c, l2) == 0
+    for l in (l1, l2):
+        assert G.gnn_prop_workspace_bytes(c, l) > 8000 * 512 * 4
+    auto = G.make_layer(602, 512, 604, 1024, 604, order=0)
+    assert G.gnn_prop_saved_bytes(c, auto) == 0  # 602 > 512: order 2
+    assert G.gnn_gemm_workspace_bytes(8000, 1024, 602) == 0
+    assert G.gnn_gemm_workspace_bytes(602, 512, 8000) > 0  # split along K
+    assert G.gnn_spmm_workspace_bytes(c, 512) > 0
+
+
+def _st(fn, *args):
+    return getattr(G.lib(), fn)(*args)
+
+
+def test_argument_errors_are_synchronous(lib):
+    L = G.lib()
+    c = _fake_csr()
+    lay = G.make_layer(8, 4, 8, 8, 8)
+    P = ctypes.c_void_p
+    ws = 1 << 30
+    # NULL structs
+    assert L.gnn_prop_fwd(None, ctypes.byref(lay), *([P(0x10)] * 8), ws, None) == -1
+    assert L.gnn_prop_fwd(ctypes.byref(c), None, *([P(0x10)] * 8), ws, None) == -1
+    # bad shapes
+    bad = G.make_layer(8, 4, 7, 8, 8)  # ld_x < f_in
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(bad), *([P(0x10)] * 8), ws, None) == -2
+    bad = G.make_layer(8, 4, 8, 7, 8)  # ld_y < 2h
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(bad), *([P(0x10)] * 8), ws, None) == -2
+    bad = G.make_layer(0, 4, 8, 8, 8)
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(bad), *([P(0x10)] * 8), ws, None) == -2
+    bad = G.make_layer(8, 4, 8, 8, 8, order=3)
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(bad), *([P(0x10)] * 8), ws, None) == -2
+    bad = G.make_layer(8, 4, 8, 8, 8, flags=0x80)
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(bad), *([P(0x10)] * 8), ws, None) == -4
+    # negative sizes
+    neg = G.make_csr(-1, 0, 0x1000, 0x2000, 0x3000, 0x4000, 0x5000)
+    assert L.gnn_prop_fwd(ctypes.byref(neg), ctypes.byref(lay), *([P(0x10)] * 8), ws, None) == -2
+    # workspace too small
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(lay), *([P(0x10)] * 8), 16, None) == -5
+    # missing values_t for the backward pass
+    c2 = G.make_csr(10, 30, 0x1000, 0x2000, 0x3000, None, 0x5000)
+    assert L.gnn_prop_bwd(ctypes.byref(c2), ctypes.byref(lay), *([P(0x10)] * 12), ws, None) == -1
+    # output overlapping an input
+    xs = 0x100000
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(lay), P(xs), P(0x10), P(0x20),
+                          None, None, P(xs + 8), P(0x40), P(0x50), ws, None) == -7
+    # spmm / gemm
+    assert L.gnn_spmm(ctypes.byref(c), 0, 8, P(0x10), 4, P(0x20), 8, None, 0, None) == -2
+    assert L.gnn_gemm(0, 0, 4, 4, 4, P(0x10), 3, P(0x20), 4, P(0x30), 4, 0, None, 0, None) == -2
+    assert L.gnn_gemm(0, 0, 4, 4, 4, P(0x10), 4, P(0x20), 4, P(0x30), 4, 0x80, None, 0, None) == -4
+    assert L.gnn_gemm(0, 0, -1, 4, 4, P(0x10), 4, P(0x20), 4, P(0x30), 4, 0, None, 0, None) == -2
+    # plan buffer too small
+    assert L.gnn_csr_build_plan(ctypes.byref(c), P(0x10), 8, None) == -5
+
+
+def test_empty_problems_need_no_launch(lib):
+    L = G.lib()
+    P = ctypes.c_void_p
+    # M = 0 or N = 0: nothing to do, nothing dereferenced
+    assert L.gnn_gemm(0, 0, 0, 4, 4, None, 4, None, 4, None, 4, 0, None, 0, None) == 0
+    c = G.make_csr(0, 0, 0x1000, None, None, None, None)
+    assert L.gnn_spmm(ctypes.byref(c), 0, 8, P(0x10), 8, P(0x20), 8, None, 0, None) == 0

@@ -1,0 +1,355 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Every comparison uses the same seeded inputs on both sides.  Floating-point
+results must agree to max |gpu - oracle| / max |oracle| <= 1e-4 per tensor
+(fp32 arithmetic against the double-precision oracle); the aggregation alone
+is held to 1e-5; the transposed value array and the work plan are checked
+bit for bit.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2010_03166_amd import gnnprop as G
+from paper_2010_03166_amd import runtime, synth
+
+from gpu_helpers import (empty_out, maxrel, prepared, read_plan, sample_rows,
+                         to_dev, unaligned)
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+TOL_SPMM = 1e-5
+
+
+def graphs():
+    return {
+        "path4": synth.path_graph(4),
+        "random": synth.random_graph(300, 6.0, 1, values="random"),
+        "powerlaw": synth.power_law_graph(3000, 2.1, 12.0, seed=2),
+        "star700": synth.star_graph(700),
+        "no_self_loops": synth.random_graph(200, 1.5, 3, self_loops=False),
+        "identity": synth.identity_graph(64),
+        "single": synth.identity_graph(1),
+    }
+
+
+GRAPHS = graphs()
+
+
+# ------------------------------------------------- per-subgraph preparation
+
+@pytest.mark.parametrize("name", list(GRAPHS))
+def test_transpose_values_bit_exact(name):
+    g = GRAPHS[name]
+    dg = prepared(g)
+    torch.cuda.synchronize()
+    got = dg.values_t[: g.nnz].cpu().numpy()
+    ref = O.transpose_values(g).astype(np.float32)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+@pytest.mark.parametrize("name", ["powerlaw", "star700", "no_self_loops", "single"])
+def test_plan_covers_every_entry_once(name):
+    g = GRAPHS[name]
+    dg = prepared(g)
+    torch.cuda.synchronize()
+    hdr, raw = read_plan(dg)
+    n_items, n_splits, chunk, n_slots, n = [int(v) for v in hdr[:5]]
+    assert n == g.n
+    items = raw[64: 64 + 4 * n_items].reshape(-1, 4).astype(np.int64)
+    max_items = g.n + math.ceil(g.nnz / chunk)
+    so = ((256 + 16 * max_items + 255) // 256) * 256 // 4
+    splits = raw[so: so + 4 * n_splits].reshape(-1, 4).astype(np.int64)
+    deg = g.degrees()
+    # exact expected plan, derived from the degrees alone
+    exp_items, exp_splits, slot = [], [], 0
+    for r in range(g.n):
+        b, e = int(g.indptr[r]), int(g.indptr[r + 1])
+        if e - b > chunk:
+            k = (e - b + chunk - 1) // chunk
+            exp_splits.append((r, slot, k, 0))
+            for c in range(k):
+                exp_items.append((r, b + c * chunk, min(e, b + (c + 1) * chunk), slot + c))
+            slot += k
+        else:
+            exp_items.append((r, b, e, -1))
+    assert n_items == len(exp_items) and n_splits == len(exp_splits)
+    assert n_slots == slot
+    assert np.array_equal(items, np.array(exp_items, np.int64).reshape(-1, 4))
+    if exp_splits:
+        assert np.array_equal(splits, np.array(exp_splits, np.int64))
+    assert (deg > chunk).sum() == n_splits
+
+
+# ---------------------------------------------------------------- aggregation
+
+WIDTHS = [1, 3, 16, 50, 64, 128, 200, 300, 512, 1024, 1030]
+
+
+@pytest.mark.parametrize("name", ["powerlaw", "star700", "no_self_loops",
+                                  "identity", "random"])
+@pytest.mark.parametrize("w", WIDTHS)
+@pytest.mark.parametrize("transpose", [0, 1])
+@pytest.mark.parametrize("layout", ["aligned", "unaligned"])
+def test_spmm_parity(name, w, transpose, layout):
+    g = GRAPHS[name]
+    if g.n * w > 3_000_000:
+        w = max(1, 3_000_000 // g.n)
+    dg = prepared(g)
+    x = np.random.default_rng(w).standard_normal((g.n, w)).astype(np.float32)
+    if layout == "aligned":
+        ld = (w + 3) // 4 * 4
+        xin, out = to_dev(x, ld), empty_out(g.n, w, ld)
+    else:
+        ld = w + 1
+        xin, out = unaligned(x, ld), empty_out(g.n, w, ld, shift=True)
+    ws = torch.empty(max(G.gnn_spmm_workspace_bytes(dg.struct(), w), 256),
+                     dtype=torch.uint8, device="cuda")
+    G.gnn_spmm(dg.struct(), transpose, w, xin, xin.stride(0), out, out.stride(0), ws)
+    torch.cuda.synchronize()
+    ref = O.spmm_transpose(g, x) if transpose else O.spmm(g, x)
+    assert maxrel(out, ref) <= TOL_SPMM
+
+
+def test_spmm_empty_graph_and_empty_rows():
+    g = synth.symmetric_csr(6, np.array([[0, 1]]), self_loops=False)
+    dg = prepared(g)
+    x = np.arange(24, dtype=np.float32).reshape(6, 4)
+    out = empty_out(6, 4)
+    G.gnn_spmm(dg.struct(), 0, 4, to_dev(x), 4, out, 4, None)
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert np.array_equal(o[2:], np.zeros((4, 4), np.float32))
+    assert np.array_equal(o[0], x[1]) and np.array_equal(o[1], x[0])
+
+
+# ------------------------------------------------------------------- GEMM
+
+GEMM_SHAPES = [(1, 1, 1), (37, 45, 29), (128, 128, 32), (130, 257, 70),
+               (1000, 128, 50), (602, 512, 8000), (300, 96, 4099), (64, 64, 0)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("ta", [0, 1])
+@pytest.mark.parametrize("tb", [0, 1])
+@pytest.mark.parametrize("layout", ["aligned", "unaligned"])
+def test_gemm_parity(M, N, K, ta, tb, layout):
+    rng = np.random.default_rng(M * 7 + N * 3 + K)
+    a = rng.standard_normal((K, M) if ta else (M, K)).astype(np.float32)
+    b = rng.standard_normal((N, K) if tb else (K, N)).astype(np.float32)
+    if layout == "aligned":
+        A = to_dev(a, (a.shape[1] + 3) // 4 * 4)
+        B = to_dev(b, (b.shape[1] + 3) // 4 * 4)
+        C = empty_out(M, N, (N + 3) // 4 * 4)
+    else:
+        A = unaligned(a, a.shape[1] + 1)
+        B = unaligned(b, b.shape[1] + 3)
+        C = empty_out(M, N, N + 1, shift=True)
+    ws = torch.empty(max(G.gnn_gemm_workspace_bytes(M, N, K), 256),
+                     dtype=torch.uint8, device="cuda")
+    G.gnn_gemm(ta, tb, M, N, K, A, A.stride(0), B, B.stride(0), C, C.stride(0),
+               0, ws)
+    torch.cuda.synchronize()
+    aa = a.T if ta else a
+    bb = b.T if tb else b
+    ref = O.mm_nn(aa, bb) if K > 0 else np.zeros((M, N))
+    assert maxrel(C, ref) <= TOL
+
+
+# --------------------------------------------------------------- one layer
+
+def layer_inputs(n, f_in, h, seed, bias):
+    rng = np.random.default_rng(seed)
+    g = synth.power_law_graph(n, 2.1, 8.0, seed=seed) if n > 1 else synth.identity_graph(n)
+    x = rng.standard_normal((n, f_in)).astype(np.float32)
+    p = synth.LayerParams(synth.glorot(f_in, h, rng), synth.glorot(f_in, h, rng))
+    if bias:
+        p.b_self = rng.standard_normal(h).astype(np.float32) * 0.1
+        p.b_neigh = rng.standard_normal(h).astype(np.float32) * 0.1
+    dy = rng.standard_normal((n, 2 * h)).astype(np.float32)
+    return g, x, p, dy
+
+
+def run_layer(g, x, p, y_for_bwd, dy, order, pad=16, want_dx=True):
+    f_in, h = p.w_self.shape
+    dg = prepared(g)
+    st = runtime.SageStack(dg, [p], f_in, order=order, pad=pad)
+    xd = to_dev(x, (f_in + pad - 1) // pad * pad)
+    st.forward(xd)
+    torch.cuda.synchronize()
+    y = st.layers[0]["Y"].cpu().numpy().copy()
+    # the backward pass gets the oracle's forward output as Y (teacher forcing)
+    st.layers[0]["Y"].copy_(torch.from_numpy(y_for_bwd.astype(np.float32)).cuda())
+    st.backward(to_dev(dy), want_dx_first=want_dx)
+    torch.cuda.synchronize()
+    L = st.layers[0]
+    out = {"Y": y, "dW_self": L["dW_self"].cpu().numpy(),
+           "dW_neigh": L["dW_neigh"].cpu().numpy(),
+           "dX": L["dX"].cpu().numpy() if want_dx else None}
+    if p.b_self is not None:
+        out["db_self"] = L["db_self"].cpu().numpy()
+        out["db_neigh"] = L["db_neigh"].cpu().numpy()
+    return out
+
+
+LAYER_CASES = [(1, 7, 5), (37, 7, 5), (500, 50, 128), (400, 130, 64),
+               (300, 64, 64), (257, 33, 100)]
+
+
+@pytest.mark.parametrize("n,f_in,h", LAYER_CASES)
+@pytest.mark.parametrize("order", [1, 2])
+@pytest.mark.parametrize("bias", [False, True])
+def test_layer_parity(n, f_in, h, order, bias):
+    g, x, p, dy = layer_inputs(n, f_in, h, n + f_in + h, bias)
+    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh, p.b_self, p.b_neigh)
+    y32 = y_ref.astype(np.float32)
+    got = run_layer(g, x, p, y32, dy, order)
+    assert maxrel(got["Y"], y_ref) <= TOL
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy, want_db=bias)
+    for k in ("dX", "dW_self", "dW_neigh") + (("db_self", "db_neigh") if bias else ()):
+        assert maxrel(got[k], r[k]) <= TOL, k
+
+
+@pytest.mark.parametrize("order", [1, 2])
+def test_layer_without_input_gradient(order):
+    g, x, p, dy = layer_inputs(200, 40, 24, 5, False)
+    y32 = O.sage_fwd(g, x, p.w_self, p.w_neigh).astype(np.float32)
+    got = run_layer(g, x, p, y32, dy, order, want_dx=False)
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy, want_dx=False)
+    assert maxrel(got["dW_self"], r["dW_self"]) <= TOL
+    assert maxrel(got["dW_neigh"], r["dW_neigh"]) <= TOL
+
+
+@pytest.mark.parametrize("order", [1, 2])
+def test_layer_unpadded_rows(order):
+    # row strides equal to the widths (602 floats is not a multiple of 4)
+    g, x, p, dy = layer_inputs(300, 602, 40, 11, False)
+    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh)
+    y32 = y_ref.astype(np.float32)
+    got = run_layer(g, x, p, y32, dy, order, pad=1)
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy)
+    assert maxrel(got["Y"], y_ref) <= TOL
+    for k in ("dX", "dW_self", "dW_neigh"):
+        assert maxrel(got[k], r[k]) <= TOL, k
+
+
+def test_layer_zero_nodes():
+    g = synth.identity_graph(0)
+    p = synth.LayerParams(np.ones((4, 3), np.float32), np.ones((4, 3), np.float32))
+    dg = prepared(g)
+    st = runtime.SageStack(dg, [p], 4)
+    st.forward(torch.empty((0, 4), device="cuda"))
+    st.backward(torch.empty((0, 6), device="cuda"))
+    torch.cuda.synchronize()
+    assert float(st.layers[0]["dW_self"].abs().max()) == 0.0
+    assert float(st.layers[0]["dW_neigh"].abs().max()) == 0.0
+
+
+# ------------------------------------------------------ whole stacks, C ABI
+
+def test_tiny_workload_stack_end_to_end():
+    wl = synth.WORKLOADS[synth.TINY_WORKLOAD]
+    inp = synth.workload_inputs(wl)
+    g, x, params, dy = inp["graph"], inp["x"], inp["params"], inp["dy"]
+    ref = O.sage_stack(g, x, params, dy)
+    dg = prepared(g)
+    st = runtime.SageStack(dg, params, wl.f_in)
+    y = st.forward(to_dev(x, 64))
+    st.backward(to_dev(dy))
+    torch.cuda.synchronize()
+    assert maxrel(y, ref["ys"][-1]) <= TOL
+    for l in range(wl.layers):
+        L, R = st.layers[l], ref["grads"][l]
+        assert maxrel(L["Y"], ref["ys"][l]) <= TOL
+        for k in ("dX", "dW_self", "dW_neigh"):
+            assert maxrel(L[k], R[k]) <= TOL, (l, k)
+
+
+def test_bitwise_reproducible():
+    wl = synth.WORKLOADS[synth.TINY_WORKLOAD]
+    inp = synth.workload_inputs(wl)
+    outs = []
+    for _ in range(2):
+        dg = prepared(inp["graph"])
+        st = runtime.SageStack(dg, inp["params"], wl.f_in)
+        st.forward(to_dev(inp["x"], 64))
+        st.backward(to_dev(inp["dy"]))
+        torch.cuda.synchronize()
+        outs.append([t.cpu().numpy().copy() for L in st.layers
+                     for t in (L["Y"], L["dX"], L["dW_self"], L["dW_neigh"])])
+    for a, b in zip(*outs):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+# ---------------------------------------- full-size workloads, spot checked
+
+@pytest.mark.parametrize("name", list(synth.WORKLOADS))
+def test_workload_layers_full_size(name):
+    """Every layer shape of every workload at its real size, in the launch
+    configuration the benchmark uses; outputs checked on sampled rows and
+    weight-gradient entries against the oracle's per-output evaluation."""
+    wl = synth.WORKLOADS[name]
+    g = synth.workload_graph(wl)
+    dg = prepared(g)
+    deg = g.degrees()
+    hub = int(np.argmax(deg))
+    for l, (f_in, h) in enumerate(synth.layer_dims(wl)):
+        rng = np.random.default_rng(1000 + l)
+        x = rng.standard_normal((g.n, f_in)).astype(np.float32)
+        if l > 0:  # post-ReLU activations
+            x = np.maximum(x, 0)
+        p = synth.LayerParams(synth.glorot(f_in, h, rng), synth.glorot(f_in, h, rng))
+        ysyn = rng.standard_normal((g.n, 2 * h)).astype(np.float32)
+        dy = rng.standard_normal((g.n, 2 * h)).astype(np.float32)
+        st = runtime.SageStack(dg, [p], f_in)
+        st.forward(to_dev(x, (f_in + 15) // 16 * 16))
+        torch.cuda.synchronize()
+        rows = sample_rows(g.n, 24, l, must=(0, g.n - 1, hub))
+        y = st.layers[0]["Y"][torch.from_numpy(rows).cuda()].cpu().numpy()
+        yr = O.sage_fwd_rows(g, x, p.w_self, p.w_neigh, rows)
+        assert maxrel(y, yr) <= TOL, ("Y", l)
+        st.layers[0]["Y"].copy_(torch.from_numpy(ysyn).cuda())
+        st.backward(to_dev(dy))
+        torch.cuda.synchronize()
+        dx = st.layers[0]["dX"][torch.from_numpy(rows).cuda()].cpu().numpy()
+        dxr = O.sage_bwd_dx_rows(g, p.w_self, p.w_neigh, ysyn, dy, rows)
+        assert maxrel(dx, dxr) <= TOL, ("dX", l)
+        ei = np.concatenate([[0, f_in - 1], rng.integers(0, f_in, 14)])
+        ej = np.concatenate([[0, h - 1], rng.integers(0, h, 14)])
+        ws, wn = O.sage_bwd_dw_entries(g, x, ysyn, dy, h, ei, ej)
+        gs = st.layers[0]["dW_self"].cpu().numpy()[ei, ej]
+        gn = st.layers[0]["dW_neigh"].cpu().numpy()[ei, ej]
+        assert maxrel(gs, ws) <= TOL, ("dW_self", l)
+        assert maxrel(gn, wn) <= TOL, ("dW_neigh", l)
+        del st
+        torch.cuda.empty_cache()
+
+
+# -------------------------------------------------------------- validation
+
+def test_validate_accepts_and_rejects():
+    good = prepared(synth.power_law_graph(500, 2.1, 6.0, seed=4))
+    assert good.validate(True) == G.GNN_OK
+    # asymmetric pattern
+    g = synth.csr_from_pairs(3, np.array([0, 0, 1, 2]), np.array([0, 1, 1, 2]))
+    assert runtime.DeviceGraph(g).validate(True) == -3
+    assert runtime.DeviceGraph(g).validate(False) == G.GNN_OK
+    # unsorted row
+    g = synth.path_graph(5)
+    g.indices = g.indices.copy()
+    g.indices[[0, 1]] = g.indices[[1, 0]]
+    assert runtime.DeviceGraph(g).validate(False) == -3
+    # index out of range
+    g = synth.path_graph(5)
+    g.indices = g.indices.copy()
+    g.indices[-1] = 5
+    assert runtime.DeviceGraph(g).validate(False) == -3
+    # indptr not ending at nnz
+    g = synth.path_graph(5)
+    g.indptr = g.indptr.copy()
+    g.indptr[-1] -= 1
+    assert runtime.DeviceGraph(g).validate(False) == -3
