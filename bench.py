@@ -1,0 +1,205 @@
+#!/usr/bin/env python
+"""Benchmark of GraphSAGE feature propagation (forward + backward) on MI355X.
+
+One step is one pass of the whole hot path over one sampled subgraph:
+per-subgraph preparation (transposed values of Algorithm 6, aggregation
+plan), then for every layer the forward pass (aggregation, matrix-core
+transforms, concat + ReLU) and, from the top layer down, the backward pass
+(ReLU mask, transposed aggregation, weight and input gradients).  The top
+layer's gradient is a fixed synthetic N(0,1) matrix standing in for the
+classifier and loss.  All inputs are resident in HBM before timing starts.
+
+Prints one JSON line: `value` is milliseconds per subgraph layer
+(forward + backward, step time / layers), with the dominant kernel's
+roofline and the CPU oracle timed on this host as a reference.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "ms per subgraph layer fwd+bwd; SpMM HBM GB/s and GEMM MFMA util vs peak"
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--skip-input-grad", action="store_true",
+                    help="do not compute the first layer's input gradient")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the path runs one subgraph per GPU and "
+              "this build has no multi-GPU leg (requested --gpus %d, WORLD_SIZE %d)"
+              % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2010_03166_amd import gnnprop as G
+    from paper_2010_03166_amd import runtime, synth
+
+    G.lib()  # fail loudly if the HIP library is not built
+    name = args.workload or synth.BENCH_WORKLOAD
+    wl = synth.WORKLOADS[name]
+    torch.cuda.set_device(0)
+    log("workload", name)
+    inp = synth.workload_inputs(wl)
+    g, x, params, dy = inp["graph"], inp["x"], inp["params"], inp["dy"]
+    stats = g.stats()
+    log("graph", stats)
+
+    pad = 16
+    dg = runtime.DeviceGraph(g)
+    st = runtime.SageStack(dg, params, wl.f_in, pad=pad)
+    ld_x = (wl.f_in + pad - 1) // pad * pad
+    X = runtime.padded(torch.from_numpy(x).cuda(), ld_x)
+    dY = torch.from_numpy(dy).cuda()
+    want_dx_first = not args.skip_input_grad
+
+    def step():
+        dg.prepare()
+        st.forward(X)
+        st.backward(dY, want_dx_first=want_dx_first)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: wall clock and stream events around exactly K steps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    ms_step_events = e0.elapsed_time(e1) / args.steps
+    log("step %.4f ms (wall), %.4f ms (events)" % (ms_step, ms_step_events))
+
+    # the same K steps again with every kernel bracketed by HIP events on the
+    # stream it runs on
+    G.gnn_timer_reset()
+    G.gnn_timer_enable(True)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step_timed = (time.perf_counter() - t2) * 1e3 / args.steps
+    G.gnn_timer_enable(False)
+    kernels = {}
+    for kname in G.KERNELS:
+        ms, launches, work = G.gnn_timer_read(kname)
+        if launches:
+            kernels[kname] = {"ms_per_step": ms / args.steps,
+                              "launches_per_step": launches / args.steps,
+                              "avg_launch_us": 1e3 * ms / launches, "work": work / launches}
+    G.gnn_timer_reset()
+
+    dtype = "f32"
+    gemm_names = [k for k in kernels if k.startswith("gemm_") and k != "gemm_reduce"]
+    for k in gemm_names:
+        kernels[k]["tflops"] = kernels[k]["work"] / (kernels[k]["avg_launch_us"] * 1e6)
+    if "spmm" in kernels:
+        kernels["spmm"]["gbs"] = kernels["spmm"]["work"] / (kernels["spmm"]["avg_launch_us"] * 1e3)
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    if dom in gemm_names:
+        ach = kernels[dom]["tflops"]
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2),
+                "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
+                "frac": round(ach / PEAK_TFLOPS[dtype], 4), "traffic": None,
+                "flops_per_launch": kernels[dom]["work"],
+                "avg_launch_us": round(kernels[dom]["avg_launch_us"], 2)}
+    else:
+        ach = kernels[dom].get("gbs", 0.0)
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                "bytes_per_launch": kernels[dom]["work"],
+                "avg_launch_us": round(kernels[dom]["avg_launch_us"], 2)}
+    roof_spmm = None
+    if "spmm" in kernels:
+        a = kernels["spmm"]["gbs"]
+        roof_spmm = {"kernel": "spmm", "bound": "hbm", "achieved": round(a, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(a / PEAK_HBM_GBS, 4),
+                     "bytes_per_launch": kernels["spmm"]["work"],
+                     "avg_launch_us": round(kernels["spmm"]["avg_launch_us"], 2)}
+
+    out = {
+        "metric": METRIC,
+        "value": round(ms_step / wl.layers, 5),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": name, "n": wl.n, "nnz": stats["nnz"],
+                   "max_deg": stats["max_deg"], "f_in": wl.f_in,
+                   "hidden_per_half": wl.hidden, "layers": wl.layers,
+                   "graph": "%s mean %g gamma %g kmax %s" % (wl.graph, wl.mean_deg,
+                                                             wl.gamma, wl.kmax),
+                   "input_grad_first_layer": want_dx_first},
+        "roofline": roof,
+        "roofline_spmm": roof_spmm,
+        "ms_per_step_events": round(ms_step_events, 5),
+        "ms_per_step_with_kernel_timer": round(ms_step_timed, 5),
+        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv)
+                        for kk, vv in v.items()} for k, v in kernels.items()},
+    }
+
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        import numpy as np  # noqa: F811
+        reps, t_cpu = 0, 0.0
+        while reps == 0 or (t_cpu < args.cpu_seconds and reps < 8):
+            t = time.perf_counter()
+            O.transpose_values(g)
+            O.sage_stack(g, x, params, dy, want_dx_first=want_dx_first)
+            t_cpu += time.perf_counter() - t
+            reps += 1
+        out["cpu_baseline"] = {
+            "value": round(t_cpu * 1e3 / reps / wl.layers, 3), "unit": "ms",
+            "cores": O.num_threads(), "kind": "oracle",
+            "sample": "%d full step(s) of the same workload (Algorithm 6 + %d "
+                      "layers forward + backward), double precision, plain loops"
+                      % (reps, wl.layers)}
+        log("cpu oracle %.1f ms/layer on %d threads" % (
+            out["cpu_baseline"]["value"], out["cpu_baseline"]["cores"]))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
