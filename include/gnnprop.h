@@ -111,7 +111,10 @@ int32_t gnn_choose_order(int32_t f_in, int32_t h);
  * each stored (v,u), writes values[pos(v,u)] to values_t[pos(u,v)]; a pure
  * permutation, bit-exact.  Requires csr->indptr/indices/values; the pattern
  * must be symmetric with ascending indices per row (check with
- * gnn_csr_validate).  values_t is device memory of nnz floats. */
+ * gnn_csr_validate).  values_t is device memory of nnz floats.  If
+ * csr->plan is non-NULL it must hold this graph's plan (gnn_csr_build_plan,
+ * enqueued before), whose work items then spread long rows over many
+ * wavefronts; with plan == NULL one wavefront handles each row. */
 gnn_status gnn_csr_transpose_values(const gnn_csr* csr, float* values_t,
                                     hipStream_t stream);
 

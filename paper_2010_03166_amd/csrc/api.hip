@@ -301,8 +301,8 @@ gnn_status gnn_csr_transpose_values(const gnn_csr* csr, float* values_t,
   if (csr->nnz > 0 && !values_t) return GNN_ERR_NULL;
   if (ranges_overlap(values_t, csr->nnz * 4, csr->values, csr->nnz * 4))
     return GNN_ERR_ALIAS;
-  GNN_HIP(transpose_values_launch(csr->n, csr->indptr, csr->indices,
-                                  csr->values, values_t, stream));
+  GNN_HIP(transpose_values_launch(csr->n, csr->nnz, csr->indptr, csr->indices,
+                                  csr->values, values_t, csr->plan, stream));
   return GNN_OK;
 }
 

@@ -2,17 +2,39 @@
 // three kernels of Section 5.1).
 //
 // C = sum_s op(A_s) op(B_s) (+ bias, ReLU), fp32 in and out, on
-// v_mfma_f32_32x32x2_f32.  A block of 256 threads (4 wavefronts in 2 x 2)
-// owns a 128 x 128 output tile; each wavefront holds a 64 x 64 sub-tile as
-// 2 x 2 MFMA accumulators (64 accumulator registers per lane).  K advances
-// in 32-deep slices staged through double-buffered LDS: while the matrix
-// cores consume slice k, the global loads of slice k+1 are in flight, and
-// one barrier per slice separates the two buffers.  Both operands live in
-// LDS as [k][m] / [k][n] rows, so every MFMA operand read is 32 consecutive
-// floats per half-wavefront; operands stored the other way round are
-// transposed on their way into LDS.  Shapes with few output tiles (the
-// weight gradients, K = n) are split along K; the partial tiles are summed
-// in split order by a second kernel, so results are deterministic.
+// v_mfma_f32_32x32x2_f32.
+//
+// Tiling.  A block of 256 threads (4 wavefronts in 2 x 2) computes a
+// 128 x 128 output tile; each wavefront holds a 64 x 64 sub-tile as 2 x 2
+// MFMA accumulators (64 accumulator registers per lane).  K advances in
+// 32-deep slices staged through double-buffered LDS with one barrier per
+// slice; the global loads of slice k+1 are in flight while the matrix cores
+// consume slice k.
+//
+// LDS layouts follow the operand's storage so that every global float4 lands
+// in LDS as one float4 (no transposition on the way in):
+//   K-contiguous operand (A row-major M x K, or B stored N x K): [x][k]
+//     rows of 32 + 4 floats; each lane fetches its MFMA fragments for 16
+//     consecutive k with four 128-bit reads;
+//   X-contiguous operand (A stored K x M, or B row-major K x N): [k][x]
+//     rows of 128 + 32 floats; one 32-bit read per MFMA.
+// The MFMA contracts over k in any order, so within a slice the lane half
+// h = lane / 32 takes k = 16 h + s at step s (s = 0..15), which is what
+// lets a K-contiguous fragment be read as consecutive floats.  X-contiguous
+// rows are stored in the order (k mod 16) * 2 + k / 16 so that the two lane
+// halves of a step read adjacent rows (different LDS banks).
+//
+// Work split (stream-K).  The launch's tiles x K-slices are cut into P
+// equal, contiguous ranges, one per block (P = 512 blocks = 2 per CU, or one
+// block per tile when the tiles already fill the machine).  A block writes a
+// tile it covers completely straight to C with the fused epilogue; a tile
+// shared by several blocks gets one partial tile per block, and a second
+// kernel adds them in block order (deterministic) before the epilogue.  This
+// keeps every CU busy for shapes whose tile count does not fill the chip
+// (weight gradients with K = n, f_in = 602 input gradients) without atomics.
+// Blocks are numbered so that each XCD (blocks are dispatched round-robin
+// over the 8 XCDs) works on a contiguous range of iterations: the tiles of a
+// row band (same A rows) or the same K range stay in one XCD's L2.
 #include "internal.hpp"
 
 namespace gnnprop {
@@ -20,20 +42,35 @@ namespace gnnprop {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128, BN = 128, BK = 32;
-constexpr int LDS_STRIDE = 160;  // floats per LDS row: 128 + 32 padding
+constexpr int KC_STRIDE = BK + 4;   // floats per [x][k] row
+constexpr int XC_STRIDE = 128 + 32; // floats per [k][x] row
+constexpr int KC_FLOATS = 128 * KC_STRIDE;
+constexpr int XC_FLOATS = BK * XC_STRIDE;
+constexpr int NUM_XCD = 8;
+constexpr int MAX_BLOCKS = 512;     // 2 resident blocks on each of 256 CUs
 
 struct GemmKArgs {
   GemmProblem p[2];
   int32_t nprob;
-  int32_t tiles_m[2];
-  int32_t tile_start[2];
-  int32_t ktiles0[2];  // K slices of segment 0
-  int32_t ktiles[2];   // K slices over all segments
-  int32_t total_tiles;
-  int32_t splits;
-  float* part[2];
+  int32_t M;           // shared by the problems of a launch
+  int32_t tiles_m;
+  int32_t tiles_n0;    // column tiles of problem 0
+  int32_t tiles_n;     // column tiles of both problems
+  int32_t tiles;       // tiles_m * tiles_n
+  int32_t ktiles;      // K slices per tile (same for every problem)
+  int32_t ktiles0[2];  // K slices of segment 0, per problem
+  int64_t iters;       // tiles * ktiles
+  int32_t nblocks;     // P
+  float* part;         // 2 partial tiles per block, BM * BN floats each
   int32_t vec_a, vec_b;
 };
+
+__device__ inline float4 ld4(const float* p) {
+  return *reinterpret_cast<const float4*>(p);
+}
+__device__ inline float comp(const float4& v, int u) {
+  return u == 0 ? v.x : u == 1 ? v.y : u == 2 ? v.z : v.w;
+}
 
 // Element (r, c..c+3) of a row-major R x C matrix with row stride ld; zeros
 // outside the matrix.
@@ -43,7 +80,7 @@ __device__ inline float4 load4(const float* base, int64_t ld, int r, int c,
   if (r < R && c < C) {
     const float* p = base + (int64_t)r * ld + c;
     if (vec && c + 3 < C) {
-      v = *reinterpret_cast<const float4*>(p);
+      v = ld4(p);
     } else {
       v.x = p[0];
       if (c + 1 < C) v.y = p[1];
@@ -54,213 +91,293 @@ __device__ inline float4 load4(const float* base, int64_t ld, int r, int c,
   return v;
 }
 
+__device__ inline int64_t block_lo(int b, int64_t iters, int nblocks) {
+  return (int64_t)b * iters / nblocks;
+}
+// The block whose range contains iteration x.
+__device__ inline int block_of(int64_t x, int64_t iters, int nblocks) {
+  return (int)(((x + 1) * nblocks - 1) / iters);
+}
+
+// Logical block of physical block b: XCD x (= b mod 8) gets a contiguous
+// range of logical blocks.
+__device__ inline int logical_block(int b, int nblocks) {
+  const int x = b % NUM_XCD, c = b / NUM_XCD;
+  const int base = nblocks / NUM_XCD, rem = nblocks % NUM_XCD;
+  return x * base + min(x, rem) + c;
+}
+
+struct TileInfo {
+  int pi, m0, n0;
+};
+
+__device__ inline TileInfo tile_info(const GemmKArgs& g, int t) {
+  TileInfo ti;
+  const int tm = t / g.tiles_n, j = t % g.tiles_n;
+  ti.pi = (g.nprob > 1 && j >= g.tiles_n0) ? 1 : 0;
+  ti.m0 = tm * BM;
+  ti.n0 = (ti.pi ? j - g.tiles_n0 : j) * BN;
+  return ti;
+}
+
 template <bool AT, bool BT>
 __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
-  __shared__ float As[2][BK][LDS_STRIDE];
-  __shared__ float Bs[2][BK][LDS_STRIDE];
+  constexpr bool A_KC = !AT;  // A row-major M x K: k contiguous
+  constexpr bool B_KC = BT;   // B stored N x K: k contiguous
+  constexpr int A_FLOATS = A_KC ? KC_FLOATS : XC_FLOATS;
+  constexpr int B_FLOATS = B_KC ? KC_FLOATS : XC_FLOATS;
+  __shared__ __attribute__((aligned(16))) float As[2][A_FLOATS];
+  __shared__ __attribute__((aligned(16))) float Bs[2][B_FLOATS];
 
   const int tid = threadIdx.x;
-  const int split = blockIdx.x / g.total_tiles;
-  int t = blockIdx.x % g.total_tiles;
-  const int pi = (g.nprob > 1 && t >= g.tile_start[1]) ? 1 : 0;
-  t -= pi ? g.tile_start[1] : 0;
-
-  // Problem fields, selected without dynamic indexing.
-  const GemmProblem& P0 = g.p[0];
-  const GemmProblem& P1 = g.p[1];
-  const int M = pi ? P1.M : P0.M;
-  const int N = pi ? P1.N : P0.N;
-  const int tiles_m = pi ? g.tiles_m[1] : g.tiles_m[0];
-  const int kt0 = pi ? g.ktiles0[1] : g.ktiles0[0];
-  const int ktiles = pi ? g.ktiles[1] : g.ktiles[0];
-  const float* A0 = pi ? P1.seg[0].A : P0.seg[0].A;
-  const float* A1 = pi ? P1.seg[1].A : P0.seg[1].A;
-  const float* B0 = pi ? P1.seg[0].B : P0.seg[0].B;
-  const float* B1 = pi ? P1.seg[1].B : P0.seg[1].B;
-  const int64_t lda0 = pi ? P1.seg[0].lda : P0.seg[0].lda;
-  const int64_t lda1 = pi ? P1.seg[1].lda : P0.seg[1].lda;
-  const int64_t ldb0 = pi ? P1.seg[0].ldb : P0.seg[0].ldb;
-  const int64_t ldb1 = pi ? P1.seg[1].ldb : P0.seg[1].ldb;
-  const int K0 = pi ? P1.seg[0].K : P0.seg[0].K;
-  const int K1 = pi ? P1.seg[1].K : P0.seg[1].K;
-
-  const int m0 = (t % tiles_m) * BM;
-  const int n0 = (t / tiles_m) * BN;
-  const int kt_per = (ktiles + g.splits - 1) / g.splits;
-  const int kt_begin = min(ktiles, split * kt_per);
-  const int kt_end = min(ktiles, kt_begin + kt_per);
-  const bool va = g.vec_a != 0, vb = g.vec_b != 0;
-
-  float4 ra[4], rb[4];
-  auto load_slice = [&](int gt) {
-    const bool s1 = gt >= kt0;
-    const int k0 = (s1 ? gt - kt0 : gt) * BK;
-    const float* A = s1 ? A1 : A0;
-    const float* B = s1 ? B1 : B0;
-    const int64_t lda = s1 ? lda1 : lda0;
-    const int64_t ldb = s1 ? ldb1 : ldb0;
-    const int K = s1 ? K1 : K0;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      if (!AT) {  // A is M x K row-major: 8 float4 per tile row
-        const int row = (tid >> 3) + 32 * p, kq = tid & 7;
-        ra[p] = load4(A, lda, m0 + row, k0 + 4 * kq, M, K, va);
-      } else {    // A stored K x M
-        const int kk = (tid >> 5) + 8 * p, mq = tid & 31;
-        ra[p] = load4(A, lda, k0 + kk, m0 + 4 * mq, K, M, va);
-      }
-      if (!BT) {  // B is K x N row-major
-        const int kk = (tid >> 5) + 8 * p, nq = tid & 31;
-        rb[p] = load4(B, ldb, k0 + kk, n0 + 4 * nq, K, N, vb);
-      } else {    // B stored N x K
-        const int col = (tid >> 3) + 32 * p, kq = tid & 7;
-        rb[p] = load4(B, ldb, n0 + col, k0 + 4 * kq, N, K, vb);
-      }
-    }
-  };
-  auto store_slice = [&](int buf) {
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      if (!AT) {
-        const int row = (tid >> 3) + 32 * p, kq = tid & 7;
-        As[buf][4 * kq + 0][row] = ra[p].x;
-        As[buf][4 * kq + 1][row] = ra[p].y;
-        As[buf][4 * kq + 2][row] = ra[p].z;
-        As[buf][4 * kq + 3][row] = ra[p].w;
-      } else {
-        const int kk = (tid >> 5) + 8 * p, mq = tid & 31;
-        *reinterpret_cast<float4*>(&As[buf][kk][4 * mq]) = ra[p];
-      }
-      if (!BT) {
-        const int kk = (tid >> 5) + 8 * p, nq = tid & 31;
-        *reinterpret_cast<float4*>(&Bs[buf][kk][4 * nq]) = rb[p];
-      } else {
-        const int col = (tid >> 3) + 32 * p, kq = tid & 7;
-        Bs[buf][4 * kq + 0][col] = rb[p].x;
-        Bs[buf][4 * kq + 1][col] = rb[p].y;
-        Bs[buf][4 * kq + 2][col] = rb[p].z;
-        Bs[buf][4 * kq + 3][col] = rb[p].w;
-      }
-    }
-  };
-
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave & 1, wn = wave >> 1;
-  const int lr = lane & 31, lk = lane >> 5;
+  const int lr = lane & 31, lh = lane >> 5;
+  const bool va = g.vec_a != 0, vb = g.vec_b != 0;
+  const int M = g.M;
 
-  floatx16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  const int lb = logical_block(blockIdx.x, g.nblocks);
+  const int64_t lo = block_lo(lb, g.iters, g.nblocks);
+  const int64_t hi = block_lo(lb + 1, g.iters, g.nblocks);
 
-  if (kt_begin < kt_end) load_slice(kt_begin);
   int buf = 0;
-  for (int gt = kt_begin; gt < kt_end; ++gt) {
-    store_slice(buf);
-    __syncthreads();
-    if (gt + 1 < kt_end) load_slice(gt + 1);
-#pragma unroll
-    for (int s = 0; s < BK / 2; ++s) {
-      const int kr = 2 * s + lk;
-      const float a0 = As[buf][kr][wm * 64 + lr];
-      const float a1 = As[buf][kr][wm * 64 + 32 + lr];
-      const float b0 = Bs[buf][kr][wn * 64 + lr];
-      const float b1 = Bs[buf][kr][wn * 64 + 32 + lr];
-      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
-    }
-    buf ^= 1;
-  }
+  int seg = 0;
+  for (int64_t it = lo; it < hi; ++seg) {
+    const int t = (int)(it / g.ktiles);
+    const int kbeg = (int)(it - (int64_t)t * g.ktiles);
+    const int kend = (int)min<int64_t>(g.ktiles, hi - (int64_t)t * g.ktiles);
+    it = (int64_t)t * g.ktiles + kend;
+    const TileInfo ti = tile_info(g, t);
+    const GemmProblem& P = ti.pi ? g.p[1] : g.p[0];
+    const int N = P.N;
+    const int kt0 = ti.pi ? g.ktiles0[1] : g.ktiles0[0];
 
-  // Accumulator layout of v_mfma_f32_32x32x2_f32: lane l, register r holds
-  // row 8*(r/4) + 4*(l/32) + r%4 and column l%32 of the 32 x 32 block.
-  float* C = pi ? P1.C : P0.C;
-  const int64_t ldc = pi ? P1.ldc : P0.ldc;
-  const float* bias = pi ? P1.bias : P0.bias;
-  const int relu = pi ? P1.relu : P0.relu;
-  float* part = pi ? g.part[1] : g.part[0];
+    float4 ra[4], rb[4];
+    auto load_slice = [&](int ks) {
+      const bool s1 = ks >= kt0;
+      const GemmSeg& S = s1 ? P.seg[1] : P.seg[0];
+      const int k0 = (s1 ? ks - kt0 : ks) * BK;
+      const int K = S.K;
+      const bool full_k = k0 + BK <= K;
+      // A: K-contiguous -> thread owns (row x, 4 k); else (row k, 4 m)
+      const int ax = A_KC ? (tid >> 3) : (tid >> 5);
+      const int ay = A_KC ? 4 * (tid & 7) : 4 * (tid & 31);
+      const int astep = A_KC ? 32 : 8;
+      if (va && full_k && ti.m0 + BM <= M) {
+        const float* base = A_KC ? S.A + (int64_t)(ti.m0 + ax) * S.lda + k0 + ay
+                                 : S.A + (int64_t)(k0 + ax) * S.lda + ti.m0 + ay;
+        const int64_t stride = (int64_t)astep * S.lda;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+        for (int p = 0; p < 4; ++p) ra[p] = ld4(base + p * stride);
+      } else {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn * 64 + j * 32 + lr;
-      if (col >= N) continue;
-      const float bc = (g.splits == 1 && bias) ? bias[col] : 0.f;
+        for (int p = 0; p < 4; ++p)
+          ra[p] = A_KC ? load4(S.A, S.lda, ti.m0 + ax + astep * p, k0 + ay, M, K, va)
+                       : load4(S.A, S.lda, k0 + ax + astep * p, ti.m0 + ay, K, M, va);
+      }
+      const int bx = B_KC ? (tid >> 3) : (tid >> 5);
+      const int by = B_KC ? 4 * (tid & 7) : 4 * (tid & 31);
+      const int bstep = B_KC ? 32 : 8;
+      if (vb && full_k && ti.n0 + BN <= N) {
+        const float* base = B_KC ? S.B + (int64_t)(ti.n0 + bx) * S.ldb + k0 + by
+                                 : S.B + (int64_t)(k0 + bx) * S.ldb + ti.n0 + by;
+        const int64_t stride = (int64_t)bstep * S.ldb;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + i * 32 + (r >> 2) * 8 + lk * 4 + (r & 3);
-        if (row < M) {
+        for (int p = 0; p < 4; ++p) rb[p] = ld4(base + p * stride);
+      } else {
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+          rb[p] = B_KC ? load4(S.B, S.ldb, ti.n0 + bx + bstep * p, k0 + by, N, K, vb)
+                       : load4(S.B, S.ldb, k0 + bx + bstep * p, ti.n0 + by, K, N, vb);
+      }
+    };
+    auto store_slice = [&](int bb) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        if (A_KC) {
+          const int x = (tid >> 3) + 32 * p, kq = tid & 7;
+          *reinterpret_cast<float4*>(&As[bb][x * KC_STRIDE + 4 * kq]) = ra[p];
+        } else {
+          const int kk = (tid >> 5) + 8 * p, xq = tid & 31;
+          const int row = ((kk & 15) << 1) | (kk >> 4);
+          *reinterpret_cast<float4*>(&As[bb][row * XC_STRIDE + 4 * xq]) = ra[p];
+        }
+        if (B_KC) {
+          const int x = (tid >> 3) + 32 * p, kq = tid & 7;
+          *reinterpret_cast<float4*>(&Bs[bb][x * KC_STRIDE + 4 * kq]) = rb[p];
+        } else {
+          const int kk = (tid >> 5) + 8 * p, xq = tid & 31;
+          const int row = ((kk & 15) << 1) | (kk >> 4);
+          *reinterpret_cast<float4*>(&Bs[bb][row * XC_STRIDE + 4 * xq]) = rb[p];
+        }
+      }
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    load_slice(kbeg);
+    for (int ks = kbeg; ks < kend; ++ks) {
+      store_slice(buf);
+      __syncthreads();
+      if (ks + 1 < kend) load_slice(ks + 1);
+      const float* as = As[buf];
+      const float* bs = Bs[buf];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float4 af[2], bf[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          if (A_KC)
+            af[i] = ld4(as + (wm * 64 + i * 32 + lr) * KC_STRIDE + lh * 16 + 4 * q);
+          if (B_KC)
+            bf[i] = ld4(bs + (wn * 64 + i * 32 + lr) * KC_STRIDE + lh * 16 + 4 * q);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int s = 4 * q + u;
+          const int row = 2 * s + lh;  // stored row of k = 16 lh + s
+          float a[2], b[2];
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            a[i] = A_KC ? comp(af[i], u) : as[row * XC_STRIDE + wm * 64 + i * 32 + lr];
+            b[i] = B_KC ? comp(bf[i], u) : bs[row * XC_STRIDE + wn * 64 + i * 32 + lr];
+          }
+          acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], acc[0][0], 0, 0, 0);
+          acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[1], acc[0][1], 0, 0, 0);
+          acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[0], acc[1][0], 0, 0, 0);
+          acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[1], acc[1][1], 0, 0, 0);
+        }
+      }
+      buf ^= 1;
+    }
+
+    // Accumulator layout of v_mfma_f32_32x32x2_f32: lane l, register r holds
+    // row 8*(r/4) + 4*(l/32) + r%4 and column l%32 of the 32 x 32 block.
+    const bool whole = kbeg == 0 && kend == g.ktiles;
+    float* part = g.part + ((int64_t)lb * 2 + (seg > 0 ? 1 : 0)) * (BM * BN);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int cl = wn * 64 + j * 32 + lr;
+        const int col = ti.n0 + cl;
+        const float bc = (whole && P.bias && col < N) ? P.bias[col] : 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rl = wm * 64 + i * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+          const int row = ti.m0 + rl;
           float v = acc[i][j][r];
-          if (g.splits > 1) {
-            part[((int64_t)split * M + row) * N + col] = v;
+          if (whole) {
+            if (row < M && col < N) {
+              v += bc;
+              if (P.relu) v = fmaxf(v, 0.f);
+              P.C[(int64_t)row * P.ldc + col] = v;
+            }
           } else {
-            v += bc;
-            if (relu) v = fmaxf(v, 0.f);
-            C[(int64_t)row * ldc + col] = v;
+            part[rl * BN + cl] = v;
           }
         }
       }
-    }
+  }
 }
 
-// Sum of the split-K partial tiles in split order, then bias and ReLU.
-__global__ __launch_bounds__(256) void gemm_splitk_reduce_kernel(GemmKArgs g) {
-  const int pi = blockIdx.y;
-  const GemmProblem& P0 = g.p[0];
-  const GemmProblem& P1 = g.p[1];
-  const int M = pi ? P1.M : P0.M;
-  const int N = pi ? P1.N : P0.N;
-  float* C = pi ? P1.C : P0.C;
-  const int64_t ldc = pi ? P1.ldc : P0.ldc;
-  const float* bias = pi ? P1.bias : P0.bias;
-  const int relu = pi ? P1.relu : P0.relu;
-  const float* part = pi ? g.part[1] : g.part[0];
-  const int64_t total = (int64_t)M * N;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * blockDim.x) {
-    float v = 0.f;
-    for (int s = 0; s < g.splits; ++s) v += part[(int64_t)s * total + e];
-    const int row = (int)(e / N), col = (int)(e % N);
-    if (bias) v += bias[col];
-    if (relu) v = fmaxf(v, 0.f);
-    C[(int64_t)row * ldc + col] = v;
+// Tiles shared by several blocks: add the blocks' partial tiles in block
+// order, then bias and ReLU.  Block (t, c) handles 1024 elements of tile t,
+// four consecutive columns per thread.
+constexpr int FIX_CHUNKS = BM * BN / 1024;
+
+__global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
+  const int t = blockIdx.x;
+  const int64_t first = (int64_t)t * g.ktiles, last = first + g.ktiles - 1;
+  const int b0 = block_of(first, g.iters, g.nblocks);
+  const int b1 = block_of(last, g.iters, g.nblocks);
+  if (b0 == b1) return;  // written directly by its only block
+  const TileInfo ti = tile_info(g, t);
+  const GemmProblem& P = ti.pi ? g.p[1] : g.p[0];
+  const int e = blockIdx.y * 1024 + threadIdx.x * 4;
+  const int rl = e / BN, cl = e % BN;
+  const int row = ti.m0 + rl, col = ti.n0 + cl;
+  if (row >= g.M || col >= P.N) return;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int b = b0; b <= b1; ++b) {
+    // the tile is block b's first tile iff b's range starts inside it
+    const int slot = block_lo(b, g.iters, g.nblocks) >= first ? 0 : 1;
+    const float4 p = ld4(g.part + ((int64_t)b * 2 + slot) * (BM * BN) + e);
+    v.x += p.x;
+    v.y += p.y;
+    v.z += p.z;
+    v.w += p.w;
+  }
+  float o[4] = {v.x, v.y, v.z, v.w};
+  float* dst = P.C + (int64_t)row * P.ldc + col;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (col + u >= P.N) break;
+    float x = o[u];
+    if (P.bias) x += P.bias[col + u];
+    if (P.relu) x = fmaxf(x, 0.f);
+    dst[u] = x;
   }
 }
 
 // ------------------------------------------------------------------ host
 
-static int problem_ktiles(const GemmProblem& p, int* kt0) {
-  int k0 = (int)ceil_div(p.seg[0].K, BK);
-  int k1 = p.nseg > 1 ? (int)ceil_div(p.seg[1].K, BK) : 0;
-  if (kt0) *kt0 = k0;
-  return k0 + k1;
-}
+struct Shape {
+  int tiles_m, tiles_n0, tiles_n, tiles, ktiles, kt0[2];
+  int64_t iters;
+  int nblocks;
+};
 
-static int choose_splits(const GemmBatch& b) {
-  int tiles = 0, kt = 0;
+static Shape gemm_shape(const GemmBatch& b) {
+  Shape s;
+  memset(&s, 0, sizeof(s));
+  const int M = b.p[0].M;
+  s.tiles_m = (int)ceil_div(M, BM);
+  s.tiles_n0 = (int)ceil_div(b.p[0].N, BN);
+  s.tiles_n = s.tiles_n0 + (b.nprob > 1 ? (int)ceil_div(b.p[1].N, BN) : 0);
+  s.tiles = s.tiles_m * s.tiles_n;
   for (int i = 0; i < b.nprob; ++i) {
     const GemmProblem& p = b.p[i];
-    tiles += (int)(ceil_div(p.M, BM) * ceil_div(p.N, BN));
-    kt = std::max(kt, problem_ktiles(p, nullptr));
+    s.kt0[i] = (int)ceil_div(p.seg[0].K, BK);
+    const int kt = s.kt0[i] + (p.nseg > 1 ? (int)ceil_div(p.seg[1].K, BK) : 0);
+    s.ktiles = std::max(s.ktiles, kt);
   }
-  if (tiles >= 256 || tiles == 0) return 1;
-  int s = (int)ceil_div(512, tiles);
-  s = std::min(s, std::max(1, kt / 4));
-  return std::max(1, std::min(s, 32));
+  s.ktiles = std::max(s.ktiles, 1);
+  s.iters = (int64_t)s.tiles * s.ktiles;
+  // One block per tile when the tiles fill the resident slots well enough,
+  // else an even split of all tile x K-slice iterations over MAX_BLOCKS.
+  const int64_t rounds = ceil_div(s.tiles, MAX_BLOCKS);
+  const double fill = (double)s.tiles / (double)(rounds * MAX_BLOCKS);
+  if (fill >= 0.85 || s.iters <= MAX_BLOCKS)
+    s.nblocks = s.tiles;
+  else
+    s.nblocks = MAX_BLOCKS;
+  return s;
+}
+
+static bool batch_ok(const GemmBatch& b) {
+  if (b.nprob < 1 || b.nprob > 2) return false;
+  if (b.nprob == 2) {
+    if (b.p[0].M != b.p[1].M) return false;
+    const auto kt = [](const GemmProblem& p) {
+      return ceil_div(p.seg[0].K, BK) + (p.nseg > 1 ? ceil_div(p.seg[1].K, BK) : 0);
+    };
+    if (kt(b.p[0]) != kt(b.p[1])) return false;
+  }
+  return true;
 }
 
 size_t gemm_workspace_bytes(const GemmBatch& b) {
-  const int s = choose_splits(b);
-  if (s <= 1) return 0;
-  size_t bytes = 0;
-  for (int i = 0; i < b.nprob; ++i)
-    bytes += round_up((size_t)s * b.p[i].M * b.p[i].N * 4, 256);
-  return bytes;
+  if (!batch_ok(b)) return 0;
+  const Shape s = gemm_shape(b);
+  if (s.tiles == 0 || s.nblocks == s.tiles) return 0;
+  return round_up((size_t)s.nblocks * 2 * BM * BN * 4, 256);
 }
 
 double gemm_flops(const GemmBatch& b) {
@@ -274,40 +391,43 @@ double gemm_flops(const GemmBatch& b) {
 
 hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
                        hipStream_t s) {
+  if (!batch_ok(b)) return hipErrorInvalidValue;
+  const Shape sh = gemm_shape(b);
+  if (sh.tiles == 0) return hipSuccess;
   GemmKArgs g;
   memset(&g, 0, sizeof(g));
   g.nprob = b.nprob;
-  g.splits = choose_splits(b);
-  int tiles = 0;
+  g.M = b.p[0].M;
+  g.tiles_m = sh.tiles_m;
+  g.tiles_n0 = sh.tiles_n0;
+  g.tiles_n = sh.tiles_n;
+  g.tiles = sh.tiles;
+  g.ktiles = sh.ktiles;
+  g.iters = sh.iters;
+  g.nblocks = sh.nblocks;
   bool va = true, vb = true;
-  char* ws = static_cast<char*>(workspace);
   for (int i = 0; i < b.nprob; ++i) {
     g.p[i] = b.p[i];
     if (g.p[i].nseg < 2) {
       g.p[i].seg[1] = g.p[i].seg[0];
       g.p[i].seg[1].K = 0;
     }
+    g.ktiles0[i] = sh.kt0[i];
     const GemmProblem& p = g.p[i];
-    g.tiles_m[i] = (int)ceil_div(p.M, BM);
-    g.tile_start[i] = tiles;
-    tiles += g.tiles_m[i] * (int)ceil_div(p.N, BN);
-    g.ktiles[i] = problem_ktiles(p, &g.ktiles0[i]);
     for (int k = 0; k < p.nseg; ++k) {
       va = va && vec4_ok(p.seg[k].A, p.seg[k].lda);
       vb = vb && vec4_ok(p.seg[k].B, p.seg[k].ldb);
     }
-    if (g.splits > 1) {
-      g.part[i] = reinterpret_cast<float*>(ws);
-      ws += round_up((size_t)g.splits * p.M * p.N * 4, 256);
-    }
   }
-  if (g.splits > 1 && (size_t)(ws - static_cast<char*>(workspace)) > ws_bytes)
-    return hipErrorInvalidValue;
-  g.total_tiles = tiles;
   g.vec_a = va;
   g.vec_b = vb;
-  if (tiles == 0) return hipSuccess;
-  const unsigned grid = (unsigned)tiles * (unsigned)g.splits;
+  const bool streamk = sh.nblocks != sh.tiles;
+  if (streamk) {
+    if (ws_bytes < gemm_workspace_bytes(b) || !workspace)
+      return hipErrorInvalidValue;
+    g.part = static_cast<float*>(workspace);
+  }
+  const unsigned grid = (unsigned)sh.nblocks;
   const int kid = b.trans_a ? (b.trans_b ? GNN_K_GEMM_TT : GNN_K_GEMM_TN)
                             : (b.trans_b ? GNN_K_GEMM_NT : GNN_K_GEMM_NN);
   timer_begin(kid, s);
@@ -321,14 +441,9 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
     gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g);
   timer_end(kid, gemm_flops(b), s);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || g.splits <= 1) return e;
-  int64_t maxmn = 0;
-  for (int i = 0; i < b.nprob; ++i)
-    maxmn = std::max<int64_t>(maxmn, (int64_t)b.p[i].M * b.p[i].N);
-  const unsigned rgrid = (unsigned)std::min<int64_t>(ceil_div(maxmn, 256), 4096);
-  dim3 grid2(rgrid > 0 ? rgrid : 1, b.nprob);
+  if (e != hipSuccess || !streamk) return e;
   timer_begin(GNN_K_GEMM_REDUCE, s);
-  gemm_splitk_reduce_kernel<<<grid2, 256, 0, s>>>(g);
+  gemm_fixup_kernel<<<dim3((unsigned)sh.tiles, FIX_CHUNKS), 256, 0, s>>>(g);
   timer_end(GNN_K_GEMM_REDUCE, 0.0, s);
   return hipGetLastError();
 }

@@ -89,9 +89,13 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s);
 
 hipError_t plan_build_launch(int32_t n, int64_t nnz, const int32_t* indptr,
                              void* plan, hipStream_t s);
-hipError_t transpose_values_launch(int32_t n, const int32_t* indptr,
+// Uses the plan's work items when `plan` is non-null (built for this graph),
+// else one wavefront per row.
+hipError_t transpose_values_launch(int32_t n, int64_t nnz,
+                                   const int32_t* indptr,
                                    const int32_t* indices, const float* vals,
-                                   float* vals_t, hipStream_t s);
+                                   float* vals_t, const void* plan,
+                                   hipStream_t s);
 // Returns 0 if valid, else a nonzero code; synchronises.
 hipError_t validate_csr(int32_t n, int64_t nnz, const int32_t* indptr,
                         const int32_t* indices, int32_t symmetric,

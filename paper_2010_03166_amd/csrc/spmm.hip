@@ -22,7 +22,7 @@ namespace gnnprop {
 static int32_t plan_chunk(int32_t n, int64_t nnz) {
   (void)n;
   (void)nnz;
-  return 128;
+  return 64;
 }
 
 PlanDims plan_dims(int32_t n, int64_t nnz) {
@@ -160,6 +160,23 @@ hipError_t plan_build_launch(int32_t n, int64_t nnz, const int32_t* indptr,
 // Stored entry (v,u) of A_s is entry (u,v) of the transpose, which lives in
 // row u at the position of column v.  Rows are sorted, so that position is
 // found by binary search; every entry is moved exactly once.
+__device__ inline void transpose_entry(int v, int j, const int32_t* indptr,
+                                       const int32_t* indices,
+                                       const float* vals, float* vals_t) {
+  const int u = indices[j];
+  int lo = indptr[u], hi = indptr[u + 1];
+  const int end = hi;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (indices[mid] < v)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  if (lo < end && indices[lo] == v) vals_t[lo] = vals[j];
+}
+
+// One wavefront per row.
 __global__ __launch_bounds__(256) void transpose_values_kernel(
     int32_t n, const int32_t* __restrict__ indptr,
     const int32_t* __restrict__ indices, const float* __restrict__ vals,
@@ -168,28 +185,42 @@ __global__ __launch_bounds__(256) void transpose_values_kernel(
   if (v >= n) return;
   const int lane = threadIdx.x & 63;
   const int b = indptr[v], e = indptr[v + 1];
-  for (int j = b + lane; j < e; j += 64) {
-    const int u = indices[j];
-    int lo = indptr[u], hi = indptr[u + 1];
-    const int end = hi;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (indices[mid] < v)
-        lo = mid + 1;
-      else
-        hi = mid;
-    }
-    if (lo < end && indices[lo] == v) vals_t[lo] = vals[j];
-  }
+  for (int j = b + lane; j < e; j += 64)
+    transpose_entry(v, j, indptr, indices, vals, vals_t);
 }
 
-hipError_t transpose_values_launch(int32_t n, const int32_t* indptr,
+// One wavefront per work item of the aggregation plan (at most `chunk`
+// entries), so a hub row is spread over many wavefronts.
+__global__ __launch_bounds__(256) void transpose_values_items_kernel(
+    const PlanHeader* __restrict__ hdr, const int4* __restrict__ items,
+    const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
+    const float* __restrict__ vals, float* __restrict__ vals_t) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= hdr->n_items) return;
+  const int4 it = items[i];
+  const int lane = threadIdx.x & 63;
+  for (int j = it.y + lane; j < it.z; j += 64)
+    transpose_entry(it.x, j, indptr, indices, vals, vals_t);
+}
+
+hipError_t transpose_values_launch(int32_t n, int64_t nnz,
+                                   const int32_t* indptr,
                                    const int32_t* indices, const float* vals,
-                                   float* vals_t, hipStream_t s) {
+                                   float* vals_t, const void* plan,
+                                   hipStream_t s) {
   if (n <= 0) return hipSuccess;
   timer_begin(GNN_K_TRANSPOSE, s);
-  transpose_values_kernel<<<(unsigned)ceil_div(n, 4), 256, 0, s>>>(
-      n, indptr, indices, vals, vals_t);
+  if (plan) {
+    const PlanDims d = plan_dims(n, nnz);
+    const char* base = static_cast<const char*>(plan);
+    transpose_values_items_kernel<<<(unsigned)ceil_div(d.max_items, 4), 256, 0, s>>>(
+        reinterpret_cast<const PlanHeader*>(base),
+        reinterpret_cast<const int4*>(base + d.items_offset), indptr, indices,
+        vals, vals_t);
+  } else {
+    transpose_values_kernel<<<(unsigned)ceil_div(n, 4), 256, 0, s>>>(
+        n, indptr, indices, vals, vals_t);
+  }
   timer_end(GNN_K_TRANSPOSE, 0.0, s);
   return hipGetLastError();
 }
@@ -266,6 +297,8 @@ struct SpmmArgs {
   int64_t ld_res;
   float* part;
   int64_t ldp;
+  int32_t nslices;  // column slices (blocks b with b % nslices == q own slice q)
+  int32_t sw;       // slice width in columns
 };
 
 template <bool VEC>
@@ -337,60 +370,71 @@ __device__ inline void spmm_epilogue(const SpmmArgs& a, int row, int col,
 }
 
 // One work item per group of G lanes; NC column vectors per lane per pass.
+// Block b covers column slice b % nslices of the items of item block
+// b / nslices.  With 8 slices, the blocks of one slice all run on one XCD
+// (blocks are dispatched round-robin over the 8 XCDs), so each XCD gathers
+// from its own n x sw slice of the input, which stays in that XCD's L2.
+//
+// The item's entries are taken in batches of G: each lane loads one index
+// and value (a coalesced read), then the batch is walked with lane
+// shuffles, eight neighbour rows in flight at a time, accumulating in entry
+// order.  A 64-entry item thus costs a handful of memory round trips
+// instead of one per entry.
+constexpr int GATHER_DEPTH = 8;
+
 template <int G, int NC, bool VEC>
 __global__ __launch_bounds__(256) void spmm_items_kernel(SpmmArgs a) {
   using V = Vec<VEC>;
   using T = typename V::T;
   constexpr int IPB = 256 / G;
   constexpr int COLS = G * V::W * NC;
-  int item = blockIdx.x * IPB + threadIdx.x / G;
+  const int slice = blockIdx.x % a.nslices;
+  int item = (blockIdx.x / a.nslices) * IPB + threadIdx.x / G;
   if (G == 64) item = __builtin_amdgcn_readfirstlane(item);
   if (item >= a.hdr->n_items) return;
   const int4 it = a.items[item];
   const int row = it.x, b = it.y, e = it.z, slot = it.w;
   const int lane = threadIdx.x % G;
-  const int w = a.w;
+  const int c_lo = slice * a.sw;
+  const int c_hi = min(a.w, c_lo + a.sw);
   const float* __restrict__ in = a.in;
-  for (int c0 = 0; c0 < w; c0 += COLS) {
+  for (int c0 = c_lo; c0 < c_hi; c0 += COLS) {
     T acc[NC];
 #pragma unroll
     for (int q = 0; q < NC; ++q) acc[q] = V::zero();
-    int j = b;
-    for (; j + 4 <= e; j += 4) {
-      int idx[4];
-      float val[4];
+    for (int jb = b; jb < e; jb += G) {
+      const int cnt = min(G, e - jb);
+      const int my_idx = lane < cnt ? a.indices[jb + lane] : 0;
+      const float my_val = lane < cnt ? a.vals[jb + lane] : 0.f;
+      for (int k = 0; k < cnt; k += GATHER_DEPTH) {
+        int idx[GATHER_DEPTH];
+        float val[GATHER_DEPTH];
+        T x[GATHER_DEPTH][NC];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        idx[u] = a.indices[j + u];
-        val[u] = a.vals[j + u];
-      }
-      T x[4][NC];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int q = 0; q < NC; ++q) {
-          const int col = c0 + (q * G + lane) * V::W;
-          x[u][q] = col < w ? V::load(in + (int64_t)idx[u] * a.ld_in + col)
-                            : V::zero();
+        for (int u = 0; u < GATHER_DEPTH; ++u) {
+          idx[u] = __shfl(my_idx, k + u, G);
+          val[u] = __shfl(my_val, k + u, G);
         }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < GATHER_DEPTH; ++u)
 #pragma unroll
-        for (int q = 0; q < NC; ++q) V::fma(acc[q], val[u], x[u][q]);
-    }
-    for (; j < e; ++j) {
-      const int idx = a.indices[j];
-      const float val = a.vals[j];
+          for (int q = 0; q < NC; ++q) {
+            const int col = c0 + (q * G + lane) * V::W;
+            x[u][q] = (k + u < cnt && col < c_hi)
+                          ? V::load(in + (int64_t)idx[u] * a.ld_in + col)
+                          : V::zero();
+          }
 #pragma unroll
-      for (int q = 0; q < NC; ++q) {
-        const int col = c0 + (q * G + lane) * V::W;
-        if (col < w) V::fma(acc[q], val, V::load(in + (int64_t)idx * a.ld_in + col));
+        for (int u = 0; u < GATHER_DEPTH; ++u)
+#pragma unroll
+          for (int q = 0; q < NC; ++q)
+            if (k + u < cnt) V::fma(acc[q], val[u], x[u][q]);
       }
     }
 #pragma unroll
     for (int q = 0; q < NC; ++q) {
       const int col = c0 + (q * G + lane) * V::W;
-      if (col < w) {
+      if (col < c_hi) {
         if (slot >= 0)
           V::store(a.part + (int64_t)slot * a.ldp + col, acc[q]);
         else
@@ -407,17 +451,20 @@ __global__ __launch_bounds__(256) void spmm_reduce_kernel(SpmmArgs a) {
   using T = typename V::T;
   constexpr int IPB = 256 / G;
   constexpr int COLS = G * V::W * NC;
-  int s = blockIdx.x * IPB + threadIdx.x / G;
+  const int slice = blockIdx.x % a.nslices;
+  int s = (blockIdx.x / a.nslices) * IPB + threadIdx.x / G;
   if (G == 64) s = __builtin_amdgcn_readfirstlane(s);
   if (s >= a.hdr->n_splits) return;
   const int4 sp = a.splits[s];
   const int row = sp.x, first = sp.y, cnt = sp.z;
   const int lane = threadIdx.x % G;
-  for (int c0 = 0; c0 < a.w; c0 += COLS) {
+  const int c_lo = slice * a.sw;
+  const int c_hi = min(a.w, c_lo + a.sw);
+  for (int c0 = c_lo; c0 < c_hi; c0 += COLS) {
 #pragma unroll
     for (int q = 0; q < NC; ++q) {
       const int col = c0 + (q * G + lane) * V::W;
-      if (col < a.w) {
+      if (col < c_hi) {
         T acc = V::zero();
         for (int k = 0; k < cnt; ++k)
           V::add(acc, V::load(a.part + (int64_t)(first + k) * a.ldp + col));
@@ -446,13 +493,13 @@ static hipError_t spmm_run(const SpmmArgs& a, const PlanDims& d, int32_t n,
   if (d.max_items > 0) {
     timer_begin(GNN_K_SPMM, s);
     spmm_items_kernel<G, NC, VEC>
-        <<<(unsigned)ceil_div(d.max_items, IPB), 256, 0, s>>>(a);
+        <<<(unsigned)(ceil_div(d.max_items, IPB) * a.nslices), 256, 0, s>>>(a);
     timer_end(GNN_K_SPMM, spmm_bytes(n, nnz, a.w), s);
   }
   if (d.max_splits > 0) {
     timer_begin(GNN_K_SPMM_REDUCE, s);
     spmm_reduce_kernel<G, NC, VEC>
-        <<<(unsigned)ceil_div(d.max_splits, IPB), 256, 0, s>>>(a);
+        <<<(unsigned)(ceil_div(d.max_splits, IPB) * a.nslices), 256, 0, s>>>(a);
     timer_end(GNN_K_SPMM_REDUCE, 0.0, s);
   }
   return hipGetLastError();
@@ -461,7 +508,7 @@ static hipError_t spmm_run(const SpmmArgs& a, const PlanDims& d, int32_t n,
 template <bool VEC>
 static hipError_t spmm_dispatch(const SpmmArgs& a, const PlanDims& d,
                                 int32_t n, int64_t nnz, hipStream_t s) {
-  const int units = VEC ? a.w / 4 : a.w;  // column vectors per row
+  const int units = VEC ? a.sw / 4 : a.sw;  // column vectors per slice row
   if (units <= 4) return spmm_run<4, 1, VEC>(a, d, n, nnz, s);
   if (units <= 8) return spmm_run<8, 1, VEC>(a, d, n, nnz, s);
   if (units <= 16) return spmm_run<16, 1, VEC>(a, d, n, nnz, s);
@@ -493,6 +540,11 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   a.ld_res = c.ld_res;
   a.part = c.partials;
   a.ldp = round_up(c.w, 4);
+  // Wide rows are cut into 8 column slices, one per XCD (the GPU form of
+  // the feature-column partition of Section 5.3, Theorem 2 / Algorithm 7,
+  // with each XCD's L2 as the cache that a slice must fit).
+  a.nslices = c.w >= 256 ? 8 : 1;
+  a.sw = (int32_t)round_up(ceil_div(c.w, a.nslices), 4);
   const bool vec = (c.w % 4 == 0) && vec4_ok(c.in, c.ld_in) &&
                    vec4_ok(c.out, c.ld_out) &&
                    (c.epilogue != SPMM_BIAS_RELU || !c.bias || aligned16(c.bias)) &&

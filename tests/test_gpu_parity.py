@@ -52,6 +52,20 @@ def test_transpose_values_bit_exact(name):
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
 
 
+@pytest.mark.parametrize("name", ["powerlaw", "star700", "random"])
+def test_transpose_values_without_plan(name):
+    # with plan == NULL the transpose runs one wavefront per row
+    g = GRAPHS[name]
+    dg = runtime.DeviceGraph(g)
+    c = dg.struct()
+    c.plan = None
+    G.gnn_csr_transpose_values(c, dg.values_t)
+    torch.cuda.synchronize()
+    got = dg.values_t[: g.nnz].cpu().numpy()
+    ref = O.transpose_values(g).astype(np.float32)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
 @pytest.mark.parametrize("name", ["powerlaw", "star700", "no_self_loops", "single"])
 def test_plan_covers_every_entry_once(name):
     g = GRAPHS[name]
