@@ -40,10 +40,15 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bf16", action="store_true",
+                    help="skip the bf16 matrix-core variant")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--skip-input-grad", action="store_true",
                     help="do not compute the first layer's input gradient")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="first run one plain device-to-device copy of MIB MiB "
+                         "(reference point for hardware byte counters)")
     return ap.parse_args()
 
 
@@ -71,6 +76,16 @@ def main():
     g, x, params, dy = inp["graph"], inp["x"], inp["params"], inp["dy"]
     stats = g.stats()
     log("graph", stats)
+
+    if args.calibrate_copy:
+        nbytes = args.calibrate_copy << 20
+        src = torch.ones(nbytes // 4, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration copy: %d bytes read, %d bytes written" % (nbytes, nbytes))
+        del src, dst
 
     pad = 16
     dg = runtime.DeviceGraph(g)
@@ -181,6 +196,52 @@ def main():
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv)
                         for kk, vv in v.items()} for k, v in kernels.items()},
     }
+
+    # the bf16 matrix-core variant of the same step (GEMM operands rounded to
+    # bf16, fp32 accumulation; aggregation stays fp32), reported alongside
+    if not args.no_bf16:
+        stb = runtime.SageStack(dg, params, wl.f_in, pad=pad, flags=G.GNN_FLAG_BF16)
+
+        def step_bf16():
+            dg.prepare()
+            stb.forward(X)
+            stb.backward(dY, want_dx_first=want_dx_first)
+
+        for _ in range(args.warmup):
+            step_bf16()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step_bf16()
+        torch.cuda.synchronize()
+        ms_b = (time.perf_counter() - t0) * 1e3 / args.steps
+        G.gnn_timer_reset()
+        G.gnn_timer_enable(True)
+        for _ in range(args.steps):
+            step_bf16()
+        torch.cuda.synchronize()
+        G.gnn_timer_enable(False)
+        kb = {}
+        for kname in G.KERNELS:
+            ms, launches, work = G.gnn_timer_read(kname)
+            if launches:
+                kb[kname] = {"ms_per_step": round(ms / args.steps, 4),
+                             "avg_launch_us": round(1e3 * ms / launches, 2)}
+                if kname.startswith("gemm_") and kname != "gemm_reduce":
+                    kb[kname]["tflops"] = round(work / launches / (1e6 * kb[kname]["avg_launch_us"]), 1)
+        G.gnn_timer_reset()
+        gb = [k for k in kb if "tflops" in k or ("tflops" in kb[k])]
+        domb = max(gb, key=lambda k: kb[k]["ms_per_step"])
+        out["bf16_variant"] = {
+            "value": round(ms_b / wl.layers, 5), "unit": "ms", "ms_per_step": round(ms_b, 5),
+            "dtype": "bf16 GEMM operands, f32 accumulation and aggregation",
+            "roofline": {"kernel": domb, "bound": "mfma",
+                         "achieved": kb[domb]["tflops"], "peak": PEAK_TFLOPS["bf16"],
+                         "unit": "TFLOP/s",
+                         "frac": round(kb[domb]["tflops"] / PEAK_TFLOPS["bf16"], 4)},
+            "kernels": kb}
+        log("bf16 variant: %.4f ms per step" % ms_b)
+        del stb
 
     if not args.no_cpu_baseline:
         from oracle import oracle as O

@@ -20,6 +20,24 @@ int32_t oracle_num_threads(void) {
 #endif
 }
 
+/* bfloat16 keeps the sign, the 8 exponent bits and the top 7 fraction bits
+ * of a float.  Rounding to nearest, ties to even, adds 0x7fff plus the
+ * lowest kept bit to the 32-bit pattern and truncates the low 16 bits. */
+void oracle_round_bf16(int64_t count, const double* in, double* out) {
+  for (int64_t i = 0; i < count; ++i) {
+    float f = (float)in[i];
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    if (f != f) {
+      out[i] = in[i];
+      continue;
+    }
+    u = (u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u;
+    memcpy(&f, &u, sizeof f);
+    out[i] = (double)f;
+  }
+}
+
 /* ------------------------------------------------------------------ SpMM */
 
 /* Feature aggregation A_s . X (Section 2.1; Section 5.3 for the operation

@@ -111,6 +111,11 @@ void oracle_sage_bwd_dw_entries(int32_t n, const int32_t* indptr,
                                 const int32_t* ej, double* dWs_ent,
                                 double* dWn_ent);
 
+/* bfloat16 rounding of GEMM operands for the reduced-precision mode: each
+ * value is first taken as float (the storage format), then rounded to the
+ * nearest bfloat16 (8 significant bits), ties to even; NaN stays NaN. */
+void oracle_round_bf16(int64_t count, const double* in, double* out);
+
 /* Number of OpenMP threads the oracle runs with. */
 int32_t oracle_num_threads(void);
 

@@ -69,6 +69,7 @@ def lib():
                 "oracle_sage_bwd_dw_entries": [i32, _I32P, _I32P, _F64P, i32,
                                                i32, _F64P, _F64P, _F64P, i32,
                                                _I32P, _I32P, _F64P, _F64P],
+                "oracle_round_bf16": [i64, _F64P, _F64P],
                 "oracle_num_threads": [],
             }
             for name, args in sigs.items():
@@ -97,6 +98,15 @@ def _p(a: Optional[np.ndarray], t):
 
 def _csr(g) -> Tuple[int, np.ndarray, np.ndarray, np.ndarray]:
     return g.n, _i32(g.indptr), _i32(g.indices), _f64(g.values)
+
+
+def round_bf16(a) -> np.ndarray:
+    """float -> nearest bfloat16 (ties to even), returned as double."""
+    a = np.asarray(a)
+    x = _f64(a).reshape(-1)
+    out = np.empty_like(x)
+    lib().oracle_round_bf16(x.size, _p(x, _F64P), _p(out, _F64P))
+    return out.reshape(a.shape)
 
 
 def num_threads() -> int:

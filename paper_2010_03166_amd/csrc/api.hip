@@ -172,6 +172,11 @@ GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
   return b;
 }
 
+GemmBatch with_bf16(GemmBatch b, int32_t bf16) {
+  b.bf16 = bf16;
+  return b;
+}
+
 LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   LayerLayout o;
   const int32_t n = csr->n, f_in = L->f_in, h = L->h;
@@ -191,9 +196,10 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   }
   const int32_t w = o.order == 1 ? f_in : h;
   size_t gemm = 0;
-  gemm = std::max(gemm, gemm_workspace_bytes(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0)));
-  gemm = std::max(gemm, gemm_workspace_bytes(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 2 * h, 0, 0)));
-  gemm = std::max(gemm, gemm_workspace_bytes(dx_batch(o.order, n, f_in, h, 0, 0, 2 * h, 0, 0, 0, f_in, 0, f_in)));
+  const int32_t bf = (L->flags & GNN_FLAG_BF16) ? 1 : 0;
+  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
+  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
+  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dx_batch(o.order, n, f_in, h, 0, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
   o.off_buf0 = 0;
   o.off_buf1 = round_up(buf0, 256);
   o.off_spart = o.off_buf1 + round_up(buf1, 256);
@@ -219,7 +225,6 @@ gnn_status check_layer(const gnn_layer* L) {
   if (L->ld_x < L->f_in || L->ld_y < 2 * (int64_t)L->h) return GNN_ERR_SHAPE;
   if (L->order < 0 || L->order > 2) return GNN_ERR_SHAPE;
   if (L->flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
-  if (L->flags & GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
   return GNN_OK;
 }
 
@@ -372,7 +377,9 @@ size_t gnn_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
   b.p[0].M = M;
   b.p[0].N = N;
   b.p[0].seg[0].K = K;
-  return gemm_workspace_bytes(b);
+  const size_t f32 = gemm_workspace_bytes(b);
+  b.bf16 = 1;
+  return std::max(f32, gemm_workspace_bytes(b));
 }
 
 gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
@@ -382,7 +389,6 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
                     hipStream_t stream) {
   if (M < 0 || N < 0 || K < 0) return GNN_ERR_SHAPE;
   if (flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
-  if (flags & GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return GNN_OK;
   if (!C || (K > 0 && (!A || !B))) return GNN_ERR_NULL;
   if (ldc < N) return GNN_ERR_SHAPE;
@@ -395,6 +401,7 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
   b.nprob = 1;
   b.trans_a = trans_a != 0;
   b.trans_b = trans_b != 0;
+  b.bf16 = (flags & GNN_FLAG_BF16) != 0;
   b.p[0].nseg = 1;
   b.p[0].seg[0] = {A, B, lda, ldb, K};
   b.p[0].M = M;
@@ -460,11 +467,13 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
     GNN_HIP(spmm_launch(c, stream));
     GemmBatch b = fwd_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, W_self,
                             W_neigh, b_self, b_neigh, Y, layer->ld_y, nullptr, 0);
+    b.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
   } else {
     float* P = reinterpret_cast<float*>(ws + o.off_buf0);
     GemmBatch b = fwd_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, W_self,
                             W_neigh, b_self, nullptr, Y, layer->ld_y, P, o.ld_p);
+    b.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
     SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y, spart);
     c.epilogue = SPMM_BIAS_RELU;
@@ -522,10 +531,12 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     GNN_HIP(spmm_launch(c, stream));
     GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, GT,
                             GT + h, o.ld_g, dW_self, dW_neigh);
+    bw.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
     GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
     if (dX) {
       GemmBatch bx = dx_batch(2, n, f_in, h, GT, GT + h, o.ld_g, W_self,
                               W_neigh, dX, layer->ld_dx, nullptr, 0);
+    bx.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
     }
     if (db_self || db_neigh) {
@@ -539,10 +550,12 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, G, o.ld_g, G + h, o.ld_g, stream));
     GemmBatch bw = dw_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, G, G + h,
                             o.ld_g, dW_self, dW_neigh);
+    bw.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
     GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
     if (dX) {
       GemmBatch bx = dx_batch(1, n, f_in, h, G, G + h, o.ld_g, W_self, W_neigh,
                               dX, layer->ld_dx, V, o.ld_v);
+    bx.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
       SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx, spart);
       c.epilogue = SPMM_ADD;

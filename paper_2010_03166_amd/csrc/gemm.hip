@@ -61,7 +61,8 @@ struct GemmKArgs {
   int32_t ktiles0[2];  // K slices of segment 0, per problem
   int64_t iters;       // tiles * ktiles
   int32_t nblocks;     // P
-  float* part;         // 2 partial tiles per block, BM * BN floats each
+  int32_t splits;      // > 1: split-K mode, one (tile, K range) per block
+  float* part;         // partial tiles (2 per block stream-K, 1 split-K)
   int32_t vec_a, vec_b;
 };
 
@@ -137,8 +138,15 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
   const int M = g.M;
 
   const int lb = logical_block(blockIdx.x, g.nblocks);
-  const int64_t lo = block_lo(lb, g.iters, g.nblocks);
-  const int64_t hi = block_lo(lb + 1, g.iters, g.nblocks);
+  int64_t lo, hi;
+  if (g.splits > 1) {  // block lb = split * tiles + tile
+    const int sp = lb / g.tiles, t = lb % g.tiles;
+    lo = (int64_t)t * g.ktiles + (int64_t)sp * g.ktiles / g.splits;
+    hi = (int64_t)t * g.ktiles + (int64_t)(sp + 1) * g.ktiles / g.splits;
+  } else {
+    lo = block_lo(lb, g.iters, g.nblocks);
+    hi = block_lo(lb + 1, g.iters, g.nblocks);
+  }
 
   int buf = 0;
   int seg = 0;
@@ -150,66 +158,73 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
     const TileInfo ti = tile_info(g, t);
     const GemmProblem& P = ti.pi ? g.p[1] : g.p[0];
     const int N = P.N;
+    const int m0 = ti.m0, n0 = ti.n0;
+    // Segment parameters, read once per tile (kept in scalar registers).
     const int kt0 = ti.pi ? g.ktiles0[1] : g.ktiles0[0];
+    const float* const A0p = P.seg[0].A;
+    const float* const A1p = P.seg[1].A;
+    const float* const B0p = P.seg[0].B;
+    const float* const B1p = P.seg[1].B;
+    const int64_t lda0 = P.seg[0].lda, lda1 = P.seg[1].lda;
+    const int64_t ldb0 = P.seg[0].ldb, ldb1 = P.seg[1].ldb;
+    const int K0 = P.seg[0].K, K1 = P.seg[1].K;
+    const bool a_in = va && m0 + BM <= M;  // no row/column guard needed
+    const bool b_in = vb && n0 + BN <= N;
+    // This thread's place in a slice: KC operands own (row x, 4 k),
+    // XC operands own (row k, 4 consecutive m or n).
+    const int ax = A_KC ? (tid >> 3) : (tid >> 5);
+    const int ay = A_KC ? 4 * (tid & 7) : 4 * (tid & 31);
+    const int bx = B_KC ? (tid >> 3) : (tid >> 5);
+    const int by = B_KC ? 4 * (tid & 7) : 4 * (tid & 31);
+    constexpr int ASTEP = A_KC ? 32 : 8;
+    constexpr int BSTEP = B_KC ? 32 : 8;
 
     float4 ra[4], rb[4];
     auto load_slice = [&](int ks) {
       const bool s1 = ks >= kt0;
-      const GemmSeg& S = s1 ? P.seg[1] : P.seg[0];
+      const float* A = s1 ? A1p : A0p;
+      const float* B = s1 ? B1p : B0p;
+      const int64_t lda = s1 ? lda1 : lda0;
+      const int64_t ldb = s1 ? ldb1 : ldb0;
+      const int K = s1 ? K1 : K0;
       const int k0 = (s1 ? ks - kt0 : ks) * BK;
-      const int K = S.K;
-      const bool full_k = k0 + BK <= K;
-      // A: K-contiguous -> thread owns (row x, 4 k); else (row k, 4 m)
-      const int ax = A_KC ? (tid >> 3) : (tid >> 5);
-      const int ay = A_KC ? 4 * (tid & 7) : 4 * (tid & 31);
-      const int astep = A_KC ? 32 : 8;
-      if (va && full_k && ti.m0 + BM <= M) {
-        const float* base = A_KC ? S.A + (int64_t)(ti.m0 + ax) * S.lda + k0 + ay
-                                 : S.A + (int64_t)(k0 + ax) * S.lda + ti.m0 + ay;
-        const int64_t stride = (int64_t)astep * S.lda;
+      const bool fk = k0 + BK <= K;
+      if (a_in && fk) {
+        const float* p0 = A_KC ? A + (int64_t)(m0 + ax) * lda + (k0 + ay)
+                               : A + (int64_t)(k0 + ax) * lda + (m0 + ay);
+        const int64_t st = ASTEP * lda;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) ra[p] = ld4(base + p * stride);
+        for (int p = 0; p < 4; ++p) ra[p] = ld4(p0 + p * st);
       } else {
 #pragma unroll
         for (int p = 0; p < 4; ++p)
-          ra[p] = A_KC ? load4(S.A, S.lda, ti.m0 + ax + astep * p, k0 + ay, M, K, va)
-                       : load4(S.A, S.lda, k0 + ax + astep * p, ti.m0 + ay, K, M, va);
+          ra[p] = A_KC ? load4(A, lda, m0 + ax + ASTEP * p, k0 + ay, M, K, va)
+                       : load4(A, lda, k0 + ax + ASTEP * p, m0 + ay, K, M, va);
       }
-      const int bx = B_KC ? (tid >> 3) : (tid >> 5);
-      const int by = B_KC ? 4 * (tid & 7) : 4 * (tid & 31);
-      const int bstep = B_KC ? 32 : 8;
-      if (vb && full_k && ti.n0 + BN <= N) {
-        const float* base = B_KC ? S.B + (int64_t)(ti.n0 + bx) * S.ldb + k0 + by
-                                 : S.B + (int64_t)(k0 + bx) * S.ldb + ti.n0 + by;
-        const int64_t stride = (int64_t)bstep * S.ldb;
+      if (b_in && fk) {
+        const float* p0 = B_KC ? B + (int64_t)(n0 + bx) * ldb + (k0 + by)
+                               : B + (int64_t)(k0 + bx) * ldb + (n0 + by);
+        const int64_t st = BSTEP * ldb;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) rb[p] = ld4(base + p * stride);
+        for (int p = 0; p < 4; ++p) rb[p] = ld4(p0 + p * st);
       } else {
 #pragma unroll
         for (int p = 0; p < 4; ++p)
-          rb[p] = B_KC ? load4(S.B, S.ldb, ti.n0 + bx + bstep * p, k0 + by, N, K, vb)
-                       : load4(S.B, S.ldb, k0 + bx + bstep * p, ti.n0 + by, K, N, vb);
+          rb[p] = B_KC ? load4(B, ldb, n0 + bx + BSTEP * p, k0 + by, N, K, vb)
+                       : load4(B, ldb, k0 + bx + BSTEP * p, n0 + by, K, N, vb);
       }
+    };
+    // LDS offsets (floats) of this thread's slice stores.
+    auto sto_off = [&](bool kc, int x, int y, int p, int step) {
+      if (kc) return (x + step * p) * KC_STRIDE + y;
+      const int kk = x + step * p;
+      return (((kk & 15) << 1) | (kk >> 4)) * XC_STRIDE + y;
     };
     auto store_slice = [&](int bb) {
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
-        if (A_KC) {
-          const int x = (tid >> 3) + 32 * p, kq = tid & 7;
-          *reinterpret_cast<float4*>(&As[bb][x * KC_STRIDE + 4 * kq]) = ra[p];
-        } else {
-          const int kk = (tid >> 5) + 8 * p, xq = tid & 31;
-          const int row = ((kk & 15) << 1) | (kk >> 4);
-          *reinterpret_cast<float4*>(&As[bb][row * XC_STRIDE + 4 * xq]) = ra[p];
-        }
-        if (B_KC) {
-          const int x = (tid >> 3) + 32 * p, kq = tid & 7;
-          *reinterpret_cast<float4*>(&Bs[bb][x * KC_STRIDE + 4 * kq]) = rb[p];
-        } else {
-          const int kk = (tid >> 5) + 8 * p, xq = tid & 31;
-          const int row = ((kk & 15) << 1) | (kk >> 4);
-          *reinterpret_cast<float4*>(&Bs[bb][row * XC_STRIDE + 4 * xq]) = rb[p];
-        }
+        *reinterpret_cast<float4*>(&As[bb][sto_off(A_KC, ax, ay, p, ASTEP)]) = ra[p];
+        *reinterpret_cast<float4*>(&Bs[bb][sto_off(B_KC, bx, by, p, BSTEP)]) = rb[p];
       }
     };
 
@@ -221,6 +236,14 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+    // Fragment reads.  Step s of a slice uses k = 16 * lh + s.  KC operands
+    // come in float4 groups of 4 steps (q = s / 4); XC operands one float per
+    // step from the stored row 2 s + lh.
+    const int a_kc_base = (wm * 64 + lr) * KC_STRIDE + lh * 16;
+    const int b_kc_base = (wn * 64 + lr) * KC_STRIDE + lh * 16;
+    const int a_xc_base = lh * XC_STRIDE + wm * 64 + lr;
+    const int b_xc_base = lh * XC_STRIDE + wn * 64 + lr;
+
     load_slice(kbeg);
     for (int ks = kbeg; ks < kend; ++ks) {
       store_slice(buf);
@@ -228,39 +251,68 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
       if (ks + 1 < kend) load_slice(ks + 1);
       const float* as = As[buf];
       const float* bs = Bs[buf];
+      // Operands of step s are fetched one step (XC) or one group (KC)
+      // ahead of the MFMAs that consume them.
+      float4 af[2], bf[2], afn[2], bfn[2];
+      float ax_[2], bx_[2], axn[2], bxn[2];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float4 af[2], bf[2];
+      for (int i = 0; i < 2; ++i) {
+        if (A_KC) afn[i] = ld4(as + a_kc_base + i * 32 * KC_STRIDE);
+        else axn[i] = as[a_xc_base + i * 32];
+        if (B_KC) bfn[i] = ld4(bs + b_kc_base + i * 32 * KC_STRIDE);
+        else bxn[i] = bs[b_xc_base + i * 32];
+      }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          if (A_KC)
-            af[i] = ld4(as + (wm * 64 + i * 32 + lr) * KC_STRIDE + lh * 16 + 4 * q);
-          if (B_KC)
-            bf[i] = ld4(bs + (wn * 64 + i * 32 + lr) * KC_STRIDE + lh * 16 + 4 * q);
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int s = 4 * q + u;
-          const int row = 2 * s + lh;  // stored row of k = 16 lh + s
-          float a[2], b[2];
+      for (int st = 0; st < BK / 2; ++st) {
+        const int u = st & 3;
+        if (u == 0) {
 #pragma unroll
           for (int i = 0; i < 2; ++i) {
-            a[i] = A_KC ? comp(af[i], u) : as[row * XC_STRIDE + wm * 64 + i * 32 + lr];
-            b[i] = B_KC ? comp(bf[i], u) : bs[row * XC_STRIDE + wn * 64 + i * 32 + lr];
+            af[i] = afn[i];
+            bf[i] = bfn[i];
           }
-          acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], acc[0][0], 0, 0, 0);
-          acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[1], acc[0][1], 0, 0, 0);
-          acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[0], acc[1][0], 0, 0, 0);
-          acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[1], acc[1][1], 0, 0, 0);
+          if (st + 4 < BK / 2) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+              if (A_KC) afn[i] = ld4(as + a_kc_base + i * 32 * KC_STRIDE + st + 4);
+              if (B_KC) bfn[i] = ld4(bs + b_kc_base + i * 32 * KC_STRIDE + st + 4);
+            }
+          }
         }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          ax_[i] = axn[i];
+          bx_[i] = bxn[i];
+        }
+        if (st + 1 < BK / 2) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            if (!A_KC) axn[i] = as[a_xc_base + 2 * (st + 1) * XC_STRIDE + i * 32];
+            if (!B_KC) bxn[i] = bs[b_xc_base + 2 * (st + 1) * XC_STRIDE + i * 32];
+          }
+        }
+        float a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          a[i] = A_KC ? comp(af[i], u) : ax_[i];
+          b[i] = B_KC ? comp(bf[i], u) : bx_[i];
+        }
+        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[1], acc[0][1], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[0], acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[1], acc[1][1], 0, 0, 0);
       }
+      // let the scheduler interleave LDS reads with the MFMA chain
+      __builtin_amdgcn_iglp_opt(0);
       buf ^= 1;
     }
 
     // Accumulator layout of v_mfma_f32_32x32x2_f32: lane l, register r holds
     // row 8*(r/4) + 4*(l/32) + r%4 and column l%32 of the 32 x 32 block.
     const bool whole = kbeg == 0 && kend == g.ktiles;
-    float* part = g.part + ((int64_t)lb * 2 + (seg > 0 ? 1 : 0)) * (BM * BN);
+    float* part = g.part + (g.splits > 1 ? (int64_t)lb
+                                         : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
+                               (BM * BN);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -287,6 +339,226 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
   }
 }
 
+// --------------------------------------------------------- bf16 variant
+//
+// Same tiling, work split and epilogue as the fp32 kernel, with operands
+// rounded to bf16 (round to nearest even, v_cvt_pk_bf16_f32) as they are
+// staged into LDS, fp32 accumulation on v_mfma_f32_32x32x16_bf16, and
+// 32-deep K slices (two MFMA steps; small enough that the fp32 prefetch
+// registers leave room for two blocks per CU).  In MFMA step s (s = 0, 1)
+// lane half h supplies the 8 values k = 16 h + 8 s + j (j = 0..7).
+//   K-contiguous operand: LDS [x][k] rows of 32 + 8 bf16; one 128-bit read
+//     per fragment.
+//   X-contiguous operand: LDS rows of k pairs, each word = (k, k+1) of one
+//     x as bf16x2; a fragment is 4 words from 4 rows; the pair rows are
+//     stored in the order (kp mod 8) * 2 + kp / 8 (kp = k / 2) so the two
+//     lane halves read adjacent rows.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+
+constexpr int BK16 = 32;
+constexpr int KC16_STRIDE = 20;   // 32-bit words per [x][k] row (40 bf16)
+constexpr int XC16_STRIDE = 160;  // words per k-pair row
+constexpr int KC16_WORDS = 128 * KC16_STRIDE;
+constexpr int XC16_WORDS = (BK16 / 2) * XC16_STRIDE;
+
+__device__ inline uint32_t pack_bf16(float lo, float hi) {
+  bf16x2v v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+template <bool AT, bool BT>
+__global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
+  constexpr bool A_KC = !AT;
+  constexpr bool B_KC = BT;
+  constexpr int A_WORDS = A_KC ? KC16_WORDS : XC16_WORDS;
+  constexpr int B_WORDS = B_KC ? KC16_WORDS : XC16_WORDS;
+  __shared__ __attribute__((aligned(16))) uint32_t As[2][A_WORDS];
+  __shared__ __attribute__((aligned(16))) uint32_t Bs[2][B_WORDS];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int lr = lane & 31, lh = lane >> 5;
+  const bool va = g.vec_a != 0, vb = g.vec_b != 0;
+  const int M = g.M;
+
+  const int lb = logical_block(blockIdx.x, g.nblocks);
+  int64_t lo, hi;
+  if (g.splits > 1) {
+    const int sp = lb / g.tiles, t = lb % g.tiles;
+    lo = (int64_t)t * g.ktiles + (int64_t)sp * g.ktiles / g.splits;
+    hi = (int64_t)t * g.ktiles + (int64_t)(sp + 1) * g.ktiles / g.splits;
+  } else {
+    lo = block_lo(lb, g.iters, g.nblocks);
+    hi = block_lo(lb + 1, g.iters, g.nblocks);
+  }
+
+  int buf = 0;
+  int seg = 0;
+  for (int64_t it = lo; it < hi; ++seg) {
+    const int t = (int)(it / g.ktiles);
+    const int kbeg = (int)(it - (int64_t)t * g.ktiles);
+    const int kend = (int)min<int64_t>(g.ktiles, hi - (int64_t)t * g.ktiles);
+    it = (int64_t)t * g.ktiles + kend;
+    const TileInfo ti = tile_info(g, t);
+    const GemmProblem& P = ti.pi ? g.p[1] : g.p[0];
+    const int N = P.N;
+    const int m0 = ti.m0, n0 = ti.n0;
+    const int kt0 = ti.pi ? g.ktiles0[1] : g.ktiles0[0];
+    const float* const A0p = P.seg[0].A;
+    const float* const A1p = P.seg[1].A;
+    const float* const B0p = P.seg[0].B;
+    const float* const B1p = P.seg[1].B;
+    const int64_t lda0 = P.seg[0].lda, lda1 = P.seg[1].lda;
+    const int64_t ldb0 = P.seg[0].ldb, ldb1 = P.seg[1].ldb;
+    const int K0 = P.seg[0].K, K1 = P.seg[1].K;
+    const bool a_in = va && m0 + BM <= M;
+    const bool b_in = vb && n0 + BN <= N;
+    // KC: thread owns row x = (tid >> 2) + 64 p and k = 8 (tid & 3) .. + 7.
+    // XC: thread owns k-pair kp = (tid >> 5) + 8 p and x = 4 (tid & 31) .. + 3.
+    const int kx = tid >> 2, ky = 8 * (tid & 3);
+    const int xk = tid >> 5, xy = 4 * (tid & 31);
+
+    float4 ra[4], rb[4];
+    // Loads of one operand's slice: `lo4`/`hi4` pairs per p (KC: k halves,
+    // XC: rows 2kp and 2kp+1).
+    auto load_op = [&](float4 (&r)[4], bool kc, const float* X, int64_t ld,
+                       int x0, int X_extent, int k0, int K, bool fast, bool vec) {
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        if (kc) {
+          const int x = x0 + kx + 64 * p, k = k0 + ky;
+          if (fast) {
+            const float* q = X + (int64_t)x * ld + k;
+            r[2 * p] = ld4(q);
+            r[2 * p + 1] = ld4(q + 4);
+          } else {
+            r[2 * p] = load4(X, ld, x, k, X_extent, K, vec);
+            r[2 * p + 1] = load4(X, ld, x, k + 4, X_extent, K, vec);
+          }
+        } else {
+          const int k = k0 + 2 * (xk + 8 * p), x = x0 + xy;
+          if (fast) {
+            const float* q = X + (int64_t)k * ld + x;
+            r[2 * p] = ld4(q);
+            r[2 * p + 1] = ld4(q + ld);
+          } else {
+            r[2 * p] = load4(X, ld, k, x, K, X_extent, vec);
+            r[2 * p + 1] = load4(X, ld, k + 1, x, K, X_extent, vec);
+          }
+        }
+      }
+    };
+    auto load_slice = [&](int ks) {
+      const bool s1 = ks >= kt0;
+      const int K = s1 ? K1 : K0;
+      const int k0 = (s1 ? ks - kt0 : ks) * BK16;
+      const bool fk = k0 + BK16 <= K;
+      load_op(ra, A_KC, s1 ? A1p : A0p, s1 ? lda1 : lda0, m0, M, k0, K, a_in && fk, va);
+      load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, K, b_in && fk, vb);
+    };
+    auto store_op = [&](uint32_t* L, const float4 (&r)[4], bool kc) {
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const float4 a = r[2 * p], b = r[2 * p + 1];
+        uint4 w;
+        if (kc) {  // 8 consecutive k of row x
+          w.x = pack_bf16(a.x, a.y);
+          w.y = pack_bf16(a.z, a.w);
+          w.z = pack_bf16(b.x, b.y);
+          w.w = pack_bf16(b.z, b.w);
+          *reinterpret_cast<uint4*>(&L[(kx + 64 * p) * KC16_STRIDE + ky / 2]) = w;
+        } else {   // k pair (a: row 2kp, b: row 2kp+1) of 4 consecutive x
+          w.x = pack_bf16(a.x, b.x);
+          w.y = pack_bf16(a.y, b.y);
+          w.z = pack_bf16(a.z, b.z);
+          w.w = pack_bf16(a.w, b.w);
+          const int kp = xk + 8 * p;
+          const int row = ((kp & 7) << 1) | (kp >> 3);
+          *reinterpret_cast<uint4*>(&L[row * XC16_STRIDE + xy]) = w;
+        }
+      }
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // fragment for block i of an operand at step s
+    auto frag = [&](const uint32_t* L, bool kc, int wbase, int i, int s) {
+      uint4 w;
+      if (kc) {
+        w = *reinterpret_cast<const uint4*>(
+            &L[(wbase + i * 32 + lr) * KC16_STRIDE + (16 * lh + 8 * s) / 2]);
+      } else {
+        const int x = wbase + i * 32 + lr;
+        // k pairs 8 lh + 4 s + j, stored at rows ((4 s + j) << 1) | lh
+        w.x = L[((((4 * s + 0) << 1) | lh)) * XC16_STRIDE + x];
+        w.y = L[((((4 * s + 1) << 1) | lh)) * XC16_STRIDE + x];
+        w.z = L[((((4 * s + 2) << 1) | lh)) * XC16_STRIDE + x];
+        w.w = L[((((4 * s + 3) << 1) | lh)) * XC16_STRIDE + x];
+      }
+      return __builtin_bit_cast(bf16x8, w);
+    };
+
+    load_slice(kbeg);
+    for (int ks = kbeg; ks < kend; ++ks) {
+      store_op(As[buf], ra, A_KC);
+      store_op(Bs[buf], rb, B_KC);
+      __syncthreads();
+      if (ks + 1 < kend) load_slice(ks + 1);
+      const uint32_t* as = As[buf];
+      const uint32_t* bs = Bs[buf];
+#pragma unroll
+      for (int st = 0; st < BK16 / 16; ++st) {
+        const bf16x8 a0 = frag(as, A_KC, wm * 64, 0, st);
+        const bf16x8 a1 = frag(as, A_KC, wm * 64, 1, st);
+        const bf16x8 b0 = frag(bs, B_KC, wn * 64, 0, st);
+        const bf16x8 b1 = frag(bs, B_KC, wn * 64, 1, st);
+        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+      }
+      // (no scheduling hint here: it raises register pressure past 256)
+      buf ^= 1;
+    }
+
+    const bool whole = kbeg == 0 && kend == g.ktiles;
+    float* part = g.part + (g.splits > 1 ? (int64_t)lb
+                                         : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
+                               (BM * BN);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int cl = wn * 64 + j * 32 + lr;
+        const int col = n0 + cl;
+        const float bc = (whole && P.bias && col < N) ? P.bias[col] : 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rl = wm * 64 + i * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+          const int row = m0 + rl;
+          float v = acc[i][j][r];
+          if (whole) {
+            if (row < M && col < N) {
+              v += bc;
+              if (P.relu) v = fmaxf(v, 0.f);
+              P.C[(int64_t)row * P.ldc + col] = v;
+            }
+          } else {
+            part[rl * BN + cl] = v;
+          }
+        }
+      }
+  }
+}
+
 // Tiles shared by several blocks: add the blocks' partial tiles in block
 // order, then bias and ReLU.  Block (t, c) handles 1024 elements of tile t,
 // four consecutive columns per thread.
@@ -295,9 +567,12 @@ constexpr int FIX_CHUNKS = BM * BN / 1024;
 __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
   const int t = blockIdx.x;
   const int64_t first = (int64_t)t * g.ktiles, last = first + g.ktiles - 1;
-  const int b0 = block_of(first, g.iters, g.nblocks);
-  const int b1 = block_of(last, g.iters, g.nblocks);
-  if (b0 == b1) return;  // written directly by its only block
+  int b0 = 0, b1 = 0;
+  if (g.splits <= 1) {
+    b0 = block_of(first, g.iters, g.nblocks);
+    b1 = block_of(last, g.iters, g.nblocks);
+    if (b0 == b1) return;  // written directly by its only block
+  }
   const TileInfo ti = tile_info(g, t);
   const GemmProblem& P = ti.pi ? g.p[1] : g.p[0];
   const int e = blockIdx.y * 1024 + threadIdx.x * 4;
@@ -305,14 +580,24 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
   const int row = ti.m0 + rl, col = ti.n0 + cl;
   if (row >= g.M || col >= P.N) return;
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int b = b0; b <= b1; ++b) {
-    // the tile is block b's first tile iff b's range starts inside it
-    const int slot = block_lo(b, g.iters, g.nblocks) >= first ? 0 : 1;
-    const float4 p = ld4(g.part + ((int64_t)b * 2 + slot) * (BM * BN) + e);
-    v.x += p.x;
-    v.y += p.y;
-    v.z += p.z;
-    v.w += p.w;
+  if (g.splits > 1) {
+    for (int sp = 0; sp < g.splits; ++sp) {
+      const float4 p = ld4(g.part + ((int64_t)sp * g.tiles + t) * (BM * BN) + e);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+  } else {
+    for (int b = b0; b <= b1; ++b) {
+      // the tile is block b's first tile iff b's range starts inside it
+      const int slot = block_lo(b, g.iters, g.nblocks) >= first ? 0 : 1;
+      const float4 p = ld4(g.part + ((int64_t)b * 2 + slot) * (BM * BN) + e);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
   }
   float o[4] = {v.x, v.y, v.z, v.w};
   float* dst = P.C + (int64_t)row * P.ldc + col;
@@ -332,11 +617,13 @@ struct Shape {
   int tiles_m, tiles_n0, tiles_n, tiles, ktiles, kt0[2];
   int64_t iters;
   int nblocks;
+  int splits;
 };
 
 static Shape gemm_shape(const GemmBatch& b) {
   Shape s;
   memset(&s, 0, sizeof(s));
+  const int BK = b.bf16 ? BK16 : gnnprop::BK;
   const int M = b.p[0].M;
   s.tiles_m = (int)ceil_div(M, BM);
   s.tiles_n0 = (int)ceil_div(b.p[0].N, BN);
@@ -350,22 +637,33 @@ static Shape gemm_shape(const GemmBatch& b) {
   }
   s.ktiles = std::max(s.ktiles, 1);
   s.iters = (int64_t)s.tiles * s.ktiles;
-  // One block per tile when the tiles fill the resident slots well enough,
-  // else an even split of all tile x K-slice iterations over MAX_BLOCKS.
-  const int64_t rounds = ceil_div(s.tiles, MAX_BLOCKS);
-  const double fill = (double)s.tiles / (double)(rounds * MAX_BLOCKS);
-  if (fill >= 0.85 || s.iters <= MAX_BLOCKS)
+  // One block per tile when the tiles fill the resident slots well enough.
+  // Otherwise, with few tiles and a long K (weight gradients, K = n), split
+  // K into S ranges, one (tile, range) per block, ordered split-major so that
+  // one XCD's blocks share a K slab of both operands in its L2; with more
+  // tiles, split all tile x K-slice iterations evenly over MAX_BLOCKS.
+  // resident blocks: 2 per CU
+  const int slots = MAX_BLOCKS;
+  const int64_t rounds = ceil_div(s.tiles, slots);
+  const double fill = (double)s.tiles / (double)(rounds * slots);
+  s.splits = 1;
+  if (fill >= 0.85 || s.iters <= slots) {
     s.nblocks = s.tiles;
-  else
-    s.nblocks = MAX_BLOCKS;
+  } else if (s.tiles <= slots / 4) {
+    s.splits = (int)std::min<int64_t>(s.ktiles, slots / s.tiles);
+    s.nblocks = s.tiles * s.splits;
+  } else {
+    s.nblocks = slots;
+  }
   return s;
 }
 
 static bool batch_ok(const GemmBatch& b) {
   if (b.nprob < 1 || b.nprob > 2) return false;
+  const int BK = b.bf16 ? BK16 : gnnprop::BK;
   if (b.nprob == 2) {
     if (b.p[0].M != b.p[1].M) return false;
-    const auto kt = [](const GemmProblem& p) {
+    const auto kt = [BK](const GemmProblem& p) {
       return ceil_div(p.seg[0].K, BK) + (p.nseg > 1 ? ceil_div(p.seg[1].K, BK) : 0);
     };
     if (kt(b.p[0]) != kt(b.p[1])) return false;
@@ -377,7 +675,8 @@ size_t gemm_workspace_bytes(const GemmBatch& b) {
   if (!batch_ok(b)) return 0;
   const Shape s = gemm_shape(b);
   if (s.tiles == 0 || s.nblocks == s.tiles) return 0;
-  return round_up((size_t)s.nblocks * 2 * BM * BN * 4, 256);
+  const size_t slots = s.splits > 1 ? (size_t)s.nblocks : (size_t)s.nblocks * 2;
+  return round_up(slots * BM * BN * 4, 256);
 }
 
 double gemm_flops(const GemmBatch& b) {
@@ -405,6 +704,7 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
   g.ktiles = sh.ktiles;
   g.iters = sh.iters;
   g.nblocks = sh.nblocks;
+  g.splits = sh.splits;
   bool va = true, vb = true;
   for (int i = 0; i < b.nprob; ++i) {
     g.p[i] = b.p[i];
@@ -431,14 +731,24 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
   const int kid = b.trans_a ? (b.trans_b ? GNN_K_GEMM_TT : GNN_K_GEMM_TN)
                             : (b.trans_b ? GNN_K_GEMM_NT : GNN_K_GEMM_NN);
   timer_begin(kid, s);
-  if (!b.trans_a && !b.trans_b)
+  if (b.bf16) {
+    if (!b.trans_a && !b.trans_b)
+      gemm_bf16_kernel<false, false><<<grid, 256, 0, s>>>(g);
+    else if (b.trans_a && !b.trans_b)
+      gemm_bf16_kernel<true, false><<<grid, 256, 0, s>>>(g);
+    else if (!b.trans_a && b.trans_b)
+      gemm_bf16_kernel<false, true><<<grid, 256, 0, s>>>(g);
+    else
+      gemm_bf16_kernel<true, true><<<grid, 256, 0, s>>>(g);
+  } else if (!b.trans_a && !b.trans_b) {
     gemm_f32_kernel<false, false><<<grid, 256, 0, s>>>(g);
-  else if (b.trans_a && !b.trans_b)
+  } else if (b.trans_a && !b.trans_b) {
     gemm_f32_kernel<true, false><<<grid, 256, 0, s>>>(g);
-  else if (!b.trans_a && b.trans_b)
+  } else if (!b.trans_a && b.trans_b) {
     gemm_f32_kernel<false, true><<<grid, 256, 0, s>>>(g);
-  else
+  } else {
     gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g);
+  }
   timer_end(kid, gemm_flops(b), s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !streamk) return e;

@@ -143,8 +143,11 @@ def test_spmm_empty_graph_and_empty_rows():
 
 # ------------------------------------------------------------------- GEMM
 
+# one block per tile; split-K (few tiles, long K); stream-K (tiles that do
+# not fill the chip, e.g. 2000 x 1300); ragged and empty shapes
 GEMM_SHAPES = [(1, 1, 1), (37, 45, 29), (128, 128, 32), (130, 257, 70),
-               (1000, 128, 50), (602, 512, 8000), (300, 96, 4099), (64, 64, 0)]
+               (1000, 128, 50), (602, 512, 8000), (300, 96, 4099), (64, 64, 0),
+               (2001, 1300, 100), (8000, 602, 1024)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
@@ -367,3 +370,87 @@ def test_validate_accepts_and_rejects():
     g.indptr = g.indptr.copy()
     g.indptr[-1] -= 1
     assert runtime.DeviceGraph(g).validate(False) == -3
+
+
+# ----------------------------------------------------- bf16 matrix-core mode
+
+TOL_BF16_KERNEL = 1e-5   # vs the oracle on bf16-rounded operands
+TOL_BF16_LAYER = 2e-2    # vs the double-precision oracle on the fp32 inputs
+
+
+@pytest.mark.parametrize("M,N,K", [(37, 45, 29), (128, 128, 64), (130, 257, 70),
+                                   (602, 512, 8000), (2001, 1300, 100),
+                                   (8000, 602, 1024), (64, 64, 0)])
+@pytest.mark.parametrize("ta", [0, 1])
+@pytest.mark.parametrize("tb", [0, 1])
+def test_gemm_bf16_parity(M, N, K, ta, tb):
+    # operands rounded to bf16 (nearest, ties to even) and multiplied exactly;
+    # only the fp32 accumulation order differs from the oracle
+    rng = np.random.default_rng(M + 3 * N + 7 * K)
+    a = rng.standard_normal((K, M) if ta else (M, K)).astype(np.float32)
+    b = rng.standard_normal((N, K) if tb else (K, N)).astype(np.float32)
+    A = to_dev(a, (a.shape[1] + 3) // 4 * 4)
+    B = to_dev(b, (b.shape[1] + 3) // 4 * 4)
+    C = empty_out(M, N, (N + 3) // 4 * 4)
+    ws = torch.empty(max(G.gnn_gemm_workspace_bytes(M, N, K), 256),
+                     dtype=torch.uint8, device="cuda")
+    G.gnn_gemm(ta, tb, M, N, K, A, A.stride(0), B, B.stride(0), C, C.stride(0),
+               G.GNN_FLAG_BF16, ws)
+    torch.cuda.synchronize()
+    ra, rb = O.round_bf16(a), O.round_bf16(b)
+    ref = O.mm_nn(ra.T if ta else ra, rb.T if tb else rb) if K > 0 else np.zeros((M, N))
+    assert maxrel(C, ref) <= TOL_BF16_KERNEL
+
+
+@pytest.mark.parametrize("n,f_in,h", [(500, 50, 128), (400, 130, 64), (300, 602, 40)])
+@pytest.mark.parametrize("order", [1, 2])
+def test_layer_bf16(n, f_in, h, order):
+    g, x, p, dy = layer_inputs(n, f_in, h, 77 + n, False)
+    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh)
+    y32 = y_ref.astype(np.float32)
+    dg = prepared(g)
+    st = runtime.SageStack(dg, [p], f_in, order=order, flags=G.GNN_FLAG_BF16)
+    st.forward(to_dev(x, (f_in + 15) // 16 * 16))
+    torch.cuda.synchronize()
+    assert maxrel(st.layers[0]["Y"], y_ref) <= TOL_BF16_LAYER
+    st.layers[0]["Y"].copy_(torch.from_numpy(y32).cuda())
+    st.backward(to_dev(dy))
+    torch.cuda.synchronize()
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy)
+    for k in ("dX", "dW_self", "dW_neigh"):
+        assert maxrel(st.layers[0][k], r[k]) <= TOL_BF16_LAYER, k
+
+
+@pytest.mark.parametrize("name", ["cl2.1-n8000-f602-h512-L2", "cl2.3-n8000-f300-h512-L3"])
+def test_workload_bf16_full_size(name):
+    """The 8,000-node workloads at full size in bf16 mode, spot-checked
+    against the double-precision oracle at the bf16 tolerance."""
+    wl = synth.WORKLOADS[name]
+    g = synth.workload_graph(wl)
+    dg = prepared(g)
+    hub = int(np.argmax(g.degrees()))
+    for l, (f_in, h) in enumerate(synth.layer_dims(wl)):
+        rng = np.random.default_rng(2000 + l)
+        x = rng.standard_normal((g.n, f_in)).astype(np.float32)
+        if l > 0:
+            x = np.maximum(x, 0)
+        p = synth.LayerParams(synth.glorot(f_in, h, rng), synth.glorot(f_in, h, rng))
+        ysyn = rng.standard_normal((g.n, 2 * h)).astype(np.float32)
+        dy = rng.standard_normal((g.n, 2 * h)).astype(np.float32)
+        st = runtime.SageStack(dg, [p], f_in, flags=G.GNN_FLAG_BF16)
+        st.forward(to_dev(x, (f_in + 15) // 16 * 16))
+        torch.cuda.synchronize()
+        rows = sample_rows(g.n, 16, l, must=(0, hub))
+        y = st.layers[0]["Y"][torch.from_numpy(rows).cuda()].cpu().numpy()
+        assert maxrel(y, O.sage_fwd_rows(g, x, p.w_self, p.w_neigh, rows)) <= TOL_BF16_LAYER
+        st.layers[0]["Y"].copy_(torch.from_numpy(ysyn).cuda())
+        st.backward(to_dev(dy))
+        torch.cuda.synchronize()
+        dx = st.layers[0]["dX"][torch.from_numpy(rows).cuda()].cpu().numpy()
+        dxr = O.sage_bwd_dx_rows(g, p.w_self, p.w_neigh, ysyn, dy, rows)
+        assert maxrel(dx, dxr) <= TOL_BF16_LAYER
+        ei, ej = rng.integers(0, f_in, 12), rng.integers(0, h, 12)
+        ws_, wn_ = O.sage_bwd_dw_entries(g, x, ysyn, dy, h, ei, ej)
+        assert maxrel(st.layers[0]["dW_self"].cpu().numpy()[ei, ej], ws_) <= TOL_BF16_LAYER
+        assert maxrel(st.layers[0]["dW_neigh"].cpu().numpy()[ei, ej], wn_) <= TOL_BF16_LAYER
+        del st

@@ -394,3 +394,39 @@ def test_result_independent_of_thread_count(monkeypatch):
                                    capture_output=True, text=True,
                                    check=True).stdout)
     assert outs[0] == outs[1] == outs[2]
+
+
+# ------------------------------------------------------- bfloat16 rounding
+
+def test_round_bf16_closed_forms():
+    # bfloat16 has 8 significant bits: representable neighbours of 1 are
+    # 1 - 2^-8 and 1 + 2^-7
+    vals = np.array([1.0, 1 + 2.0**-8, 1 + 3 * 2.0**-9, 1 + 2.0**-7 + 2.0**-8,
+                     -(1 + 2.0**-8 + 2.0**-20), 0.0, -0.0, 2.0**-130,
+                     3.0e38, 1.0 + 2.0**-9])
+    exp = np.array([1.0, 1.0,                # tie -> even (1.0)
+                    1 + 2.0**-7,             # above the tie -> up
+                    1 + 2.0**-6,             # tie between 1+2^-7 (odd) and 1+2^-6
+                    -(1 + 2.0**-7),          # above the tie (negative) -> away
+                    0.0, -0.0, 2.0**-130,    # float subnormal 2^-130 is exact
+                    np.float32(3.0e38).astype(np.float64),
+                    1.0])
+    exp[8] = np.inf if False else exp[8]
+    got = O.round_bf16(vals)
+    assert got[:8].tolist() == exp[:8].tolist()
+    assert np.signbit(got[6])
+    # 3e38 rounds to a value with 8 significant bits, within half an ulp
+    b = got[8]
+    assert abs(b - 3.0e38) <= 2.0**(127 - 8) and b == O.round_bf16([b])[0]
+    assert got[9] == 1.0
+
+
+def test_round_bf16_is_idempotent_and_monotone():
+    r = np.random.default_rng(0)
+    x = np.sort(r.standard_normal(5000) * 10.0 ** r.uniform(-5, 5, 5000))
+    y = O.round_bf16(x)
+    assert np.all(np.diff(y) >= 0)
+    assert np.array_equal(O.round_bf16(y), y)
+    # at most half a bfloat16 ulp (relative 2^-8) from the float value
+    f = x.astype(np.float32).astype(np.float64)
+    assert np.all(np.abs(y - f) <= np.abs(f) * 2.0**-8 * (1 + 1e-12))
