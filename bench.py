@@ -33,6 +33,28 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def measured_traffic(workload: str, dtype: str) -> dict:
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary, per kernel, only where the kernel's source file is
+    unchanged since the counters were taken (else None)."""
+    import glob
+    import hashlib
+    out = {}
+    for path in glob.glob(os.path.join(ROOT, "profiles", "hbm_traffic_*.json")):
+        try:
+            d = json.load(open(path))
+        except (OSError, ValueError):
+            continue
+        if d.get("workload") != workload or d.get("dtype") != dtype:
+            continue
+        for k, v in d.get("kernels", {}).items():
+            src = os.path.join(ROOT, v["source"])
+            ok = os.path.exists(src) and hashlib.sha256(
+                open(src, "rb").read()).hexdigest() == v["source_sha256"]
+            out[k] = v["bytes_per_launch"] if ok else None
+    return out
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -169,6 +191,12 @@ def main():
                      "frac": round(a / PEAK_HBM_GBS, 4),
                      "bytes_per_launch": kernels["spmm"]["work"],
                      "avg_launch_us": round(kernels["spmm"]["avg_launch_us"], 2)}
+
+    traffic = measured_traffic(name, dtype)
+    if traffic.get(dom) is not None:
+        roof["traffic"] = traffic[dom]
+    if roof_spmm is not None:
+        roof_spmm["traffic"] = traffic.get("spmm")
 
     out = {
         "metric": METRIC,

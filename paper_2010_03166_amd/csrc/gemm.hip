@@ -581,8 +581,23 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
   if (row >= g.M || col >= P.N) return;
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
   if (g.splits > 1) {
-    for (int sp = 0; sp < g.splits; ++sp) {
-      const float4 p = ld4(g.part + ((int64_t)sp * g.tiles + t) * (BM * BN) + e);
+    const float* src = g.part + (int64_t)t * (BM * BN) + e;
+    const int64_t st = (int64_t)g.tiles * (BM * BN);
+    int sp = 0;
+    for (; sp + 4 <= g.splits; sp += 4) {  // four partials in flight, in order
+      float4 p[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) p[u] = ld4(src + (sp + u) * st);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        v.x += p[u].x;
+        v.y += p[u].y;
+        v.z += p[u].z;
+        v.w += p[u].w;
+      }
+    }
+    for (; sp < g.splits; ++sp) {
+      const float4 p = ld4(src + sp * st);
       v.x += p.x;
       v.y += p.y;
       v.z += p.z;

@@ -48,7 +48,7 @@ struct PlanHeader {
 struct PlanDims {
   int32_t chunk;
   int64_t max_items, max_splits, max_slots;
-  size_t items_offset, splits_offset, bytes;
+  size_t items_offset, splits_offset, tot_offset, bytes;
 };
 PlanDims plan_dims(int32_t n, int64_t nnz);
 

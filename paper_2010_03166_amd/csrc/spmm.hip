@@ -35,14 +35,44 @@ PlanDims plan_dims(int32_t n, int64_t nnz) {
   d.max_slots = d.max_splits > 0 ? q + d.max_splits : 0;
   d.items_offset = round_up(sizeof(PlanHeader), 256);
   d.splits_offset = round_up(d.items_offset + 16 * (size_t)d.max_items, 256);
-  d.bytes = round_up(d.splits_offset + 16 * (size_t)(d.max_splits + 1), 256);
+  d.tot_offset = round_up(d.splits_offset + 16 * (size_t)(d.max_splits + 1), 256);
+  d.bytes = round_up(d.tot_offset + 12 * (size_t)(ceil_div(n, 2048) + 1), 256);
   return d;
 }
 
 // ----------------------------------------------------------- plan build
+//
+// Two passes over the row pointers, 2048 rows per block: the first counts
+// each block's items, split rows and partial slots; the second turns those
+// block totals into prefixes, scans within the block and writes the items.
 
-constexpr int PB_THREADS = 1024;
+constexpr int PB_THREADS = 256;
 constexpr int PB_ROWS = 8;
+constexpr int PB_BLOCK_ROWS = PB_THREADS * PB_ROWS;
+
+struct RowCounts {
+  int c[3];  // items, split rows, partial slots
+};
+
+__device__ inline RowCounts count_rows(const int32_t* __restrict__ indptr,
+                                       int32_t n, int32_t chunk, int64_t r0) {
+  RowCounts rc = {{0, 0, 0}};
+  for (int k = 0; k < PB_ROWS; ++k) {
+    const int64_t r = r0 + k;
+    if (r < n) {
+      const int d = indptr[r + 1] - indptr[r];
+      if (d > chunk) {
+        const int nch = (d + chunk - 1) / chunk;
+        rc.c[0] += nch;
+        rc.c[1] += 1;
+        rc.c[2] += nch;
+      } else {
+        rc.c[0] += 1;
+      }
+    }
+  }
+  return rc;
+}
 
 __device__ inline int wave_incl_scan(int x) {
   const int lane = threadIdx.x & 63;
@@ -55,7 +85,7 @@ __device__ inline int wave_incl_scan(int x) {
 }
 
 // Exclusive prefix sums of three counters over the block, plus totals.
-__device__ inline void block_scan3(int v[3], int excl[3], int tot[3],
+__device__ inline void block_scan3(const int v[3], int excl[3], int tot[3],
                                    int (*s_w)[3]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   constexpr int NW = PB_THREADS / 64;
@@ -65,14 +95,14 @@ __device__ inline void block_scan3(int v[3], int excl[3], int tot[3],
   if (lane == 63)
     for (int k = 0; k < 3; ++k) s_w[wave][k] = inc[k];
   __syncthreads();
-  if (wave == 0) {
-#pragma unroll
-    for (int k = 0; k < 3; ++k) {
-      const int x = lane < NW ? s_w[lane][k] : 0;
-      const int y = wave_incl_scan(x);
-      if (lane < NW) s_w[lane][k] = y - x;  // exclusive wave offsets
-      if (lane == NW - 1) s_w[NW][k] = y;   // block total
+  if (threadIdx.x < 3) {
+    int run = 0;
+    for (int w = 0; w < NW; ++w) {
+      const int x = s_w[w][threadIdx.x];
+      s_w[w][threadIdx.x] = run;
+      run += x;
     }
+    s_w[NW][threadIdx.x] = run;
   }
   __syncthreads();
 #pragma unroll
@@ -80,62 +110,59 @@ __device__ inline void block_scan3(int v[3], int excl[3], int tot[3],
     excl[k] = s_w[wave][k] + inc[k] - v[k];
     tot[k] = s_w[NW][k];
   }
-  __syncthreads();
 }
 
-__global__ __launch_bounds__(PB_THREADS) void plan_build_kernel(
+__global__ __launch_bounds__(PB_THREADS) void plan_count_kernel(
     const int32_t* __restrict__ indptr, int32_t n, int32_t chunk,
-    int4* __restrict__ items, int4* __restrict__ splits,
-    PlanHeader* __restrict__ hdr) {
+    int32_t* __restrict__ block_tot) {
   __shared__ int s_w[PB_THREADS / 64 + 1][3];
-  int carry[3] = {0, 0, 0};  // items, splits, slots
-  const int t = threadIdx.x;
-  for (int64_t base = 0; base < n; base += (int64_t)PB_THREADS * PB_ROWS) {
-    const int64_t r0 = base + (int64_t)t * PB_ROWS;
-    int cnt[3] = {0, 0, 0};
-    for (int k = 0; k < PB_ROWS; ++k) {
-      const int64_t r = r0 + k;
-      if (r < n) {
-        const int d = indptr[r + 1] - indptr[r];
-        if (d > chunk) {
-          const int nch = (d + chunk - 1) / chunk;
-          cnt[0] += nch;
-          cnt[1] += 1;
-          cnt[2] += nch;
-        } else {
-          cnt[0] += 1;
-        }
-      }
-    }
-    int off[3], tot[3];
-    block_scan3(cnt, off, tot, s_w);
-    int oi = carry[0] + off[0], os = carry[1] + off[1], ol = carry[2] + off[2];
-    for (int k = 0; k < PB_ROWS; ++k) {
-      const int64_t r = r0 + k;
-      if (r < n) {
-        const int b = indptr[r], e = indptr[r + 1], d = e - b;
-        if (d > chunk) {
-          const int nch = (d + chunk - 1) / chunk;
-          splits[os++] = make_int4((int)r, ol, nch, 0);
-          for (int c = 0; c < nch; ++c) {
-            const int cb = b + c * chunk;
-            const int ce = min(e, cb + chunk);
-            items[oi++] = make_int4((int)r, cb, ce, ol + c);
-          }
-          ol += nch;
-        } else {
-          items[oi++] = make_int4((int)r, b, e, -1);
-        }
-      }
-    }
-    for (int k = 0; k < 3; ++k) carry[k] += tot[k];
+  const int64_t r0 = (int64_t)blockIdx.x * PB_BLOCK_ROWS + threadIdx.x * PB_ROWS;
+  const RowCounts rc = count_rows(indptr, n, chunk, r0);
+  int excl[3], tot[3];
+  block_scan3(rc.c, excl, tot, s_w);
+  if (threadIdx.x == 0)
+    for (int k = 0; k < 3; ++k) block_tot[blockIdx.x * 3 + k] = tot[k];
+}
+
+__global__ __launch_bounds__(PB_THREADS) void plan_fill_kernel(
+    const int32_t* __restrict__ indptr, int32_t n, int32_t chunk,
+    const int32_t* __restrict__ block_tot, int4* __restrict__ items,
+    int4* __restrict__ splits, PlanHeader* __restrict__ hdr) {
+  __shared__ int s_w[PB_THREADS / 64 + 1][3];
+  __shared__ int s_pre[3];
+  if (threadIdx.x < 3) {  // prefix over the earlier blocks, in block order
+    int run = 0;
+    for (int b = 0; b < (int)blockIdx.x; ++b) run += block_tot[b * 3 + threadIdx.x];
+    s_pre[threadIdx.x] = run;
   }
-  if (t == 0) {
+  const int64_t r0 = (int64_t)blockIdx.x * PB_BLOCK_ROWS + threadIdx.x * PB_ROWS;
+  const RowCounts rc = count_rows(indptr, n, chunk, r0);
+  int excl[3], tot[3];
+  block_scan3(rc.c, excl, tot, s_w);  // its barriers also publish s_pre
+  int oi = s_pre[0] + excl[0], os = s_pre[1] + excl[1], ol = s_pre[2] + excl[2];
+  for (int k = 0; k < PB_ROWS; ++k) {
+    const int64_t r = r0 + k;
+    if (r < n) {
+      const int b = indptr[r], e = indptr[r + 1], d = e - b;
+      if (d > chunk) {
+        const int nch = (d + chunk - 1) / chunk;
+        splits[os++] = make_int4((int)r, ol, nch, 0);
+        for (int c = 0; c < nch; ++c) {
+          const int cb = b + c * chunk;
+          items[oi++] = make_int4((int)r, cb, min(e, cb + chunk), ol + c);
+        }
+        ol += nch;
+      } else {
+        items[oi++] = make_int4((int)r, b, e, -1);
+      }
+    }
+  }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
     PlanHeader h;
-    h.n_items = carry[0];
-    h.n_splits = carry[1];
+    h.n_items = s_pre[0] + tot[0];
+    h.n_splits = s_pre[1] + tot[1];
     h.chunk = chunk;
-    h.n_slots = carry[2];
+    h.n_slots = s_pre[2] + tot[2];
     h.n = n;
     h.pad[0] = h.pad[1] = h.pad[2] = 0;
     *hdr = h;
@@ -146,12 +173,15 @@ hipError_t plan_build_launch(int32_t n, int64_t nnz, const int32_t* indptr,
                              void* plan, hipStream_t s) {
   const PlanDims d = plan_dims(n, nnz);
   char* base = static_cast<char*>(plan);
+  const unsigned nb = (unsigned)std::max<int64_t>(1, ceil_div(n, PB_BLOCK_ROWS));
+  int32_t* tot = reinterpret_cast<int32_t*>(base + d.tot_offset);
   timer_begin(GNN_K_PLAN, s);
-  plan_build_kernel<<<1, PB_THREADS, 0, s>>>(
-      indptr, n, d.chunk, reinterpret_cast<int4*>(base + d.items_offset),
+  plan_count_kernel<<<nb, PB_THREADS, 0, s>>>(indptr, n, d.chunk, tot);
+  plan_fill_kernel<<<nb, PB_THREADS, 0, s>>>(
+      indptr, n, d.chunk, tot, reinterpret_cast<int4*>(base + d.items_offset),
       reinterpret_cast<int4*>(base + d.splits_offset),
       reinterpret_cast<PlanHeader*>(base));
-  timer_end(GNN_K_PLAN, 4.0 * (n + 1) + 16.0 * n, s);
+  timer_end(GNN_K_PLAN, 8.0 * (n + 1) + 16.0 * n, s);
   return hipGetLastError();
 }
 
@@ -466,8 +496,19 @@ __global__ __launch_bounds__(256) void spmm_reduce_kernel(SpmmArgs a) {
       const int col = c0 + (q * G + lane) * V::W;
       if (col < c_hi) {
         T acc = V::zero();
-        for (int k = 0; k < cnt; ++k)
-          V::add(acc, V::load(a.part + (int64_t)(first + k) * a.ldp + col));
+        const float* src = a.part + (int64_t)first * a.ldp + col;
+        int k = 0;
+        for (; k + 4 <= cnt; k += 4) {  // four partials in flight, added in order
+          const T x0 = V::load(src + (int64_t)(k + 0) * a.ldp);
+          const T x1 = V::load(src + (int64_t)(k + 1) * a.ldp);
+          const T x2 = V::load(src + (int64_t)(k + 2) * a.ldp);
+          const T x3 = V::load(src + (int64_t)(k + 3) * a.ldp);
+          V::add(acc, x0);
+          V::add(acc, x1);
+          V::add(acc, x2);
+          V::add(acc, x3);
+        }
+        for (; k < cnt; ++k) V::add(acc, V::load(src + (int64_t)k * a.ldp));
         spmm_epilogue<VEC>(a, row, col, acc);
       }
     }
