@@ -8,8 +8,12 @@
 // 128 x 128 output tile; each wavefront holds a 64 x 64 sub-tile as 2 x 2
 // MFMA accumulators (64 accumulator registers per lane).  K advances in
 // 32-deep slices staged through double-buffered LDS with one barrier per
-// slice; the global loads of slice k+1 are in flight while the matrix cores
-// consume slice k.
+// slice.  For interior tiles over full slices the loop is a three-stage
+// software pipeline in one basic block: while the matrix cores consume slice
+// k from one LDS stage, slice k+1 goes from registers into the other stage
+// and the global loads of slice k+2 are issued, interleaved with the MFMAs.
+// Edge tiles and partial slices take a guarded path with one slice of
+// register prefetch.
 //
 // LDS layouts follow the operand's storage so that every global float4 lands
 // in LDS as one float4 (no transposition on the way in):
@@ -127,8 +131,12 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
   constexpr bool B_KC = BT;   // B stored N x K: k contiguous
   constexpr int A_FLOATS = A_KC ? KC_FLOATS : XC_FLOATS;
   constexpr int B_FLOATS = B_KC ? KC_FLOATS : XC_FLOATS;
-  __shared__ __attribute__((aligned(16))) float As[2][A_FLOATS];
-  __shared__ __attribute__((aligned(16))) float Bs[2][B_FLOATS];
+  // Two LDS stages as separate arrays, so that the compiler sees that the
+  // stores into one stage never alias the fragment reads of the other.
+  __shared__ __attribute__((aligned(16))) float As0[A_FLOATS];
+  __shared__ __attribute__((aligned(16))) float As1[A_FLOATS];
+  __shared__ __attribute__((aligned(16))) float Bs0[B_FLOATS];
+  __shared__ __attribute__((aligned(16))) float Bs1[B_FLOATS];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -148,7 +156,6 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
     hi = block_lo(lb + 1, g.iters, g.nblocks);
   }
 
-  int buf = 0;
   int seg = 0;
   for (int64_t it = lo; it < hi; ++seg) {
     const int t = (int)(it / g.ktiles);
@@ -180,6 +187,7 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
     constexpr int BSTEP = B_KC ? 32 : 8;
 
     float4 ra[4], rb[4];
+    // Any slice: guarded loads, zeros outside the operands.
     auto load_slice = [&](int ks) {
       const bool s1 = ks >= kt0;
       const float* A = s1 ? A1p : A0p;
@@ -214,17 +222,36 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
                        : load4(B, ldb, k0 + bx + BSTEP * p, n0 + by, K, N, vb);
       }
     };
+    // A full slice of an interior tile: no guards, no branches.
+    auto load_full = [&](int ks) {
+      const bool s1 = ks >= kt0;
+      const float* A = s1 ? A1p : A0p;
+      const float* B = s1 ? B1p : B0p;
+      const int64_t lda = s1 ? lda1 : lda0;
+      const int64_t ldb = s1 ? ldb1 : ldb0;
+      const int k0 = (s1 ? ks - kt0 : ks) * BK;
+      const float* pa = A_KC ? A + (int64_t)(m0 + ax) * lda + (k0 + ay)
+                             : A + (int64_t)(k0 + ax) * lda + (m0 + ay);
+      const float* pb = B_KC ? B + (int64_t)(n0 + bx) * ldb + (k0 + by)
+                             : B + (int64_t)(k0 + bx) * ldb + (n0 + by);
+      const int64_t sa = ASTEP * lda, sb = BSTEP * ldb;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        ra[p] = ld4(pa + p * sa);
+        rb[p] = ld4(pb + p * sb);
+      }
+    };
     // LDS offsets (floats) of this thread's slice stores.
     auto sto_off = [&](bool kc, int x, int y, int p, int step) {
       if (kc) return (x + step * p) * KC_STRIDE + y;
       const int kk = x + step * p;
       return (((kk & 15) << 1) | (kk >> 4)) * XC_STRIDE + y;
     };
-    auto store_slice = [&](int bb) {
+    auto store_slice = [&](float* as, float* bs) {
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
-        *reinterpret_cast<float4*>(&As[bb][sto_off(A_KC, ax, ay, p, ASTEP)]) = ra[p];
-        *reinterpret_cast<float4*>(&Bs[bb][sto_off(B_KC, bx, by, p, BSTEP)]) = rb[p];
+        *reinterpret_cast<float4*>(&as[sto_off(A_KC, ax, ay, p, ASTEP)]) = ra[p];
+        *reinterpret_cast<float4*>(&bs[sto_off(B_KC, bx, by, p, BSTEP)]) = rb[p];
       }
     };
 
@@ -244,13 +271,7 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
     const int a_xc_base = lh * XC_STRIDE + wm * 64 + lr;
     const int b_xc_base = lh * XC_STRIDE + wn * 64 + lr;
 
-    load_slice(kbeg);
-    for (int ks = kbeg; ks < kend; ++ks) {
-      store_slice(buf);
-      __syncthreads();
-      if (ks + 1 < kend) load_slice(ks + 1);
-      const float* as = As[buf];
-      const float* bs = Bs[buf];
+    auto compute = [&](const float* as, const float* bs) {
       // Operands of step s are fetched one step (XC) or one group (KC)
       // ahead of the MFMAs that consume them.
       float4 af[2], bf[2], afn[2], bfn[2];
@@ -302,9 +323,80 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
         acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[0], acc[1][0], 0, 0, 0);
         acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[1], acc[1][1], 0, 0, 0);
       }
-      // let the scheduler interleave LDS reads with the MFMA chain
-      __builtin_amdgcn_iglp_opt(0);
-      buf ^= 1;
+    };
+
+    // One pipelined step over a full slice: store the next slice (already
+    // in registers) into the other stage, issue the global loads of the
+    // slice after it, compute on the current stage, then one barrier.  The
+    // three are one basic block, so the MFMAs interleave with the memory
+    // operations.  Near the end of the range the load repeats the last
+    // slice and the store fills the idle stage; neither is read again.
+    auto step = [&](const float* as, const float* bs, float* as_n, float* bs_n,
+                    int kl) {
+      store_slice(as_n, bs_n);
+      load_full(kl);
+      compute(as, bs);
+      // The stores go out with the first eight MFMAs, the loads with the
+      // next eight (a whole step ahead of the stores that consume them),
+      // and the fragment reads are spread over the rest.
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      }
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // MFMA
+      }
+      __syncthreads();
+    };
+
+    // Slices [kbeg, kf) are full and the tile is interior: pipelined path.
+    // Every section ends with a barrier, so the next one may write either
+    // stage.
+    int kf = kbeg;
+    if (a_in && b_in) {
+      const int f0 = K0 / BK, e1 = kt0 + K1 / BK;
+      if (kbeg < f0)
+        kf = min(kend, f0 == kt0 ? e1 : f0);
+      else if (kbeg >= kt0 && kbeg < e1)
+        kf = min(kend, e1);
+    }
+    if (kf > kbeg) {
+      load_full(kbeg);
+      store_slice(As0, Bs0);
+      load_full(min(kbeg + 1, kf - 1));
+      __syncthreads();
+      for (int k = kbeg; k < kf; k += 2) {
+        step(As0, Bs0, As1, Bs1, min(k + 2, kf - 1));
+        if (k + 1 >= kf) break;
+        step(As1, Bs1, As0, Bs0, min(k + 3, kf - 1));
+      }
+    }
+    // Remaining slices (edge tiles, partial slices): guarded loads, one
+    // slice in registers ahead.
+    if (kf < kend) {
+      int buf = 0;
+      load_slice(kf);
+      for (int ks = kf; ks < kend; ++ks) {
+        float* as = buf ? As1 : As0;
+        float* bs = buf ? Bs1 : Bs0;
+        store_slice(as, bs);
+        __syncthreads();
+        if (ks + 1 < kend) load_slice(ks + 1);
+        compute(as, bs);
+        __builtin_amdgcn_iglp_opt(0);
+        buf ^= 1;
+      }
+      __syncthreads();
     }
 
     // Accumulator layout of v_mfma_f32_32x32x2_f32: lane l, register r holds
