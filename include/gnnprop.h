@@ -69,7 +69,8 @@ typedef enum gnn_status {
  *                  indptr/indices, so the pattern must be symmetric
  *                  (undirected subgraph, Section 5.2).
  *   plan           device buffer written by gnn_csr_build_plan: the
- *                  degree-binned work list of the aggregation kernel. */
+ *                  aggregation kernel's work lists (packed short rows, long
+ *                  rows), a flagged copy of indices and each entry's row. */
 typedef struct gnn_csr {
   int32_t n;
   int64_t nnz;
@@ -113,8 +114,8 @@ int32_t gnn_choose_order(int32_t f_in, int32_t h);
  * must be symmetric with ascending indices per row (check with
  * gnn_csr_validate).  values_t is device memory of nnz floats.  If
  * csr->plan is non-NULL it must hold this graph's plan (gnn_csr_build_plan,
- * enqueued before), whose work items then spread long rows over many
- * wavefronts; with plan == NULL one wavefront handles each row. */
+ * enqueued before), whose per-entry rows then give one thread to each
+ * entry; with plan == NULL one wavefront handles each row. */
 gnn_status gnn_csr_transpose_values(const gnn_csr* csr, float* values_t,
                                     hipStream_t stream);
 
@@ -122,10 +123,11 @@ gnn_status gnn_csr_transpose_values(const gnn_csr* csr, float* values_t,
 size_t gnn_plan_bytes(int32_t n, int64_t nnz);
 
 /* Builds the aggregation work plan into `plan` (device memory of at least
- * gnn_plan_bytes(n, nnz) bytes): rows are binned by degree; a row with more
- * stored entries than the plan's chunk length is split into chunks whose
- * partial sums are combined in a fixed order, so results are deterministic.
- * Reads only csr->n, nnz and indptr. */
+ * gnn_plan_bytes(n, nnz) bytes).  Rows with at most 64 stored entries are
+ * packed into items (runs of consecutive rows whose first entries share a
+ * 64-entry window); longer rows are listed to be split across a whole
+ * workgroup, with the parts added in a fixed order, so results are
+ * deterministic.  Reads csr->n, nnz, indptr and indices. */
 gnn_status gnn_csr_build_plan(const gnn_csr* csr, void* plan,
                               size_t plan_bytes, hipStream_t stream);
 
@@ -186,8 +188,8 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
  *   out = A_s . in        (transpose = 0, uses csr->values)
  *   out = (A_s)^T . in    (transpose = 1, uses csr->values_t)
  * in and out are n x w with strides ld_in, ld_out; needs csr->plan;
- * `workspace` of gnn_spmm_workspace_bytes(csr, w) bytes (may be NULL if 0).
- * out must not overlap in. */
+ * `workspace` of gnn_spmm_workspace_bytes(csr, w) bytes (may be NULL if 0;
+ * the current kernel needs none and returns 0).  out must not overlap in. */
 size_t gnn_spmm_workspace_bytes(const gnn_csr* csr, int32_t w);
 gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
                     const float* in, int64_t ld_in, float* out,
@@ -209,8 +211,8 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
 /* ----------------------------------------------------- kernel timing */
 
 /* Kernels timed by the optional event timer. */
-#define GNN_K_SPMM 0          /* aggregation over work items */
-#define GNN_K_SPMM_REDUCE 1   /* chunk-partial reduction of long rows */
+#define GNN_K_SPMM 0          /* aggregation (one kernel per product) */
+#define GNN_K_SPMM_REDUCE 1   /* reserved: no separate reduction is launched */
 #define GNN_K_GEMM_NN 2       /* C = A B            (forward transforms) */
 #define GNN_K_GEMM_TN 3       /* C = A^T B          (weight gradients) */
 #define GNN_K_GEMM_NT 4       /* C = A B^T          (input gradients) */

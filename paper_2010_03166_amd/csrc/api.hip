@@ -60,7 +60,7 @@ size_t mat_bytes(int64_t rows, int64_t cols, int64_t ld) {
 struct LayerLayout {
   int order;
   int64_t ld_s, ld_p, ld_g, ld_gn, ld_v;
-  size_t off_buf0, off_buf1, off_spart, off_gemm, off_cs, total;
+  size_t off_buf0, off_buf1, off_gemm, off_cs, total;
 };
 
 int resolve_order(const gnn_layer* L) {
@@ -194,7 +194,6 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
     buf0 = (size_t)n * o.ld_g * 4;  // G
     buf1 = (size_t)n * o.ld_v * 4;  // V
   }
-  const int32_t w = o.order == 1 ? f_in : h;
   size_t gemm = 0;
   const int32_t bf = (L->flags & GNN_FLAG_BF16) ? 1 : 0;
   gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
@@ -202,8 +201,7 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dx_batch(o.order, n, f_in, h, 0, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
   o.off_buf0 = 0;
   o.off_buf1 = round_up(buf0, 256);
-  o.off_spart = o.off_buf1 + round_up(buf1, 256);
-  o.off_gemm = o.off_spart + spmm_partials_bytes(n, csr->nnz, w);
+  o.off_gemm = o.off_buf1 + round_up(buf1, 256);
   o.off_cs = o.off_gemm + round_up(gemm, 256);
   o.total = o.off_cs + colsum_partials_bytes(n, h);
   return o;
@@ -229,12 +227,12 @@ gnn_status check_layer(const gnn_layer* L) {
 }
 
 SpmmCall spmm_call(const gnn_csr* c, bool transpose, int32_t w,
-                   const float* in, int64_t ld_in, float* out, int64_t ld_out,
-                   float* partials) {
+                   const float* in, int64_t ld_in, float* out, int64_t ld_out) {
   SpmmCall s;
   memset(&s, 0, sizeof(s));
   s.n = c->n;
   s.nnz = c->nnz;
+  s.indptr = c->indptr;
   s.indices = c->indices;
   s.vals = transpose ? c->values_t : c->values;
   s.plan = c->plan;
@@ -244,7 +242,6 @@ SpmmCall spmm_call(const gnn_csr* c, bool transpose, int32_t w,
   s.out = out;
   s.ld_out = ld_out;
   s.epilogue = SPMM_STORE;
-  s.partials = partials;
   return s;
 }
 
@@ -317,7 +314,8 @@ gnn_status gnn_csr_build_plan(const gnn_csr* csr, void* plan,
   if (st != GNN_OK) return st;
   if (!plan) return GNN_ERR_NULL;
   if (plan_bytes < gnn_plan_bytes(csr->n, csr->nnz)) return GNN_ERR_WORKSPACE;
-  GNN_HIP(plan_build_launch(csr->n, csr->nnz, csr->indptr, plan, stream));
+  GNN_HIP(plan_build_launch(csr->n, csr->nnz, csr->indptr, csr->indices,
+                            plan, stream));
   return GNN_OK;
 }
 
@@ -362,8 +360,7 @@ gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
   if (ranges_overlap(in, mat_bytes(csr->n, w, ld_in), out,
                      mat_bytes(csr->n, w, ld_out)))
     return GNN_ERR_ALIAS;
-  SpmmCall c = spmm_call(csr, transpose != 0, w, in, ld_in, out, ld_out,
-                         static_cast<float*>(workspace));
+  SpmmCall c = spmm_call(csr, transpose != 0, w, in, ld_in, out, ld_out);
   GNN_HIP(spmm_launch(c, stream));
   return GNN_OK;
 }
@@ -458,12 +455,11 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
     return GNN_ERR_ALIAS;
 
   char* ws = static_cast<char*>(workspace);
-  float* spart = reinterpret_cast<float*>(ws + o.off_spart);
   void* gws = ws + o.off_gemm;
   const size_t gws_bytes = o.off_cs - o.off_gemm;
   if (o.order == 1) {
     float* S = static_cast<float*>(saved);
-    SpmmCall c = spmm_call(csr, false, f_in, X, layer->ld_x, S, o.ld_s, spart);
+    SpmmCall c = spmm_call(csr, false, f_in, X, layer->ld_x, S, o.ld_s);
     GNN_HIP(spmm_launch(c, stream));
     GemmBatch b = fwd_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, W_self,
                             W_neigh, b_self, b_neigh, Y, layer->ld_y, nullptr, 0);
@@ -475,7 +471,7 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
                             W_neigh, b_self, nullptr, Y, layer->ld_y, P, o.ld_p);
     b.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
-    SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y, spart);
+    SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y);
     c.epilogue = SPMM_BIAS_RELU;
     c.bias = b_neigh;
     GNN_HIP(spmm_launch(c, stream));
@@ -518,7 +514,6 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   char* ws = static_cast<char*>(workspace);
   float* buf0 = reinterpret_cast<float*>(ws + o.off_buf0);
   float* buf1 = reinterpret_cast<float*>(ws + o.off_buf1);
-  float* spart = reinterpret_cast<float*>(ws + o.off_spart);
   void* gws = ws + o.off_gemm;
   const size_t gws_bytes = o.off_cs - o.off_gemm;
   float* cspart = reinterpret_cast<float*>(ws + o.off_cs);
@@ -527,7 +522,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     float* GT = buf0;  // [G_s | T], n x ld_g
     float* Gn = buf1;  // G_n, n x ld_gn
     GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, GT, o.ld_g, Gn, o.ld_gn, stream));
-    SpmmCall c = spmm_call(csr, true, h, Gn, o.ld_gn, GT + h, o.ld_g, spart);
+    SpmmCall c = spmm_call(csr, true, h, Gn, o.ld_gn, GT + h, o.ld_g);
     GNN_HIP(spmm_launch(c, stream));
     GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, GT,
                             GT + h, o.ld_g, dW_self, dW_neigh);
@@ -557,7 +552,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
                               dX, layer->ld_dx, V, o.ld_v);
     bx.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
-      SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx, spart);
+      SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx);
       c.epilogue = SPMM_ADD;
       c.res = dX;
       c.ld_res = layer->ld_dx;

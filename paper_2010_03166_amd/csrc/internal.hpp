@@ -29,26 +29,25 @@ inline bool vec4_ok(const void* p, int64_t ld) {
 
 // ------------------------------------------------------------ work plan
 
-// Layout of the aggregation plan buffer (device memory):
-//   PlanHeader, then int4 items[max_items], then int4 splits[max_splits].
-// item  = {row, begin, end, slot}: the stored entries [begin,end) of `row`;
-//         slot < 0 -> the item covers the whole row and writes the output
-//         row; slot >= 0 -> partial sum written to partial row `slot`.
-// split = {row, first_slot, n_slots, 0}: a row cut into n_slots chunks whose
-//         partials are summed in slot order by the reduction kernel.
+// Layout of the aggregation plan buffer (device memory), at the offsets of
+// plan_dims():
+//   PlanHeader;
+//   int4 binfo[nblk]  per aggregation workgroup: rows [x, y) and their
+//                     entries [z, w); the rows whose first entry lies in
+//                     window [k, k+1) * block_entries;
+//   int32 erow[nnz]   row of each entry.
 struct PlanHeader {
-  int32_t n_items;
-  int32_t n_splits;
-  int32_t chunk;
-  int32_t n_slots;
+  int32_t nblk;
+  int32_t block_entries;
   int32_t n;
-  int32_t pad[3];
+  int32_t nnz;
+  int32_t pad[4];
 };
 
 struct PlanDims {
-  int32_t chunk;
-  int64_t max_items, max_splits, max_slots;
-  size_t items_offset, splits_offset, tot_offset, bytes;
+  int32_t block_entries;
+  int64_t nblk;
+  size_t binfo_offset, erow_offset, bytes;
 };
 PlanDims plan_dims(int32_t n, int64_t nnz);
 
@@ -70,6 +69,7 @@ enum SpmmEpilogue : int32_t {
 struct SpmmCall {
   int32_t n;
   int64_t nnz;
+  const int32_t* indptr;
   const int32_t* indices;
   const float* vals;
   const void* plan;
@@ -82,15 +82,14 @@ struct SpmmCall {
   const float* bias;
   const float* res;
   int64_t ld_res;
-  float* partials;  // workspace: max_slots x round_up(w,4) floats
 };
 size_t spmm_partials_bytes(int32_t n, int64_t nnz, int32_t w);
 hipError_t spmm_launch(const SpmmCall& c, hipStream_t s);
 
 hipError_t plan_build_launch(int32_t n, int64_t nnz, const int32_t* indptr,
-                             void* plan, hipStream_t s);
-// Uses the plan's work items when `plan` is non-null (built for this graph),
-// else one wavefront per row.
+                             const int32_t* indices, void* plan, hipStream_t s);
+// One thread per entry (rows from the plan) when `plan` is non-null (built
+// for this graph), else one wavefront per row.
 hipError_t transpose_values_launch(int32_t n, int64_t nnz,
                                    const int32_t* indptr,
                                    const int32_t* indices, const float* vals,

@@ -61,7 +61,7 @@ def prepared(csr) -> runtime.DeviceGraph:
 def read_plan(g: runtime.DeviceGraph):
     raw = g.plan.cpu().numpy().view(np.int32)
     hdr = raw[:8]
-    # offsets must match plan_dims(): header rounded to 256 B, items, splits
+    # the header's first four words: items, long rows, chunk, n
     return hdr, raw
 
 

@@ -70,7 +70,8 @@ def test_order_rule_agrees_with_oracle(lib, f_in, h):
 
 def test_plan_bytes_monotone(lib):
     a = G.gnn_plan_bytes(1000, 10000)
-    assert a > 0 and G.gnn_plan_bytes(2000, 10000) > a
+    assert a >= 4 * 10000  # the row of every entry
+    assert G.gnn_plan_bytes(2000, 10000) >= a
     assert G.gnn_plan_bytes(1000, 100000) > a
     assert G.gnn_plan_bytes(0, 0) > 0
     assert G.gnn_plan_bytes(-1, 0) == 0
@@ -94,7 +95,7 @@ def test_size_queries(lib):
     assert G.gnn_prop_saved_bytes(c, auto) == 0  # 602 > 512: order 2
     assert G.gnn_gemm_workspace_bytes(8000, 1024, 602) == 0
     assert G.gnn_gemm_workspace_bytes(602, 512, 8000) > 0  # split along K
-    assert G.gnn_spmm_workspace_bytes(c, 512) > 0
+    assert G.gnn_spmm_workspace_bytes(c, 512) == 0  # one kernel, no partials
 
 
 def _st(fn, *args):

@@ -6,7 +6,6 @@ results must agree to max |gpu - oracle| / max |oracle| <= 1e-4 per tensor
 is held to 1e-5; the transposed value array and the work plan are checked
 bit for bit.
 """
-import math
 
 import numpy as np
 import pytest
@@ -25,8 +24,29 @@ TOL = 1e-4
 TOL_SPMM = 1e-5
 
 
+def boundary_graph():
+    """Rows of every kind the aggregation plan distinguishes, side by side:
+    empty rows, rows of exactly 64 and 65 entries (the long-row threshold),
+    long rows next to short ones, and short rows straddling 64-entry
+    windows; random values (asymmetric), no self loops."""
+    rng = np.random.default_rng(11)
+    e = [(3, v) for v in range(100, 164)]            # row 3: 64 entries
+    e += [(4, v) for v in range(200, 265)]           # row 4: 65 entries
+    e += [(10, v) for v in range(100, 400) if v != 10]  # a long row
+    e += [(11, v) for v in range(300, 380)]          # adjacent long row
+    for u in range(20, 60):                          # short rows
+        for v in rng.choice(np.arange(20, 60), size=3, replace=False):
+            if u < v:
+                e.append((u, int(v)))
+    # rows 70..89 stay empty
+    e = np.unique(np.array([(min(a, b), max(a, b)) for a, b in e]), axis=0)
+    return synth.symmetric_csr(400, e, self_loops=False, values="random",
+                               rng=np.random.default_rng(12))
+
+
 def graphs():
     return {
+        "boundary": boundary_graph(),
         "path4": synth.path_graph(4),
         "random": synth.random_graph(300, 6.0, 1, values="random"),
         "powerlaw": synth.power_law_graph(3000, 2.1, 12.0, seed=2),
@@ -66,37 +86,37 @@ def test_transpose_values_without_plan(name):
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
 
 
-@pytest.mark.parametrize("name", ["powerlaw", "star700", "no_self_loops", "single"])
-def test_plan_covers_every_entry_once(name):
+def _ru(x, m=256):
+    return (x + m - 1) // m * m
+
+
+@pytest.mark.parametrize("name", ["powerlaw", "star700", "no_self_loops", "single",
+                                  "random", "boundary"])
+def test_plan_exact(name):
     g = GRAPHS[name]
     dg = prepared(g)
     torch.cuda.synchronize()
     hdr, raw = read_plan(dg)
-    n_items, n_splits, chunk, n_slots, n = [int(v) for v in hdr[:5]]
-    assert n == g.n
-    items = raw[64: 64 + 4 * n_items].reshape(-1, 4).astype(np.int64)
-    max_items = g.n + math.ceil(g.nnz / chunk)
-    so = ((256 + 16 * max_items + 255) // 256) * 256 // 4
-    splits = raw[so: so + 4 * n_splits].reshape(-1, 4).astype(np.int64)
-    deg = g.degrees()
-    # exact expected plan, derived from the degrees alone
-    exp_items, exp_splits, slot = [], [], 0
-    for r in range(g.n):
-        b, e = int(g.indptr[r]), int(g.indptr[r + 1])
-        if e - b > chunk:
-            k = (e - b + chunk - 1) // chunk
-            exp_splits.append((r, slot, k, 0))
-            for c in range(k):
-                exp_items.append((r, b + c * chunk, min(e, b + (c + 1) * chunk), slot + c))
-            slot += k
-        else:
-            exp_items.append((r, b, e, -1))
-    assert n_items == len(exp_items) and n_splits == len(exp_splits)
-    assert n_slots == slot
-    assert np.array_equal(items, np.array(exp_items, np.int64).reshape(-1, 4))
-    if exp_splits:
-        assert np.array_equal(splits, np.array(exp_splits, np.int64))
-    assert (deg > chunk).sum() == n_splits
+    nblk, be, n, nnz = [int(v) for v in hdr[:4]]
+    assert (n, nnz) == (g.n, g.nnz)
+    assert be >= 64 and be & (be - 1) == 0
+    assert nblk == max(1, -(-g.nnz // be))
+    # window table right after the 256-byte header, then the entry rows
+    binfo = raw[64: 64 + 4 * nblk].reshape(-1, 4).astype(np.int64)
+    off_erow = _ru(256 + 16 * nblk)
+    erow = raw[off_erow // 4: off_erow // 4 + g.nnz]
+    ip = g.indptr.astype(np.int64)
+    deg = np.diff(ip)
+    # workgroup k owns the rows whose first entry is in window k (the last
+    # one also the trailing empty rows): derived from the row pointers alone
+    lo = [int(np.searchsorted(ip, k * be, side="left")) for k in range(nblk)] + [g.n]
+    exp = np.array([(lo[k], lo[k + 1], ip[lo[k]], ip[lo[k + 1]]) for k in range(nblk)],
+                   np.int64)
+    assert np.array_equal(binfo, exp)
+    # the windows partition rows and entries
+    assert binfo[0, 0] == 0 and binfo[-1, 1] == g.n and binfo[-1, 3] == g.nnz
+    assert (binfo[1:, 0] == binfo[:-1, 1]).all() and (binfo[1:, 2] == binfo[:-1, 3]).all()
+    assert np.array_equal(erow, np.repeat(np.arange(g.n), deg))
 
 
 # ---------------------------------------------------------------- aggregation
@@ -105,7 +125,7 @@ WIDTHS = [1, 3, 16, 50, 64, 128, 200, 300, 512, 1024, 1030]
 
 
 @pytest.mark.parametrize("name", ["powerlaw", "star700", "no_self_loops",
-                                  "identity", "random"])
+                                  "identity", "random", "boundary"])
 @pytest.mark.parametrize("w", WIDTHS)
 @pytest.mark.parametrize("transpose", [0, 1])
 @pytest.mark.parametrize("layout", ["aligned", "unaligned"])
