@@ -57,6 +57,15 @@ typedef enum gnn_status {
 /* Layer flags. */
 #define GNN_FLAG_BF16 0x1u /* GEMM operands rounded to bf16 (round to nearest
                               even), fp32 accumulation; aggregation stays fp32 */
+/* Backward pass only (Algorithm 1's layer loop, backward direction): the
+ * layers of a stack share their ReLU masks.  Layer l's input X is layer
+ * l-1's output, so 1[X > 0] is layer l-1's mask and can be applied where
+ * layer l produces dX; layer l-1 then receives its G directly. */
+#define GNN_FLAG_DY_MASKED 0x2u /* dY is already G = dY * 1[Y > 0]: no
+                                   masking pass, dY is read in place */
+#define GNN_FLAG_DX_MASKED 0x4u /* dX is written as dX * 1[X > 0] (selected,
+                                   not multiplied), i.e. the next layer
+                                   down's G when X is that layer's output */
 
 /* The sampled subgraph's adjacency A_s in CSR (Section 5.2: Indptr,
  * Indices, Data).  All arrays are device memory.
@@ -170,6 +179,8 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
  *   dX       = G[:, 0:h] W_self^T + (A_s)^T G[:, h:2h] W_neigh^T
  *   db_self, db_neigh = column sums of the two halves of G
  * dX may be NULL (not computed; e.g. the first layer).  db_* may be NULL.
+ * layer->flags may add GNN_FLAG_DY_MASKED (dY already masked) and
+ * GNN_FLAG_DX_MASKED (dX returned masked by 1[X > 0]).
  * Needs csr->values, csr->values_t and csr->plan, and the `saved` buffer of
  * the matching gnn_prop_fwd call with the same layer (same order).  Outputs
  * must not overlap inputs. */

@@ -109,8 +109,8 @@ GemmBatch fwd_batch(int order, int32_t n, int32_t f_in, int32_t h,
 // dW_self = X^T G_s ; dW_neigh = (order 1: S, order 2: X)^T (G_n or T)
 GemmBatch dw_batch(int order, int32_t n, int32_t f_in, int32_t h,
                    const float* X, int64_t ld_x, const float* S, int64_t ld_s,
-                   const float* Gs, const float* Gn, int64_t ld_g,
-                   float* dWs, float* dWn) {
+                   const float* Gs, int64_t ld_gs, const float* Gn,
+                   int64_t ld_gn, float* dWs, float* dWn) {
   GemmBatch b;
   memset(&b, 0, sizeof(b));
   b.nprob = 2;
@@ -125,12 +125,12 @@ GemmBatch dw_batch(int order, int32_t n, int32_t f_in, int32_t h,
     p.relu = 0;
     p.bias = nullptr;
   }
-  b.p[0].seg[0] = {X, Gs, ld_x, ld_g, n};
+  b.p[0].seg[0] = {X, Gs, ld_x, ld_gs, n};
   b.p[0].C = dWs;
   if (order == 1)
-    b.p[1].seg[0] = {S, Gn, ld_s, ld_g, n};
+    b.p[1].seg[0] = {S, Gn, ld_s, ld_gn, n};
   else
-    b.p[1].seg[0] = {X, Gn, ld_x, ld_g, n};
+    b.p[1].seg[0] = {X, Gn, ld_x, ld_gn, n};
   b.p[1].C = dWn;
   return b;
 }
@@ -138,9 +138,9 @@ GemmBatch dw_batch(int order, int32_t n, int32_t f_in, int32_t h,
 // order 2: dX = G_s W_s^T + T W_n^T (one problem, two K parts)
 // order 1: dX = G_s W_s^T ; V = G_n W_n^T
 GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
-                   const float* Gs, const float* Gn, int64_t ld_g,
-                   const float* Ws, const float* Wn, float* dX, int64_t ld_dx,
-                   float* V, int64_t ld_v) {
+                   const float* Gs, int64_t ld_gs, const float* Gn,
+                   int64_t ld_gn, const float* Ws, const float* Wn, float* dX,
+                   int64_t ld_dx, float* V, int64_t ld_v) {
   GemmBatch b;
   memset(&b, 0, sizeof(b));
   b.trans_a = 0;
@@ -149,8 +149,8 @@ GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
     b.nprob = 1;
     GemmProblem& p = b.p[0];
     p.nseg = 2;
-    p.seg[0] = {Gs, Ws, ld_g, h, h};
-    p.seg[1] = {Gn, Wn, ld_g, h, h};
+    p.seg[0] = {Gs, Ws, ld_gs, h, h};
+    p.seg[1] = {Gn, Wn, ld_gn, h, h};
     p.M = n;
     p.N = f_in;
     p.C = dX;
@@ -162,10 +162,10 @@ GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
       b.p[i].M = n;
       b.p[i].N = f_in;
     }
-    b.p[0].seg[0] = {Gs, Ws, ld_g, h, h};
+    b.p[0].seg[0] = {Gs, Ws, ld_gs, h, h};
     b.p[0].C = dX;
     b.p[0].ldc = ld_dx;
-    b.p[1].seg[0] = {Gn, Wn, ld_g, h, h};
+    b.p[1].seg[0] = {Gn, Wn, ld_gn, h, h};
     b.p[1].C = V;
     b.p[1].ldc = ld_v;
   }
@@ -197,8 +197,8 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   size_t gemm = 0;
   const int32_t bf = (L->flags & GNN_FLAG_BF16) ? 1 : 0;
   gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
-  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
-  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dx_batch(o.order, n, f_in, h, 0, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
+  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 2 * h, 0, 2 * h, 0, 0), bf)));
+  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dx_batch(o.order, n, f_in, h, 0, 2 * h, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
   o.off_buf0 = 0;
   o.off_buf1 = round_up(buf0, 256);
   o.off_gemm = o.off_buf1 + round_up(buf1, 256);
@@ -222,7 +222,8 @@ gnn_status check_layer(const gnn_layer* L) {
   if (L->f_in <= 0 || L->h <= 0) return GNN_ERR_SHAPE;
   if (L->ld_x < L->f_in || L->ld_y < 2 * (int64_t)L->h) return GNN_ERR_SHAPE;
   if (L->order < 0 || L->order > 2) return GNN_ERR_SHAPE;
-  if (L->flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  if (L->flags & ~(GNN_FLAG_BF16 | GNN_FLAG_DY_MASKED | GNN_FLAG_DX_MASKED))
+    return GNN_ERR_UNSUPPORTED;
   return GNN_OK;
 }
 
@@ -518,50 +519,85 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   const size_t gws_bytes = o.off_cs - o.off_gemm;
   float* cspart = reinterpret_cast<float*>(ws + o.off_cs);
 
+  const int32_t bf = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
+  const bool dy_masked = (layer->flags & GNN_FLAG_DY_MASKED) != 0;
+  // dX masked by 1[X > 0]: the next layer down's G, in the epilogue that
+  // writes the final dX
+  const float* dx_mask = (layer->flags & GNN_FLAG_DX_MASKED) ? X : nullptr;
   if (o.order == 2) {
-    float* GT = buf0;  // [G_s | T], n x ld_g
-    float* Gn = buf1;  // G_n, n x ld_gn
-    GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, GT, o.ld_g, Gn, o.ld_gn, stream));
-    SpmmCall c = spmm_call(csr, true, h, Gn, o.ld_gn, GT + h, o.ld_g);
+    // G_s and G_n: dY itself when already masked, else a masking pass
+    // writes them into [G_s | T] (n x ld_g) and G_n (n x ld_gn).
+    const float *Gs, *Gn;
+    int64_t ld_gs, ld_gn;
+    float* T;
+    int64_t ld_t;
+    if (dy_masked) {
+      Gs = dY;
+      Gn = dY + h;
+      ld_gs = ld_gn = layer->ld_y;
+      T = buf1;
+      ld_t = o.ld_gn;
+    } else {
+      float* GT = buf0;
+      float* G_n = buf1;
+      GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, GT, o.ld_g, G_n, o.ld_gn, stream));
+      Gs = GT;
+      ld_gs = o.ld_g;
+      Gn = G_n;
+      ld_gn = o.ld_gn;
+      T = GT + h;
+      ld_t = o.ld_g;
+    }
+    SpmmCall c = spmm_call(csr, true, h, Gn, ld_gn, T, ld_t);
     GNN_HIP(spmm_launch(c, stream));
-    GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, GT,
-                            GT + h, o.ld_g, dW_self, dW_neigh);
-    bw.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
+    GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, Gs,
+                            ld_gs, T, ld_t, dW_self, dW_neigh);
+    bw.bf16 = bf;
     GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
     if (dX) {
-      GemmBatch bx = dx_batch(2, n, f_in, h, GT, GT + h, o.ld_g, W_self,
+      GemmBatch bx = dx_batch(2, n, f_in, h, Gs, ld_gs, T, ld_t, W_self,
                               W_neigh, dX, layer->ld_dx, nullptr, 0);
-    bx.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
+      bx.bf16 = bf;
+      bx.p[0].mask = dx_mask;
+      bx.p[0].ld_mask = layer->ld_x;
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
     }
-    if (db_self || db_neigh) {
-      if (db_self) GNN_HIP(colsum_launch(n, h, GT, o.ld_g, db_self, cspart, stream));
-      if (db_neigh) GNN_HIP(colsum_launch(n, h, Gn, o.ld_gn, db_neigh, cspart, stream));
-    }
+    if (db_self) GNN_HIP(colsum_launch(n, h, Gs, ld_gs, db_self, cspart, stream));
+    if (db_neigh) GNN_HIP(colsum_launch(n, h, Gn, ld_gn, db_neigh, cspart, stream));
   } else {
-    float* G = buf0;  // [G_s | G_n], n x ld_g
+    const float* G;  // [G_s | G_n]
+    int64_t ld_g;
+    if (dy_masked) {
+      G = dY;
+      ld_g = layer->ld_y;
+    } else {
+      float* Gm = buf0;
+      GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, Gm, o.ld_g, Gm + h, o.ld_g, stream));
+      G = Gm;
+      ld_g = o.ld_g;
+    }
     float* V = buf1;  // G_n W_n^T, n x ld_v
     const float* S = static_cast<const float*>(saved);
-    GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, G, o.ld_g, G + h, o.ld_g, stream));
-    GemmBatch bw = dw_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, G, G + h,
-                            o.ld_g, dW_self, dW_neigh);
-    bw.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
+    GemmBatch bw = dw_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, G, ld_g,
+                            G + h, ld_g, dW_self, dW_neigh);
+    bw.bf16 = bf;
     GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
     if (dX) {
-      GemmBatch bx = dx_batch(1, n, f_in, h, G, G + h, o.ld_g, W_self, W_neigh,
-                              dX, layer->ld_dx, V, o.ld_v);
-    bx.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
+      GemmBatch bx = dx_batch(1, n, f_in, h, G, ld_g, G + h, ld_g, W_self,
+                              W_neigh, dX, layer->ld_dx, V, o.ld_v);
+      bx.bf16 = bf;
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
+      // dX = G_s W_s^T + A_s^T V, then the mask, in the aggregation epilogue
       SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx);
       c.epilogue = SPMM_ADD;
       c.res = dX;
       c.ld_res = layer->ld_dx;
+      c.mask = dx_mask;
+      c.ld_mask = layer->ld_x;
       GNN_HIP(spmm_launch(c, stream));
     }
-    if (db_self || db_neigh) {
-      if (db_self) GNN_HIP(colsum_launch(n, h, G, o.ld_g, db_self, cspart, stream));
-      if (db_neigh) GNN_HIP(colsum_launch(n, h, G + h, o.ld_g, db_neigh, cspart, stream));
-    }
+    if (db_self) GNN_HIP(colsum_launch(n, h, G, ld_g, db_self, cspart, stream));
+    if (db_neigh) GNN_HIP(colsum_launch(n, h, G + h, ld_g, db_neigh, cspart, stream));
   }
   return GNN_OK;
 }

@@ -125,6 +125,60 @@ __device__ inline TileInfo tile_info(const GemmKArgs& g, int t) {
   return ti;
 }
 
+// Writes a wavefront's 64 x 64 accumulators (layout of the 32 x 32 MFMAs:
+// lane l, register r holds row 8*(r/4) + 4*(l/32) + r%4 and column l%32 of a
+// block): straight to C with bias, ReLU and mask when the block covered the
+// whole K range, else to its partial tile.  Interior tiles take a path
+// without per-element guards, so the mask loads go out sixteen at a time.
+__device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
+                                 int M, const floatx16 (&acc)[2][2],
+                                 bool whole, float* part, int wm, int wn,
+                                 int lr, int lh) {
+  const int N = P.N;
+  const bool interior = ti.m0 + BM <= M && ti.n0 + BN <= N;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int cl = wn * 64 + j * 32 + lr;
+      const int col = ti.n0 + cl;
+      const int rl0 = wm * 64 + i * 32 + lh * 4;
+      if (!whole) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          part[(rl0 + (r >> 2) * 8 + (r & 3)) * BN + cl] = acc[i][j][r];
+      } else if (interior) {
+        const float bc = P.bias ? P.bias[col] : 0.f;
+        float mv[16];
+        if (P.mask) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            mv[r] = P.mask[(int64_t)(ti.m0 + rl0 + (r >> 2) * 8 + (r & 3)) * P.ld_mask + col];
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = ti.m0 + rl0 + (r >> 2) * 8 + (r & 3);
+          float v = acc[i][j][r] + bc;
+          if (P.relu) v = fmaxf(v, 0.f);
+          if (P.mask && !(mv[r] > 0.f)) v = 0.f;
+          P.C[(int64_t)row * P.ldc + col] = v;
+        }
+      } else {
+        const float bc = (P.bias && col < N) ? P.bias[col] : 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = ti.m0 + rl0 + (r >> 2) * 8 + (r & 3);
+          if (row < M && col < N) {
+            float v = acc[i][j][r] + bc;
+            if (P.relu) v = fmaxf(v, 0.f);
+            if (P.mask && !(P.mask[(int64_t)row * P.ld_mask + col] > 0.f)) v = 0.f;
+            P.C[(int64_t)row * P.ldc + col] = v;
+          }
+        }
+      }
+    }
+}
+
 template <bool AT, bool BT>
 __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
   constexpr bool A_KC = !AT;  // A row-major M x K: k contiguous
@@ -399,35 +453,11 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
       __syncthreads();
     }
 
-    // Accumulator layout of v_mfma_f32_32x32x2_f32: lane l, register r holds
-    // row 8*(r/4) + 4*(l/32) + r%4 and column l%32 of the 32 x 32 block.
     const bool whole = kbeg == 0 && kend == g.ktiles;
     float* part = g.part + (g.splits > 1 ? (int64_t)lb
                                          : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
                                (BM * BN);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int cl = wn * 64 + j * 32 + lr;
-        const int col = ti.n0 + cl;
-        const float bc = (whole && P.bias && col < N) ? P.bias[col] : 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int rl = wm * 64 + i * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
-          const int row = ti.m0 + rl;
-          float v = acc[i][j][r];
-          if (whole) {
-            if (row < M && col < N) {
-              v += bc;
-              if (P.relu) v = fmaxf(v, 0.f);
-              P.C[(int64_t)row * P.ldc + col] = v;
-            }
-          } else {
-            part[rl * BN + cl] = v;
-          }
-        }
-      }
+    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh);
   }
 }
 
@@ -625,29 +655,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
     float* part = g.part + (g.splits > 1 ? (int64_t)lb
                                          : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
                                (BM * BN);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int cl = wn * 64 + j * 32 + lr;
-        const int col = n0 + cl;
-        const float bc = (whole && P.bias && col < N) ? P.bias[col] : 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int rl = wm * 64 + i * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
-          const int row = m0 + rl;
-          float v = acc[i][j][r];
-          if (whole) {
-            if (row < M && col < N) {
-              v += bc;
-              if (P.relu) v = fmaxf(v, 0.f);
-              P.C[(int64_t)row * P.ldc + col] = v;
-            }
-          } else {
-            part[rl * BN + cl] = v;
-          }
-        }
-      }
+    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh);
   }
 }
 
@@ -714,6 +722,7 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
     float x = o[u];
     if (P.bias) x += P.bias[col + u];
     if (P.relu) x = fmaxf(x, 0.f);
+    if (P.mask && !(P.mask[(int64_t)row * P.ld_mask + col + u] > 0.f)) x = 0.f;
     dst[u] = x;
   }
 }

@@ -64,7 +64,7 @@ enum SpmmEpilogue : int32_t {
   SPMM_STORE = 0,      // out = acc
   SPMM_BIAS_RELU = 1,  // out = max(acc + bias[c], 0)   (bias may be null)
   SPMM_ADD = 2,        // out = acc + res[row, c]         (res may alias out)
-};
+};                     // with `mask` set: out = mask[row, c] > 0 ? out : 0
 
 struct SpmmCall {
   int32_t n;
@@ -82,6 +82,8 @@ struct SpmmCall {
   const float* bias;
   const float* res;
   int64_t ld_res;
+  const float* mask;
+  int64_t ld_mask;
 };
 size_t spmm_partials_bytes(int32_t n, int64_t nnz, int32_t w);
 hipError_t spmm_launch(const SpmmCall& c, hipStream_t s);
@@ -117,6 +119,8 @@ struct GemmProblem {
   int64_t ldc;
   const float* bias;
   int32_t relu;
+  const float* mask;  // if set: C = mask[r, c] > 0 ? C : 0 (after bias/ReLU)
+  int64_t ld_mask;
 };
 struct GemmBatch {
   GemmProblem p[2];

@@ -243,6 +243,8 @@ struct SpmmArgs {
   const float* bias;
   const float* res;
   int64_t ld_res;
+  const float* mask;
+  int64_t ld_mask;
   int32_t nslices;  // column slices (blocks b with b % nslices == q own slice q)
   int32_t sw;       // slice width in columns
 };
@@ -292,6 +294,14 @@ struct Vec<true> {
     v.w = fmaxf(v.w, 0.f);
     return v;
   }
+  // v where m > 0, else 0 (a selection: NaN or infinite v is not spread)
+  __device__ static T select_pos(T m, T v) {
+    v.x = m.x > 0.f ? v.x : 0.f;
+    v.y = m.y > 0.f ? v.y : 0.f;
+    v.z = m.z > 0.f ? v.z : 0.f;
+    v.w = m.w > 0.f ? v.w : 0.f;
+    return v;
+  }
 };
 template <>
 struct Vec<false> {
@@ -303,6 +313,7 @@ struct Vec<false> {
   __device__ static void fma(T& acc, float a, T x) { acc = fmaf(a, x, acc); }
   __device__ static void add(T& acc, T x) { acc += x; }
   __device__ static T relu(T v) { return fmaxf(v, 0.f); }
+  __device__ static T select_pos(T m, T v) { return m > 0.f ? v : 0.f; }
 };
 
 template <int G, int D, bool VEC, int EPI, bool OFF32>
@@ -347,6 +358,7 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
         acc = V::relu(acc);
       } else if (EPI == SPMM_ADD) {
         V::add(acc, V::load(a.res + (int64_t)row * a.ld_res + col));
+        if (a.mask) acc = V::select_pos(V::load(a.mask + (int64_t)row * a.ld_mask + col), acc);
       }
       V::store(a.out + (int64_t)row * a.ld_out + col, acc);
     };
@@ -452,6 +464,7 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
               v = fmaxf(a.bias ? a.bias[c] : 0.f, 0.f);
             } else if (EPI == SPMM_ADD) {
               v = a.res[(int64_t)r * a.ld_res + c];
+              if (a.mask && !(a.mask[(int64_t)r * a.ld_mask + c] > 0.f)) v = 0.f;
             }
             a.out[(int64_t)r * a.ld_out + c] = v;
           }
@@ -528,12 +541,15 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   a.bias = c.bias;
   a.res = c.res;
   a.ld_res = c.ld_res;
+  a.mask = c.mask;
+  a.ld_mask = c.ld_mask;
   a.nslices = c.w >= 256 ? 8 : 1;
   a.sw = (int32_t)round_up(ceil_div(c.w, a.nslices), 4);
   const bool vec = (c.w % 4 == 0) && vec4_ok(c.in, c.ld_in) &&
                    vec4_ok(c.out, c.ld_out) &&
                    (c.epilogue != SPMM_BIAS_RELU || !c.bias || aligned16(c.bias)) &&
-                   (c.epilogue != SPMM_ADD || vec4_ok(c.res, c.ld_res));
+                   (c.epilogue != SPMM_ADD || vec4_ok(c.res, c.ld_res)) &&
+                   (!c.mask || vec4_ok(c.mask, c.ld_mask));
   // Gather offsets in 32 bits when the input spans less than 4 GiB.
   const bool off32 = ((int64_t)(c.n - 1) * c.ld_in + c.w) * 4 < (int64_t(1) << 32);
   timer_begin(GNN_K_SPMM, s);

@@ -18,6 +18,8 @@ LIB_PATH = os.path.join(PKG, "libgnnprop.so")
 
 GNN_OK = 0
 GNN_FLAG_BF16 = 0x1
+GNN_FLAG_DY_MASKED = 0x2
+GNN_FLAG_DX_MASKED = 0x4
 KERNELS = {"spmm": 0, "spmm_reduce": 1, "gemm_nn": 2, "gemm_tn": 3,
            "gemm_nt": 4, "gemm_tt": 5, "gemm_reduce": 6, "mask": 7,
            "colsum": 8, "plan": 9, "transpose": 10}

@@ -65,10 +65,18 @@ class SageStack:
 
     def __init__(self, graph: DeviceGraph, params: Sequence, f_in: int,
                  order: int = 0, flags: int = 0, pad: int = 16,
-                 device: str = "cuda"):
+                 fuse_masks: bool = False, device: str = "cuda"):
+        """fuse_masks: in the backward pass layer l > 0 writes its dX already
+        masked by its input's sign (the ReLU mask of layer l - 1), which layer
+        l - 1 then takes as its masked dY, so no separate masking pass runs
+        below the top layer.  The dX buffers of layers l > 0 then hold those
+        masked gradients; the first layer's dX is always the plain one.  Off
+        by default: the mask read lands in the tail of the dX product, where
+        it costs about what the masking pass it replaces does."""
         self.g = graph
         self.n = graph.n
         self.order, self.flags, self.pad = order, flags, pad
+        self.fuse_masks = fuse_masks
         self.layers = []
         f = f_in
         ws_bytes = 0
@@ -102,11 +110,11 @@ class SageStack:
         self.workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=device)
         self.inputs: List[Optional[torch.Tensor]] = [None] * len(self.layers)
 
-    def _layer(self, i: int, ld_x: int) -> G.gnn_layer:
+    def _layer(self, i: int, ld_x: int, extra_flags: int = 0) -> G.gnn_layer:
         L = self.layers[i]
         return G.make_layer(L["f_in"], L["h"], ld_x, L["Y"].stride(0) if self.n else 2 * L["h"],
                             L["dX"].stride(0) if self.n else L["f_in"], self.order,
-                            self.flags)
+                            self.flags | extra_flags)
 
     def forward(self, X: torch.Tensor, stream=None) -> torch.Tensor:
         csr = self.g.struct()
@@ -127,7 +135,13 @@ class SageStack:
             L = self.layers[i]
             x = self.inputs[i]
             ld_x = x.stride(0) if self.n else L["f_in"]
-            lay = self._layer(i, ld_x)
+            extra = 0
+            if self.fuse_masks:
+                if i < len(self.layers) - 1:
+                    extra |= G.GNN_FLAG_DY_MASKED
+                if i > 0:
+                    extra |= G.GNN_FLAG_DX_MASKED
+            lay = self._layer(i, ld_x, extra)
             # the upstream gradient must share Y's row stride
             if self.n and d.stride(0) != L["Y"].stride(0):
                 d = padded(d.contiguous(), L["Y"].stride(0))

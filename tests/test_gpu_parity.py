@@ -288,13 +288,14 @@ def test_layer_zero_nodes():
 
 # ------------------------------------------------------ whole stacks, C ABI
 
-def test_tiny_workload_stack_end_to_end():
+@pytest.mark.parametrize("fuse", [True, False])
+def test_tiny_workload_stack_end_to_end(fuse):
     wl = synth.WORKLOADS[synth.TINY_WORKLOAD]
     inp = synth.workload_inputs(wl)
     g, x, params, dy = inp["graph"], inp["x"], inp["params"], inp["dy"]
     ref = O.sage_stack(g, x, params, dy)
     dg = prepared(g)
-    st = runtime.SageStack(dg, params, wl.f_in)
+    st = runtime.SageStack(dg, params, wl.f_in, fuse_masks=fuse)
     y = st.forward(to_dev(x, 64))
     st.backward(to_dev(dy))
     torch.cuda.synchronize()
@@ -302,8 +303,53 @@ def test_tiny_workload_stack_end_to_end():
     for l in range(wl.layers):
         L, R = st.layers[l], ref["grads"][l]
         assert maxrel(L["Y"], ref["ys"][l]) <= TOL
-        for k in ("dX", "dW_self", "dW_neigh"):
+        for k in ("dW_self", "dW_neigh"):
             assert maxrel(L[k], R[k]) <= TOL, (l, k)
+        dx_ref = R["dX"]
+        if fuse and l > 0:  # masked by the sign of this layer's input
+            dx_ref = dx_ref * (st.layers[l - 1]["Y"].cpu().numpy() > 0)
+        assert maxrel(L["dX"], dx_ref) <= TOL, (l, "dX")
+
+
+@pytest.mark.parametrize("order", [1, 2])
+@pytest.mark.parametrize("bias", [False, True])
+def test_layer_mask_flags_exact(order, bias):
+    """GNN_FLAG_DY_MASKED with a pre-masked dY, plus GNN_FLAG_DX_MASKED,
+    gives bit for bit the plain backward's weight and bias gradients and its
+    dX with the input's sign mask applied."""
+    g = GRAPHS["powerlaw"]
+    f_in, h = 40, 24
+    rng = np.random.default_rng(7)
+    p = synth.LayerParams(synth.glorot(f_in, h, rng), synth.glorot(f_in, h, rng),
+                          rng.standard_normal(h) if bias else None,
+                          rng.standard_normal(h) if bias else None)
+    x = np.maximum(rng.standard_normal((g.n, f_in)), 0).astype(np.float32)  # post-ReLU input
+    x[: g.n // 3] = rng.standard_normal((g.n // 3, f_in))   # and some signed rows
+    dy = rng.standard_normal((g.n, 2 * h)).astype(np.float32)
+    dg = prepared(g)
+    outs = {}
+    for mode in ("plain", "fused"):
+        st = runtime.SageStack(dg, [p], f_in, order=order)
+        xin = to_dev(x, 48)
+        y = st.forward(xin)
+        torch.cuda.synchronize()
+        L = st.layers[0]
+        d = to_dev(dy, L["Y"].stride(0))
+        flags = 0
+        if mode == "fused":
+            d = to_dev(np.where(y.cpu().numpy() > 0, dy, 0), L["Y"].stride(0))
+            flags = G.GNN_FLAG_DY_MASKED | G.GNN_FLAG_DX_MASKED
+        lay = st._layer(0, xin.stride(0), flags)
+        G.gnn_prop_bwd(dg.struct(), lay, xin, L["W_self"], L["W_neigh"], L["Y"], d,
+                       L["saved"], L["dX"], L["dW_self"], L["dW_neigh"],
+                       L["db_self"], L["db_neigh"], st.workspace)
+        torch.cuda.synchronize()
+        outs[mode] = {k: L[k].cpu().numpy().copy() for k in
+                      ("dX", "dW_self", "dW_neigh") + (("db_self", "db_neigh") if bias else ())}
+    a, b = outs["plain"], outs["fused"]
+    for k in a:
+        exp = a[k] if k != "dX" else np.where(x > 0, a[k], 0).astype(np.float32)
+        assert np.array_equal(b[k].view(np.uint32), exp.view(np.uint32)), k
 
 
 def test_bitwise_reproducible():
