@@ -254,6 +254,162 @@ void oracle_sage_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
   free(S);
 }
 
+/* ------------------------------------------------- GCN and MixHop layers */
+
+/* Column sums of an n x w matrix, rows in ascending order. */
+static void colsum(int32_t n, int32_t w, const double* G, double* out) {
+  for (int32_t c = 0; c < w; ++c) {
+    double s = 0.0;
+    for (int32_t v = 0; v < n; ++v) s += G[(int64_t)v * w + c];
+    out[c] = s;
+  }
+}
+
+/* G = dY * 1[Y > 0] over an n x w block (the layer's ReLU derivative). */
+static void mask_all(int64_t count, const double* Y, const double* dY,
+                     double* G) {
+  for (int64_t i = 0; i < count; ++i) G[i] = Y[i] > 0.0 ? dY[i] : 0.0;
+}
+
+/* Section 2.1, Eq. "gcn forward": Y = ReLU(A_hat X W + b).  values hold
+ * A_hat; S (n x f_in, may be NULL) receives A_hat X. */
+void oracle_gcn_fwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                    const double* values, int32_t f_in, int32_t h,
+                    const double* X, const double* W, const double* b,
+                    double* Y, double* S_out) {
+  const size_t nf = (size_t)n * (size_t)f_in;
+  double* S = S_out ? S_out : (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  oracle_spmm(n, indptr, indices, values, f_in, X, S); /* A_hat X */
+  oracle_mm_nn(n, h, f_in, S, W, Y);                   /* (A_hat X) W */
+  for (int64_t v = 0; v < n; ++v)
+    for (int32_t c = 0; c < h; ++c) {
+      double* y = Y + v * h + c;
+      *y = relu(*y + (b ? b[c] : 0.0));
+    }
+  if (!S_out) free(S);
+}
+
+/* Section 5.1 for GCN: the GraphSAGE gradients with only the A_hat terms
+ * kept.  G = dY * 1[Y > 0];  dW = (A_hat X)^T G;  dX = A_hat^T G W^T;
+ * db = column sums of G.  dX and db may be NULL. */
+void oracle_gcn_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                    const double* values, int32_t f_in, int32_t h,
+                    const double* X, const double* W, const double* Y,
+                    const double* dY, double* dX, double* dW, double* db) {
+  const size_t nf = (size_t)n * (size_t)f_in, nh = (size_t)n * (size_t)h;
+  double* G = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  double* S = (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  mask_all((int64_t)nh, Y, dY, G);
+  oracle_spmm(n, indptr, indices, values, f_in, X, S); /* A_hat X */
+  oracle_mm_tn(f_in, h, n, S, G, dW);                  /* (A_hat X)^T G */
+  if (db) colsum(n, h, G, db);
+  if (dX) {
+    double* T = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+    oracle_spmm_transpose(n, indptr, indices, values, h, G, T); /* A_hat^T G */
+    oracle_mm_nt(n, f_in, h, T, W, dX);                         /* (A_hat^T G) W^T */
+    free(T);
+  }
+  free(G);
+  free(S);
+}
+
+/* Section 2.1, Eq. "mixhop forward": Y = ReLU( ||_{k=0..K} A_hat^k X W_k
+ * + b ), Y n x (K+1)h with hop k in columns [k h, (k+1) h).  W is
+ * f_in x (K+1)h with W_k in the same columns; A_hat^k X is A_hat applied k
+ * times. */
+void oracle_mixhop_fwd(int32_t n, const int32_t* indptr,
+                       const int32_t* indices, const double* values,
+                       int32_t K, int32_t f_in, int32_t h, const double* X,
+                       const double* W, const double* b, double* Y) {
+  const int32_t wy = (K + 1) * h;
+  const size_t nf = (size_t)n * (size_t)f_in, nh = (size_t)n * (size_t)h;
+  double* P = (double*)malloc(sizeof(double) * (nf ? nf : 1));  /* A_hat^k X */
+  double* Q = (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  double* Wk = (double*)malloc(sizeof(double) * ((size_t)f_in * h + 1));
+  double* Z = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  memcpy(P, X, sizeof(double) * nf);
+  for (int32_t k = 0; k <= K; ++k) {
+    if (k > 0) {
+      oracle_spmm(n, indptr, indices, values, f_in, P, Q);
+      double* s = P;
+      P = Q;
+      Q = s;
+    }
+    for (int32_t i = 0; i < f_in; ++i)
+      for (int32_t c = 0; c < h; ++c)
+        Wk[(int64_t)i * h + c] = W[(int64_t)i * wy + (int64_t)k * h + c];
+    oracle_mm_nn(n, h, f_in, P, Wk, Z); /* A_hat^k X W_k */
+    for (int64_t v = 0; v < n; ++v)
+      for (int32_t c = 0; c < h; ++c)
+        Y[v * wy + (int64_t)k * h + c] =
+            relu(Z[v * h + c] + (b ? b[(int64_t)k * h + c] : 0.0));
+  }
+  free(P);
+  free(Q);
+  free(Wk);
+  free(Z);
+}
+
+/* Backward for MixHop (Section 5.1 with K paths): G = dY * 1[Y > 0], G_k
+ * its hop-k columns;  dW_k = (A_hat^k X)^T G_k;
+ * dX = sum_k (A_hat^k)^T G_k W_k^T, each term applying A_hat^T k times to
+ * G_k W_k^T;  db = column sums of G.  dX and db may be NULL. */
+void oracle_mixhop_bwd(int32_t n, const int32_t* indptr,
+                       const int32_t* indices, const double* values,
+                       int32_t K, int32_t f_in, int32_t h, const double* X,
+                       const double* W, const double* Y, const double* dY,
+                       double* dX, double* dW, double* db) {
+  const int32_t wy = (K + 1) * h;
+  const size_t nf = (size_t)n * (size_t)f_in, nh = (size_t)n * (size_t)h;
+  double* G = (double*)malloc(sizeof(double) * ((size_t)n * wy + 1));
+  double* Gk = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  double* P = (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  double* Q = (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  double* Wk = (double*)malloc(sizeof(double) * ((size_t)f_in * h + 1));
+  double* D = (double*)malloc(sizeof(double) * ((size_t)f_in * h + 1));
+  double* V = (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  double* U = (double*)malloc(sizeof(double) * (nf ? nf : 1));
+  mask_all((int64_t)n * wy, Y, dY, G);
+  if (db) colsum(n, wy, G, db);
+  if (dX) memset(dX, 0, sizeof(double) * nf);
+  memcpy(P, X, sizeof(double) * nf);
+  for (int32_t k = 0; k <= K; ++k) {
+    if (k > 0) { /* P = A_hat^k X */
+      oracle_spmm(n, indptr, indices, values, f_in, P, Q);
+      double* s = P;
+      P = Q;
+      Q = s;
+    }
+    for (int64_t v = 0; v < n; ++v)
+      for (int32_t c = 0; c < h; ++c)
+        Gk[v * h + c] = G[v * wy + (int64_t)k * h + c];
+    oracle_mm_tn(f_in, h, n, P, Gk, D); /* (A_hat^k X)^T G_k */
+    for (int32_t i = 0; i < f_in; ++i)
+      for (int32_t c = 0; c < h; ++c) {
+        dW[(int64_t)i * wy + (int64_t)k * h + c] = D[(int64_t)i * h + c];
+        Wk[(int64_t)i * h + c] = W[(int64_t)i * wy + (int64_t)k * h + c];
+      }
+    if (dX) {
+      oracle_mm_nt(n, f_in, h, Gk, Wk, V); /* G_k W_k^T */
+      for (int32_t j = 0; j < k; ++j) {    /* (A_hat^T)^k applied */
+        oracle_spmm_transpose(n, indptr, indices, values, f_in, V, U);
+        double* s = V;
+        V = U;
+        U = s;
+      }
+      for (size_t i = 0; i < nf; ++i) dX[i] += V[i];
+    }
+  }
+  free(G);
+  free(Gk);
+  free(P);
+  free(Q);
+  free(Wk);
+  free(D);
+  free(V);
+  free(U);
+}
+
 /* ---------------------------------------------- per-output spot evaluation */
 
 void oracle_sage_fwd_rows(int32_t n, const int32_t* indptr,

@@ -1,7 +1,8 @@
 /*
- * CPU oracle for one GraphSAGE layer's feature propagation, forward and
- * backward, on a sampled subgraph ("Accurate, Efficient and Scalable
- * Training of Graph Neural Networks", Zeng et al.).
+ * CPU oracle for one GNN layer's feature propagation (GraphSAGE, and the
+ * GCN and MixHop variants), forward and backward, on a sampled subgraph
+ * ("Accurate, Efficient and Scalable Training of Graph Neural Networks",
+ * Zeng et al.).
  *
  * TEST INFRASTRUCTURE ONLY.  This library is the slow, obviously-correct
  * reference that the GPU path is checked against.  Only the test suite, the
@@ -110,6 +111,34 @@ void oracle_sage_bwd_dw_entries(int32_t n, const int32_t* indptr,
                                 int32_t nent, const int32_t* ei,
                                 const int32_t* ej, double* dWs_ent,
                                 double* dWn_ent);
+
+/* GCN layer (Section 2.1, Eq. "gcn forward"), values = A_hat:
+ *   Y = ReLU(A_hat X W + b)                    (n x h; S = A_hat X, may be NULL)
+ * Backward (Section 5.1 with only the A_hat terms kept):
+ *   G = dY * 1[Y > 0];  dW = (A_hat X)^T G;  dX = A_hat^T G W^T;  db = colsum G */
+void oracle_gcn_fwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                    const double* values, int32_t f_in, int32_t h,
+                    const double* X, const double* W, const double* b,
+                    double* Y, double* S);
+void oracle_gcn_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                    const double* values, int32_t f_in, int32_t h,
+                    const double* X, const double* W, const double* Y,
+                    const double* dY, double* dX, double* dW, double* db);
+
+/* MixHop layer (Section 2.1, Eq. "mixhop forward"), values = A_hat:
+ *   Y = ReLU( X W_0 || A_hat X W_1 || ... || A_hat^K X W_K  + b )
+ * Y is n x (K+1)h, W is f_in x (K+1)h (W_k in columns [kh, (k+1)h)), b is
+ * (K+1)h (may be NULL).  Backward: G = dY * 1[Y > 0], G_k its hop-k columns;
+ *   dW_k = (A_hat^k X)^T G_k;  dX = sum_k (A_hat^k)^T G_k W_k^T;  db = colsum G */
+void oracle_mixhop_fwd(int32_t n, const int32_t* indptr,
+                       const int32_t* indices, const double* values,
+                       int32_t K, int32_t f_in, int32_t h, const double* X,
+                       const double* W, const double* b, double* Y);
+void oracle_mixhop_bwd(int32_t n, const int32_t* indptr,
+                       const int32_t* indices, const double* values,
+                       int32_t K, int32_t f_in, int32_t h, const double* X,
+                       const double* W, const double* Y, const double* dY,
+                       double* dX, double* dW, double* db);
 
 /* bfloat16 rounding of GEMM operands for the reduced-precision mode: each
  * value is first taken as float (the storage format), then rounded to the

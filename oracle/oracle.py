@@ -70,6 +70,15 @@ def lib():
                                                i32, _F64P, _F64P, _F64P, i32,
                                                _I32P, _I32P, _F64P, _F64P],
                 "oracle_round_bf16": [i64, _F64P, _F64P],
+                "oracle_gcn_fwd": [i32, _I32P, _I32P, _F64P, i32, i32, _F64P,
+                                   _F64P, _F64P, _F64P, _F64P],
+                "oracle_gcn_bwd": [i32, _I32P, _I32P, _F64P, i32, i32, _F64P,
+                                   _F64P, _F64P, _F64P, _F64P, _F64P, _F64P],
+                "oracle_mixhop_fwd": [i32, _I32P, _I32P, _F64P, i32, i32, i32,
+                                      _F64P, _F64P, _F64P, _F64P],
+                "oracle_mixhop_bwd": [i32, _I32P, _I32P, _F64P, i32, i32, i32,
+                                      _F64P, _F64P, _F64P, _F64P, _F64P, _F64P,
+                                      _F64P],
                 "oracle_num_threads": [],
             }
             for name, args in sigs.items():
@@ -243,6 +252,68 @@ def sage_bwd_dw_entries(g, x, y, dy, h, ei, ej):
                                      _p(ei, _I32P), _p(ej, _I32P),
                                      _p(ws, _F64P), _p(wn, _F64P))
     return ws, wn
+
+
+def gcn_fwd(g, x, w, b=None, want_s: bool = False):
+    """Y = ReLU(A_hat X W + b); g.values must hold A_hat."""
+    n, ip, ix, v = _csr(g)
+    x, w = _f64(x), _f64(w)
+    f_in, h = w.shape
+    assert x.shape == (n, f_in)
+    bb = None if b is None else _f64(b)
+    y = np.empty((n, h), np.float64)
+    s = np.empty((n, f_in), np.float64) if want_s else None
+    lib().oracle_gcn_fwd(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P), f_in, h,
+                         _p(x, _F64P), _p(w, _F64P), _p(bb, _F64P), _p(y, _F64P),
+                         _p(s, _F64P))
+    return (y, s) if want_s else y
+
+
+def gcn_bwd(g, x, w, y, dy, want_dx: bool = True, want_db: bool = False) -> dict:
+    n, ip, ix, v = _csr(g)
+    x, w, y, dy = _f64(x), _f64(w), _f64(y), _f64(dy)
+    f_in, h = w.shape
+    assert y.shape == (n, h) == dy.shape
+    out = {"dW": np.empty((f_in, h)),
+           "dX": np.empty((n, f_in)) if want_dx else None,
+           "db": np.empty(h) if want_db else None}
+    lib().oracle_gcn_bwd(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P), f_in, h,
+                         _p(x, _F64P), _p(w, _F64P), _p(y, _F64P), _p(dy, _F64P),
+                         _p(out["dX"], _F64P), _p(out["dW"], _F64P),
+                         _p(out["db"], _F64P))
+    return out
+
+
+def mixhop_fwd(g, x, w, K: int, b=None):
+    """Y = ReLU(||_k A_hat^k X W_k + b); w is f_in x (K+1)h."""
+    n, ip, ix, v = _csr(g)
+    x, w = _f64(x), _f64(w)
+    f_in, wy = w.shape
+    assert wy % (K + 1) == 0 and x.shape == (n, f_in)
+    h = wy // (K + 1)
+    bb = None if b is None else _f64(b)
+    y = np.empty((n, wy), np.float64)
+    lib().oracle_mixhop_fwd(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P), K, f_in,
+                            h, _p(x, _F64P), _p(w, _F64P), _p(bb, _F64P),
+                            _p(y, _F64P))
+    return y
+
+
+def mixhop_bwd(g, x, w, K: int, y, dy, want_dx: bool = True,
+               want_db: bool = False) -> dict:
+    n, ip, ix, v = _csr(g)
+    x, w, y, dy = _f64(x), _f64(w), _f64(y), _f64(dy)
+    f_in, wy = w.shape
+    h = wy // (K + 1)
+    assert y.shape == (n, wy) == dy.shape
+    out = {"dW": np.empty((f_in, wy)),
+           "dX": np.empty((n, f_in)) if want_dx else None,
+           "db": np.empty(wy) if want_db else None}
+    lib().oracle_mixhop_bwd(n, _p(ip, _I32P), _p(ix, _I32P), _p(v, _F64P), K, f_in,
+                            h, _p(x, _F64P), _p(w, _F64P), _p(y, _F64P),
+                            _p(dy, _F64P), _p(out["dX"], _F64P), _p(out["dW"], _F64P),
+                            _p(out["db"], _F64P))
+    return out
 
 
 def sage_stack(g, x, params, dy_top, want_dx_first: bool = True):

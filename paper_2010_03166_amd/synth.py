@@ -121,6 +121,9 @@ def symmetric_csr(n: int, edges: np.ndarray, self_loops: bool = True,
     """Undirected graph from unique edges (u != v) -> symmetric CSR.
 
     values: "row-normalized" (1/deg, deg counting the self loop),
+            "sym-normalized" (1/sqrt(deg_u deg_v), the symmetric
+            normalisation a GCN or MixHop layer aggregates with; with the
+            self loops this is (I + D)^-1/2 (I + A) (I + D)^-1/2),
             "ones", or "random" (independent N(0,1) per stored entry, a
             pattern-symmetric but value-asymmetric matrix for tests).
     """
@@ -135,6 +138,8 @@ def symmetric_csr(n: int, edges: np.ndarray, self_loops: bool = True,
     cols = np.concatenate(c) if c else np.zeros(0, np.int64)
     if values == "row-normalized":
         return csr_from_pairs(n, rows, cols, None)
+    if values == "sym-normalized":
+        return sym_normalized(csr_from_pairs(n, rows, cols, None))
     if values == "ones":
         return csr_from_pairs(n, rows, cols, np.ones(rows.size, np.float32))
     if values == "random":
@@ -142,6 +147,17 @@ def symmetric_csr(n: int, edges: np.ndarray, self_loops: bool = True,
         return csr_from_pairs(n, rows, cols,
                               rng.standard_normal(rows.size).astype(np.float32))
     raise ValueError(values)
+
+
+def sym_normalized(g: Csr) -> Csr:
+    """The same pattern with values 1/sqrt(deg_u deg_v) (deg = stored
+    entries of the row, self loop included)."""
+    deg = g.degrees().astype(np.float64)
+    rows = np.repeat(np.arange(g.n), g.degrees())
+    cols = g.indices.astype(np.int64)
+    vals = (1.0 / np.sqrt(deg[rows] * deg[cols])).astype(np.float32) if g.nnz else \
+        np.zeros(0, np.float32)
+    return Csr(g.n, g.indptr.copy(), g.indices.copy(), vals)
 
 
 # ------------------------------------------------------------- graph models

@@ -430,3 +430,147 @@ def test_round_bf16_is_idempotent_and_monotone():
     # at most half a bfloat16 ulp (relative 2^-8) from the float value
     f = x.astype(np.float32).astype(np.float64)
     assert np.all(np.abs(y - f) <= np.abs(f) * 2.0**-8 * (1 + 1e-12))
+
+
+# --------------------------------------------------- GCN and MixHop layers
+
+def gcn_graph(seed, n=14, deg=3.0):
+    return synth.sym_normalized(synth.random_graph(n, deg, seed))
+
+
+def test_sym_normalization_matches_definition():
+    # A_hat = (I + D)^-1/2 (I + A) (I + D)^-1/2 with A the binary adjacency
+    # without self loops and D its degree matrix, written out densely.
+    g0 = synth.random_graph(25, 4.0, 3, self_loops=False, values="ones")
+    a = dense(g0)
+    d = a.sum(axis=1)
+    ref = np.diag((1 + d) ** -0.5) @ (np.eye(25) + a) @ np.diag((1 + d) ** -0.5)
+    g = synth.sym_normalized(synth.random_graph(25, 4.0, 3))
+    assert np.allclose(dense(g), ref, rtol=1e-6, atol=0)
+    assert np.allclose(dense(g), dense(g).T)
+
+
+def test_gcn_forward_dense_brute_force():
+    rng = np.random.default_rng(4)
+    g = gcn_graph(5)
+    x, w, b = rng.standard_normal((14, 5)), rng.standard_normal((5, 3)), rng.standard_normal(3)
+    ref = np.maximum(dense(g) @ x @ w + b, 0)
+    assert rel(O.gcn_fwd(g, x, w, b), ref) < 1e-14
+
+
+def test_gcn_regular_graph_preserves_constant_rows():
+    # On a cycle (2-regular, 3 stored entries per row) every A_hat entry is
+    # 1/3, so A_hat maps constant columns to themselves: Y = ReLU(X W), up
+    # to the float32 storage of 1/3 (relative 3e-8).
+    n = 9
+    e = np.array([[i, (i + 1) % n] for i in range(n)])
+    g = synth.sym_normalized(synth.symmetric_csr(n, e))
+    assert np.all(g.values == np.float32(1 / 3))
+    x = np.tile(np.random.default_rng(1).standard_normal(4), (n, 1))
+    w = np.random.default_rng(2).standard_normal((4, 3))
+    assert rel(O.gcn_fwd(g, x, w), np.maximum(x @ w, 0)) < 1e-7
+
+
+def test_mixhop_forward_dense_matrix_powers():
+    rng = np.random.default_rng(6)
+    g = gcn_graph(7)
+    K, f_in, h = 3, 4, 2
+    x = rng.standard_normal((14, f_in))
+    w = rng.standard_normal((f_in, (K + 1) * h))
+    b = rng.standard_normal((K + 1) * h)
+    a = dense(g)
+    ref = np.hstack([np.linalg.matrix_power(a, k) @ x @ w[:, k * h:(k + 1) * h]
+                     for k in range(K + 1)]) + b
+    assert rel(O.mixhop_fwd(g, x, w, K, b), np.maximum(ref, 0)) < 1e-13
+
+
+def test_mixhop_special_cases():
+    rng = np.random.default_rng(8)
+    g = gcn_graph(9)
+    x = rng.standard_normal((14, 5))
+    w0, w1 = rng.standard_normal((5, 3)), rng.standard_normal((5, 3))
+    # K = 0: a dense layer
+    assert rel(O.mixhop_fwd(g, x, w0, 0), np.maximum(x @ w0, 0)) < 1e-14
+    # K = 1: the two-path GraphSAGE layer aggregating with A_hat
+    assert rel(O.mixhop_fwd(g, x, np.hstack([w0, w1]), 1),
+               O.sage_fwd(g, x, w0, w1)) < 1e-14
+    # K = 1 with W_0 = 0: hop 0 is zero, hop 1 is the GCN layer
+    y = O.mixhop_fwd(g, x, np.hstack([np.zeros_like(w0), w1]), 1)
+    assert np.all(y[:, :3] == 0) and rel(y[:, 3:], O.gcn_fwd(g, x, w1)) < 1e-14
+
+
+def _fd_grads(loss, arrays, eps=1e-6):
+    out = []
+    for arr in arrays:
+        d = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            old = arr[idx]
+            arr[idx] = old + eps
+            lp = loss()
+            arr[idx] = old - eps
+            lm = loss()
+            arr[idx] = old
+            d[idx] = (lp - lm) / (2 * eps)
+        out.append(d)
+    return out
+
+
+@pytest.mark.parametrize("bias", [False, True])
+def test_gcn_backward_finite_differences(bias):
+    # L = <dY, Y>; cases with a pre-activation near the ReLU kink re-drawn
+    for s in range(20, 80):
+        rng = np.random.default_rng(s)
+        g = synth.sym_normalized(synth.random_graph(10, 3.0, s))
+        x, w = rng.standard_normal((10, 4)), rng.standard_normal((4, 3))
+        b = rng.standard_normal(3) if bias else None
+        z = dense(g) @ x @ w + (b if bias else 0)
+        if np.abs(z).min() > 1e-3:
+            break
+    dy = np.random.default_rng(5).standard_normal((10, 3))
+    r = O.gcn_bwd(g, x, w, O.gcn_fwd(g, x, w, b), dy, want_db=bias)
+    arrs = [x, w] + ([b] if bias else [])
+    fds = _fd_grads(lambda: float(np.sum(dy * O.gcn_fwd(g, x, w, b))), arrs)
+    assert rel(r["dX"], fds[0]) < 1e-6 and rel(r["dW"], fds[1]) < 1e-6
+    if bias:
+        assert rel(r["db"], fds[2]) < 1e-6
+
+
+@pytest.mark.parametrize("K", [1, 2, 3])
+def test_mixhop_backward_finite_differences(K):
+    h = 2
+    for s in range(40, 120):
+        rng = np.random.default_rng(s)
+        g = synth.sym_normalized(synth.random_graph(9, 3.0, s))
+        x = rng.standard_normal((9, 3))
+        w = rng.standard_normal((3, (K + 1) * h))
+        b = rng.standard_normal((K + 1) * h)
+        a = dense(g)
+        z = np.hstack([np.linalg.matrix_power(a, k) @ x @ w[:, k * h:(k + 1) * h]
+                       for k in range(K + 1)]) + b
+        if np.abs(z).min() > 1e-3:
+            break
+    dy = np.random.default_rng(6).standard_normal((9, (K + 1) * h))
+    y = O.mixhop_fwd(g, x, w, K, b)
+    r = O.mixhop_bwd(g, x, w, K, y, dy, want_db=True)
+    fds = _fd_grads(lambda: float(np.sum(dy * O.mixhop_fwd(g, x, w, K, b))), [x, w, b])
+    assert rel(r["dX"], fds[0]) < 1e-6
+    assert rel(r["dW"], fds[1]) < 1e-6
+    assert rel(r["db"], fds[2]) < 1e-6
+
+
+def test_mixhop_backward_on_asymmetric_values():
+    # the backward uses A_hat^T, not A_hat: random (value-asymmetric)
+    # entries on a symmetric pattern check the transposes against dense
+    # matrix powers of the transpose
+    rng = np.random.default_rng(12)
+    g = synth.random_graph(12, 3.0, 4, values="random")
+    K, h = 2, 2
+    x, w = rng.standard_normal((12, 3)), rng.standard_normal((3, (K + 1) * h))
+    y = O.mixhop_fwd(g, x, w, K)
+    dy = rng.standard_normal(y.shape)
+    r = O.mixhop_bwd(g, x, w, K, y, dy)
+    at = dense(g).T
+    gm = np.where(y > 0, dy, 0)
+    ref = sum(np.linalg.matrix_power(at, k) @ gm[:, k * h:(k + 1) * h] @ w[:, k * h:(k + 1) * h].T
+              for k in range(K + 1))
+    assert rel(r["dX"], ref) < 1e-13
