@@ -68,6 +68,8 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--skip-input-grad", action="store_true",
                     help="do not compute the first layer's input gradient")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the GCN and MixHop layer timings")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run one plain device-to-device copy of MIB MiB "
                          "(reference point for hardware byte counters)")
@@ -271,6 +273,11 @@ def main():
         log("bf16 variant: %.4f ms per step" % ms_b)
         del stb
 
+    # the GCN and MixHop layers (Section 2.1) on the same subgraph with the
+    # symmetric normalisation, one layer each, forward + backward with dX
+    if not args.no_variants:
+        out["variants"] = bench_variants(G, runtime, synth, torch, np, g, x, wl, args)
+
     if not args.no_cpu_baseline:
         from oracle import oracle as O
         import numpy as np  # noqa: F811
@@ -290,6 +297,90 @@ def main():
         log("cpu oracle %.1f ms/layer on %d threads" % (
             out["cpu_baseline"]["value"], out["cpu_baseline"]["cores"]))
     print(json.dumps(out), flush=True)
+
+
+def bench_variants(G, runtime, synth, torch, np, g, x, wl, args):
+    """ms per layer (forward + backward, first-layer shape) of a GCN layer
+    (f_in -> h) and a MixHop layer with K = 2 hops of h/2 columns each."""
+    gs = synth.sym_normalized(g)
+    dg = runtime.DeviceGraph(gs)
+    dg.prepare()
+    c = dg.struct()
+    f_in, h, n = wl.f_in, wl.hidden, g.n
+    pad = 16
+    rup = lambda v: (v + pad - 1) // pad * pad
+    rng = np.random.default_rng(5)
+    X = runtime.padded(torch.from_numpy(x).cuda(), rup(f_in))
+    res = {}
+
+    def buf(nb):
+        return torch.empty(max(int(nb), 256), dtype=torch.uint8, device="cuda")
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        G.gnn_timer_reset()
+        G.gnn_timer_enable(True)
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        G.gnn_timer_enable(False)
+        kern = {}
+        for kname in G.KERNELS:
+            kms, launches, work = G.gnn_timer_read(kname)
+            if launches:
+                kern[kname] = {"ms_per_layer": round(kms / args.steps, 4),
+                               "launches": launches // args.steps}
+                if kname.startswith("gemm_") and kname != "gemm_reduce":
+                    kern[kname]["tflops"] = round(work / kms / 1e9, 1)
+        G.gnn_timer_reset()
+        return ms, kern
+
+    # GCN: Y = ReLU(A_hat X W)
+    W = torch.from_numpy(synth.glorot(f_in, h, rng)).cuda()
+    lay = G.make_layer(f_in, h, X.stride(0), rup(h), X.stride(0), 0, 0)
+    Y = torch.empty((n, rup(h)), device="cuda")[:, :h]
+    dY = torch.from_numpy(rng.standard_normal((n, h)).astype(np.float32)).cuda()
+    dYp = runtime.padded(dY, rup(h))
+    dX = torch.empty((n, rup(f_in)), device="cuda")[:, :f_in]
+    dW = torch.empty((f_in, h), device="cuda")
+    saved, ws = buf(G.gnn_gcn_saved_bytes(c, lay)), buf(G.gnn_gcn_workspace_bytes(c, lay))
+
+    def gcn():
+        G.gnn_gcn_fwd(c, lay, X, W, None, Y, saved, ws)
+        G.gnn_gcn_bwd(c, lay, X, W, Y, dYp, saved, dX, dW, None, ws)
+
+    ms, kern = timed(gcn)
+    res["gcn"] = {"ms_per_layer": round(ms, 5), "shape": "%d -> %d, order %d" % (
+        f_in, h, G.gnn_choose_order(f_in, h)), "kernels": kern}
+    log("gcn layer: %.4f ms" % ms)
+    # MixHop, K = 2 hops of h/2 columns: Y = ReLU(X W_0 || A X W_1 || A^2 X W_2)
+    K, hk = 2, h // 2
+    wy = (K + 1) * hk
+    Wm = torch.from_numpy(synth.glorot(f_in, wy, rng)).cuda()
+    laym = G.make_layer(f_in, hk, X.stride(0), rup(wy), X.stride(0), 0, 0)
+    Ym = torch.empty((n, rup(wy)), device="cuda")[:, :wy]
+    dYm = runtime.padded(torch.from_numpy(rng.standard_normal((n, wy)).astype(np.float32)).cuda(),
+                         rup(wy))
+    dWm = torch.empty((f_in, wy), device="cuda")
+    savedm = buf(G.gnn_mixhop_saved_bytes(c, laym, K))
+    wsm = buf(G.gnn_mixhop_workspace_bytes(c, laym, K))
+
+    def mixhop():
+        G.gnn_mixhop_fwd(c, laym, K, X, Wm, None, Ym, savedm, wsm)
+        G.gnn_mixhop_bwd(c, laym, K, X, Wm, Ym, dYm, savedm, dX, dWm, None, wsm)
+
+    ms, kern = timed(mixhop)
+    res["mixhop_k2"] = {"ms_per_layer": round(ms, 5),
+                        "shape": "%d -> 3 x %d" % (f_in, hk), "kernels": kern}
+    log("mixhop layer: %.4f ms" % ms)
+    return res
 
 
 if __name__ == "__main__":

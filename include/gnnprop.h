@@ -192,6 +192,58 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
                         void* workspace, size_t workspace_bytes,
                         hipStream_t stream);
 
+/* ------------------------------------------------- GCN and MixHop layers */
+
+/* The GNN variants of Section 2.1 on the same three kernels; their
+ * backward keeps the A_hat terms of the Section 5.1 gradients.
+ * csr->values must hold A_hat = (I + D)^-1/2 (I + A) (I + D)^-1/2 (the
+ * pattern storing the self loops); it is symmetric, so csr->values_t may
+ * point to csr->values.  layer->h is one path's output width; layer->flags
+ * may hold GNN_FLAG_BF16 only.  Sizes of `saved` and workspace come from the
+ * matching queries; ownership and aliasing rules are those of
+ * gnn_prop_fwd / gnn_prop_bwd.
+ *
+ * GCN (Eq. "gcn forward"): Y = ReLU(A_hat X W + b), Y n x h (stride
+ * ld_y >= h), W f_in x h row-major, b [h] or NULL; order as for GraphSAGE
+ * (1: (A_hat X) W, A_hat X saved; 2: A_hat (X W)).  Backward: G = dY *
+ * 1[Y > 0], dW = (A_hat X)^T G, dX = A_hat^T G W^T (dX may be NULL),
+ * db = column sums of G (db may be NULL). */
+size_t gnn_gcn_saved_bytes(const gnn_csr* csr, const gnn_layer* layer);
+size_t gnn_gcn_workspace_bytes(const gnn_csr* csr, const gnn_layer* layer);
+gnn_status gnn_gcn_fwd(const gnn_csr* csr, const gnn_layer* layer,
+                       const float* X, const float* W, const float* b,
+                       float* Y, void* saved, void* workspace,
+                       size_t workspace_bytes, hipStream_t stream);
+gnn_status gnn_gcn_bwd(const gnn_csr* csr, const gnn_layer* layer,
+                       const float* X, const float* W, const float* Y,
+                       const float* dY, const void* saved, float* dX,
+                       float* dW, float* db, void* workspace,
+                       size_t workspace_bytes, hipStream_t stream);
+
+/* MixHop (Eq. "mixhop forward"), K >= 0 hops:
+ *   Y = ReLU( X W_0 || A_hat X W_1 || ... || A_hat^K X W_K  + b )
+ * Y is n x (K+1)h (stride ld_y >= (K+1)h), hop k in columns [kh, (k+1)h);
+ * W is f_in x (K+1)h row-major with W_k in the same columns; b is [(K+1)h]
+ * or NULL.  The features are propagated first (A_hat^k X for k = 1..K, kept
+ * in `saved`); layer->order must be 0 or 1.  Backward: G = dY * 1[Y > 0],
+ * G_k its hop-k columns; dW_k = (A_hat^k X)^T G_k (dW laid out like W);
+ * dX = sum_k (A_hat^k)^T G_k W_k^T (may be NULL); db = column sums of G
+ * (may be NULL). */
+size_t gnn_mixhop_saved_bytes(const gnn_csr* csr, const gnn_layer* layer,
+                              int32_t K);
+size_t gnn_mixhop_workspace_bytes(const gnn_csr* csr, const gnn_layer* layer,
+                                  int32_t K);
+gnn_status gnn_mixhop_fwd(const gnn_csr* csr, const gnn_layer* layer,
+                          int32_t K, const float* X, const float* W,
+                          const float* b, float* Y, void* saved,
+                          void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+gnn_status gnn_mixhop_bwd(const gnn_csr* csr, const gnn_layer* layer,
+                          int32_t K, const float* X, const float* W,
+                          const float* Y, const float* dY, const void* saved,
+                          float* dX, float* dW, float* db, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------- kernels */
 
 /* Feature / gradient propagation alone (Section 5.1's first kernel, the

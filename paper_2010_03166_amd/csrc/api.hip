@@ -19,16 +19,11 @@
 #include <cstring>
 #include <vector>
 
-#include "internal.hpp"
+#include "abi.hpp"
 
 using namespace gnnprop;
 
 namespace {
-
-#define GNN_HIP(expr)                         \
-  do {                                        \
-    if ((expr) != hipSuccess) return GNN_ERR_HIP; \
-  } while (0)
 
 // ------------------------------------------------------------- timer
 
@@ -42,18 +37,6 @@ std::vector<hipEvent_t> g_pool;
 size_t g_pool_used = 0;
 std::vector<TimerRec> g_recs;
 TimerRec g_cur;
-
-bool ranges_overlap(const void* a, size_t an, const void* b, size_t bn) {
-  if (!a || !b || an == 0 || bn == 0) return false;
-  const char* pa = static_cast<const char*>(a);
-  const char* pb = static_cast<const char*>(b);
-  return pa < pb + bn && pb < pa + an;
-}
-
-size_t mat_bytes(int64_t rows, int64_t cols, int64_t ld) {
-  if (rows <= 0 || cols <= 0) return 0;
-  return (size_t)(((rows - 1) * ld + cols) * 4);
-}
 
 // ------------------------------------------------------- layer layout
 
@@ -207,16 +190,6 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   return o;
 }
 
-gnn_status check_csr(const gnn_csr* c, bool need_vals, bool need_vals_t) {
-  if (!c) return GNN_ERR_NULL;
-  if (c->n < 0 || c->nnz < 0 || c->nnz > INT32_MAX) return GNN_ERR_SHAPE;
-  if (!c->indptr) return GNN_ERR_NULL;
-  if (c->nnz > 0 && !c->indices) return GNN_ERR_NULL;
-  if (need_vals && c->nnz > 0 && !c->values) return GNN_ERR_NULL;
-  if (need_vals_t && c->nnz > 0 && !c->values_t) return GNN_ERR_NULL;
-  return GNN_OK;
-}
-
 gnn_status check_layer(const gnn_layer* L) {
   if (!L) return GNN_ERR_NULL;
   if (L->f_in <= 0 || L->h <= 0) return GNN_ERR_SHAPE;
@@ -226,26 +199,6 @@ gnn_status check_layer(const gnn_layer* L) {
     return GNN_ERR_UNSUPPORTED;
   return GNN_OK;
 }
-
-SpmmCall spmm_call(const gnn_csr* c, bool transpose, int32_t w,
-                   const float* in, int64_t ld_in, float* out, int64_t ld_out) {
-  SpmmCall s;
-  memset(&s, 0, sizeof(s));
-  s.n = c->n;
-  s.nnz = c->nnz;
-  s.indptr = c->indptr;
-  s.indices = c->indices;
-  s.vals = transpose ? c->values_t : c->values;
-  s.plan = c->plan;
-  s.w = w;
-  s.in = in;
-  s.ld_in = ld_in;
-  s.out = out;
-  s.ld_out = ld_out;
-  s.epilogue = SPMM_STORE;
-  return s;
-}
-
 
 }  // namespace
 
@@ -540,7 +493,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     } else {
       float* GT = buf0;
       float* G_n = buf1;
-      GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, GT, o.ld_g, G_n, o.ld_gn, stream));
+      GNN_HIP(mask_launch(n, 2 * h, h, Y, dY, layer->ld_y, GT, o.ld_g, G_n, o.ld_gn, stream));
       Gs = GT;
       ld_gs = o.ld_g;
       Gn = G_n;
@@ -572,7 +525,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       ld_g = layer->ld_y;
     } else {
       float* Gm = buf0;
-      GNN_HIP(mask_launch(n, h, Y, dY, layer->ld_y, Gm, o.ld_g, Gm + h, o.ld_g, stream));
+      GNN_HIP(mask_launch(n, 2 * h, h, Y, dY, layer->ld_y, Gm, o.ld_g, Gm + h, o.ld_g, stream));
       G = Gm;
       ld_g = o.ld_g;
     }

@@ -5,23 +5,25 @@
 
 namespace gnnprop {
 
-// G = dY * 1[Y > 0]; the self half goes to dst0, the neighbour half to
-// dst1.  One thread per 4 columns when every row start is 16-byte aligned.
+// G = dY * 1[Y > 0] over n x width; columns [0, split) go to dst0, the rest
+// to dst1 (the self and neighbour halves of a GraphSAGE output, or one block
+// when split = width).  One thread per 4 columns when every row start is
+// 16-byte aligned.
 template <bool VEC>
 __global__ __launch_bounds__(256) void mask_kernel(
-    int32_t n, int32_t h, const float* __restrict__ Y,
+    int32_t n, int32_t width, int32_t split, const float* __restrict__ Y,
     const float* __restrict__ dY, int64_t ld_y, float* __restrict__ dst0,
     int64_t ld0, float* __restrict__ dst1, int64_t ld1) {
   constexpr int W = VEC ? 4 : 1;
-  const int per_row = 2 * h / W;
+  const int per_row = width / W;
   const int64_t total = (int64_t)n * per_row;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
        e += (int64_t)gridDim.x * blockDim.x) {
     const int row = (int)(e / per_row);
     const int col = (int)(e % per_row) * W;
     const int64_t src = (int64_t)row * ld_y + col;
-    float* dst = col < h ? dst0 + (int64_t)row * ld0 + col
-                         : dst1 + (int64_t)row * ld1 + (col - h);
+    float* dst = col < split ? dst0 + (int64_t)row * ld0 + col
+                             : dst1 + (int64_t)row * ld1 + (col - split);
     if (VEC) {
       const float4 y = *reinterpret_cast<const float4*>(Y + src);
       const float4 d = *reinterpret_cast<const float4*>(dY + src);
@@ -37,20 +39,22 @@ __global__ __launch_bounds__(256) void mask_kernel(
   }
 }
 
-hipError_t mask_launch(int32_t n, int32_t h, const float* Y, const float* dY,
-                       int64_t ld_y, float* dst0, int64_t ld0, float* dst1,
-                       int64_t ld1, hipStream_t s) {
-  if (n <= 0 || h <= 0) return hipSuccess;
-  const bool vec = (h % 4 == 0) && vec4_ok(Y, ld_y) && vec4_ok(dY, ld_y) &&
-                   vec4_ok(dst0, ld0) && vec4_ok(dst1, ld1);
-  const int64_t units = (int64_t)n * 2 * h / (vec ? 4 : 1);
+hipError_t mask_launch(int32_t n, int32_t width, int32_t split,
+                       const float* Y, const float* dY, int64_t ld_y,
+                       float* dst0, int64_t ld0, float* dst1, int64_t ld1,
+                       hipStream_t s) {
+  if (n <= 0 || width <= 0) return hipSuccess;
+  const bool vec = (width % 4 == 0) && (split % 4 == 0) && vec4_ok(Y, ld_y) &&
+                   vec4_ok(dY, ld_y) && vec4_ok(dst0, ld0) &&
+                   (split == width || vec4_ok(dst1, ld1));
+  const int64_t units = (int64_t)n * width / (vec ? 4 : 1);
   const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(units, 256), 8192);
   timer_begin(GNN_K_MASK, s);
   if (vec)
-    mask_kernel<true><<<grid, 256, 0, s>>>(n, h, Y, dY, ld_y, dst0, ld0, dst1, ld1);
+    mask_kernel<true><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
   else
-    mask_kernel<false><<<grid, 256, 0, s>>>(n, h, Y, dY, ld_y, dst0, ld0, dst1, ld1);
-  timer_end(GNN_K_MASK, 12.0 * n * 2.0 * h, s);
+    mask_kernel<false><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
+  timer_end(GNN_K_MASK, 12.0 * n * width, s);
   return hipGetLastError();
 }
 

@@ -135,11 +135,12 @@ double gemm_flops(const GemmBatch& b);
 
 // ----------------------------------------------------- elementwise
 
-// G = dY * 1[Y > 0] over an n x 2h block; columns [0,h) -> dst0, [h,2h)
-// -> dst1.
-hipError_t mask_launch(int32_t n, int32_t h, const float* Y, const float* dY,
-                       int64_t ld_y, float* dst0, int64_t ld0, float* dst1,
-                       int64_t ld1, hipStream_t s);
+// G = dY * 1[Y > 0] over an n x width block; columns [0, split) -> dst0,
+// [split, width) -> dst1 (dst1 unused when split = width).
+hipError_t mask_launch(int32_t n, int32_t width, int32_t split,
+                       const float* Y, const float* dY, int64_t ld_y,
+                       float* dst0, int64_t ld0, float* dst1, int64_t ld1,
+                       hipStream_t s);
 // out[c] = sum over rows of G[r, c], rows in ascending blocks of 256 summed
 // in a fixed order.  partials: colsum_partials_bytes.
 size_t colsum_partials_bytes(int32_t n, int32_t w);

@@ -294,6 +294,20 @@ struct Vec<true> {
     v.w = fmaxf(v.w, 0.f);
     return v;
   }
+  // the first k (1..3) components only: the ragged end of a row whose width
+  // is not a multiple of 4
+  __device__ static T load_part(const float* p, int k) {
+    T v = zero();
+    v.x = p[0];
+    if (k > 1) v.y = p[1];
+    if (k > 2) v.z = p[2];
+    return v;
+  }
+  __device__ static void store_part(float* p, T v, int k) {
+    p[0] = v.x;
+    if (k > 1) p[1] = v.y;
+    if (k > 2) p[2] = v.z;
+  }
   // v where m > 0, else 0 (a selection: NaN or infinite v is not spread)
   __device__ static T select_pos(T m, T v) {
     v.x = m.x > 0.f ? v.x : 0.f;
@@ -314,9 +328,11 @@ struct Vec<false> {
   __device__ static void add(T& acc, T x) { acc += x; }
   __device__ static T relu(T v) { return fmaxf(v, 0.f); }
   __device__ static T select_pos(T m, T v) { return m > 0.f ? v : 0.f; }
+  __device__ static T load_part(const float* p, int) { return *p; }
+  __device__ static void store_part(float* p, T v, int) { *p = v; }
 };
 
-template <int G, int D, bool VEC, int EPI, bool OFF32>
+template <int G, int D, bool VEC, int EPI, bool OFF32, bool RAG>
 __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
   using V = Vec<VEC>;
   using T = typename V::T;
@@ -351,16 +367,24 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
   for (int c0 = c_lo; c0 < c_hi; c0 += CW) {
     const int col = c0 + lane * V::W;
     const bool ok = col < c_hi;
+    // a lane holding the ragged end of the row (fewer than W columns left)
+    const int nv = c_hi - col;
+    const bool part = RAG && ok && nv < V::W;
+    auto ld = [&](const float* p) { return part ? V::load_part(p, nv) : V::load(p); };
     auto finish = [&](int row, T acc) {
       if (!ok) return;
       if (EPI == SPMM_BIAS_RELU) {
-        if (a.bias) V::add(acc, V::load(a.bias + col));
+        if (a.bias) V::add(acc, ld(a.bias + col));
         acc = V::relu(acc);
       } else if (EPI == SPMM_ADD) {
-        V::add(acc, V::load(a.res + (int64_t)row * a.ld_res + col));
-        if (a.mask) acc = V::select_pos(V::load(a.mask + (int64_t)row * a.ld_mask + col), acc);
+        V::add(acc, ld(a.res + (int64_t)row * a.ld_res + col));
+        if (a.mask) acc = V::select_pos(ld(a.mask + (int64_t)row * a.ld_mask + col), acc);
       }
-      V::store(a.out + (int64_t)row * a.ld_out + col, acc);
+      float* dst = a.out + (int64_t)row * a.ld_out + col;
+      if (part)
+        V::store_part(dst, acc, nv);
+      else
+        V::store(dst, acc);
     };
 
     int hr = EMPTY, tr = -1, nstart = 0;
@@ -408,11 +432,11 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
             const int idx = __shfl(fi, k + u, G);
             if (k + u < cnt && ok) {
               if (OFF32)
-                x[u] = V::load(reinterpret_cast<const float*>(
+                x[u] = ld(reinterpret_cast<const float*>(
                     reinterpret_cast<const char*>(in) +
                     (((uint32_t)idx * ld_in + (uint32_t)col) << 2)));
               else
-                x[u] = V::load(in + (int64_t)idx * a.ld_in + col);
+                x[u] = ld(in + (int64_t)idx * a.ld_in + col);
             } else {
               x[u] = V::zero();
             }
@@ -485,33 +509,35 @@ static double spmm_bytes(int32_t n, int64_t nnz, int32_t w) {
 #define SPMM_DEPTH 4
 #endif
 
-template <int G, bool VEC, int EPI>
+template <int G, bool VEC, int EPI, bool RAG>
 static void spmm_go(const SpmmArgs& a, const PlanDims& d, bool off32,
                     hipStream_t s) {
   const unsigned grid = (unsigned)(d.nblk * a.nslices);
   if (off32)
-    spmm_kernel<G, SPMM_DEPTH, VEC, EPI, true><<<grid, 256, 0, s>>>(a);
+    spmm_kernel<G, SPMM_DEPTH, VEC, EPI, true, RAG><<<grid, 256, 0, s>>>(a);
   else
-    spmm_kernel<G, SPMM_DEPTH, VEC, EPI, false><<<grid, 256, 0, s>>>(a);
+    spmm_kernel<G, SPMM_DEPTH, VEC, EPI, false, RAG><<<grid, 256, 0, s>>>(a);
 }
 
-template <int G, bool VEC>
+template <int G, bool VEC, bool RAG>
 static void spmm_epi(const SpmmArgs& a, const PlanDims& d, bool off32,
                      hipStream_t s) {
   switch (a.epilogue) {
-    case SPMM_BIAS_RELU: return spmm_go<G, VEC, SPMM_BIAS_RELU>(a, d, off32, s);
-    case SPMM_ADD: return spmm_go<G, VEC, SPMM_ADD>(a, d, off32, s);
-    default: return spmm_go<G, VEC, SPMM_STORE>(a, d, off32, s);
+    case SPMM_BIAS_RELU: return spmm_go<G, VEC, SPMM_BIAS_RELU, RAG>(a, d, off32, s);
+    case SPMM_ADD: return spmm_go<G, VEC, SPMM_ADD, RAG>(a, d, off32, s);
+    default: return spmm_go<G, VEC, SPMM_STORE, RAG>(a, d, off32, s);
   }
 }
 
-template <bool VEC>
+// RAG: float4 lanes on a width that is not a multiple of 4 (the lane at the
+// row's end reads and writes its 1..3 columns one by one).
+template <bool VEC, bool RAG>
 static void spmm_dispatch(const SpmmArgs& a, const PlanDims& d, bool off32,
                           hipStream_t s) {
   const int units = VEC ? a.sw / 4 : a.sw;  // column vectors per slice row
-  if (units <= 16) return spmm_epi<16, VEC>(a, d, off32, s);
-  if (units <= 32) return spmm_epi<32, VEC>(a, d, off32, s);
-  return spmm_epi<64, VEC>(a, d, off32, s);
+  if (units <= 16) return spmm_epi<16, VEC, RAG>(a, d, off32, s);
+  if (units <= 32) return spmm_epi<32, VEC, RAG>(a, d, off32, s);
+  return spmm_epi<64, VEC, RAG>(a, d, off32, s);
 }
 
 size_t spmm_partials_bytes(int32_t n, int64_t nnz, int32_t w) {
@@ -545,7 +571,9 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   a.ld_mask = c.ld_mask;
   a.nslices = c.w >= 256 ? 8 : 1;
   a.sw = (int32_t)round_up(ceil_div(c.w, a.nslices), 4);
-  const bool vec = (c.w % 4 == 0) && vec4_ok(c.in, c.ld_in) &&
+  // float4 lanes whenever rows start 16-byte aligned (the ragged end of a
+  // width that is not a multiple of 4 is read and written per component)
+  const bool vec = vec4_ok(c.in, c.ld_in) &&
                    vec4_ok(c.out, c.ld_out) &&
                    (c.epilogue != SPMM_BIAS_RELU || !c.bias || aligned16(c.bias)) &&
                    (c.epilogue != SPMM_ADD || vec4_ok(c.res, c.ld_res)) &&
@@ -553,10 +581,12 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   // Gather offsets in 32 bits when the input spans less than 4 GiB.
   const bool off32 = ((int64_t)(c.n - 1) * c.ld_in + c.w) * 4 < (int64_t(1) << 32);
   timer_begin(GNN_K_SPMM, s);
-  if (vec)
-    spmm_dispatch<true>(a, d, off32, s);
+  if (vec && c.w % 4 != 0)
+    spmm_dispatch<true, true>(a, d, off32, s);
+  else if (vec)
+    spmm_dispatch<true, false>(a, d, off32, s);
   else
-    spmm_dispatch<false>(a, d, off32, s);
+    spmm_dispatch<false, false>(a, d, off32, s);
   timer_end(GNN_K_SPMM, spmm_bytes(c.n, c.nnz, c.w), s);
   return hipGetLastError();
 }

@@ -77,6 +77,25 @@ EXPORTS = {
         ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
         ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32, ctypes.c_void_p,
         ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_gcn_saved_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                              ctypes.POINTER(gnn_layer)]),
+    "gnn_gcn_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                                  ctypes.POINTER(gnn_layer)]),
+    "gnn_gcn_fwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer)]
+                    + [ctypes.c_void_p] * 6 + [ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_gcn_bwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer)]
+                    + [ctypes.c_void_p] * 9 + [ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_mixhop_saved_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                                 ctypes.POINTER(gnn_layer), ctypes.c_int32]),
+    "gnn_mixhop_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                                     ctypes.POINTER(gnn_layer),
+                                                     ctypes.c_int32]),
+    "gnn_mixhop_fwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer),
+                                        ctypes.c_int32] + [ctypes.c_void_p] * 6
+                       + [ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_mixhop_bwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer),
+                                        ctypes.c_int32] + [ctypes.c_void_p] * 9
+                       + [ctypes.c_size_t, ctypes.c_void_p]),
     "gnn_timer_enable": (ctypes.c_int32, [ctypes.c_int32]),
     "gnn_timer_reset": (ctypes.c_int32, []),
     "gnn_timer_read": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
@@ -203,6 +222,53 @@ def gnn_prop_bwd(csr: gnn_csr, layer: gnn_layer, X, W_self, W_neigh, Y, dY,
                               _ptr(dW_neigh), _ptr(db_self), _ptr(db_neigh),
                               _ptr(workspace), _nbytes(workspace),
                               _stream(stream)), "gnn_prop_bwd")
+
+
+def gnn_gcn_saved_bytes(csr: gnn_csr, layer: gnn_layer) -> int:
+    return int(lib().gnn_gcn_saved_bytes(ctypes.byref(csr), ctypes.byref(layer)))
+
+
+def gnn_gcn_workspace_bytes(csr: gnn_csr, layer: gnn_layer) -> int:
+    return int(lib().gnn_gcn_workspace_bytes(ctypes.byref(csr), ctypes.byref(layer)))
+
+
+def gnn_gcn_fwd(csr: gnn_csr, layer: gnn_layer, X, W, b, Y, saved, workspace,
+                stream=None):
+    _check(lib().gnn_gcn_fwd(ctypes.byref(csr), ctypes.byref(layer), _ptr(X), _ptr(W),
+                             _ptr(b), _ptr(Y), _ptr(saved), _ptr(workspace),
+                             _nbytes(workspace), _stream(stream)), "gnn_gcn_fwd")
+
+
+def gnn_gcn_bwd(csr: gnn_csr, layer: gnn_layer, X, W, Y, dY, saved, dX, dW, db,
+                workspace, stream=None):
+    _check(lib().gnn_gcn_bwd(ctypes.byref(csr), ctypes.byref(layer), _ptr(X), _ptr(W),
+                             _ptr(Y), _ptr(dY), _ptr(saved), _ptr(dX), _ptr(dW),
+                             _ptr(db), _ptr(workspace), _nbytes(workspace),
+                             _stream(stream)), "gnn_gcn_bwd")
+
+
+def gnn_mixhop_saved_bytes(csr: gnn_csr, layer: gnn_layer, K: int) -> int:
+    return int(lib().gnn_mixhop_saved_bytes(ctypes.byref(csr), ctypes.byref(layer), int(K)))
+
+
+def gnn_mixhop_workspace_bytes(csr: gnn_csr, layer: gnn_layer, K: int) -> int:
+    return int(lib().gnn_mixhop_workspace_bytes(ctypes.byref(csr), ctypes.byref(layer),
+                                                int(K)))
+
+
+def gnn_mixhop_fwd(csr: gnn_csr, layer: gnn_layer, K: int, X, W, b, Y, saved,
+                   workspace, stream=None):
+    _check(lib().gnn_mixhop_fwd(ctypes.byref(csr), ctypes.byref(layer), int(K), _ptr(X),
+                                _ptr(W), _ptr(b), _ptr(Y), _ptr(saved), _ptr(workspace),
+                                _nbytes(workspace), _stream(stream)), "gnn_mixhop_fwd")
+
+
+def gnn_mixhop_bwd(csr: gnn_csr, layer: gnn_layer, K: int, X, W, Y, dY, saved, dX, dW,
+                   db, workspace, stream=None):
+    _check(lib().gnn_mixhop_bwd(ctypes.byref(csr), ctypes.byref(layer), int(K), _ptr(X),
+                                _ptr(W), _ptr(Y), _ptr(dY), _ptr(saved), _ptr(dX),
+                                _ptr(dW), _ptr(db), _ptr(workspace), _nbytes(workspace),
+                                _stream(stream)), "gnn_mixhop_bwd")
 
 
 def gnn_spmm_workspace_bytes(csr: gnn_csr, w: int) -> int:
