@@ -6,6 +6,7 @@
  */
 #include "gnn_oracle.h"
 
+#include <math.h>
 #include <stdlib.h>
 #include <string.h>
 #ifdef _OPENMP
@@ -408,6 +409,81 @@ void oracle_mixhop_bwd(int32_t n, const int32_t* indptr,
   free(D);
   free(V);
   free(U);
+}
+
+/* ------------------------------------- classifier, loss and weight update */
+
+/* Section 3.1 (Eqs. "mlp forward", "loss forward") and Algorithm 1:
+ *   Z = X W  (n x C),  X_MLP = ReLU(Z),  Y = sigma(X_MLP)
+ * sigma: kind 0 = row-wise softmax, kind 1 = element-wise sigmoid.
+ *   L = (1/n) sum_v CE(Y_v, T_v): softmax  -sum_c T log Y,
+ *                                  sigmoid -sum_c [T log Y + (1-T) log(1-Y)]
+ * Section 5.1: dL/dX_MLP = (Y - T) / n;  G = that * 1[X_MLP > 0] (the MLP's
+ * ReLU);  dW = X^T G;  dX = G W^T.  probs, dX may be NULL.  Returns L. */
+double oracle_classifier(int32_t n, int32_t f, int32_t C, const double* X,
+                         const double* W, const double* T, int32_t kind,
+                         double* probs, double* dW, double* dX) {
+  const size_t nc = (size_t)n * (size_t)C;
+  double* Z = (double*)malloc(sizeof(double) * (nc ? nc : 1));
+  double* G = (double*)malloc(sizeof(double) * (nc ? nc : 1));
+  oracle_mm_nn(n, C, f, X, W, Z);
+  double loss = 0.0;
+  for (int64_t v = 0; v < n; ++v) {
+    const double* z = Z + v * C;
+    const double* t = T + v * C;
+    double* g = G + v * C;
+    double row = 0.0;
+    if (kind == 0) {
+      double m = relu(z[0]);
+      for (int32_t c = 1; c < C; ++c) m = relu(z[c]) > m ? relu(z[c]) : m;
+      double s = 0.0;
+      for (int32_t c = 0; c < C; ++c) s += exp(relu(z[c]) - m);
+      for (int32_t c = 0; c < C; ++c) {
+        const double lp = relu(z[c]) - m - log(s); /* log Y */
+        const double y = exp(lp);
+        row -= t[c] * lp;
+        g[c] = y;
+      }
+    } else {
+      for (int32_t c = 0; c < C; ++c) {
+        const double x = relu(z[c]);
+        const double y = 1.0 / (1.0 + exp(-x));
+        /* log Y = -log(1 + e^-x), log(1-Y) = -x - log(1 + e^-x) */
+        const double l1 = -log1p(exp(-x));
+        row -= t[c] * l1 + (1.0 - t[c]) * (l1 - x);
+        g[c] = y;
+      }
+    }
+    loss += row;
+    for (int32_t c = 0; c < C; ++c) {
+      if (probs) probs[v * C + c] = g[c];
+      g[c] = z[c] > 0.0 ? (g[c] - t[c]) / (double)n : 0.0;
+    }
+  }
+  oracle_mm_tn(f, C, n, X, G, dW);
+  if (dX) oracle_mm_nt(n, f, C, G, W, dX);
+  free(Z);
+  free(G);
+  return loss / (double)n;
+}
+
+/* Weight update by the gradient (Algorithm 1): W -= lr g. */
+void oracle_sgd(int64_t count, double* W, const double* g, double lr) {
+  for (int64_t i = 0; i < count; ++i) W[i] -= lr * g[i];
+}
+
+/* Adam (the optimizer Algorithm 1 names): step t >= 1,
+ *   m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2;
+ *   W -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps). */
+void oracle_adam(int64_t count, double* W, const double* g, double* m,
+                 double* v, double lr, double b1, double b2, double eps,
+                 int32_t t) {
+  const double c1 = 1.0 - pow(b1, t), c2 = 1.0 - pow(b2, t);
+  for (int64_t i = 0; i < count; ++i) {
+    m[i] = b1 * m[i] + (1.0 - b1) * g[i];
+    v[i] = b2 * v[i] + (1.0 - b2) * g[i] * g[i];
+    W[i] -= lr * (m[i] / c1) / (sqrt(v[i] / c2) + eps);
+  }
 }
 
 /* ---------------------------------------------- per-output spot evaluation */

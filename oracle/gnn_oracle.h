@@ -140,6 +140,23 @@ void oracle_mixhop_bwd(int32_t n, const int32_t* indptr,
                        const double* W, const double* Y, const double* dY,
                        double* dX, double* dW, double* db);
 
+/* Classifier head and loss (Section 3.1, Algorithm 1): Z = X W (n x C),
+ * X_MLP = ReLU(Z), Y = sigma(X_MLP) with sigma a row softmax (kind 0) or an
+ * element-wise sigmoid (kind 1); L = mean over rows of the cross-entropy
+ * against T (n x C, 0/1).  Gradients (Section 5.1): dL/dX_MLP = (Y - T)/n,
+ * G = that * 1[X_MLP > 0], dW = X^T G, dX = G W^T.  probs (Y) and dX may be
+ * NULL.  Returns L. */
+double oracle_classifier(int32_t n, int32_t f, int32_t C, const double* X,
+                         const double* W, const double* T, int32_t kind,
+                         double* probs, double* dW, double* dX);
+
+/* Weight updates: plain gradient step, and Adam with bias correction at
+ * step t >= 1 (moments m, v updated in place). */
+void oracle_sgd(int64_t count, double* W, const double* g, double lr);
+void oracle_adam(int64_t count, double* W, const double* g, double* m,
+                 double* v, double lr, double b1, double b2, double eps,
+                 int32_t t);
+
 /* bfloat16 rounding of GEMM operands for the reduced-precision mode: each
  * value is first taken as float (the storage format), then rounded to the
  * nearest bfloat16 (8 significant bits), ties to even; NaN stays NaN. */

@@ -31,7 +31,7 @@ def build(force: bool = True) -> str:
         return _LIB
     tmp = _LIB + ".tmp%d" % os.getpid()
     cmd = ["gcc", "-O3", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
-           "-shared", "-fPIC", "-std=c99", "-Wall", "-o", tmp, _SRC]
+           "-shared", "-fPIC", "-std=c99", "-Wall", "-o", tmp, _SRC, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, _LIB)
     return _LIB
@@ -74,6 +74,11 @@ def lib():
                                    _F64P, _F64P, _F64P, _F64P],
                 "oracle_gcn_bwd": [i32, _I32P, _I32P, _F64P, i32, i32, _F64P,
                                    _F64P, _F64P, _F64P, _F64P, _F64P, _F64P],
+                "oracle_classifier": [i32, i32, i32, _F64P, _F64P, _F64P, i32,
+                                      _F64P, _F64P, _F64P],
+                "oracle_sgd": [i64, _F64P, _F64P, ctypes.c_double],
+                "oracle_adam": [i64, _F64P, _F64P, _F64P, _F64P, ctypes.c_double,
+                                ctypes.c_double, ctypes.c_double, ctypes.c_double, i32],
                 "oracle_mixhop_fwd": [i32, _I32P, _I32P, _F64P, i32, i32, i32,
                                       _F64P, _F64P, _F64P, _F64P],
                 "oracle_mixhop_bwd": [i32, _I32P, _I32P, _F64P, i32, i32, i32,
@@ -87,6 +92,8 @@ def lib():
                 fn.restype = ctypes.c_int32 if name in (
                     "oracle_transpose_values", "oracle_choose_order",
                     "oracle_num_threads") else None
+                if name == "oracle_classifier":
+                    fn.restype = ctypes.c_double
             _lib = L
         return _lib
 
@@ -314,6 +321,40 @@ def mixhop_bwd(g, x, w, K: int, y, dy, want_dx: bool = True,
                             _p(dy, _F64P), _p(out["dX"], _F64P), _p(out["dW"], _F64P),
                             _p(out["db"], _F64P))
     return out
+
+
+SOFTMAX, SIGMOID = 0, 1
+
+
+def classifier(x, w, t, kind: int, want_dx: bool = True) -> dict:
+    """Head + loss: returns loss, probs, dW, dX (see oracle_classifier)."""
+    x, w, t = _f64(x), _f64(w), _f64(t)
+    n, f = x.shape
+    C = w.shape[1]
+    assert w.shape == (f, C) and t.shape == (n, C)
+    probs = np.empty((n, C))
+    dw = np.empty((f, C))
+    dx = np.empty((n, f)) if want_dx else None
+    loss = lib().oracle_classifier(n, f, C, _p(x, _F64P), _p(w, _F64P), _p(t, _F64P),
+                                   int(kind), _p(probs, _F64P), _p(dw, _F64P),
+                                   _p(dx, _F64P))
+    return {"loss": float(loss), "probs": probs, "dW": dw, "dX": dx}
+
+
+def sgd(w, g, lr: float) -> np.ndarray:
+    w = _f64(w).copy()
+    g = _f64(g)
+    lib().oracle_sgd(w.size, _p(w, _F64P), _p(g, _F64P), float(lr))
+    return w
+
+
+def adam(w, g, m, v, lr, b1, b2, eps, t: int):
+    """Returns updated (w, m, v) as new arrays."""
+    w, m, v = _f64(w).copy(), _f64(m).copy(), _f64(v).copy()
+    g = _f64(g)
+    lib().oracle_adam(w.size, _p(w, _F64P), _p(g, _F64P), _p(m, _F64P), _p(v, _F64P),
+                      float(lr), float(b1), float(b2), float(eps), int(t))
+    return w, m, v
 
 
 def sage_stack(g, x, params, dy_top, want_dx_first: bool = True):

@@ -574,3 +574,71 @@ def test_mixhop_backward_on_asymmetric_values():
     ref = sum(np.linalg.matrix_power(at, k) @ gm[:, k * h:(k + 1) * h] @ w[:, k * h:(k + 1) * h].T
               for k in range(K + 1))
     assert rel(r["dX"], ref) < 1e-13
+
+
+# ------------------------------------ classifier head, loss, weight update
+
+def _cls_case(seed, n=12, f=5, C=4, kind=0):
+    for s in range(seed, seed + 60):
+        rng = np.random.default_rng(s)
+        x, w = rng.standard_normal((n, f)), rng.standard_normal((f, C))
+        if np.abs(x @ w).min() > 1e-3:  # away from the MLP ReLU kink
+            break
+    if kind == O.SOFTMAX:
+        t = np.eye(C)[rng.integers(0, C, n)]
+    else:
+        t = (rng.random((n, C)) < 0.4).astype(np.float64)
+    return x, w, t
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_classifier_gradients_finite_differences(kind):
+    x, w, t = _cls_case(30 + kind, kind=kind)
+    r = O.classifier(x, w, t, kind)
+    fd = _fd_grads(lambda: O.classifier(x, w, t, kind, want_dx=False)["loss"], [x, w])
+    assert rel(r["dX"], fd[0]) < 1e-6 and rel(r["dW"], fd[1]) < 1e-6
+
+
+def test_classifier_zero_weights_closed_forms():
+    x, _, t = _cls_case(5, C=7)
+    w = np.zeros((5, 7))
+    r = O.classifier(x, w, t, O.SOFTMAX)
+    assert abs(r["loss"] - np.log(7)) < 1e-15 and np.allclose(r["probs"], 1 / 7)
+    ts = (np.random.default_rng(1).random((12, 7)) < 0.5).astype(float)
+    r = O.classifier(x, w, ts, O.SIGMOID)
+    assert abs(r["loss"] - 7 * np.log(2)) < 1e-14 and np.allclose(r["probs"], 0.5)
+    # all logits at the ReLU floor: no gradient reaches W or X
+    assert np.all(r["dW"] == 0) and np.all(r["dX"] == 0)
+
+
+def test_classifier_probabilities():
+    x, w, t = _cls_case(8, kind=0)
+    p = O.classifier(x, w, t, O.SOFTMAX)["probs"]
+    assert np.allclose(p.sum(axis=1), 1, rtol=0, atol=1e-15) and np.all(p > 0)
+    z = np.maximum(x @ w, 0)
+    ps = O.classifier(x, w, t, O.SIGMOID)["probs"]
+    assert np.allclose(ps, 1 / (1 + np.exp(-z)), rtol=1e-14, atol=0)
+
+
+def test_classifier_confident_loss_closed_form():
+    # logit 20 on the true class, 0 on the other two: every row's softmax
+    # cross-entropy is log(1 + 2 e^-20) = 4.12e-9, here reached through
+    # log(sum of exponentials), i.e. to within the rounding of log near 1
+    n, C = 6, 3
+    x = np.eye(C)[np.arange(n) % C]
+    w = np.eye(C) * 20.0
+    r = O.classifier(x, w, x.copy(), O.SOFTMAX)
+    assert abs(r["loss"] - np.log1p(2 * np.exp(-20.0))) < 5e-16
+
+
+def test_adam_constant_gradient_closed_form():
+    # with a constant gradient the bias-corrected moments are g and g^2, so
+    # every step moves W by lr * g / (|g| + eps)
+    rng = np.random.default_rng(3)
+    w0, g = rng.standard_normal(50), rng.standard_normal(50)
+    w, m, v = w0.copy(), np.zeros(50), np.zeros(50)
+    lr, eps = 1e-3, 1e-8
+    for step in range(1, 6):
+        w, m, v = O.adam(w, g, m, v, lr, 0.9, 0.999, eps, step)
+    assert np.allclose(w, w0 - 5 * lr * g / (np.abs(g) + eps), rtol=0, atol=1e-12)
+    assert np.array_equal(O.sgd(w0, g, 0.5), w0 - 0.5 * g)
