@@ -70,6 +70,8 @@ def parse():
                     help="do not compute the first layer's input gradient")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the GCN and MixHop layer timings")
+    ap.add_argument("--no-train", action="store_true",
+                    help="skip the full training iteration timing")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run one plain device-to-device copy of MIB MiB "
                          "(reference point for hardware byte counters)")
@@ -278,6 +280,11 @@ def main():
     if not args.no_variants:
         out["variants"] = bench_variants(G, runtime, synth, torch, np, g, x, wl, args)
 
+    # one whole training iteration of Algorithm 1 on the same subgraph
+    if not args.no_train:
+        out["train_iteration"] = bench_train(G, runtime, synth, torch, dg, X, params, wl,
+                                             args, ms_step)
+
     if not args.no_cpu_baseline:
         from oracle import oracle as O
         import numpy as np  # noqa: F811
@@ -297,6 +304,48 @@ def main():
         log("cpu oracle %.1f ms/layer on %d threads" % (
             out["cpu_baseline"]["value"], out["cpu_baseline"]["cores"]))
     print(json.dumps(out), flush=True)
+
+
+def bench_train(G, runtime, synth, torch, dg, X, params, wl, args, ms_prop):
+    """ms per training iteration: preparation, the stack forward, classifier
+    and loss (the workload's class count and loss), the backward pass from
+    the classifier's input gradient, and an Adam update of every weight."""
+    c = synth.classifier_inputs(wl)
+    T = torch.from_numpy(c["targets"]).cuda()
+    tr = runtime.Trainer(dg, params, wl.f_in, c["w_mlp"], wl.multilabel, "adam", lr=1e-3)
+
+    def it():
+        dg.prepare()
+        tr.step(X, T)
+
+    for _ in range(args.warmup):
+        it()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        it()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    G.gnn_timer_reset()
+    G.gnn_timer_enable(True)
+    for _ in range(args.steps):
+        it()
+    torch.cuda.synchronize()
+    G.gnn_timer_enable(False)
+    kern = {}
+    for kname in G.KERNELS:
+        kms, launches, _ = G.gnn_timer_read(kname)
+        if launches:
+            kern[kname] = {"ms_per_iteration": round(kms / args.steps, 4),
+                           "launches": launches // args.steps}
+    G.gnn_timer_reset()
+    loss = float(tr.loss.item())
+    log("train iteration: %.4f ms (loss %.4f after %d Adam steps)" % (ms, loss, tr.t))
+    return {"ms_per_iteration": round(ms, 5),
+            "head": "%d classes, %s" % (wl.classes, "sigmoid, multi-label"
+                                         if wl.multilabel else "softmax"),
+            "optimizer": "adam", "propagation_share": round(ms_prop / ms, 4),
+            "loss_after": round(loss, 6), "kernels": kern}
 
 
 def bench_variants(G, runtime, synth, torch, np, g, x, wl, args):

@@ -244,6 +244,49 @@ gnn_status gnn_mixhop_bwd(const gnn_csr* csr, const gnn_layer* layer,
                           float* dX, float* dW, float* db, void* workspace,
                           size_t workspace_bytes, hipStream_t stream);
 
+/* --------------------------------------- classifier, loss, weight update */
+
+/* Section 3.1 (Eqs. "mlp forward", "loss forward") and Algorithm 1: the
+ * classifier head and loss that follow the GNN layers, with the gradients
+ * of Section 5.1:
+ *   XM = ReLU(X W)      X n x f (stride ld_x), W f x C row-major
+ *   Y  = row softmax of XM (GNN_LOSS_SOFTMAX) or sigmoid(XM) element-wise
+ *        (GNN_LOSS_SIGMOID)
+ *   loss = (1/n) sum over rows of the cross-entropy of Y against T
+ *        (n x C, stride ld_t, entries 0 or 1; one 1 per row for softmax)
+ *   G  = (Y - T) / n * 1[XM > 0];   dW = X^T G (f x C);   dX = G W^T
+ * `loss` is one float of device memory.  Optional outputs (NULL to skip):
+ * xm = X_MLP (n x C, stride ld_xm), probs = Y (stride ld_p), dX (stride
+ * ld_dx).  flags: GNN_FLAG_BF16 for the three products.  The loss is summed
+ * in a fixed order (bit-reproducible).  No output may overlap an input,
+ * another output or the workspace.  Workspace:
+ * gnn_classifier_workspace_bytes(n, f, C).  n = 0 gives loss 0 and dW = 0. */
+#define GNN_LOSS_SOFTMAX 0
+#define GNN_LOSS_SIGMOID 1
+size_t gnn_classifier_workspace_bytes(int32_t n, int32_t f, int32_t C);
+gnn_status gnn_classifier(int32_t n, int32_t f, int32_t C, int32_t kind,
+                          uint32_t flags, const float* X, int64_t ld_x,
+                          const float* W, const float* T, int64_t ld_t,
+                          float* xm, int64_t ld_xm, float* probs, int64_t ld_p,
+                          float* loss, float* dW, float* dX, int64_t ld_dx,
+                          void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
+/* Weight update of Algorithm 1 (which leaves the rule open: plain gradient
+ * descent, or Adam) on `count` contiguous floats (device):
+ *   SGD:   W -= lr G
+ *   Adam:  m = b1 m + (1 - b1) G;  v = b2 v + (1 - b2) G^2;
+ *          W -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps),  t >= 1
+ * m and v (zero before the first step) are updated in place; no two
+ * arrays may overlap.  The hyperparameters are host doubles: 1 - b1,
+ * 1 - b2 and the bias corrections are formed in double and rounded once to
+ * fp32, the precision of the update itself. */
+gnn_status gnn_sgd_step(int64_t count, float* W, const float* G, double lr,
+                        hipStream_t stream);
+gnn_status gnn_adam_step(int64_t count, float* W, const float* G, float* m,
+                         float* v, double lr, double beta1, double beta2,
+                         double eps, int32_t t, hipStream_t stream);
+
 /* ------------------------------------------------------------- kernels */
 
 /* Feature / gradient propagation alone (Section 5.1's first kernel, the
@@ -285,7 +328,9 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
 #define GNN_K_COLSUM 8        /* bias-gradient column sums */
 #define GNN_K_PLAN 9          /* aggregation plan build */
 #define GNN_K_TRANSPOSE 10    /* transposed values (Algorithm 6) */
-#define GNN_K_COUNT 11
+#define GNN_K_LOSS 11         /* classifier loss and its gradient */
+#define GNN_K_UPDATE 12       /* weight update (SGD or Adam) */
+#define GNN_K_COUNT 13
 
 /* When enabled, every kernel launch is bracketed by a pair of HIP events on
  * its stream.  gnn_timer_read synchronises on the recorded events and

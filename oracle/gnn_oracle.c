@@ -419,14 +419,24 @@ void oracle_mixhop_bwd(int32_t n, const int32_t* indptr,
  *   L = (1/n) sum_v CE(Y_v, T_v): softmax  -sum_c T log Y,
  *                                  sigmoid -sum_c [T log Y + (1-T) log(1-Y)]
  * Section 5.1: dL/dX_MLP = (Y - T) / n;  G = that * 1[X_MLP > 0] (the MLP's
- * ReLU);  dW = X^T G;  dX = G W^T.  probs, dX may be NULL.  Returns L. */
+ * ReLU);  dW = X^T G;  dX = G W^T.  probs, dX may be NULL.  Returns L.
+ * relu_on (n x C, may be NULL) supplies the ReLU's decision instead of
+ * Z > 0: X_MLP = Z where it is 1, else 0, and the derivative is relu_on
+ * (the decision another implementation took at its own rounding). */
 double oracle_classifier(int32_t n, int32_t f, int32_t C, const double* X,
                          const double* W, const double* T, int32_t kind,
-                         double* probs, double* dW, double* dX) {
+                         double* probs, double* dW, double* dX,
+                         const uint8_t* relu_on) {
   const size_t nc = (size_t)n * (size_t)C;
   double* Z = (double*)malloc(sizeof(double) * (nc ? nc : 1));
   double* G = (double*)malloc(sizeof(double) * (nc ? nc : 1));
   oracle_mm_nn(n, C, f, X, W, Z);
+  /* Z becomes X_MLP; `on` keeps the ReLU's derivative */
+  uint8_t* on = (uint8_t*)malloc(nc ? nc : 1);
+  for (size_t i = 0; i < nc; ++i) {
+    on[i] = relu_on ? (relu_on[i] != 0) : (Z[i] > 0.0);
+    Z[i] = on[i] ? Z[i] : 0.0;
+  }
   double loss = 0.0;
   for (int64_t v = 0; v < n; ++v) {
     const double* z = Z + v * C;
@@ -434,19 +444,19 @@ double oracle_classifier(int32_t n, int32_t f, int32_t C, const double* X,
     double* g = G + v * C;
     double row = 0.0;
     if (kind == 0) {
-      double m = relu(z[0]);
-      for (int32_t c = 1; c < C; ++c) m = relu(z[c]) > m ? relu(z[c]) : m;
+      double m = z[0];
+      for (int32_t c = 1; c < C; ++c) m = z[c] > m ? z[c] : m;
       double s = 0.0;
-      for (int32_t c = 0; c < C; ++c) s += exp(relu(z[c]) - m);
+      for (int32_t c = 0; c < C; ++c) s += exp(z[c] - m);
       for (int32_t c = 0; c < C; ++c) {
-        const double lp = relu(z[c]) - m - log(s); /* log Y */
+        const double lp = z[c] - m - log(s); /* log Y */
         const double y = exp(lp);
         row -= t[c] * lp;
         g[c] = y;
       }
     } else {
       for (int32_t c = 0; c < C; ++c) {
-        const double x = relu(z[c]);
+        const double x = z[c];
         const double y = 1.0 / (1.0 + exp(-x));
         /* log Y = -log(1 + e^-x), log(1-Y) = -x - log(1 + e^-x) */
         const double l1 = -log1p(exp(-x));
@@ -457,11 +467,12 @@ double oracle_classifier(int32_t n, int32_t f, int32_t C, const double* X,
     loss += row;
     for (int32_t c = 0; c < C; ++c) {
       if (probs) probs[v * C + c] = g[c];
-      g[c] = z[c] > 0.0 ? (g[c] - t[c]) / (double)n : 0.0;
+      g[c] = on[v * C + c] ? (g[c] - t[c]) / (double)n : 0.0;
     }
   }
   oracle_mm_tn(f, C, n, X, G, dW);
   if (dX) oracle_mm_nt(n, f, C, G, W, dX);
+  free(on);
   free(Z);
   free(G);
   return loss / (double)n;
@@ -472,7 +483,8 @@ void oracle_sgd(int64_t count, double* W, const double* g, double lr) {
   for (int64_t i = 0; i < count; ++i) W[i] -= lr * g[i];
 }
 
-/* Adam (the optimizer Algorithm 1 names): step t >= 1,
+/* Adam (Algorithm 1 leaves the update rule open; Adam is offered beside
+ * plain gradient descent): step t >= 1,
  *   m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2;
  *   W -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps). */
 void oracle_adam(int64_t count, double* W, const double* g, double* m,

@@ -145,10 +145,12 @@ void oracle_mixhop_bwd(int32_t n, const int32_t* indptr,
  * element-wise sigmoid (kind 1); L = mean over rows of the cross-entropy
  * against T (n x C, 0/1).  Gradients (Section 5.1): dL/dX_MLP = (Y - T)/n,
  * G = that * 1[X_MLP > 0], dW = X^T G, dX = G W^T.  probs (Y) and dX may be
- * NULL.  Returns L. */
+ * NULL.  Returns L.  relu_on (n x C bytes, may be NULL) gives the MLP ReLU's
+ * decision instead of Z > 0. */
 double oracle_classifier(int32_t n, int32_t f, int32_t C, const double* X,
                          const double* W, const double* T, int32_t kind,
-                         double* probs, double* dW, double* dX);
+                         double* probs, double* dW, double* dX,
+                         const uint8_t* relu_on);
 
 /* Weight updates: plain gradient step, and Adam with bias correction at
  * step t >= 1 (moments m, v updated in place). */

@@ -23,6 +23,7 @@ _lib = None
 
 _I32P = ctypes.POINTER(ctypes.c_int32)
 _F64P = ctypes.POINTER(ctypes.c_double)
+_U8P = ctypes.POINTER(ctypes.c_uint8)
 
 
 def build(force: bool = True) -> str:
@@ -75,7 +76,7 @@ def lib():
                 "oracle_gcn_bwd": [i32, _I32P, _I32P, _F64P, i32, i32, _F64P,
                                    _F64P, _F64P, _F64P, _F64P, _F64P, _F64P],
                 "oracle_classifier": [i32, i32, i32, _F64P, _F64P, _F64P, i32,
-                                      _F64P, _F64P, _F64P],
+                                      _F64P, _F64P, _F64P, _U8P],
                 "oracle_sgd": [i64, _F64P, _F64P, ctypes.c_double],
                 "oracle_adam": [i64, _F64P, _F64P, _F64P, _F64P, ctypes.c_double,
                                 ctypes.c_double, ctypes.c_double, ctypes.c_double, i32],
@@ -326,18 +327,23 @@ def mixhop_bwd(g, x, w, K: int, y, dy, want_dx: bool = True,
 SOFTMAX, SIGMOID = 0, 1
 
 
-def classifier(x, w, t, kind: int, want_dx: bool = True) -> dict:
-    """Head + loss: returns loss, probs, dW, dX (see oracle_classifier)."""
+def classifier(x, w, t, kind: int, want_dx: bool = True, relu_on=None) -> dict:
+    """Head + loss: returns loss, probs, dW, dX (see oracle_classifier).
+    relu_on: optional n x C booleans, the MLP ReLU's decision."""
     x, w, t = _f64(x), _f64(w), _f64(t)
     n, f = x.shape
     C = w.shape[1]
     assert w.shape == (f, C) and t.shape == (n, C)
+    on = None
+    if relu_on is not None:
+        on = np.ascontiguousarray(relu_on, np.uint8)
+        assert on.shape == (n, C)
     probs = np.empty((n, C))
     dw = np.empty((f, C))
     dx = np.empty((n, f)) if want_dx else None
     loss = lib().oracle_classifier(n, f, C, _p(x, _F64P), _p(w, _F64P), _p(t, _F64P),
                                    int(kind), _p(probs, _F64P), _p(dw, _F64P),
-                                   _p(dx, _F64P))
+                                   _p(dx, _F64P), _p(on, _U8P))
     return {"loss": float(loss), "probs": probs, "dW": dw, "dX": dx}
 
 
@@ -376,3 +382,58 @@ def sage_stack(g, x, params, dy_top, want_dx_first: bool = True):
         grads[l] = r
         dy = r["dX"]
     return {"acts": acts, "ys": ys, "grads": grads}
+
+
+def train_step(g, x, params, w_mlp, targets, kind: int, opt: str = "sgd",
+               lr: float = 0.01, state=None, t: int = 1, b1: float = 0.9,
+               b2: float = 0.999, eps: float = 1e-8, forced=None):
+    """One iteration of Algorithm 1 on a given subgraph: the L layers forward,
+    classifier and loss (Section 3.1), the backward pass of Section 5.1 from
+    the classifier's input gradient down, then every weight updated by SGD or
+    Adam.  state: per-parameter (m, v) pairs for Adam, in the order
+    [W_MLP, then W_self, W_neigh (, b_self, b_neigh) of each layer].
+    forced: optional {"ys": [Y of layer 1..L], "relu_on": n x C booleans}
+    taken in place of the forward pass's own layer outputs (the inputs of
+    the layers above, the ReLU masks of the backward pass) and of the MLP
+    ReLU's decision, so that every ReLU decision is another implementation's.
+    Returns the loss, the gradients, the updated weights and the new state."""
+    acts, ys = [_f64(x)], []
+    for l, p in enumerate(params):
+        if forced is not None:
+            y = _f64(forced["ys"][l])
+        else:
+            y = sage_fwd(g, acts[-1], p.w_self, p.w_neigh, p.b_self, p.b_neigh)
+        ys.append(y)
+        acts.append(y)
+    head = classifier(acts[-1], w_mlp, targets, kind, want_dx=True,
+                      relu_on=None if forced is None else forced.get("relu_on"))
+    grads = [None] * len(params)
+    dy = head["dX"]
+    for l in reversed(range(len(params))):
+        p = params[l]
+        r = sage_bwd(g, acts[l], p.w_self, p.w_neigh, ys[l], dy, want_dx=l > 0,
+                     want_db=p.b_self is not None)
+        grads[l] = r
+        dy = r["dX"]
+    weights = [_f64(w_mlp)]
+    gs = [head["dW"]]
+    for p, r in zip(params, grads):
+        weights += [_f64(p.w_self), _f64(p.w_neigh)]
+        gs += [r["dW_self"], r["dW_neigh"]]
+        if p.b_self is not None:
+            weights += [_f64(p.b_self), _f64(p.b_neigh)]
+            gs += [r["db_self"], r["db_neigh"]]
+    if state is None:
+        state = [(np.zeros_like(w), np.zeros_like(w)) for w in weights]
+    new_w, new_state = [], []
+    for w, gr, (m, v) in zip(weights, gs, state):
+        if opt == "sgd":
+            new_w.append(sgd(w, gr, lr))
+            new_state.append((m, v))
+        else:
+            w2, m2, v2 = adam(w, gr, m, v, lr, b1, b2, eps, t)
+            new_w.append(w2)
+            new_state.append((m2, v2))
+    return {"loss": head["loss"], "probs": head["probs"], "acts": acts,
+            "head": head, "grads": grads, "flat_grads": gs, "weights": new_w,
+            "state": new_state}

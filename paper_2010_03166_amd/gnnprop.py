@@ -20,9 +20,11 @@ GNN_OK = 0
 GNN_FLAG_BF16 = 0x1
 GNN_FLAG_DY_MASKED = 0x2
 GNN_FLAG_DX_MASKED = 0x4
+GNN_LOSS_SOFTMAX = 0
+GNN_LOSS_SIGMOID = 1
 KERNELS = {"spmm": 0, "spmm_reduce": 1, "gemm_nn": 2, "gemm_tn": 3,
            "gemm_nt": 4, "gemm_tt": 5, "gemm_reduce": 6, "mask": 7,
-           "colsum": 8, "plan": 9, "transpose": 10}
+           "colsum": 8, "plan": 9, "transpose": 10, "loss": 11, "update": 12}
 
 _lib = None
 
@@ -96,6 +98,16 @@ EXPORTS = {
     "gnn_mixhop_bwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer),
                                         ctypes.c_int32] + [ctypes.c_void_p] * 9
                        + [ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_classifier_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32] * 3),
+    "gnn_classifier": (ctypes.c_int32, [ctypes.c_int32] * 4 + [ctypes.c_uint32,
+                       ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                       ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                       ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                       ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_sgd_step": (ctypes.c_int32, [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_double, ctypes.c_void_p]),
+    "gnn_adam_step": (ctypes.c_int32, [ctypes.c_int64] + [ctypes.c_void_p] * 4
+                      + [ctypes.c_double] * 4 + [ctypes.c_int32, ctypes.c_void_p]),
     "gnn_timer_enable": (ctypes.c_int32, [ctypes.c_int32]),
     "gnn_timer_reset": (ctypes.c_int32, []),
     "gnn_timer_read": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
@@ -269,6 +281,32 @@ def gnn_mixhop_bwd(csr: gnn_csr, layer: gnn_layer, K: int, X, W, Y, dY, saved, d
                                 _ptr(W), _ptr(Y), _ptr(dY), _ptr(saved), _ptr(dX),
                                 _ptr(dW), _ptr(db), _ptr(workspace), _nbytes(workspace),
                                 _stream(stream)), "gnn_mixhop_bwd")
+
+
+def gnn_classifier_workspace_bytes(n: int, f: int, C: int) -> int:
+    return int(lib().gnn_classifier_workspace_bytes(int(n), int(f), int(C)))
+
+
+def gnn_classifier(n: int, f: int, C: int, kind: int, flags: int, X, ld_x: int, W, T,
+                   ld_t: int, xm, ld_xm: int, probs, ld_p: int, loss, dW, dX, ld_dx: int,
+                   workspace, stream=None):
+    _check(lib().gnn_classifier(int(n), int(f), int(C), int(kind), int(flags), _ptr(X),
+                                int(ld_x), _ptr(W), _ptr(T), int(ld_t), _ptr(xm),
+                                int(ld_xm), _ptr(probs), int(ld_p), _ptr(loss), _ptr(dW),
+                                _ptr(dX), int(ld_dx), _ptr(workspace), _nbytes(workspace),
+                                _stream(stream)), "gnn_classifier")
+
+
+def gnn_sgd_step(count: int, W, G_, lr: float, stream=None):
+    _check(lib().gnn_sgd_step(int(count), _ptr(W), _ptr(G_), float(lr), _stream(stream)),
+           "gnn_sgd_step")
+
+
+def gnn_adam_step(count: int, W, G_, m, v, lr: float, beta1: float, beta2: float,
+                  eps: float, t: int, stream=None):
+    _check(lib().gnn_adam_step(int(count), _ptr(W), _ptr(G_), _ptr(m), _ptr(v), float(lr),
+                               float(beta1), float(beta2), float(eps), int(t),
+                               _stream(stream)), "gnn_adam_step")
 
 
 def gnn_spmm_workspace_bytes(csr: gnn_csr, w: int) -> int:

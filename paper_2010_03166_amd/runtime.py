@@ -151,3 +151,80 @@ class SageStack:
                            L["db_self"], L["db_neigh"], self.workspace, stream)
             d = dx
         return self.layers[0]["dX"] if want_dx_first else None
+
+
+class Trainer:
+    """One training iteration of Algorithm 1 on a prepared subgraph: the
+    stack's forward pass, the classifier and loss (Section 3.1), the backward
+    pass from the classifier's input gradient down (Section 5.1), then SGD or
+    Adam on every weight.  All arithmetic runs in libgnnprop; the loss stays
+    on the device (read it with `loss.item()` when needed)."""
+
+    def __init__(self, graph: DeviceGraph, params: Sequence, f_in: int, w_mlp,
+                 multilabel: bool, optimizer: str = "adam", lr: float = 0.01,
+                 betas=(0.9, 0.999), eps: float = 1e-8, order: int = 0,
+                 flags: int = 0, pad: int = 16, fuse_masks: bool = False,
+                 want_probs: bool = False, keep_xm: bool = False,
+                 device: str = "cuda"):
+        """want_probs / keep_xm: keep the class probabilities Y / the MLP
+        output X_MLP = ReLU(X^(L) W_MLP) of the last iteration in `probs` /
+        `xm` (n x C views)."""
+        if optimizer not in ("sgd", "adam"):
+            raise ValueError("optimizer must be 'sgd' or 'adam'")
+        self.stack = SageStack(graph, params, f_in, order, flags, pad, fuse_masks, device)
+        self.n = graph.n
+        self.kind = G.GNN_LOSS_SIGMOID if multilabel else G.GNN_LOSS_SOFTMAX
+        self.flags = flags & G.GNN_FLAG_BF16
+        self.optimizer, self.lr, self.betas, self.eps = optimizer, lr, betas, eps
+        top = self.stack.layers[-1]
+        self.f_top = 2 * top["h"]
+        self.C = int(w_mlp.shape[1])
+        assert w_mlp.shape == (self.f_top, self.C)
+        self.W_mlp = torch.from_numpy(np.ascontiguousarray(w_mlp, np.float32)).to(device)
+        self.dW_mlp = torch.empty_like(self.W_mlp)
+        # the classifier writes dX^(L) at the top layer's Y stride, which is
+        # the stride the stack's backward pass expects
+        self.dX_top = torch.empty((max(self.n, 1), top["Y"].stride(0)),
+                                  device=device)[: self.n, : self.f_top]
+        ld_p = _round_up(self.C, 4)
+        self.probs = torch.empty((max(self.n, 1), ld_p), device=device)[: self.n, : self.C] \
+            if want_probs else None
+        self.xm = torch.empty((max(self.n, 1), ld_p), device=device)[: self.n, : self.C] \
+            if keep_xm else None
+        self.loss = torch.zeros(1, device=device)
+        self.cls_ws = torch.empty(max(G.gnn_classifier_workspace_bytes(self.n, self.f_top,
+                                                                      self.C), 256),
+                                  dtype=torch.uint8, device=device)
+        # (weight, gradient) pairs in a fixed order: W_MLP, then per layer
+        # W_self, W_neigh (, b_self, b_neigh)
+        self.pairs = [(self.W_mlp, self.dW_mlp)]
+        for L in self.stack.layers:
+            self.pairs += [(L["W_self"], L["dW_self"]), (L["W_neigh"], L["dW_neigh"])]
+            if L["b_self"] is not None:
+                self.pairs += [(L["b_self"], L["db_self"]), (L["b_neigh"], L["db_neigh"])]
+        self.state = [(torch.zeros_like(w), torch.zeros_like(w)) for w, _ in self.pairs] \
+            if optimizer == "adam" else None
+        self.t = 0
+
+    def step(self, X: torch.Tensor, targets: torch.Tensor, stream=None) -> torch.Tensor:
+        """X: n x f_in (any row stride); targets: n x C 0/1 floats."""
+        top = self.stack.forward(X, stream)
+        ld_top = top.stride(0) if self.n else self.f_top
+        ld_t = targets.stride(0) if self.n else self.C
+        G.gnn_classifier(self.n, self.f_top, self.C, self.kind, self.flags, top, ld_top,
+                         self.W_mlp, targets, ld_t, self.xm,
+                         self.xm.stride(0) if self.xm is not None else self.C, self.probs,
+                         self.probs.stride(0) if self.probs is not None else self.C,
+                         self.loss, self.dW_mlp, self.dX_top,
+                         self.dX_top.stride(0) if self.n else self.f_top, self.cls_ws,
+                         stream)
+        self.stack.backward(self.dX_top, want_dx_first=False, stream=stream)
+        self.t += 1
+        for i, (w, gr) in enumerate(self.pairs):
+            if self.optimizer == "sgd":
+                G.gnn_sgd_step(w.numel(), w, gr, self.lr, stream)
+            else:
+                m, v = self.state[i]
+                G.gnn_adam_step(w.numel(), w, gr, m, v, self.lr, self.betas[0],
+                                self.betas[1], self.eps, self.t, stream)
+        return self.loss

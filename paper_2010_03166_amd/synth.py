@@ -26,6 +26,8 @@ import numpy as np
 STREAM_GRAPH = 0
 STREAM_X = 1
 STREAM_DY = 99
+STREAM_LABELS = 98
+STREAM_W_MLP = 97
 STREAM_W0 = 10  # + layer index
 
 
@@ -42,20 +44,26 @@ class Workload:
     f_in: int = 50        # input feature width
     layers: int = 2
     hidden: int = 128     # width of each concat half
+    classes: int = 2      # C: columns of the classifier output
+    multilabel: bool = False  # sigmoid + per-class CE, else softmax + CE
 
 
 WORKLOADS: Dict[str, Workload] = {w.name: w for w in [
     Workload("er-n1000-f50-h128-L2", 0, 1000, "er", 10.0,
-             f_in=50, layers=2, hidden=128),
+             f_in=50, layers=2, hidden=128, classes=121, multilabel=True),
     Workload("cl2.1-n8000-f602-h512-L2", 1, 8000, "chung-lu", 15.0,
-             gamma=2.1, kmax=1000.0, f_in=602, layers=2, hidden=512),
+             gamma=2.1, kmax=1000.0, f_in=602, layers=2, hidden=512, classes=41),
     Workload("cl2.3-n8000-f300-h512-L3", 2, 8000, "chung-lu", 20.0,
-             gamma=2.3, f_in=300, layers=3, hidden=512),
+             gamma=2.3, f_in=300, layers=3, hidden=512, classes=100, multilabel=True),
     Workload("cl2.1-n20000-f200-h512-L5", 3, 20000, "chung-lu", 30.0,
-             gamma=2.1, f_in=200, layers=5, hidden=512),
+             gamma=2.1, f_in=200, layers=5, hidden=512, classes=107, multilabel=True),
     Workload("cl1.9-n50000-f256-h1024-L3", 4, 50000, "chung-lu", 40.0,
-             gamma=1.9, kmax=5000.0, f_in=256, layers=3, hidden=1024),
+             gamma=1.9, kmax=5000.0, f_in=256, layers=3, hidden=1024, classes=107,
+             multilabel=True),
 ]}
+# Classes follow the paper's dataset table for the feature width each
+# workload copies (50: 121 labels, 602: 41 classes, 300: 100 labels, 200: 107
+# labels); the 256-wide one takes 107 labels.
 
 # The workload the benchmark times and the small one the oracle finishes fast.
 BENCH_WORKLOAD = "cl2.1-n8000-f602-h512-L2"
@@ -312,3 +320,27 @@ def workload_inputs(wl: Workload, bias: bool = False) -> dict:
     dy = rng_for(wl.case, STREAM_DY).standard_normal(
         (wl.n, 2 * wl.hidden)).astype(np.float32)
     return {"graph": g, "x": x, "params": params, "dy": dy}
+
+
+# ------------------------------------------------------ classifier inputs
+
+LABEL_DENSITY = 0.25  # probability that a label is on (multi-label targets)
+
+
+def labels(n: int, C: int, multilabel: bool, seed_or_rng) -> np.ndarray:
+    """0/1 float32 targets (n, C): one uniform class per row (single label),
+    or each label on independently with probability LABEL_DENSITY."""
+    rng = seed_or_rng if isinstance(seed_or_rng, np.random.Generator) else \
+        np.random.default_rng(seed_or_rng)
+    if multilabel:
+        return (rng.random((n, C)) < LABEL_DENSITY).astype(np.float32)
+    t = np.zeros((n, C), np.float32)
+    t[np.arange(n), rng.integers(0, C, size=n)] = 1.0
+    return t
+
+
+def classifier_inputs(wl: Workload) -> dict:
+    """Glorot W_MLP (2 * hidden x C) and the synthetic targets."""
+    w = glorot(2 * wl.hidden, wl.classes, rng_for(wl.case, STREAM_W_MLP))
+    t = labels(wl.n, wl.classes, wl.multilabel, rng_for(wl.case, STREAM_LABELS))
+    return {"w_mlp": w, "targets": t}

@@ -642,3 +642,109 @@ def test_adam_constant_gradient_closed_form():
         w, m, v = O.adam(w, g, m, v, lr, 0.9, 0.999, eps, step)
     assert np.allclose(w, w0 - 5 * lr * g / (np.abs(g) + eps), rtol=0, atol=1e-12)
     assert np.array_equal(O.sgd(w0, g, 0.5), w0 - 0.5 * g)
+
+
+# ------------------------------------------------- full training iteration
+
+def _train_case(kind, bias, seed=4):
+    g = synth.random_graph(10, 3.0, seed)
+    g.values = g.values.astype(np.float64)
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((10, 4))
+    params = []
+    for f, h in ((4, 3), (6, 3)):
+        p = synth.LayerParams(rng.standard_normal((f, h)), rng.standard_normal((f, h)))
+        if bias:
+            p.b_self, p.b_neigh = rng.standard_normal(h), rng.standard_normal(h)
+        params.append(p)
+    w_mlp = rng.standard_normal((6, 3))
+    t = np.eye(3)[rng.integers(0, 3, 10)] if kind == O.SOFTMAX else \
+        (rng.random((10, 3)) < 0.4).astype(np.float64)
+    return g, x, params, w_mlp, t
+
+
+def _loss_only(g, x, params, w_mlp, t, kind):
+    a = x
+    for p in params:
+        a = O.sage_fwd(g, a, p.w_self, p.w_neigh, p.b_self, p.b_neigh)
+    return O.classifier(a, w_mlp, t, kind, want_dx=False)["loss"]
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("bias", [False, True])
+def test_train_step_gradients_finite_differences(kind, bias):
+    # the composed backward pass (classifier gradient fed into the top layer
+    # as its dY, the top layer's ReLU mask applied there) against central
+    # differences of the end-to-end loss in every weight
+    g, x, params, w_mlp, t = _train_case(kind, bias)
+    r = O.train_step(g, x, params, w_mlp, t, kind, "sgd", lr=0.0)
+    arrays = [w_mlp]
+    for p in params:
+        arrays += [p.w_self, p.w_neigh] + ([p.b_self, p.b_neigh] if bias else [])
+    fd = _fd_grads(lambda: _loss_only(g, x, params, w_mlp, t, kind), arrays)
+    assert len(fd) == len(r["flat_grads"])
+    for a, b in zip(r["flat_grads"], fd):
+        assert rel(a, b) < 1e-6
+    assert abs(r["loss"] - _loss_only(g, x, params, w_mlp, t, kind)) < 1e-14
+    # lr = 0 leaves every weight as it was
+    for a, b in zip(r["weights"], arrays):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_train_step_descends(kind):
+    # a small SGD step along the gradient lowers the loss by about
+    # lr * |grad|^2 (first-order Taylor term)
+    g, x, params, w_mlp, t = _train_case(kind, True, seed=7)
+    lr = 1e-5
+    r = O.train_step(g, x, params, w_mlp, t, kind, "sgd", lr=lr)
+    ws = r["weights"]
+    newp, k = [], 1
+    for p in params:
+        newp.append(synth.LayerParams(ws[k], ws[k + 1], ws[k + 2], ws[k + 3]))
+        k += 4
+    drop = r["loss"] - _loss_only(g, x, newp, ws[0], t, kind)
+    sq = sum(float((gr ** 2).sum()) for gr in r["flat_grads"])
+    assert drop > 0 and abs(drop - lr * sq) < 1e-3 * lr * sq
+
+
+def test_train_step_adam_first_step():
+    # at t = 1 the bias-corrected moments are g and g^2: each weight moves by
+    # lr * g / (|g| + eps)
+    g, x, params, w_mlp, t = _train_case(O.SOFTMAX, False)
+    r = O.train_step(g, x, params, w_mlp, t, O.SOFTMAX, "adam", lr=1e-2, t=1)
+    arrays = [w_mlp] + [a for p in params for a in (p.w_self, p.w_neigh)]
+    for w0, w1, gr in zip(arrays, r["weights"], r["flat_grads"]):
+        assert np.allclose(w1, w0 - 1e-2 * gr / (np.abs(gr) + 1e-8), rtol=0, atol=1e-15)
+
+
+def test_classifier_supplied_relu_decision():
+    # the natural decision given explicitly reproduces the default exactly;
+    # with every unit on, the head is linear and its loss smooth, so central
+    # differences of that loss pin the gradient under a supplied decision
+    for kind in (O.SOFTMAX, O.SIGMOID):
+        x, w, t = _cls_case(40 + kind, kind=kind)
+        a = O.classifier(x, w, t, kind)
+        b = O.classifier(x, w, t, kind, relu_on=(x @ w) > 0)
+        assert a["loss"] == b["loss"]
+        for k in ("probs", "dW", "dX"):
+            assert np.array_equal(a[k], b[k]), k
+        on = np.ones((x.shape[0], w.shape[1]), bool)
+        r = O.classifier(x, w, t, kind, relu_on=on)
+        fd = _fd_grads(lambda: O.classifier(x, w, t, kind, want_dx=False, relu_on=on)["loss"],
+                       [x, w])
+        assert rel(r["dX"], fd[0]) < 1e-6 and rel(r["dW"], fd[1]) < 1e-6
+        # and it differs from the ReLU head (some logits are negative)
+        assert not np.allclose(r["dW"], a["dW"])
+
+
+def test_train_step_forced_decisions_reproduce_default():
+    # supplying the oracle's own layer outputs and MLP decision changes nothing
+    g, x, params, w_mlp, t = _train_case(O.SIGMOID, True)
+    r = O.train_step(g, x, params, w_mlp, t, O.SIGMOID, "sgd", lr=0.1)
+    z = r["acts"][-1] @ w_mlp
+    f = O.train_step(g, x, params, w_mlp, t, O.SIGMOID, "sgd", lr=0.1,
+                     forced={"ys": r["acts"][1:], "relu_on": z > 0})
+    assert f["loss"] == r["loss"]
+    for a, b in zip(f["flat_grads"] + f["weights"], r["flat_grads"] + r["weights"]):
+        assert np.array_equal(a, b)
