@@ -287,6 +287,51 @@ gnn_status gnn_adam_step(int64_t count, float* W, const float* G, float* m,
                          float* v, double lr, double beta1, double beta2,
                          double eps, int32_t t, hipStream_t stream);
 
+/* ------------------------------------------- subgraph preparation (prep) */
+
+/* The subgraph of the full training graph induced by a sampled node set
+ * (the last step of the samplers, Section 4, Algorithms 2 and 3; Algorithm
+ * 1's adjacency matrix of G_s), on the GPU against a full graph resident in
+ * device memory:
+ *   full graph: n_full nodes, CSR with int64 row pointers indptr (n_full + 1)
+ *     and int32 indices (nnz_full), rows sorted, symmetric, unweighted;
+ *   nodes: n_s full-graph ids (device), strictly ascending; node nodes[i]
+ *     becomes node i of the subgraph;
+ *   result: CSR sub_indptr (n_s + 1), sub_indices / sub_values (room for
+ *     `capacity` entries; the sum over V_s of (full degree + 1) always
+ *     suffices), every node with its self loop, rows sorted; values
+ *     1/len_u (GNN_NORM_ROW: D^-1 A of Eq. "graphsage forward", D counting
+ *     the stored entries) or 1/sqrt(len_u len_v) (GNN_NORM_SYM, the GCN
+ *     layer's normalisation of Section 2.1);
+ *   nnz_out (device int64) receives the number of stored entries;
+ *   status_out (device int32) receives 0, or bits 1 (an id out of range:
+ *     that row keeps its self loop only), 2 (ids not strictly ascending:
+ *     the result is not meaningful), 4 (more entries than capacity: the
+ *     excess is not written);
+ *   map: n_full int32 of device scratch, all -1 on entry, all -1 again
+ *     when the call's work completes (it maps full ids to V_s positions).
+ * Nothing is read back to the host: the caller copies nnz_out / status_out
+ * when it needs them.  Workspace: gnn_induce_workspace_bytes(n_s). */
+#define GNN_NORM_ROW 0
+#define GNN_NORM_SYM 1
+size_t gnn_induce_workspace_bytes(int32_t n_s);
+gnn_status gnn_induce_subgraph(int64_t n_full, int64_t nnz_full,
+                               const int64_t* indptr, const int32_t* indices,
+                               int32_t n_s, const int32_t* nodes, int32_t norm,
+                               int32_t* map, int64_t capacity,
+                               int32_t* sub_indptr, int32_t* sub_indices,
+                               float* sub_values, int64_t* nnz_out,
+                               int32_t* status_out, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
+
+/* Algorithm 1's lookup of the minibatch features / labels by V_s:
+ * dst row r = src row index[r] (width floats; src has src_rows rows of
+ * stride ld_src, dst stride ld_dst); an index outside [0, src_rows) gives a
+ * row of zeros.  dst may not overlap src or index. */
+gnn_status gnn_gather_rows(int32_t rows, const int32_t* index, int32_t width,
+                           const float* src, int64_t ld_src, int64_t src_rows,
+                           float* dst, int64_t ld_dst, hipStream_t stream);
+
 /* ------------------------------------------------------------- kernels */
 
 /* Feature / gradient propagation alone (Section 5.1's first kernel, the
@@ -330,7 +375,9 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
 #define GNN_K_TRANSPOSE 10    /* transposed values (Algorithm 6) */
 #define GNN_K_LOSS 11         /* classifier loss and its gradient */
 #define GNN_K_UPDATE 12       /* weight update (SGD or Adam) */
-#define GNN_K_COUNT 13
+#define GNN_K_INDUCE 13       /* induced subgraph on the GPU */
+#define GNN_K_GATHER 14       /* feature / label row gather */
+#define GNN_K_COUNT 15
 
 /* When enabled, every kernel launch is bracketed by a pair of HIP events on
  * its stream.  gnn_timer_read synchronises on the recorded events and

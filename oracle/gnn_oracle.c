@@ -498,6 +498,64 @@ void oracle_adam(int64_t count, double* W, const double* g, double* m,
   }
 }
 
+/* ------------------------------------------------ induced subgraph (prep) */
+
+static int cmp_i32(const void* a, const void* b) {
+  const int32_t x = *(const int32_t*)a, y = *(const int32_t*)b;
+  return (x > y) - (x < y);
+}
+
+/* Position of w in the sorted list nodes[0..n_s), or -1. */
+static int32_t find_node(int32_t n_s, const int32_t* nodes, int32_t w) {
+  int32_t lo = 0, hi = n_s;
+  while (lo < hi) {
+    const int32_t mid = lo + (hi - lo) / 2;
+    if (nodes[mid] < w) lo = mid + 1; else hi = mid;
+  }
+  return (lo < n_s && nodes[lo] == w) ? lo : -1;
+}
+
+/* Algorithm 2's last step and Algorithm 1's "adjacency matrix of G_s": the
+ * subgraph of the full graph induced by V_s = nodes (sorted, distinct;
+ * nodes[i] becomes node i), every node with its self loop, then the
+ * normalisation of Eq. "graphsage forward", D^-1 A with D counting the
+ * stored entries (norm 0: each entry of row u is 1/len_u), or the
+ * symmetric one of the GCN layer (norm 1: 1/sqrt(len_u len_v)).  Rows come
+ * out sorted.  out_indices / out_values need room for the sum over V_s of
+ * (full degree + 1).  Returns the number of stored entries. */
+int64_t oracle_induce(int64_t n_full, const int64_t* indptr,
+                      const int32_t* indices, int32_t n_s,
+                      const int32_t* nodes, int32_t norm, int32_t* out_indptr,
+                      int32_t* out_indices, double* out_values) {
+  (void)n_full;
+  int64_t nnz = 0;
+  out_indptr[0] = 0;
+  for (int32_t i = 0; i < n_s; ++i) {
+    const int32_t v = nodes[i];
+    int32_t* row = out_indices + nnz;
+    int32_t len = 0;
+    row[len++] = i; /* the self loop */
+    for (int64_t j = indptr[v]; j < indptr[v + 1]; ++j) {
+      const int32_t w = indices[j];
+      if (w == v) continue; /* a stored loop of the full graph counts once */
+      const int32_t k = find_node(n_s, nodes, w);
+      if (k >= 0) row[len++] = k;
+    }
+    qsort(row, (size_t)len, sizeof(int32_t), cmp_i32);
+    nnz += len;
+    out_indptr[i + 1] = (int32_t)nnz;
+  }
+  for (int32_t i = 0; i < n_s; ++i) {
+    const int32_t lu = out_indptr[i + 1] - out_indptr[i];
+    for (int32_t j = out_indptr[i]; j < out_indptr[i + 1]; ++j) {
+      const int32_t k = out_indices[j];
+      const int32_t lv = out_indptr[k + 1] - out_indptr[k];
+      out_values[j] = norm == 0 ? 1.0 / (double)lu : 1.0 / sqrt((double)lu * (double)lv);
+    }
+  }
+  return nnz;
+}
+
 /* ---------------------------------------------- per-output spot evaluation */
 
 void oracle_sage_fwd_rows(int32_t n, const int32_t* indptr,

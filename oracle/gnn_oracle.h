@@ -167,6 +167,14 @@ void oracle_round_bf16(int64_t count, const double* in, double* out);
 /* Number of OpenMP threads the oracle runs with. */
 int32_t oracle_num_threads(void);
 
+/* Induced subgraph of a full graph (int64 row pointers) on the sorted,
+ * distinct node list `nodes` (node nodes[i] becomes i), self loops added,
+ * values 1/len_u (norm 0) or 1/sqrt(len_u len_v) (norm 1).  Returns nnz. */
+int64_t oracle_induce(int64_t n_full, const int64_t* indptr,
+                      const int32_t* indices, int32_t n_s,
+                      const int32_t* nodes, int32_t norm, int32_t* out_indptr,
+                      int32_t* out_indices, double* out_values);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,6 +24,7 @@ _lib = None
 _I32P = ctypes.POINTER(ctypes.c_int32)
 _F64P = ctypes.POINTER(ctypes.c_double)
 _U8P = ctypes.POINTER(ctypes.c_uint8)
+_I64P = ctypes.POINTER(ctypes.c_int64)
 
 
 def build(force: bool = True) -> str:
@@ -78,6 +79,8 @@ def lib():
                 "oracle_classifier": [i32, i32, i32, _F64P, _F64P, _F64P, i32,
                                       _F64P, _F64P, _F64P, _U8P],
                 "oracle_sgd": [i64, _F64P, _F64P, ctypes.c_double],
+                "oracle_induce": [i64, _I64P, _I32P, i32, _I32P, i32, _I32P, _I32P,
+                                  _F64P],
                 "oracle_adam": [i64, _F64P, _F64P, _F64P, _F64P, ctypes.c_double,
                                 ctypes.c_double, ctypes.c_double, ctypes.c_double, i32],
                 "oracle_mixhop_fwd": [i32, _I32P, _I32P, _F64P, i32, i32, i32,
@@ -95,6 +98,8 @@ def lib():
                     "oracle_num_threads") else None
                 if name == "oracle_classifier":
                     fn.restype = ctypes.c_double
+                if name == "oracle_induce":
+                    fn.restype = ctypes.c_int64
             _lib = L
         return _lib
 
@@ -437,3 +442,33 @@ def train_step(g, x, params, w_mlp, targets, kind: int, opt: str = "sgd",
     return {"loss": head["loss"], "probs": head["probs"], "acts": acts,
             "head": head, "grads": grads, "flat_grads": gs, "weights": new_w,
             "state": new_state}
+
+
+class SubgraphCsr:
+    """CSR of an induced subgraph (the oracle's own result type)."""
+
+    def __init__(self, n, indptr, indices, values):
+        self.n, self.indptr, self.indices, self.values = n, indptr, indices, values
+
+    @property
+    def nnz(self) -> int:
+        return int(self.indptr[-1])
+
+
+def induce(full, nodes, norm: int = 0) -> SubgraphCsr:
+    """Subgraph of `full` (n, indptr, indices) induced by the sorted,
+    distinct node list `nodes`, self loops added, normalised by rows
+    (norm 0) or symmetrically (norm 1); see oracle_induce."""
+    ip = np.ascontiguousarray(full.indptr, np.int64)
+    ix = _i32(full.indices)
+    nd = _i32(nodes)
+    assert nd.ndim == 1 and (nd.size < 2 or np.all(nd[1:] > nd[:-1]))
+    assert nd.size == 0 or (nd[0] >= 0 and nd[-1] < full.n)
+    cap = int((ip[nd + 1] - ip[nd]).sum()) + nd.size
+    out_ip = np.zeros(nd.size + 1, np.int32)
+    out_ix = np.empty(max(cap, 1), np.int32)
+    out_v = np.empty(max(cap, 1), np.float64)
+    nnz = lib().oracle_induce(int(full.n), _p(ip, _I64P), _p(ix, _I32P), nd.size,
+                              _p(nd, _I32P), int(norm), _p(out_ip, _I32P),
+                              _p(out_ix, _I32P), _p(out_v, _F64P))
+    return SubgraphCsr(nd.size, out_ip, out_ix[:nnz].copy(), out_v[:nnz].copy())

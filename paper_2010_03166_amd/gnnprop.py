@@ -24,7 +24,10 @@ GNN_LOSS_SOFTMAX = 0
 GNN_LOSS_SIGMOID = 1
 KERNELS = {"spmm": 0, "spmm_reduce": 1, "gemm_nn": 2, "gemm_tn": 3,
            "gemm_nt": 4, "gemm_tt": 5, "gemm_reduce": 6, "mask": 7,
-           "colsum": 8, "plan": 9, "transpose": 10, "loss": 11, "update": 12}
+           "colsum": 8, "plan": 9, "transpose": 10, "loss": 11, "update": 12,
+           "induce": 13, "gather": 14}
+GNN_NORM_ROW = 0
+GNN_NORM_SYM = 1
 
 _lib = None
 
@@ -108,6 +111,14 @@ EXPORTS = {
                                       ctypes.c_double, ctypes.c_void_p]),
     "gnn_adam_step": (ctypes.c_int32, [ctypes.c_int64] + [ctypes.c_void_p] * 4
                       + [ctypes.c_double] * 4 + [ctypes.c_int32, ctypes.c_void_p]),
+    "gnn_induce_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32]),
+    "gnn_induce_subgraph": (ctypes.c_int32, [ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
+                            ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                            ctypes.c_void_p, ctypes.c_int64] + [ctypes.c_void_p] * 6
+                           + [ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_gather_rows": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                         ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                         ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
     "gnn_timer_enable": (ctypes.c_int32, [ctypes.c_int32]),
     "gnn_timer_reset": (ctypes.c_int32, []),
     "gnn_timer_read": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
@@ -307,6 +318,28 @@ def gnn_adam_step(count: int, W, G_, m, v, lr: float, beta1: float, beta2: float
     _check(lib().gnn_adam_step(int(count), _ptr(W), _ptr(G_), _ptr(m), _ptr(v), float(lr),
                                float(beta1), float(beta2), float(eps), int(t),
                                _stream(stream)), "gnn_adam_step")
+
+
+def gnn_induce_workspace_bytes(n_s: int) -> int:
+    return int(lib().gnn_induce_workspace_bytes(int(n_s)))
+
+
+def gnn_induce_subgraph(n_full: int, nnz_full: int, indptr, indices, n_s: int, nodes,
+                        norm: int, map_, capacity: int, sub_indptr, sub_indices, sub_values,
+                        nnz_out, status_out, workspace, stream=None):
+    _check(lib().gnn_induce_subgraph(int(n_full), int(nnz_full), _ptr(indptr), _ptr(indices),
+                                     int(n_s), _ptr(nodes), int(norm), _ptr(map_),
+                                     int(capacity), _ptr(sub_indptr), _ptr(sub_indices),
+                                     _ptr(sub_values), _ptr(nnz_out), _ptr(status_out),
+                                     _ptr(workspace), _nbytes(workspace), _stream(stream)),
+           "gnn_induce_subgraph")
+
+
+def gnn_gather_rows(rows: int, index, width: int, src, ld_src: int, src_rows: int, dst,
+                    ld_dst: int, stream=None):
+    _check(lib().gnn_gather_rows(int(rows), _ptr(index), int(width), _ptr(src), int(ld_src),
+                                 int(src_rows), _ptr(dst), int(ld_dst), _stream(stream)),
+           "gnn_gather_rows")
 
 
 def gnn_spmm_workspace_bytes(csr: gnn_csr, w: int) -> int:

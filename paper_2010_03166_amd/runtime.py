@@ -46,6 +46,20 @@ class DeviceGraph:
         self.plan = torch.empty(max(G.gnn_plan_bytes(self.n, self.nnz), 256),
                                 dtype=torch.uint8, device=device)
 
+    @classmethod
+    def on_device(cls, n: int, indptr: torch.Tensor, indices: torch.Tensor,
+                  values: torch.Tensor) -> "DeviceGraph":
+        """Wraps a CSR already in device memory (int32 indptr of n + 1,
+        int32 indices and float32 values of nnz entries, nnz >= 1)."""
+        g = cls.__new__(cls)
+        g.n, g.nnz = int(n), int(indices.numel())
+        g.device = indptr.device
+        g.indptr, g.indices, g.values = indptr, indices, values
+        g.values_t = torch.empty(max(g.nnz, 1), dtype=torch.float32, device=g.device)
+        g.plan = torch.empty(max(G.gnn_plan_bytes(g.n, g.nnz), 256), dtype=torch.uint8,
+                             device=g.device)
+        return g
+
     def struct(self) -> G.gnn_csr:
         return G.make_csr(self.n, self.nnz, self.indptr, self.indices, self.values,
                           self.values_t, self.plan)
@@ -58,6 +72,73 @@ class DeviceGraph:
 
     def validate(self, symmetric: bool = True) -> int:
         return G.gnn_csr_validate(self.struct(), symmetric)
+
+
+class FullGraphDevice:
+    """A full training graph resident in device memory with its features
+    and labels; builds minibatch subgraphs from host node lists (the
+    induction of Algorithms 2 / 3 and Algorithm 1's feature and label
+    lookup, all in libgnnprop)."""
+
+    def __init__(self, full, X: Optional[np.ndarray] = None,
+                 labels: Optional[np.ndarray] = None, norm: int = G.GNN_NORM_ROW,
+                 device: str = "cuda"):
+        self.n, self.nnz = int(full.n), int(full.nnz)
+        self.deg = np.asarray(full.degrees(), np.int64)
+        self.device, self.norm = device, norm
+        self.indptr = torch.from_numpy(np.ascontiguousarray(full.indptr, np.int64)).to(device)
+        self.indices = torch.from_numpy(np.ascontiguousarray(full.indices, np.int32)).to(device)
+        if self.nnz == 0:
+            self.indices = torch.empty(1, dtype=torch.int32, device=device)
+        self.map = torch.full((max(self.n, 1),), -1, dtype=torch.int32, device=device)
+        self.X = None if X is None else \
+            torch.from_numpy(np.ascontiguousarray(X, np.float32)).to(device)
+        self.labels = None if labels is None else \
+            torch.from_numpy(np.ascontiguousarray(labels, np.float32)).to(device)
+        self.nnz_out = torch.zeros(1, dtype=torch.int64, device=device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def capacity(self, nodes: np.ndarray) -> int:
+        """Entries the induced subgraph of `nodes` can hold at most."""
+        return int(self.deg[nodes].sum()) + len(nodes)
+
+    def induce(self, nodes: np.ndarray, stream=None, pad: int = 16):
+        """Subgraph on the sorted, distinct host node list `nodes`: returns
+        (DeviceGraph prepared for propagation, X_s, labels_s).  Reads the
+        entry count back (one synchronisation)."""
+        nodes = np.ascontiguousarray(nodes, np.int32)
+        n_s = len(nodes)
+        cap = self.capacity(nodes) if n_s else 0
+        nd = torch.from_numpy(nodes).to(self.device) if n_s else \
+            torch.empty(1, dtype=torch.int32, device=self.device)
+        ip = torch.empty(n_s + 1, dtype=torch.int32, device=self.device)
+        ix = torch.empty(max(cap, 1), dtype=torch.int32, device=self.device)
+        vals = torch.empty(max(cap, 1), dtype=torch.float32, device=self.device)
+        ws = torch.empty(max(G.gnn_induce_workspace_bytes(n_s), 256), dtype=torch.uint8,
+                         device=self.device)
+        G.gnn_induce_subgraph(self.n, self.nnz, self.indptr, self.indices, n_s, nd,
+                              self.norm, self.map, cap, ip, ix, vals, self.nnz_out,
+                              self.status, ws, stream)
+        Xs = Ts = None
+        if self.X is not None:
+            f = self.X.shape[1]
+            Xs = torch.empty((max(n_s, 1), _round_up(f, pad)), device=self.device)[:n_s, :f]
+            G.gnn_gather_rows(n_s, nd, f, self.X, self.X.stride(0), self.n, Xs,
+                              Xs.stride(0), stream)
+        if self.labels is not None:
+            C = self.labels.shape[1]
+            Ts = torch.empty((n_s, C), device=self.device)
+            G.gnn_gather_rows(n_s, nd, C, self.labels, self.labels.stride(0), self.n, Ts,
+                              C, stream)
+        st, nnz = int(self.status.item()), int(self.nnz_out.item())
+        if st:
+            raise ValueError("gnn_induce_subgraph status %d (1: id out of range, 2: ids "
+                             "not ascending, 4: over capacity)" % st)
+        dg = DeviceGraph.on_device(n_s, ip, ix[: max(nnz, 1)], vals[: max(nnz, 1)])
+        dg.nnz = nnz
+        dg.nodes = nd
+        dg.prepare(stream)
+        return dg, Xs, Ts
 
 
 class SageStack:

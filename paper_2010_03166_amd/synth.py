@@ -344,3 +344,73 @@ def classifier_inputs(wl: Workload) -> dict:
     w = glorot(2 * wl.hidden, wl.classes, rng_for(wl.case, STREAM_W_MLP))
     t = labels(wl.n, wl.classes, wl.multilabel, rng_for(wl.case, STREAM_LABELS))
     return {"w_mlp": w, "targets": t}
+
+
+# ------------------------------------------------- full graphs (for prep)
+
+@dataclasses.dataclass
+class FullGraph:
+    """Unweighted, undirected training graph: CSR with int64 row pointers,
+    rows sorted, every edge stored both ways, no self loops."""
+    n: int
+    indptr: np.ndarray   # int64, n + 1
+    indices: np.ndarray  # int32
+
+    @property
+    def nnz(self) -> int:
+        return int(self.indptr[-1])
+
+    def degrees(self) -> np.ndarray:
+        return np.diff(self.indptr)
+
+
+# Kronecker initiator of the paper's synthetic graphs (proportional to it)
+KRONECKER_INITIATOR = ((0.9, 0.5), (0.5, 0.1))
+
+
+def full_from_pairs(n: int, rows: np.ndarray, cols: np.ndarray) -> FullGraph:
+    """Symmetric CSR from undirected pairs (loops and duplicates dropped)."""
+    keep = rows != cols
+    r = np.concatenate([rows[keep], cols[keep]]).astype(np.int64)
+    c = np.concatenate([cols[keep], rows[keep]]).astype(np.int64)
+    key = np.unique(r * n + c)
+    r, c = key // n, key % n
+    indptr = np.zeros(n + 1, np.int64)
+    np.cumsum(np.bincount(r, minlength=n), out=indptr[1:])
+    return FullGraph(n, indptr, c.astype(np.int32))
+
+
+def kronecker_graph(scale: int, mean_deg: float, seed: int,
+                    initiator=KRONECKER_INITIATOR) -> FullGraph:
+    """Stochastic Kronecker graph on 2^scale nodes: each edge descends
+    `scale` levels, choosing a quadrant with probability proportional to the
+    initiator entry; pairs are drawn until round(n * mean_deg / 2) distinct
+    undirected non-loop pairs exist (the first ones drawn are kept)."""
+    n = 1 << scale
+    p = np.asarray(initiator, np.float64).ravel()
+    p = p / p.sum()
+    target = int(round(n * mean_deg / 2))
+    rng = np.random.default_rng(np.random.SeedSequence([7, seed, scale]))
+    keys = np.empty(0, np.int64)
+    while keys.size < target:
+        m = int((target - keys.size) * 1.3) + 16
+        r = np.zeros(m, np.int64)
+        c = np.zeros(m, np.int64)
+        for _ in range(scale):
+            q = rng.choice(4, size=m, p=p)
+            r = (r << 1) | (q >> 1)
+            c = (c << 1) | (q & 1)
+        lo, hi = np.minimum(r, c), np.maximum(r, c)
+        k = (lo * n + hi)[lo != hi]
+        allk = np.concatenate([keys, k])
+        _, first = np.unique(allk, return_index=True)
+        keys = allk[np.sort(first)]
+    keys = keys[:target]
+    return full_from_pairs(n, keys // n, keys % n)
+
+
+def uniform_node_sample(full: FullGraph, k: int, seed_or_rng) -> np.ndarray:
+    """k distinct nodes chosen uniformly, sorted (int32)."""
+    rng = seed_or_rng if isinstance(seed_or_rng, np.random.Generator) else \
+        np.random.default_rng(seed_or_rng)
+    return np.sort(rng.choice(full.n, size=min(k, full.n), replace=False)).astype(np.int32)

@@ -748,3 +748,79 @@ def test_train_step_forced_decisions_reproduce_default():
     assert f["loss"] == r["loss"]
     for a, b in zip(f["flat_grads"] + f["weights"], r["flat_grads"] + r["weights"]):
         assert np.array_equal(a, b)
+
+
+# ------------------------------------------------- induced subgraph (prep)
+
+def _dense_full(full):
+    A = np.zeros((full.n, full.n))
+    for u in range(full.n):
+        A[u, full.indices[full.indptr[u]:full.indptr[u + 1]]] = 1.0
+    return A
+
+
+def _dense_of(s):
+    D = np.zeros((s.n, s.n))
+    for u in range(s.n):
+        for j in range(s.indptr[u], s.indptr[u + 1]):
+            D[u, s.indices[j]] += s.values[j]
+    return D
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_induce_dense_brute_force(seed):
+    # A_s = A[V_s, V_s] + I, then D^-1 A_s (row norm) or D^-1/2 A_s D^-1/2
+    full = synth.kronecker_graph(6, 6.0, seed)
+    A = _dense_full(full)
+    rng = np.random.default_rng(seed)
+    nodes = np.sort(rng.choice(full.n, size=23, replace=False)).astype(np.int32)
+    sub = A[np.ix_(nodes, nodes)] + np.eye(len(nodes))
+    d = sub.sum(axis=1)
+    r = O.induce(full, nodes, 0)
+    assert np.array_equal(_dense_of(r), sub / d[:, None])
+    s = O.induce(full, nodes, 1)
+    assert np.allclose(_dense_of(s), sub / np.sqrt(np.outer(d, d)), rtol=1e-15, atol=0)
+    # rows sorted, pattern symmetric, row sums 1
+    for u in range(r.n):
+        row = r.indices[r.indptr[u]:r.indptr[u + 1]]
+        assert np.all(np.diff(row) > 0) and u in row
+    assert np.array_equal(_dense_of(r) > 0, (_dense_of(r) > 0).T)
+    assert np.allclose(_dense_of(r).sum(axis=1), 1.0, rtol=0, atol=1e-15)
+
+
+def test_induce_special_cases():
+    full = synth.kronecker_graph(7, 8.0, 3)
+    # all nodes: the full graph with self loops, values 1/deg
+    allv = np.arange(full.n, dtype=np.int32)
+    r = O.induce(full, allv, 0)
+    assert np.array_equal(r.indptr, full.indptr + np.arange(full.n + 1))
+    pairs = np.stack([np.repeat(np.arange(full.n), full.degrees()), full.indices], 1)
+    ref = synth.symmetric_csr(full.n, pairs[pairs[:, 0] < pairs[:, 1]], self_loops=True)
+    assert np.array_equal(r.indices, ref.indices)
+    assert np.allclose(r.values, np.repeat(1.0 / (full.degrees() + 1), full.degrees() + 1),
+                       rtol=1e-15, atol=0)
+    # one node: a single self loop of value 1
+    one = O.induce(full, np.array([5], np.int32), 1)
+    assert one.indptr.tolist() == [0, 1] and one.indices.tolist() == [0] and one.values[0] == 1
+    # isolated nodes keep only their loop; an independent set gives I
+    deg = full.degrees()
+    iso = np.flatnonzero(deg == 0)[:4].astype(np.int32)
+    if iso.size:
+        r = O.induce(full, iso, 0)
+        assert np.array_equal(r.indices, np.arange(iso.size)) and np.all(r.values == 1)
+    # a stored loop in the full graph is not counted twice
+    loop = synth.FullGraph(3, np.array([0, 2, 3, 4], np.int64), np.array([0, 1, 0, 2], np.int32))
+    r = O.induce(loop, np.array([0, 1, 2], np.int32), 0)
+    assert r.indptr.tolist() == [0, 2, 4, 5] and r.indices.tolist() == [0, 1, 0, 1, 2]
+
+
+def test_kronecker_graph_properties():
+    g = synth.kronecker_graph(10, 16.0, 0)
+    assert g.n == 1024 and g.nnz == 2 * round(1024 * 16 / 2)
+    A = _dense_full(g)
+    assert np.array_equal(A, A.T) and np.all(np.diag(A) == 0)
+    for u in range(g.n):
+        row = g.indices[g.indptr[u]:g.indptr[u + 1]]
+        assert np.all(np.diff(row) > 0)
+    # the initiator's heavy corner: node 0 has the largest expected degree
+    assert g.degrees()[0] == g.degrees().max()
