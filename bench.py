@@ -72,6 +72,10 @@ def parse():
                     help="skip the GCN and MixHop layer timings")
     ap.add_argument("--no-train", action="store_true",
                     help="skip the full training iteration timing")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the sampled-training pipeline timing (Kronecker graph)")
+    ap.add_argument("--pipeline-scale", type=int, default=20,
+                    help="log2 of the Kronecker full graph's node count")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run one plain device-to-device copy of MIB MiB "
                          "(reference point for hardware byte counters)")
@@ -285,6 +289,11 @@ def main():
         out["train_iteration"] = bench_train(G, runtime, synth, torch, dg, X, params, wl,
                                              args, ms_step)
 
+    # Algorithm 8 end to end: host sampler threads, induction on the GPU,
+    # training, on the paper's synthetic Kronecker graph
+    if not args.no_pipeline:
+        out["pipeline"] = bench_pipeline(G, runtime, synth, torch, np, args)
+
     if not args.no_cpu_baseline:
         from oracle import oracle as O
         import numpy as np  # noqa: F811
@@ -346,6 +355,99 @@ def bench_train(G, runtime, synth, torch, dg, X, params, wl, args, ms_prop):
                                          if wl.multilabel else "softmax"),
             "optimizer": "adam", "propagation_share": round(ms_prop / ms, 4),
             "loss_after": round(loss, 6), "kernels": kern}
+
+
+def bench_pipeline(G, runtime, synth, torch, np, args):
+    """ms per training iteration when every iteration draws a new subgraph:
+    frontier sampling (m 1000, budget 8000, eta 2, clip 16) on host threads,
+    induction and row gathers on the GPU, a 2-layer GraphSAGE (hidden 512
+    per half) with a 2-class softmax head and Adam, on a Kronecker graph of
+    2^scale nodes, mean degree 16, 50 features (the paper's synthetic
+    graphs).  Reported overlapped (pool + preparation stream one subgraph
+    ahead) and serial (sample, induce, train one after the other)."""
+    scale, m, budget, eta, clip, f, C, hid = args.pipeline_scale, 1000, 8000, 2.0, 16, 50, 2, 512
+    t0 = time.perf_counter()
+    full = synth.kronecker_graph(scale, 16.0, 0)
+    rng = np.random.default_rng(np.random.SeedSequence([8, scale]))
+    X = rng.standard_normal((full.n, f)).astype(np.float32)
+    Y = synth.labels(full.n, C, False, rng)
+    log("kronecker graph 2^%d: %d entries, built in %.1f s" % (scale, full.nnz,
+                                                              time.perf_counter() - t0))
+    params = [synth.LayerParams(synth.glorot(f, hid, rng), synth.glorot(f, hid, rng)),
+              synth.LayerParams(synth.glorot(2 * hid, hid, rng), synth.glorot(2 * hid, hid, rng))]
+    w_mlp = synth.glorot(2 * hid, C, rng)
+    dev = runtime.FullGraphDevice(full, X, Y)
+    try:
+        threads = min(16, len(os.sched_getaffinity(0)))
+    except AttributeError:
+        threads = min(16, os.cpu_count() or 1)
+    # sampler alone, one thread
+    t0 = time.perf_counter()
+    ns = [len(G.gnn_frontier_sample(full, m, budget, eta, clip, 3, k)) for k in range(4)]
+    samp_ms = (time.perf_counter() - t0) * 1e3 / 4
+    res = {"graph": "kronecker 2^%d nodes, mean degree 16, initiator [[0.9, 0.5], [0.5, 0.1]]"
+                    % scale,
+           "model": "2 layers, hidden 512 per half, 50 features, 2 classes softmax, Adam",
+           "sampler": {"m": m, "budget": budget, "eta": eta, "clip": clip,
+                       "ms_per_subgraph_one_thread": round(samp_ms, 3),
+                       "nodes_mean": round(float(np.mean(ns)), 1)},
+           "threads": threads}
+    iters, warm = args.steps, args.warmup
+    # overlapped
+    pool = G.gnn_sampler_pool(full, m, budget, eta, clip, 1, threads, 2 * threads)
+    pipe = runtime.SubgraphPipeline(dev, pool, max_nodes=budget)
+    tr = None
+    nnz = []
+    for k in range(warm + iters):
+        if k == warm:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        dg, Xs, Ts, _ = pipe.next()
+        nnz.append(dg.nnz)
+        if tr is None:
+            tr = runtime.Trainer(dg, params, f, w_mlp, False, "adam", lr=1e-3)
+        else:
+            tr.bind(dg)
+        tr.step(Xs, Ts)
+        pipe.release()
+    torch.cuda.synchronize()
+    res["ms_per_iteration_overlapped"] = round((time.perf_counter() - t0) * 1e3 / iters, 4)
+    pool.close()
+    res["subgraph_nnz_mean"] = int(np.mean(nnz))
+    # serial: sample (one thread), induce (waits for the entry count), train
+    tr = None
+    for k in range(warm + iters):
+        if k == warm:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        nodes = G.gnn_frontier_sample(full, m, budget, eta, clip, 1, k)
+        dg, Xs, Ts = dev.induce(nodes)
+        if tr is None:
+            tr = runtime.Trainer(dg, params, f, w_mlp, False, "adam", lr=1e-3)
+        else:
+            tr.bind(dg)
+        tr.step(Xs, Ts)
+        torch.cuda.synchronize()
+    res["ms_per_iteration_serial"] = round((time.perf_counter() - t0) * 1e3 / iters, 4)
+    # GPU-side preparation alone (induction + gathers + plan + transposed values)
+    G.gnn_timer_reset()
+    G.gnn_timer_enable(True)
+    for k in range(iters):
+        dev.induce(G.gnn_frontier_sample(full, m, budget, eta, clip, 1, k))
+    torch.cuda.synchronize()
+    G.gnn_timer_enable(False)
+    prep = {}
+    for kname in ("induce", "gather", "plan", "transpose"):
+        ms, launches, _ = G.gnn_timer_read(kname)
+        if launches:
+            prep[kname] = round(ms / iters, 4)
+    G.gnn_timer_reset()
+    res["gpu_prep_ms_per_subgraph"] = prep
+    log("pipeline: %.3f ms/iteration overlapped, %.3f serial (sampler %.2f ms on one thread, "
+        "%d threads)" % (res["ms_per_iteration_overlapped"], res["ms_per_iteration_serial"],
+                         samp_ms, threads))
+    del dev
+    return res
 
 
 def bench_variants(G, runtime, synth, torch, np, g, x, wl, args):

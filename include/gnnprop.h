@@ -332,6 +332,42 @@ gnn_status gnn_gather_rows(int32_t rows, const int32_t* index, int32_t width,
                            const float* src, int64_t ld_src, int64_t src_rows,
                            float* dst, int64_t ld_dst, hipStream_t stream);
 
+/* ------------------------------------------ sampling and the pool (host) */
+
+/* Frontier sampling (Section 4.1, Algorithm 2) through the Dashboard of
+ * Section 4.2 (Algorithms 3 and 4), host code.  Full graph in HOST memory
+ * (int64 indptr of n_full + 1, int32 indices, symmetric, rows sorted).
+ * m: frontier size; budget: n of Algorithm 2 (budget - m frontier updates;
+ * budget >= m); eta >= 1: Dashboard enlargement (eta * m * d slots, d the
+ * mean degree); clip > 1 drops |V_s| mod clip nodes chosen uniformly (the
+ * node clipping of Section 6.2; 0 or 1: none).  V_s is the initial frontier
+ * plus every node that enters the frontier, returned sorted and distinct in
+ * `nodes` (room for `budget` ints), its size in *n_nodes.  The result is a
+ * function of (graph, parameters, seed, id) only; random numbers are
+ * SplitMix64 outputs used as a counter-based generator (stream start
+ * states: outputs 4 id + k of the generator started at seed; k = 0 initial
+ * frontier, 1 probes, 2 neighbour choice, 3 clipping; an integer below K is
+ * floor(r K / 2^64)). */
+gnn_status gnn_frontier_sample(int64_t n_full, const int64_t* indptr,
+                               const int32_t* indices, int32_t m, int32_t budget,
+                               double eta, int32_t clip, uint64_t seed, int64_t id,
+                               int32_t* nodes, int32_t* n_nodes);
+
+/* The subgraph pool of Algorithm 8: `threads` worker threads sample
+ * subgraphs id = 0, 1, 2, ... (each exactly as gnn_frontier_sample with
+ * that id) and keep at most `depth` of them ready; gnn_sampler_next hands
+ * them out in id order, blocking until the next one is ready.  The graph
+ * arrays must stay valid and unchanged until gnn_sampler_destroy, which
+ * stops and joins the workers.  One consumer thread per pool. */
+typedef struct gnn_sampler gnn_sampler;
+gnn_status gnn_sampler_create(int64_t n_full, const int64_t* indptr,
+                              const int32_t* indices, int32_t m, int32_t budget,
+                              double eta, int32_t clip, uint64_t seed,
+                              int32_t threads, int32_t depth, gnn_sampler** out);
+gnn_status gnn_sampler_next(gnn_sampler* s, int32_t* nodes, int32_t* n_nodes,
+                            int64_t* id);
+void gnn_sampler_destroy(gnn_sampler* s);
+
 /* ------------------------------------------------------------- kernels */
 
 /* Feature / gradient propagation alone (Section 5.1's first kernel, the

@@ -10,6 +10,8 @@ raises instead of computing anything itself.
 from __future__ import annotations
 
 import ctypes
+
+import numpy as np
 import os
 from typing import Optional
 
@@ -119,6 +121,16 @@ EXPORTS = {
     "gnn_gather_rows": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                          ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                          ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
+    "gnn_frontier_sample": (ctypes.c_int32, [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
+                                             ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
+                                             ctypes.c_void_p, ctypes.c_void_p]),
+    "gnn_sampler_create": (ctypes.c_int32, [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
+                                            ctypes.c_int32, ctypes.c_uint64, ctypes.c_int32,
+                                            ctypes.c_int32, ctypes.c_void_p]),
+    "gnn_sampler_next": (ctypes.c_int32, [ctypes.c_void_p] * 4),
+    "gnn_sampler_destroy": (None, [ctypes.c_void_p]),
     "gnn_timer_enable": (ctypes.c_int32, [ctypes.c_int32]),
     "gnn_timer_reset": (ctypes.c_int32, []),
     "gnn_timer_read": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
@@ -340,6 +352,75 @@ def gnn_gather_rows(rows: int, index, width: int, src, ld_src: int, src_rows: in
     _check(lib().gnn_gather_rows(int(rows), _ptr(index), int(width), _ptr(src), int(ld_src),
                                  int(src_rows), _ptr(dst), int(ld_dst), _stream(stream)),
            "gnn_gather_rows")
+
+
+def _host_graph(full):
+    ip = np.ascontiguousarray(full.indptr, np.int64)
+    ix = np.ascontiguousarray(full.indices, np.int32)
+    return ip, ix
+
+
+def gnn_frontier_sample(full, m: int, budget: int, eta: float, clip: int, seed: int,
+                        sub_id: int) -> np.ndarray:
+    """Node list of subgraph sub_id (host arrays in, sorted int32 out)."""
+    ip, ix = _host_graph(full)
+    out = np.empty(max(int(budget), 1), np.int32)
+    cnt = ctypes.c_int32(0)
+    _check(lib().gnn_frontier_sample(int(full.n), ip.ctypes.data, ix.ctypes.data, int(m),
+                                     int(budget), float(eta), int(clip),
+                                     int(seed) & ((1 << 64) - 1), int(sub_id),
+                                     out.ctypes.data, ctypes.addressof(cnt)),
+           "gnn_frontier_sample")
+    return out[: cnt.value].copy()
+
+
+def gnn_sampler_create(n_full: int, indptr: np.ndarray, indices: np.ndarray, m: int,
+                       budget: int, eta: float, clip: int, seed: int, threads: int,
+                       depth: int) -> ctypes.c_void_p:
+    """Handle of a new pool; indptr / indices are host numpy arrays that
+    must outlive it."""
+    h = ctypes.c_void_p()
+    _check(lib().gnn_sampler_create(int(n_full), indptr.ctypes.data, indices.ctypes.data,
+                                    int(m), int(budget), float(eta), int(clip),
+                                    int(seed) & ((1 << 64) - 1), int(threads), int(depth),
+                                    ctypes.addressof(h)), "gnn_sampler_create")
+    return h
+
+
+def gnn_sampler_next(h, room: int):
+    """(subgraph id, sorted node list) of the pool's next subgraph."""
+    out = np.empty(max(int(room), 1), np.int32)
+    cnt, sid = ctypes.c_int32(0), ctypes.c_int64(0)
+    _check(lib().gnn_sampler_next(h, out.ctypes.data, ctypes.addressof(cnt),
+                                  ctypes.addressof(sid)), "gnn_sampler_next")
+    return int(sid.value), out[: cnt.value].copy()
+
+
+def gnn_sampler_destroy(h):
+    lib().gnn_sampler_destroy(h)
+
+
+class gnn_sampler_pool:
+    """Owns a gnn_sampler and the host graph arrays it reads."""
+
+    def __init__(self, full, m: int, budget: int, eta: float, clip: int, seed: int,
+                 threads: int, depth: int):
+        self._ip, self._ix = _host_graph(full)
+        self.budget = int(budget)
+        self._h = gnn_sampler_create(full.n, self._ip, self._ix, m, budget, eta, clip, seed,
+                                     threads, depth)
+
+    def next(self):
+        """(subgraph id, sorted node list)."""
+        return gnn_sampler_next(self._h, self.budget)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            gnn_sampler_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.close()
 
 
 def gnn_spmm_workspace_bytes(csr: gnn_csr, w: int) -> int:

@@ -30,6 +30,27 @@ def padded(t: torch.Tensor, ld: int) -> torch.Tensor:
     return buf[:, :cols]
 
 
+class _Rows:
+    """A (rows, ld) float32 device buffer that grows on demand; view(n) is
+    the first n rows, `cols` wide, at row stride ld."""
+
+    def __init__(self, cols: int, ld: int, device):
+        self.cols, self.ld, self.device = cols, ld, device
+        self.buf = torch.empty((1, ld), device=device)
+
+    def view(self, n: int) -> torch.Tensor:
+        if n > self.buf.shape[0]:
+            self.buf = torch.empty((n, self.ld), device=self.device)
+        return self.buf[:n, : self.cols]
+
+
+def _grown(buf: Optional[torch.Tensor], nbytes: int, device) -> torch.Tensor:
+    """buf if it holds nbytes, else a new byte buffer of that size (>= 256)."""
+    if buf is not None and buf.numel() >= nbytes:
+        return buf
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
 class DeviceGraph:
     def __init__(self, csr, device: str = "cuda"):
         self.n = int(csr.n)
@@ -48,16 +69,22 @@ class DeviceGraph:
 
     @classmethod
     def on_device(cls, n: int, indptr: torch.Tensor, indices: torch.Tensor,
-                  values: torch.Tensor) -> "DeviceGraph":
+                  values: torch.Tensor, nnz: Optional[int] = None,
+                  values_t: Optional[torch.Tensor] = None,
+                  plan: Optional[torch.Tensor] = None) -> "DeviceGraph":
         """Wraps a CSR already in device memory (int32 indptr of n + 1,
-        int32 indices and float32 values of nnz entries, nnz >= 1)."""
+        int32 indices and float32 values holding at least nnz entries);
+        values_t / plan buffers are allocated unless given (large enough)."""
         g = cls.__new__(cls)
-        g.n, g.nnz = int(n), int(indices.numel())
+        g.n = int(n)
+        g.nnz = int(indices.numel()) if nnz is None else int(nnz)
         g.device = indptr.device
         g.indptr, g.indices, g.values = indptr, indices, values
-        g.values_t = torch.empty(max(g.nnz, 1), dtype=torch.float32, device=g.device)
-        g.plan = torch.empty(max(G.gnn_plan_bytes(g.n, g.nnz), 256), dtype=torch.uint8,
-                             device=g.device)
+        g.values_t = values_t if values_t is not None else \
+            torch.empty(max(g.nnz, 1), dtype=torch.float32, device=g.device)
+        need = G.gnn_plan_bytes(g.n, g.nnz)
+        g.plan = plan if plan is not None and plan.numel() >= need else \
+            torch.empty(max(need, 256), dtype=torch.uint8, device=g.device)
         return g
 
     def struct(self) -> G.gnn_csr:
@@ -141,6 +168,105 @@ class FullGraphDevice:
         return dg, Xs, Ts
 
 
+class _Slot:
+    """Buffers of one subgraph in flight through the pipeline."""
+
+    def __init__(self, max_nodes: int, cap: int, f: int, C: int, pad: int, device):
+        self.host_nodes = torch.empty(max_nodes, dtype=torch.int32).pin_memory()
+        self.host_meta = torch.zeros(2, dtype=torch.int64).pin_memory()
+        self.nodes = torch.empty(max(max_nodes, 1), dtype=torch.int32, device=device)
+        self.indptr = torch.empty(max_nodes + 1, dtype=torch.int32, device=device)
+        self.indices = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
+        self.values = torch.empty(max(cap, 1), dtype=torch.float32, device=device)
+        self.values_t = torch.empty(max(cap, 1), dtype=torch.float32, device=device)
+        self.plan = torch.empty(max(G.gnn_plan_bytes(max_nodes, cap), 256),
+                                dtype=torch.uint8, device=device)
+        self.meta = torch.zeros(2, dtype=torch.int64, device=device)  # nnz, status
+        self.ws = torch.empty(max(G.gnn_induce_workspace_bytes(max_nodes), 256),
+                              dtype=torch.uint8, device=device)
+        self.X = torch.empty((max(max_nodes, 1), _round_up(f, pad)), device=device)
+        self.T = torch.empty((max(max_nodes, 1), max(C, 1)), device=device)
+        self.induced = torch.cuda.Event()
+        self.consumed = torch.cuda.Event()
+        self.n = 0
+        self.sid = -1
+
+
+class SubgraphPipeline:
+    """Algorithm 8 on one GPU.  A pool of host sampler threads keeps node
+    lists ready (gnn_sampler_pool); each subgraph is induced and its rows
+    gathered on a preparation stream while the previous subgraph trains on
+    the caller's stream, with `depth` sets of buffers in rotation.
+
+        sub = pipe.next()       # (DeviceGraph prepared, X_s, T_s, id)
+        ...launch the iteration on sub...
+        pipe.release()          # after launching: frees the slot for reuse
+                                # and starts preparing the following subgraph
+    """
+
+    def __init__(self, full_dev: FullGraphDevice, pool, max_nodes: int, depth: int = 2,
+                 pad: int = 16):
+        assert depth >= 2
+        self.full, self.pool = full_dev, pool
+        self.max_nodes = int(max_nodes)
+        deg = np.sort(full_dev.deg)[::-1]
+        cap = int(deg[: self.max_nodes].sum()) + self.max_nodes  # any max_nodes nodes fit
+        f = full_dev.X.shape[1] if full_dev.X is not None else 1
+        C = full_dev.labels.shape[1] if full_dev.labels is not None else 1
+        dev = full_dev.device
+        self.cap = cap
+        self.slots = [_Slot(self.max_nodes, cap, f, C, pad, dev) for _ in range(depth)]
+        self.prep = torch.cuda.Stream(device=dev)
+        self.k = 0
+        self._issue(self.slots[0])
+
+    def _issue(self, s: _Slot):
+        sid, nodes = self.pool.next()
+        n = len(nodes)
+        if n > self.max_nodes:
+            raise ValueError("subgraph of %d nodes exceeds max_nodes %d" % (n, self.max_nodes))
+        s.n, s.sid = n, sid
+        s.host_nodes[:n].copy_(torch.from_numpy(nodes))
+        full = self.full
+        with torch.cuda.stream(self.prep):
+            self.prep.wait_event(s.consumed)  # the iteration that last used s is done
+            s.nodes[:n].copy_(s.host_nodes[:n], non_blocking=True)
+            G.gnn_induce_subgraph(full.n, full.nnz, full.indptr, full.indices, n, s.nodes,
+                                  full.norm, full.map, self.cap, s.indptr, s.indices,
+                                  s.values, s.meta[0:1], s.meta[1:2].view(torch.int32), s.ws,
+                                  self.prep.cuda_stream)
+            if full.X is not None:
+                G.gnn_gather_rows(n, s.nodes, full.X.shape[1], full.X, full.X.stride(0),
+                                  full.n, s.X, s.X.stride(0), self.prep.cuda_stream)
+            if full.labels is not None:
+                G.gnn_gather_rows(n, s.nodes, full.labels.shape[1], full.labels,
+                                  full.labels.stride(0), full.n, s.T, s.T.stride(0),
+                                  self.prep.cuda_stream)
+            s.host_meta.copy_(s.meta, non_blocking=True)
+            s.induced.record(self.prep)
+
+    def next(self):
+        s = self.slots[self.k % len(self.slots)]
+        s.induced.synchronize()
+        nnz, status = int(s.host_meta[0]), int(s.host_meta[1])
+        if status:
+            raise ValueError("gnn_induce_subgraph status %d" % status)
+        cur = torch.cuda.current_stream()
+        cur.wait_event(s.induced)
+        dg = DeviceGraph.on_device(s.n, s.indptr[: s.n + 1], s.indices, s.values, nnz=nnz,
+                                   values_t=s.values_t, plan=s.plan)
+        dg.prepare(cur.cuda_stream)
+        f = self.full.X.shape[1] if self.full.X is not None else 0
+        C = self.full.labels.shape[1] if self.full.labels is not None else 0
+        return dg, s.X[: s.n, :f], s.T[: s.n, :C], s.sid
+
+    def release(self):
+        s = self.slots[self.k % len(self.slots)]
+        s.consumed.record(torch.cuda.current_stream())
+        self.k += 1
+        self._issue(self.slots[self.k % len(self.slots)])
+
+
 class SageStack:
     """Weights, activations and gradients of an L-layer stack on one graph."""
 
@@ -154,13 +280,11 @@ class SageStack:
         masked gradients; the first layer's dX is always the plain one.  Off
         by default: the mask read lands in the tail of the dX product, where
         it costs about what the masking pass it replaces does."""
-        self.g = graph
-        self.n = graph.n
         self.order, self.flags, self.pad = order, flags, pad
         self.fuse_masks = fuse_masks
+        self.device = device
         self.layers = []
         f = f_in
-        ws_bytes = 0
         for p in params:
             h = p.w_self.shape[1]
             assert p.w_self.shape == (f, h) == p.w_neigh.shape
@@ -171,25 +295,36 @@ class SageStack:
                 torch.from_numpy(np.ascontiguousarray(p.b_self)).to(device)
             L["b_neigh"] = None if p.b_neigh is None else \
                 torch.from_numpy(np.ascontiguousarray(p.b_neigh)).to(device)
-            ld_y = _round_up(2 * h, pad)
-            L["Y"] = torch.empty((max(self.n, 1), ld_y), device=device)[: self.n, : 2 * h]
             L["dW_self"] = torch.empty((f, h), device=device)
             L["dW_neigh"] = torch.empty((f, h), device=device)
             L["db_self"] = torch.empty(h, device=device) if p.b_self is not None else None
             L["db_neigh"] = torch.empty(h, device=device) if p.b_neigh is not None else None
-            ld_x = _round_up(f, pad)
-            L["dX"] = torch.empty((max(self.n, 1), ld_x), device=device)[: self.n, :f]
+            L["_Y"] = _Rows(2 * h, _round_up(2 * h, pad), device)
+            L["_dX"] = _Rows(f, _round_up(f, pad), device)
+            L["saved"] = None
             self.layers.append(L)
             f = 2 * h
         self.f_in = f_in
-        # layer structs need the input stride: filled at forward time
-        for i, L in enumerate(self.layers):
-            lay = self._layer(i, _round_up(L["f_in"], pad))
-            sb = G.gnn_prop_saved_bytes(graph.struct(), lay)
-            L["saved"] = torch.empty(max(sb, 256), dtype=torch.uint8, device=device)
-            ws_bytes = max(ws_bytes, G.gnn_prop_workspace_bytes(graph.struct(), lay))
-        self.workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=device)
+        self.workspace = None
         self.inputs: List[Optional[torch.Tensor]] = [None] * len(self.layers)
+        self.bind(graph)
+
+    def bind(self, graph: DeviceGraph):
+        """Moves the stack to another (prepared) subgraph: activation and
+        gradient views of its size, saved state and workspace grown as
+        needed.  Weights and their gradients are kept."""
+        self.g = graph
+        self.n = graph.n
+        ws_bytes = 0
+        for i, L in enumerate(self.layers):
+            L["Y"] = L["_Y"].view(self.n)
+            L["dX"] = L["_dX"].view(self.n)
+            lay = self._layer(i, _round_up(L["f_in"], self.pad))
+            L["saved"] = _grown(L["saved"], G.gnn_prop_saved_bytes(graph.struct(), lay),
+                                self.device)
+            ws_bytes = max(ws_bytes, G.gnn_prop_workspace_bytes(graph.struct(), lay))
+        self.workspace = _grown(self.workspace, ws_bytes, self.device)
+        self.inputs = [None] * len(self.layers)
 
     def _layer(self, i: int, ld_x: int, extra_flags: int = 0) -> G.gnn_layer:
         L = self.layers[i]
@@ -253,10 +388,10 @@ class Trainer:
         if optimizer not in ("sgd", "adam"):
             raise ValueError("optimizer must be 'sgd' or 'adam'")
         self.stack = SageStack(graph, params, f_in, order, flags, pad, fuse_masks, device)
-        self.n = graph.n
         self.kind = G.GNN_LOSS_SIGMOID if multilabel else G.GNN_LOSS_SOFTMAX
         self.flags = flags & G.GNN_FLAG_BF16
         self.optimizer, self.lr, self.betas, self.eps = optimizer, lr, betas, eps
+        self.device = device
         top = self.stack.layers[-1]
         self.f_top = 2 * top["h"]
         self.C = int(w_mlp.shape[1])
@@ -265,17 +400,13 @@ class Trainer:
         self.dW_mlp = torch.empty_like(self.W_mlp)
         # the classifier writes dX^(L) at the top layer's Y stride, which is
         # the stride the stack's backward pass expects
-        self.dX_top = torch.empty((max(self.n, 1), top["Y"].stride(0)),
-                                  device=device)[: self.n, : self.f_top]
+        self._dX_top = _Rows(self.f_top, top["_Y"].ld, device)
         ld_p = _round_up(self.C, 4)
-        self.probs = torch.empty((max(self.n, 1), ld_p), device=device)[: self.n, : self.C] \
-            if want_probs else None
-        self.xm = torch.empty((max(self.n, 1), ld_p), device=device)[: self.n, : self.C] \
-            if keep_xm else None
+        self._probs = _Rows(self.C, ld_p, device) if want_probs else None
+        self._xm = _Rows(self.C, ld_p, device) if keep_xm else None
         self.loss = torch.zeros(1, device=device)
-        self.cls_ws = torch.empty(max(G.gnn_classifier_workspace_bytes(self.n, self.f_top,
-                                                                      self.C), 256),
-                                  dtype=torch.uint8, device=device)
+        self.cls_ws = None
+        self.bind(graph, rebind_stack=False)
         # (weight, gradient) pairs in a fixed order: W_MLP, then per layer
         # W_self, W_neigh (, b_self, b_neigh)
         self.pairs = [(self.W_mlp, self.dW_mlp)]
@@ -286,6 +417,18 @@ class Trainer:
         self.state = [(torch.zeros_like(w), torch.zeros_like(w)) for w, _ in self.pairs] \
             if optimizer == "adam" else None
         self.t = 0
+
+    def bind(self, graph: DeviceGraph, rebind_stack: bool = True):
+        """Moves the iteration to another prepared subgraph (weights and
+        optimizer state are kept)."""
+        if rebind_stack:
+            self.stack.bind(graph)
+        self.n = graph.n
+        self.dX_top = self._dX_top.view(self.n)
+        self.probs = self._probs.view(self.n) if self._probs is not None else None
+        self.xm = self._xm.view(self.n) if self._xm is not None else None
+        self.cls_ws = _grown(self.cls_ws, G.gnn_classifier_workspace_bytes(
+            self.n, self.f_top, self.C), self.device)
 
     def step(self, X: torch.Tensor, targets: torch.Tensor, stream=None) -> torch.Tensor:
         """X: n x f_in (any row stride); targets: n x C 0/1 floats."""
