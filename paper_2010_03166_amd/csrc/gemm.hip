@@ -112,16 +112,24 @@ __device__ inline int logical_block(int b, int nblocks) {
   return x * base + min(x, rem) + c;
 }
 
+// A tile's origin (m0, n0) and the first row / column it owns (r0, c0).
+// The last tile of a ragged dimension of at least one tile is moved back
+// to end at the matrix edge (m0 = M - BM), so that it runs the unguarded
+// pipeline like every other tile; it recomputes the rows (columns) below
+// r0 (c0), which belong to its neighbour, and writes only its own.
 struct TileInfo {
-  int pi, m0, n0;
+  int pi, m0, n0, r0, c0;
 };
 
 __device__ inline TileInfo tile_info(const GemmKArgs& g, int t) {
   TileInfo ti;
   const int tm = t / g.tiles_n, j = t % g.tiles_n;
   ti.pi = (g.nprob > 1 && j >= g.tiles_n0) ? 1 : 0;
-  ti.m0 = tm * BM;
-  ti.n0 = (ti.pi ? j - g.tiles_n0 : j) * BN;
+  ti.r0 = tm * BM;
+  ti.c0 = (ti.pi ? j - g.tiles_n0 : j) * BN;
+  const int N = ti.pi ? g.p[1].N : g.p[0].N;
+  ti.m0 = (g.M >= BM && ti.r0 + BM > g.M) ? g.M - BM : ti.r0;
+  ti.n0 = (N >= BN && ti.c0 + BN > N) ? N - BN : ti.c0;
   return ti;
 }
 
@@ -135,7 +143,9 @@ __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
                                  bool whole, float* part, int wm, int wn,
                                  int lr, int lh) {
   const int N = P.N;
-  const bool interior = ti.m0 + BM <= M && ti.n0 + BN <= N;
+  // moved-back tiles take the guarded path, which skips what they do not own
+  const bool interior = ti.m0 + BM <= M && ti.n0 + BN <= N && ti.m0 == ti.r0 &&
+                        ti.n0 == ti.c0;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -168,7 +178,7 @@ __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int row = ti.m0 + rl0 + (r >> 2) * 8 + (r & 3);
-          if (row < M && col < N) {
+          if (row < M && col < N && row >= ti.r0 && col >= ti.c0) {
             float v = acc[i][j][r] + bc;
             if (P.relu) v = fmaxf(v, 0.f);
             if (P.mask && !(P.mask[(int64_t)row * P.ld_mask + col] > 0.f)) v = 0.f;
@@ -678,7 +688,7 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
   const int e = blockIdx.y * 1024 + threadIdx.x * 4;
   const int rl = e / BN, cl = e % BN;
   const int row = ti.m0 + rl, col = ti.n0 + cl;
-  if (row >= g.M || col >= P.N) return;
+  if (row >= g.M || col >= P.N || row < ti.r0) return;
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
   if (g.splits > 1) {
     const float* src = g.part + (int64_t)t * (BM * BN) + e;
@@ -719,6 +729,7 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     if (col + u >= P.N) break;
+    if (col + u < ti.c0) continue;  // its neighbour's column
     float x = o[u];
     if (P.bias) x += P.bias[col + u];
     if (P.relu) x = fmaxf(x, 0.f);
