@@ -243,20 +243,48 @@ __device__ inline bool chunk_of(const EntryArgs& a, int64_t& start, int64_t& end
   return true;
 }
 
+// The chunk's row offsets off[r_lo .. r_hi + 1], staged in LDS when they
+// fit, so that each slot finds its row without global reads.
+constexpr int ROW_CACHE = 512;
+
+struct Rows {
+  const int64_t* off;  // LDS copy (relative to r_lo) or the global array
+  int32_t lo, hi, base;
+};
+
+__device__ inline Rows stage_rows(const EntryArgs& a, int32_t r_lo, int32_t r_hi,
+                                  int64_t* s_off) {
+  const int32_t cnt = r_hi - r_lo + 2;
+  if (cnt > ROW_CACHE + 1) return Rows{a.off, r_lo, r_hi, 0};
+  for (int32_t k = threadIdx.x; k < cnt; k += 256) s_off[k] = a.off[r_lo + k];
+  __syncthreads();
+  return Rows{s_off, 0, r_hi - r_lo, r_lo};
+}
+
+// (row, slot within the row) of entry e
+__device__ inline int32_t row_in(const Rows& R, int64_t e, int64_t& k) {
+  const int32_t r = row_of(R.off, R.lo, R.hi, e);
+  k = e - R.off[r];
+  return r + R.base;
+}
+
 __global__ __launch_bounds__(256) void induce_count_kernel(EntryArgs a,
                                                            int64_t* __restrict__ counts) {
   __shared__ int32_t rows[2];
   __shared__ int32_t wsum[4];
+  __shared__ int64_t s_off[ROW_CACHE + 1];
   int64_t start, end;
   int32_t r_lo, r_hi;
   if (!chunk_of(a, start, end, r_lo, r_hi, rows)) {
     if (threadIdx.x == 0) counts[blockIdx.x] = 0;
     return;
   }
+  const Rows R = stage_rows(a, r_lo, r_hi, s_off);
   int32_t c = 0;
   for (int64_t e = start + threadIdx.x; e < end; e += 256) {
-    const int32_t i = row_of(a.off, r_lo, r_hi, e);
-    c += slot_target(a, i, e - a.off[i]) >= 0;
+    int64_t k;
+    const int32_t i = row_in(R, e, k);
+    c += slot_target(a, i, k) >= 0;
   }
 #pragma unroll
   for (int d = 32; d > 0; d >>= 1) c += __shfl_xor(c, d, 64);
@@ -273,6 +301,7 @@ __global__ __launch_bounds__(256) void induce_fill_kernel(
     int64_t* __restrict__ nnz_out, int32_t* __restrict__ status) {
   __shared__ int32_t rows[2];
   __shared__ int32_t wcnt[4];
+  __shared__ int64_t s_off[ROW_CACHE + 1];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     const int64_t total = boff[CHUNK_BLOCKS];
     *nnz_out = total;
@@ -282,14 +311,16 @@ __global__ __launch_bounds__(256) void induce_fill_kernel(
   int64_t start, end;
   int32_t r_lo, r_hi;
   if (!chunk_of(a, start, end, r_lo, r_hi, rows)) return;
+  const Rows R = stage_rows(a, r_lo, r_hi, s_off);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int64_t run = boff[blockIdx.x];
   for (int64_t base = start; base < end; base += 256) {
     const int64_t e = base + threadIdx.x;
     int32_t i = 0, t = -1;
+    int64_t k = -1;
     if (e < end) {
-      i = row_of(a.off, r_lo, r_hi, e);
-      t = slot_target(a, i, e - a.off[i]);
+      i = row_in(R, e, k);
+      t = slot_target(a, i, k);
     }
     const uint64_t m = __ballot(t >= 0);
     const int32_t below = __popcll(m & ((1ull << lane) - 1ull));
@@ -301,7 +332,7 @@ __global__ __launch_bounds__(256) void induce_fill_kernel(
     __syncthreads();
     const int64_t pos = run + before + below;
     if (e < end) {
-      if (e == a.off[i]) sub_indptr[i] = (int32_t)std::min<int64_t>(pos, INT32_MAX);
+      if (k == 0) sub_indptr[i] = (int32_t)std::min<int64_t>(pos, INT32_MAX);
       if (t >= 0 && pos < capacity) sub_indices[pos] = t;
     }
     run += tile;

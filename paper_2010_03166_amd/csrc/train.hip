@@ -107,28 +107,76 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(int64_t count,
     p[i] = 0.f;
 }
 
-__global__ __launch_bounds__(256) void sgd_kernel(int64_t count,
-                                                  float* __restrict__ W,
-                                                  const float* __restrict__ g,
-                                                  float lr) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count;
-       i += (int64_t)gridDim.x * 256)
-    W[i] -= lr * g[i];
+// The updates stream W, G (and m, v) once; with 16-byte aligned arrays a
+// thread takes four consecutive weights per access (the tail singly).
+template <bool VEC>
+__global__ __launch_bounds__(256) void sgd_kernel(int64_t count, float* __restrict__ W,
+                                                  const float* __restrict__ g, float lr) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t i0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (VEC) {
+    const int64_t c4 = count >> 2;
+    for (int64_t i = i0; i < c4; i += stride) {
+      float4 w = reinterpret_cast<float4*>(W)[i];
+      const float4 d = reinterpret_cast<const float4*>(g)[i];
+      w.x -= lr * d.x;
+      w.y -= lr * d.y;
+      w.z -= lr * d.z;
+      w.w -= lr * d.w;
+      reinterpret_cast<float4*>(W)[i] = w;
+    }
+    i0 += c4 << 2;
+  }
+  for (int64_t i = i0; i < count; i += stride) W[i] -= lr * g[i];
 }
 
-__global__ __launch_bounds__(256) void adam_kernel(
-    int64_t count, float* __restrict__ W, const float* __restrict__ g,
-    float* __restrict__ m, float* __restrict__ v, float lr, float b1,
-    float omb1, float b2, float omb2, float eps, float c1, float c2) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count;
-       i += (int64_t)gridDim.x * 256) {
-    const float gi = g[i];
-    const float mi = b1 * m[i] + omb1 * gi;
-    const float vi = b2 * v[i] + omb2 * gi * gi;
+struct AdamCoef {
+  float lr, b1, omb1, b2, omb2, eps, c1, c2;
+};
+
+__device__ inline void adam_one(float& w, float gi, float& m, float& v, const AdamCoef& a) {
+  m = a.b1 * m + a.omb1 * gi;
+  v = a.b2 * v + a.omb2 * gi * gi;
+  w -= a.lr * (m / a.c1) / (sqrtf(v / a.c2) + a.eps);
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(256) void adam_kernel(int64_t count, float* __restrict__ W,
+                                                   const float* __restrict__ g,
+                                                   float* __restrict__ m,
+                                                   float* __restrict__ v, AdamCoef a) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t i0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (VEC) {
+    const int64_t c4 = count >> 2;
+    for (int64_t i = i0; i < c4; i += stride) {
+      float4 w = reinterpret_cast<float4*>(W)[i];
+      const float4 d = reinterpret_cast<const float4*>(g)[i];
+      float4 mm = reinterpret_cast<float4*>(m)[i];
+      float4 vv = reinterpret_cast<float4*>(v)[i];
+      adam_one(w.x, d.x, mm.x, vv.x, a);
+      adam_one(w.y, d.y, mm.y, vv.y, a);
+      adam_one(w.z, d.z, mm.z, vv.z, a);
+      adam_one(w.w, d.w, mm.w, vv.w, a);
+      reinterpret_cast<float4*>(W)[i] = w;
+      reinterpret_cast<float4*>(m)[i] = mm;
+      reinterpret_cast<float4*>(v)[i] = vv;
+    }
+    i0 += c4 << 2;
+  }
+  for (int64_t i = i0; i < count; i += stride) {
+    float w = W[i], mi = m[i], vi = v[i];
+    adam_one(w, g[i], mi, vi, a);
+    W[i] = w;
     m[i] = mi;
     v[i] = vi;
-    W[i] -= lr * (mi / c1) / (sqrtf(vi / c2) + eps);
   }
+}
+
+inline bool al16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+
+inline unsigned update_grid(int64_t count) {
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(count, 1024), 2048));
 }
 
 struct ClsLayout {
@@ -256,9 +304,12 @@ gnn_status gnn_sgd_step(int64_t count, float* W, const float* G, double lr,
   if (count == 0) return GNN_OK;
   if (!W || !G) return GNN_ERR_NULL;
   if (ranges_overlap(W, (size_t)count * 4, G, (size_t)count * 4)) return GNN_ERR_ALIAS;
-  const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(count, 256), 4096);
+  const unsigned grid = update_grid(count);
   timer_begin(GNN_K_UPDATE, stream);
-  sgd_kernel<<<grid, 256, 0, stream>>>(count, W, G, (float)lr);
+  if (al16(W) && al16(G))
+    sgd_kernel<true><<<grid, 256, 0, stream>>>(count, W, G, (float)lr);
+  else
+    sgd_kernel<false><<<grid, 256, 0, stream>>>(count, W, G, (float)lr);
   timer_end(GNN_K_UPDATE, 12.0 * count, stream);
   GNN_HIP(hipGetLastError());
   return GNN_OK;
@@ -278,11 +329,14 @@ gnn_status gnn_adam_step(int64_t count, float* W, const float* G, float* m,
   // the coefficients in double, each rounded once to fp32
   const float c1 = (float)(1.0 - std::pow(beta1, t));
   const float c2 = (float)(1.0 - std::pow(beta2, t));
-  const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(count, 256), 4096);
+  const AdamCoef a{(float)lr, (float)beta1, (float)(1.0 - beta1), (float)beta2,
+                   (float)(1.0 - beta2), (float)eps, c1, c2};
+  const unsigned grid = update_grid(count);
   timer_begin(GNN_K_UPDATE, stream);
-  adam_kernel<<<grid, 256, 0, stream>>>(count, W, G, m, v, (float)lr, (float)beta1,
-                                        (float)(1.0 - beta1), (float)beta2,
-                                        (float)(1.0 - beta2), (float)eps, c1, c2);
+  if (al16(W) && al16(G) && al16(m) && al16(v))
+    adam_kernel<true><<<grid, 256, 0, stream>>>(count, W, G, m, v, a);
+  else
+    adam_kernel<false><<<grid, 256, 0, stream>>>(count, W, G, m, v, a);
   timer_end(GNN_K_UPDATE, 28.0 * count, stream);
   GNN_HIP(hipGetLastError());
   return GNN_OK;

@@ -407,15 +407,42 @@ class Trainer:
         self.loss = torch.zeros(1, device=device)
         self.cls_ws = None
         self.bind(graph, rebind_stack=False)
-        # (weight, gradient) pairs in a fixed order: W_MLP, then per layer
-        # W_self, W_neigh (, b_self, b_neigh)
-        self.pairs = [(self.W_mlp, self.dW_mlp)]
+        # Every weight, gradient and optimizer moment lives in one flat
+        # buffer (tensors at 256-byte offsets, zero padding between them), so
+        # that one update launch covers the whole model.  (weight, gradient)
+        # pairs in a fixed order: W_MLP, then per layer W_self, W_neigh
+        # (, b_self, b_neigh).
+        names = [(None, "W_mlp", "dW_mlp")]
         for L in self.stack.layers:
-            self.pairs += [(L["W_self"], L["dW_self"]), (L["W_neigh"], L["dW_neigh"])]
+            names += [(L, "W_self", "dW_self"), (L, "W_neigh", "dW_neigh")]
             if L["b_self"] is not None:
-                self.pairs += [(L["b_self"], L["db_self"]), (L["b_neigh"], L["db_neigh"])]
-        self.state = [(torch.zeros_like(w), torch.zeros_like(w)) for w, _ in self.pairs] \
-            if optimizer == "adam" else None
+                names += [(L, "b_self", "db_self"), (L, "b_neigh", "db_neigh")]
+        get = lambda L, k: getattr(self, k) if L is None else L[k]
+        offs, total = [], 0
+        for L, wk, _ in names:
+            offs.append(total)
+            total += _round_up(get(L, wk).numel(), 64)
+        self.flat_w = torch.zeros(max(total, 64), device=device)
+        self.flat_g = torch.zeros(max(total, 64), device=device)
+        self.pairs = []
+        for (L, wk, gk), o in zip(names, offs):
+            w = get(L, wk)
+            wv = self.flat_w[o: o + w.numel()].view(w.shape)
+            wv.copy_(w)
+            gv = self.flat_g[o: o + w.numel()].view(w.shape)
+            if L is None:
+                setattr(self, wk, wv)
+                setattr(self, gk, gv)
+            else:
+                L[wk], L[gk] = wv, gv
+            self.pairs.append((wv, gv))
+        self.state = None
+        if optimizer == "adam":
+            self.flat_m = torch.zeros_like(self.flat_w)
+            self.flat_v = torch.zeros_like(self.flat_w)
+            self.state = [(self.flat_m[o: o + w.numel()].view(w.shape),
+                           self.flat_v[o: o + w.numel()].view(w.shape))
+                          for (w, _), o in zip(self.pairs, offs)]
         self.t = 0
 
     def bind(self, graph: DeviceGraph, rebind_stack: bool = True):
@@ -444,11 +471,10 @@ class Trainer:
                          stream)
         self.stack.backward(self.dX_top, want_dx_first=False, stream=stream)
         self.t += 1
-        for i, (w, gr) in enumerate(self.pairs):
-            if self.optimizer == "sgd":
-                G.gnn_sgd_step(w.numel(), w, gr, self.lr, stream)
-            else:
-                m, v = self.state[i]
-                G.gnn_adam_step(w.numel(), w, gr, m, v, self.lr, self.betas[0],
-                                self.betas[1], self.eps, self.t, stream)
+        if self.optimizer == "sgd":
+            G.gnn_sgd_step(self.flat_w.numel(), self.flat_w, self.flat_g, self.lr, stream)
+        else:
+            G.gnn_adam_step(self.flat_w.numel(), self.flat_w, self.flat_g, self.flat_m,
+                            self.flat_v, self.lr, self.betas[0], self.betas[1], self.eps,
+                            self.t, stream)
         return self.loss
