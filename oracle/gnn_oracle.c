@@ -411,6 +411,83 @@ void oracle_mixhop_bwd(int32_t n, const int32_t* indptr,
   free(U);
 }
 
+/* ------------------------------------------------------------- GAT layer */
+
+/* Section 2.1, Eqs. "gat forward" and "gat attention", on the stored
+ * entries of the subgraph (its edges and self loops): with P = X W and
+ * a = [a1; a2] (2h), entry (u, v) of the attention matrix is
+ *   att_uv = LeakyReLU(a1 . P_u + a2 . P_v)   (slope alpha below 0)
+ * and Y = ReLU(A_att P).  The CSR's own values are not used.  att (nnz)
+ * may be NULL. */
+void oracle_gat_fwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                    int32_t f_in, int32_t h, const double* X, const double* W,
+                    const double* a, double alpha, double* Y, double* att) {
+  const size_t nh = (size_t)n * (size_t)h;
+  const int64_t nnz = n > 0 ? indptr[n] : 0;
+  double* P = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  double* A = (double*)malloc(sizeof(double) * (nnz ? nnz : 1));
+  oracle_mm_nn(n, h, f_in, X, W, P);
+  for (int32_t u = 0; u < n; ++u)
+    for (int32_t j = indptr[u]; j < indptr[u + 1]; ++j) {
+      const int32_t v = indices[j];
+      double z = 0.0;
+      for (int32_t c = 0; c < h; ++c) z += a[c] * P[(int64_t)u * h + c];
+      for (int32_t c = 0; c < h; ++c) z += a[h + c] * P[(int64_t)v * h + c];
+      A[j] = z > 0.0 ? z : alpha * z;
+    }
+  oracle_spmm(n, indptr, indices, A, h, P, Y);
+  for (size_t i = 0; i < nh; ++i) Y[i] = relu(Y[i]);
+  if (att)
+    for (int64_t j = 0; j < nnz; ++j) att[j] = A[j];
+  free(A);
+  free(P);
+}
+
+/* The chain rule through the GAT layer (Section 5.1 does it step by step
+ * for the dense parts; the attention's own terms follow from its
+ * definition): G = dY * 1[Y > 0]; with Z = A_att P,
+ *   dP = A_att^T G  +  sum over entries of dz_uv (a1 at row u, a2 at row v),
+ *   dz_uv = (G_u . P_v) * (z_uv > 0 ? 1 : alpha),
+ *   da1 = sum dz_uv P_u,  da2 = sum dz_uv P_v,
+ *   dW = X^T dP,  dX = dP W^T.
+ * dX may be NULL. */
+void oracle_gat_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                    int32_t f_in, int32_t h, const double* X, const double* W,
+                    const double* a, double alpha, const double* Y,
+                    const double* dY, double* dX, double* dW, double* da) {
+  const size_t nh = (size_t)n * (size_t)h;
+  double* P = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  double* G = (double*)malloc(sizeof(double) * (nh ? nh : 1));
+  double* dP = (double*)calloc(nh ? nh : 1, sizeof(double));
+  oracle_mm_nn(n, h, f_in, X, W, P);
+  mask_all((int64_t)nh, Y, dY, G);
+  for (int32_t c = 0; c < 2 * h; ++c) da[c] = 0.0;
+  for (int32_t u = 0; u < n; ++u)
+    for (int32_t j = indptr[u]; j < indptr[u + 1]; ++j) {
+      const int32_t v = indices[j];
+      const double* Pu = P + (int64_t)u * h;
+      const double* Pv = P + (int64_t)v * h;
+      const double* Gu = G + (int64_t)u * h;
+      double z = 0.0, dA = 0.0;
+      for (int32_t c = 0; c < h; ++c) z += a[c] * Pu[c] + a[h + c] * Pv[c];
+      const double att = z > 0.0 ? z : alpha * z;
+      for (int32_t c = 0; c < h; ++c) dA += Gu[c] * Pv[c];
+      const double dz = dA * (z > 0.0 ? 1.0 : alpha);
+      for (int32_t c = 0; c < h; ++c) {
+        dP[(int64_t)v * h + c] += att * Gu[c];      /* A_att^T G */
+        dP[(int64_t)u * h + c] += dz * a[c];        /* through a1 . P_u */
+        dP[(int64_t)v * h + c] += dz * a[h + c];    /* through a2 . P_v */
+        da[c] += dz * Pu[c];
+        da[h + c] += dz * Pv[c];
+      }
+    }
+  oracle_mm_tn(f_in, h, n, X, dP, dW);
+  if (dX) oracle_mm_nt(n, f_in, h, dP, W, dX);
+  free(dP);
+  free(G);
+  free(P);
+}
+
 /* ------------------------------------- classifier, loss and weight update */
 
 /* Section 3.1 (Eqs. "mlp forward", "loss forward") and Algorithm 1:

@@ -175,6 +175,18 @@ int64_t oracle_induce(int64_t n_full, const int64_t* indptr,
                       const int32_t* nodes, int32_t norm, int32_t* out_indptr,
                       int32_t* out_indices, double* out_values);
 
+/* GAT layer (Section 2.1): P = X W, att_uv = LeakyReLU(a1 . P_u + a2 . P_v)
+ * on the stored entries (slope alpha below 0), Y = ReLU(A_att P); att
+ * (nnz) may be NULL.  Backward by the chain rule; dX may be NULL; da has
+ * 2h entries. */
+void oracle_gat_fwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                    int32_t f_in, int32_t h, const double* X, const double* W,
+                    const double* a, double alpha, double* Y, double* att);
+void oracle_gat_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
+                    int32_t f_in, int32_t h, const double* X, const double* W,
+                    const double* a, double alpha, const double* Y,
+                    const double* dY, double* dX, double* dW, double* da);
+
 #ifdef __cplusplus
 }
 #endif

@@ -81,6 +81,10 @@ def lib():
                 "oracle_sgd": [i64, _F64P, _F64P, ctypes.c_double],
                 "oracle_induce": [i64, _I64P, _I32P, i32, _I32P, i32, _I32P, _I32P,
                                   _F64P],
+                "oracle_gat_fwd": [i32, _I32P, _I32P, i32, i32, _F64P, _F64P, _F64P,
+                                   ctypes.c_double, _F64P, _F64P],
+                "oracle_gat_bwd": [i32, _I32P, _I32P, i32, i32, _F64P, _F64P, _F64P,
+                                   ctypes.c_double, _F64P, _F64P, _F64P, _F64P, _F64P],
                 "oracle_adam": [i64, _F64P, _F64P, _F64P, _F64P, ctypes.c_double,
                                 ctypes.c_double, ctypes.c_double, ctypes.c_double, i32],
                 "oracle_mixhop_fwd": [i32, _I32P, _I32P, _F64P, i32, i32, i32,
@@ -330,6 +334,37 @@ def mixhop_bwd(g, x, w, K: int, y, dy, want_dx: bool = True,
 
 
 SOFTMAX, SIGMOID = 0, 1
+
+
+GAT_ALPHA = 0.2  # LeakyReLU slope of the attention scores
+
+
+def gat_fwd(g, x, w, a, alpha: float = GAT_ALPHA, want_att: bool = False):
+    """Y = ReLU(A_att X W) with att_uv = LeakyReLU(a1 . P_u + a2 . P_v)."""
+    n, ip, ix, _ = _csr(g)
+    x, w, a = _f64(x), _f64(w), _f64(a)
+    f_in, h = w.shape
+    assert x.shape == (n, f_in) and a.shape == (2 * h,)
+    y = np.empty((n, h))
+    att = np.empty(int(ip[-1])) if want_att else None
+    lib().oracle_gat_fwd(n, _p(ip, _I32P), _p(ix, _I32P), f_in, h, _p(x, _F64P),
+                         _p(w, _F64P), _p(a, _F64P), float(alpha), _p(y, _F64P),
+                         _p(att, _F64P))
+    return (y, att) if want_att else y
+
+
+def gat_bwd(g, x, w, a, y, dy, alpha: float = GAT_ALPHA, want_dx: bool = True) -> dict:
+    n, ip, ix, _ = _csr(g)
+    x, w, a, y, dy = _f64(x), _f64(w), _f64(a), _f64(y), _f64(dy)
+    f_in, h = w.shape
+    assert y.shape == (n, h) == dy.shape
+    out = {"dW": np.empty((f_in, h)), "da": np.empty(2 * h),
+           "dX": np.empty((n, f_in)) if want_dx else None}
+    lib().oracle_gat_bwd(n, _p(ip, _I32P), _p(ix, _I32P), f_in, h, _p(x, _F64P),
+                         _p(w, _F64P), _p(a, _F64P), float(alpha), _p(y, _F64P),
+                         _p(dy, _F64P), _p(out["dX"], _F64P), _p(out["dW"], _F64P),
+                         _p(out["da"], _F64P))
+    return out
 
 
 def classifier(x, w, t, kind: int, want_dx: bool = True, relu_on=None) -> dict:

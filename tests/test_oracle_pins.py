@@ -824,3 +824,79 @@ def test_kronecker_graph_properties():
         assert np.all(np.diff(row) > 0)
     # the initiator's heavy corner: node 0 has the largest expected degree
     assert g.degrees()[0] == g.degrees().max()
+
+
+# ------------------------------------------------------------- GAT layer
+
+def _gat_case(seed, n=9, f=4, h=3):
+    g = synth.random_graph(n, 2.5, seed)
+    for s in range(seed, seed + 200):
+        rng = np.random.default_rng(s)
+        x, w = rng.standard_normal((n, f)), rng.standard_normal((f, h))
+        a = rng.standard_normal(2 * h)
+        P = x @ w
+        z = np.array([a[:h] @ P[u] + a[h:] @ P[v] for u in range(n)
+                      for v in g.indices[g.indptr[u]:g.indptr[u + 1]]])
+        y = O.gat_fwd(g, x, w, a)
+        pre = _gat_dense(g, x, w, a) @ P
+        # away from both kinks, so that central differences are smooth
+        if np.abs(z).min() > 1e-3 and np.abs(pre).min() > 1e-3:
+            return g, x, w, a
+    raise AssertionError("no smooth case")
+
+
+def _gat_dense(g, x, w, a, alpha=O.GAT_ALPHA):
+    h = w.shape[1]
+    P = x @ w
+    A = np.zeros((g.n, g.n))
+    for u in range(g.n):
+        for v in g.indices[g.indptr[u]:g.indptr[u + 1]]:
+            z = a[:h] @ P[u] + a[h:] @ P[v]
+            A[u, v] = z if z > 0 else alpha * z
+    return A
+
+
+def test_gat_forward_dense_brute_force():
+    g, x, w, a = _gat_case(3)
+    y, att = O.gat_fwd(g, x, w, a, want_att=True)
+    A = _gat_dense(g, x, w, a)
+    assert rel(y, np.maximum(A @ (x @ w), 0)) < 1e-14
+    got = np.zeros((g.n, g.n))
+    for u in range(g.n):
+        got[u, g.indices[g.indptr[u]:g.indptr[u + 1]]] = att[g.indptr[u]:g.indptr[u + 1]]
+    assert rel(got, A) < 1e-14
+
+
+def test_gat_linear_attention_closed_form():
+    # slope 1: the attention is linear, A_att = diag(s) B + B diag(t) on the
+    # pattern B, with s = P a1 and t = P a2
+    g, x, w, a = _gat_case(5)
+    h = w.shape[1]
+    P = x @ w
+    B = np.zeros((g.n, g.n))
+    for u in range(g.n):
+        B[u, g.indices[g.indptr[u]:g.indptr[u + 1]]] = 1.0
+    s, t = P @ a[:h], P @ a[h:]
+    Z = np.diag(s) @ B @ P + B @ np.diag(t) @ P
+    assert rel(O.gat_fwd(g, x, w, a, alpha=1.0), np.maximum(Z, 0)) < 1e-13
+
+
+def test_gat_zero_attention_vector():
+    g, x, w, a = _gat_case(7)
+    a0 = np.zeros_like(a)
+    assert np.all(O.gat_fwd(g, x, w, a0) == 0)
+    dy = np.random.default_rng(1).standard_normal((g.n, w.shape[1]))
+    r = O.gat_bwd(g, x, w, a0, O.gat_fwd(g, x, w, a0), dy)
+    assert np.all(r["dW"] == 0) and np.all(r["dX"] == 0) and np.all(r["da"] == 0)
+
+
+@pytest.mark.parametrize("seed", [11, 12])
+def test_gat_gradients_finite_differences(seed):
+    g, x, w, a = _gat_case(seed)
+    dy = np.random.default_rng(seed).standard_normal((g.n, w.shape[1]))
+    y = O.gat_fwd(g, x, w, a)
+    r = O.gat_bwd(g, x, w, a, y, dy)
+    fd = _fd_grads(lambda: float((dy * O.gat_fwd(g, x, w, a)).sum()), [x, w, a])
+    assert rel(r["dX"], fd[0]) < 1e-6
+    assert rel(r["dW"], fd[1]) < 1e-6
+    assert rel(r["da"], fd[2]) < 1e-6
