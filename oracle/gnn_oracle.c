@@ -450,11 +450,13 @@ void oracle_gat_fwd(int32_t n, const int32_t* indptr, const int32_t* indices,
  *   dz_uv = (G_u . P_v) * (z_uv > 0 ? 1 : alpha),
  *   da1 = sum dz_uv P_u,  da2 = sum dz_uv P_v,
  *   dW = X^T dP,  dX = dP W^T.
- * dX may be NULL. */
+ * dX may be NULL.  z_pos (nnz bytes, may be NULL) supplies the LeakyReLU's
+ * decision z_uv > 0 (as another implementation took it at its rounding). */
 void oracle_gat_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
                     int32_t f_in, int32_t h, const double* X, const double* W,
                     const double* a, double alpha, const double* Y,
-                    const double* dY, double* dX, double* dW, double* da) {
+                    const double* dY, double* dX, double* dW, double* da,
+                    const uint8_t* z_pos) {
   const size_t nh = (size_t)n * (size_t)h;
   double* P = (double*)malloc(sizeof(double) * (nh ? nh : 1));
   double* G = (double*)malloc(sizeof(double) * (nh ? nh : 1));
@@ -470,9 +472,10 @@ void oracle_gat_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
       const double* Gu = G + (int64_t)u * h;
       double z = 0.0, dA = 0.0;
       for (int32_t c = 0; c < h; ++c) z += a[c] * Pu[c] + a[h + c] * Pv[c];
-      const double att = z > 0.0 ? z : alpha * z;
+      const int pos = z_pos ? (z_pos[j] != 0) : (z > 0.0);
+      const double att = pos ? z : alpha * z;
       for (int32_t c = 0; c < h; ++c) dA += Gu[c] * Pv[c];
-      const double dz = dA * (z > 0.0 ? 1.0 : alpha);
+      const double dz = dA * (pos ? 1.0 : alpha);
       for (int32_t c = 0; c < h; ++c) {
         dP[(int64_t)v * h + c] += att * Gu[c];      /* A_att^T G */
         dP[(int64_t)u * h + c] += dz * a[c];        /* through a1 . P_u */

@@ -178,14 +178,16 @@ int64_t oracle_induce(int64_t n_full, const int64_t* indptr,
 /* GAT layer (Section 2.1): P = X W, att_uv = LeakyReLU(a1 . P_u + a2 . P_v)
  * on the stored entries (slope alpha below 0), Y = ReLU(A_att P); att
  * (nnz) may be NULL.  Backward by the chain rule; dX may be NULL; da has
- * 2h entries. */
+ * 2h entries; z_pos (nnz bytes, may be NULL) gives the LeakyReLU's
+ * decisions. */
 void oracle_gat_fwd(int32_t n, const int32_t* indptr, const int32_t* indices,
                     int32_t f_in, int32_t h, const double* X, const double* W,
                     const double* a, double alpha, double* Y, double* att);
 void oracle_gat_bwd(int32_t n, const int32_t* indptr, const int32_t* indices,
                     int32_t f_in, int32_t h, const double* X, const double* W,
                     const double* a, double alpha, const double* Y,
-                    const double* dY, double* dX, double* dW, double* da);
+                    const double* dY, double* dX, double* dW, double* da,
+                    const uint8_t* z_pos);
 
 #ifdef __cplusplus
 }

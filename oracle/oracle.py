@@ -84,7 +84,8 @@ def lib():
                 "oracle_gat_fwd": [i32, _I32P, _I32P, i32, i32, _F64P, _F64P, _F64P,
                                    ctypes.c_double, _F64P, _F64P],
                 "oracle_gat_bwd": [i32, _I32P, _I32P, i32, i32, _F64P, _F64P, _F64P,
-                                   ctypes.c_double, _F64P, _F64P, _F64P, _F64P, _F64P],
+                                   ctypes.c_double, _F64P, _F64P, _F64P, _F64P, _F64P,
+                                   _U8P],
                 "oracle_adam": [i64, _F64P, _F64P, _F64P, _F64P, ctypes.c_double,
                                 ctypes.c_double, ctypes.c_double, ctypes.c_double, i32],
                 "oracle_mixhop_fwd": [i32, _I32P, _I32P, _F64P, i32, i32, i32,
@@ -353,8 +354,11 @@ def gat_fwd(g, x, w, a, alpha: float = GAT_ALPHA, want_att: bool = False):
     return (y, att) if want_att else y
 
 
-def gat_bwd(g, x, w, a, y, dy, alpha: float = GAT_ALPHA, want_dx: bool = True) -> dict:
+def gat_bwd(g, x, w, a, y, dy, alpha: float = GAT_ALPHA, want_dx: bool = True,
+            z_pos=None) -> dict:
+    """z_pos: optional per-entry booleans, the LeakyReLU's decisions."""
     n, ip, ix, _ = _csr(g)
+    zp = None if z_pos is None else np.ascontiguousarray(z_pos, np.uint8)
     x, w, a, y, dy = _f64(x), _f64(w), _f64(a), _f64(y), _f64(dy)
     f_in, h = w.shape
     assert y.shape == (n, h) == dy.shape
@@ -363,7 +367,7 @@ def gat_bwd(g, x, w, a, y, dy, alpha: float = GAT_ALPHA, want_dx: bool = True) -
     lib().oracle_gat_bwd(n, _p(ip, _I32P), _p(ix, _I32P), f_in, h, _p(x, _F64P),
                          _p(w, _F64P), _p(a, _F64P), float(alpha), _p(y, _F64P),
                          _p(dy, _F64P), _p(out["dX"], _F64P), _p(out["dW"], _F64P),
-                         _p(out["da"], _F64P))
+                         _p(out["da"], _F64P), _p(zp, _U8P))
     return out
 
 

@@ -900,3 +900,20 @@ def test_gat_gradients_finite_differences(seed):
     assert rel(r["dX"], fd[0]) < 1e-6
     assert rel(r["dW"], fd[1]) < 1e-6
     assert rel(r["da"], fd[2]) < 1e-6
+
+
+def test_gat_supplied_decisions():
+    # the natural decisions given explicitly change nothing; all-positive
+    # decisions equal slope 1 (the attention taken as linear)
+    g, x, w, a = _gat_case(13)
+    dy = np.random.default_rng(2).standard_normal((g.n, w.shape[1]))
+    y, att = O.gat_fwd(g, x, w, a, want_att=True)
+    r0 = O.gat_bwd(g, x, w, a, y, dy)
+    r1 = O.gat_bwd(g, x, w, a, y, dy, z_pos=att > 0)
+    for k in ("dX", "dW", "da"):
+        assert np.array_equal(r0[k], r1[k])
+    y1 = O.gat_fwd(g, x, w, a, alpha=1.0)
+    ra = O.gat_bwd(g, x, w, a, y1, dy, z_pos=np.ones(att.size, bool))
+    rb = O.gat_bwd(g, x, w, a, y1, dy, alpha=1.0)
+    for k in ("dX", "dW", "da"):
+        assert rel(ra[k], rb[k]) < 1e-14
