@@ -244,6 +244,33 @@ gnn_status gnn_mixhop_bwd(const gnn_csr* csr, const gnn_layer* layer,
                           float* dX, float* dW, float* db, void* workspace,
                           size_t workspace_bytes, hipStream_t stream);
 
+/* ----------------------------------------------------------- GAT layer */
+
+/* Section 2.1, Eqs. "gat forward" and "gat attention": on the stored
+ * entries (u, v) of the subgraph (edges and self loops; the CSR's values
+ * are not used, its pattern must be symmetric and its plan built),
+ *   P = X W,  att_uv = LeakyReLU(a1 . P_u + a2 . P_v)  (slope alpha in
+ *   [0, 1] below 0),  Y = ReLU(A_att P)
+ * with a = [a1; a2] (2h floats, device).  layer: f_in, h, ld_x, ld_y
+ * (Y is n x h), ld_dx; order is ignored; flags: GNN_FLAG_BF16 for the
+ * products.  att_out (nnz floats, may be NULL) receives the attention
+ * values in CSR order.  `saved` (gnn_gat_saved_bytes) carries P, the
+ * scores and the attention values from the forward to the backward call.
+ * Backward: dW (f_in x h), da (2h) and optionally dX, by the chain rule
+ * (the per-entry products G_u . P_v form an SDDMM).  No output may overlap
+ * an input, another output or the workspace (gnn_gat_workspace_bytes). */
+size_t gnn_gat_saved_bytes(const gnn_csr* csr, const gnn_layer* layer);
+size_t gnn_gat_workspace_bytes(const gnn_csr* csr, const gnn_layer* layer);
+gnn_status gnn_gat_fwd(const gnn_csr* csr, const gnn_layer* layer, const float* X,
+                       const float* W, const float* a, float alpha, float* Y,
+                       float* att_out, void* saved, void* workspace,
+                       size_t workspace_bytes, hipStream_t stream);
+gnn_status gnn_gat_bwd(const gnn_csr* csr, const gnn_layer* layer, const float* X,
+                       const float* W, const float* a, float alpha, const float* Y,
+                       const float* dY, const void* saved, float* dX, float* dW,
+                       float* da, void* workspace, size_t workspace_bytes,
+                       hipStream_t stream);
+
 /* --------------------------------------- classifier, loss, weight update */
 
 /* Section 3.1 (Eqs. "mlp forward", "loss forward") and Algorithm 1: the
@@ -413,7 +440,8 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
 #define GNN_K_UPDATE 12       /* weight update (SGD or Adam) */
 #define GNN_K_INDUCE 13       /* induced subgraph on the GPU */
 #define GNN_K_GATHER 14       /* feature / label row gather */
-#define GNN_K_COUNT 15
+#define GNN_K_SDDMM 15        /* GAT per-entry dot products */
+#define GNN_K_COUNT 16
 
 /* When enabled, every kernel launch is bracketed by a pair of HIP events on
  * its stream.  gnn_timer_read synchronises on the recorded events and

@@ -27,7 +27,7 @@ GNN_LOSS_SIGMOID = 1
 KERNELS = {"spmm": 0, "spmm_reduce": 1, "gemm_nn": 2, "gemm_tn": 3,
            "gemm_nt": 4, "gemm_tt": 5, "gemm_reduce": 6, "mask": 7,
            "colsum": 8, "plan": 9, "transpose": 10, "loss": 11, "update": 12,
-           "induce": 13, "gather": 14}
+           "induce": 13, "gather": 14, "sddmm": 15}
 GNN_NORM_ROW = 0
 GNN_NORM_SYM = 1
 
@@ -131,6 +131,16 @@ EXPORTS = {
                                             ctypes.c_int32, ctypes.c_void_p]),
     "gnn_sampler_next": (ctypes.c_int32, [ctypes.c_void_p] * 4),
     "gnn_sampler_destroy": (None, [ctypes.c_void_p]),
+    "gnn_gat_saved_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                              ctypes.POINTER(gnn_layer)]),
+    "gnn_gat_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
+                                                  ctypes.POINTER(gnn_layer)]),
+    "gnn_gat_fwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer)]
+                    + [ctypes.c_void_p] * 3 + [ctypes.c_float]
+                    + [ctypes.c_void_p] * 4 + [ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_gat_bwd": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.POINTER(gnn_layer)]
+                    + [ctypes.c_void_p] * 3 + [ctypes.c_float]
+                    + [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p]),
     "gnn_timer_enable": (ctypes.c_int32, [ctypes.c_int32]),
     "gnn_timer_reset": (ctypes.c_int32, []),
     "gnn_timer_read": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
@@ -304,6 +314,30 @@ def gnn_mixhop_bwd(csr: gnn_csr, layer: gnn_layer, K: int, X, W, Y, dY, saved, d
                                 _ptr(W), _ptr(Y), _ptr(dY), _ptr(saved), _ptr(dX),
                                 _ptr(dW), _ptr(db), _ptr(workspace), _nbytes(workspace),
                                 _stream(stream)), "gnn_mixhop_bwd")
+
+
+def gnn_gat_saved_bytes(csr: gnn_csr, layer: gnn_layer) -> int:
+    return int(lib().gnn_gat_saved_bytes(ctypes.byref(csr), ctypes.byref(layer)))
+
+
+def gnn_gat_workspace_bytes(csr: gnn_csr, layer: gnn_layer) -> int:
+    return int(lib().gnn_gat_workspace_bytes(ctypes.byref(csr), ctypes.byref(layer)))
+
+
+def gnn_gat_fwd(csr: gnn_csr, layer: gnn_layer, X, W, a, alpha: float, Y, att_out, saved,
+                workspace, stream=None):
+    _check(lib().gnn_gat_fwd(ctypes.byref(csr), ctypes.byref(layer), _ptr(X), _ptr(W),
+                             _ptr(a), float(alpha), _ptr(Y), _ptr(att_out), _ptr(saved),
+                             _ptr(workspace), _nbytes(workspace), _stream(stream)),
+           "gnn_gat_fwd")
+
+
+def gnn_gat_bwd(csr: gnn_csr, layer: gnn_layer, X, W, a, alpha: float, Y, dY, saved, dX,
+                dW, da, workspace, stream=None):
+    _check(lib().gnn_gat_bwd(ctypes.byref(csr), ctypes.byref(layer), _ptr(X), _ptr(W),
+                             _ptr(a), float(alpha), _ptr(Y), _ptr(dY), _ptr(saved),
+                             _ptr(dX), _ptr(dW), _ptr(da), _ptr(workspace),
+                             _nbytes(workspace), _stream(stream)), "gnn_gat_bwd")
 
 
 def gnn_classifier_workspace_bytes(n: int, f: int, C: int) -> int:

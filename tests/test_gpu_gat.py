@@ -1,0 +1,111 @@
+"""GAT layer on the GPU against the CPU oracle (through the C ABI).
+
+Forward: Y and the attention values against the oracle's.  Backward:
+teacher-forced, the oracle gets the GPU's fp32 Y (its ReLU mask) and the
+sign of the GPU's attention values (its LeakyReLU decisions), so both sides
+take the same decisions; then dX, dW, da to max-normalised 1e-4 in fp32,
+2e-2 with bf16 products.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2010_03166_amd import gnnprop as G
+from paper_2010_03166_amd import synth
+
+from gpu_helpers import maxrel, prepared, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+GRAPHS = {
+    "random": synth.random_graph(300, 6.0, 1),
+    "powerlaw": synth.power_law_graph(3000, 2.1, 12.0, seed=2),
+    "star700": synth.star_graph(700),
+    "identity": synth.identity_graph(64),
+}
+
+
+def _buf(nbytes):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+
+
+def run_gat(g, f_in, h, alpha=O.GAT_ALPHA, seed=0, pad=8, flags=0, want_dx=True,
+            a_scale=1.0):
+    dg = prepared(g)
+    c = dg.struct()
+    rng = np.random.default_rng(seed)
+    x = synth.features(g.n, f_in, rng)
+    w = synth.glorot(f_in, h, rng)
+    a = (a_scale * rng.standard_normal(2 * h) / np.sqrt(h)).astype(np.float32)
+    dy = rng.standard_normal((g.n, h)).astype(np.float32)
+    ld_x, ld_y = f_in + pad, h + pad
+    lay = G.make_layer(f_in, h, ld_x, ld_y, ld_x, 0, flags)
+    X, W, A = to_dev(x, ld_x), to_dev(w), to_dev(a)
+    Y = torch.full((g.n, ld_y), float("nan"), device="cuda")[:, :h]
+    att = torch.full((max(g.nnz, 1),), float("nan"), device="cuda")
+    saved = _buf(G.gnn_gat_saved_bytes(c, lay))
+    ws = _buf(G.gnn_gat_workspace_bytes(c, lay))
+    G.gnn_gat_fwd(c, lay, X, W, A, alpha, Y, att, saved, ws)
+    dX = torch.full((g.n, ld_x), float("nan"), device="cuda")[:, :f_in] if want_dx else None
+    dW = torch.full((f_in, h), float("nan"), device="cuda")
+    da = torch.full((2 * h,), float("nan"), device="cuda")
+    G.gnn_gat_bwd(c, lay, X, W, A, alpha, Y, to_dev(dy, ld_y), saved, dX, dW, da, ws)
+    torch.cuda.synchronize()
+    return dict(x=x, w=w, a=a, dy=dy, Y=Y.cpu().numpy(), att=att.cpu().numpy()[: g.nnz],
+                dX=None if dX is None else dX.cpu().numpy(), dW=dW.cpu().numpy(),
+                da=da.cpu().numpy())
+
+
+def check(g, r, alpha, tol=TOL):
+    y_ref, att_ref = O.gat_fwd(g, r["x"], r["w"], r["a"], alpha, want_att=True)
+    assert maxrel(r["Y"], y_ref) <= tol
+    assert maxrel(r["att"], att_ref) <= tol
+    ref = O.gat_bwd(g, r["x"], r["w"], r["a"], r["Y"], r["dy"], alpha,
+                    want_dx=r["dX"] is not None, z_pos=r["att"] > 0)
+    for k in ("dW", "da") + (("dX",) if r["dX"] is not None else ()):
+        assert maxrel(r[k], ref[k]) <= tol, k
+
+
+@pytest.mark.parametrize("name", list(GRAPHS))
+@pytest.mark.parametrize("alpha", [0.0, O.GAT_ALPHA, 1.0])
+def test_gat_layer_parity(name, alpha):
+    g = GRAPHS[name]
+    r = run_gat(g, 24, 40, alpha, seed=3)
+    check(g, r, alpha)
+
+
+def test_gat_ragged_width_and_no_dx():
+    g = GRAPHS["random"]
+    r = run_gat(g, 13, 7, seed=4, pad=1, want_dx=False)
+    check(g, r, O.GAT_ALPHA)
+
+
+def test_gat_full_size_bench_graph():
+    """f_in 602 -> 512 on the 8,000-node graph, as the benchmark times it."""
+    wl = synth.WORKLOADS[synth.BENCH_WORKLOAD]
+    g = synth.workload_graph(wl)
+    r = run_gat(g, 602, 512, seed=5, pad=6)
+    check(g, r, O.GAT_ALPHA)
+
+
+def test_gat_bf16_mode():
+    g = GRAPHS["powerlaw"]
+    r = run_gat(g, 64, 48, seed=6, flags=G.GNN_FLAG_BF16)
+    check(g, r, O.GAT_ALPHA, tol=2e-2)
+
+
+def test_gat_argument_errors():
+    g = GRAPHS["random"]
+    c = prepared(g).struct()
+    lay = G.make_layer(8, 4, 8, 4, 8, 0, 0)
+    ws = _buf(G.gnn_gat_workspace_bytes(c, lay))
+    with pytest.raises(G.GnnError):  # slope outside [0, 1]
+        G.gnn_gat_fwd(c, lay, None, torch.zeros(32, device="cuda"),
+                      torch.zeros(8, device="cuda"), 1.5, None, None, None, ws)
+    with pytest.raises(G.GnnError):  # workspace too small
+        G.gnn_gat_fwd(c, lay, torch.zeros((g.n, 8), device="cuda"),
+                      torch.zeros(32, device="cuda"), torch.zeros(8, device="cuda"), 0.2,
+                      torch.zeros((g.n, 4), device="cuda"), None, _buf(1 << 20), _buf(8)[:8])
