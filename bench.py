@@ -452,7 +452,8 @@ def bench_pipeline(G, runtime, synth, torch, np, args):
 
 def bench_variants(G, runtime, synth, torch, np, g, x, wl, args):
     """ms per layer (forward + backward, first-layer shape) of a GCN layer
-    (f_in -> h) and a MixHop layer with K = 2 hops of h/2 columns each."""
+    (f_in -> h), a MixHop layer with K = 2 hops of h/2 columns each, and a
+    GAT layer (f_in -> h, attention slope 0.2)."""
     gs = synth.sym_normalized(g)
     dg = runtime.DeviceGraph(gs)
     dg.prepare()
@@ -531,6 +532,24 @@ def bench_variants(G, runtime, synth, torch, np, g, x, wl, args):
     res["mixhop_k2"] = {"ms_per_layer": round(ms, 5),
                         "shape": "%d -> 3 x %d" % (f_in, hk), "kernels": kern}
     log("mixhop layer: %.4f ms" % ms)
+    # GAT: Y = ReLU(A_att X W), attention on the stored entries (row-normalised
+    # pattern of the same subgraph; its values are not used)
+    dgs = runtime.DeviceGraph(g)
+    dgs.prepare()
+    cg = dgs.struct()
+    a = torch.from_numpy((rng.standard_normal(2 * h) / np.sqrt(h)).astype(np.float32)).cuda()
+    layg = G.make_layer(f_in, h, X.stride(0), rup(h), X.stride(0), 0, 0)
+    savedg, wsg = buf(G.gnn_gat_saved_bytes(cg, layg)), buf(G.gnn_gat_workspace_bytes(cg, layg))
+    da = torch.empty(2 * h, device="cuda")
+
+    def gat():
+        G.gnn_gat_fwd(cg, layg, X, W, a, 0.2, Y, None, savedg, wsg)
+        G.gnn_gat_bwd(cg, layg, X, W, a, 0.2, Y, dYp, savedg, dX, dW, da, wsg)
+
+    ms, kern = timed(gat)
+    res["gat"] = {"ms_per_layer": round(ms, 5), "shape": "%d -> %d" % (f_in, h),
+                  "kernels": kern}
+    log("gat layer: %.4f ms" % ms)
     return res
 
 

@@ -58,54 +58,117 @@ hipError_t mask_launch(int32_t n, int32_t width, int32_t split,
   return hipGetLastError();
 }
 
-// Column sums in two deterministic phases: block (cb, rb) sums rows
-// [256 rb, 256 rb + 256) of 64 columns (4 row groups of 64 rows, combined in
-// group order), then one thread per column adds the row-block partials in
-// ascending rb.
-constexpr int CS_ROWS = 256;
+// Column sums in two deterministic phases.  Phase 1: block (rb, cb) covers
+// 64 columns and CS_ROWS rows; each of its 4 waves takes CS_RPT consecutive
+// rows, issuing all of their loads before the adds (the sum is latency
+// bound otherwise), and the wave sums are combined in wave order.  Phase 2:
+// per CS_FC columns, CS_FG thread groups each add a contiguous share of the
+// row-block partials in ascending order (a few loads in flight per thread,
+// so the pass is one memory round trip or two), combined in group order.
+// NW = 2 forms two weighted sums (weights w0[r], w1[r]) from one pass over G.
+constexpr int CS_RPT = 16;
+constexpr int CS_ROWS = 4 * CS_RPT;
+constexpr int CS_FC = 16, CS_FG = 256 / CS_FC;
 
+template <int NW>
 __global__ __launch_bounds__(256) void colsum_partial_kernel(
     int32_t n, int32_t w, const float* __restrict__ G, int64_t ldg,
-    float* __restrict__ part) {
-  __shared__ float s[4][64];
-  const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+    const float* __restrict__ w0, const float* __restrict__ w1,
+    float* __restrict__ part, int64_t pstride) {
+  __shared__ float s[NW][4][64];
+  const int l = threadIdx.x & 63;
   const int grp = threadIdx.x >> 6;
-  const int r0 = blockIdx.y * CS_ROWS + grp * (CS_ROWS / 4);
-  float acc = 0.f;
-  if (c < w)
-    for (int r = r0; r < min(n, r0 + CS_ROWS / 4); ++r)
-      acc += G[(int64_t)r * ldg + c];
-  s[grp][threadIdx.x & 63] = acc;
+  const int c = blockIdx.y * 64 + l;
+  const int r0 = blockIdx.x * CS_ROWS + grp * CS_RPT;
+  float acc[NW];
+#pragma unroll
+  for (int j = 0; j < NW; ++j) acc[j] = 0.f;
+  if (c < w) {
+    float v[CS_RPT];
+#pragma unroll
+    for (int k = 0; k < CS_RPT; ++k)
+      v[k] = r0 + k < n ? G[(int64_t)(r0 + k) * ldg + c] : 0.f;
+#pragma unroll
+    for (int k = 0; k < CS_RPT; ++k) {
+      if (r0 + k >= n) break;
+      acc[0] += w0 ? w0[r0 + k] * v[k] : v[k];
+      if (NW == 2) acc[NW - 1] += w1[r0 + k] * v[k];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NW; ++j) s[j][grp][l] = acc[j];
   __syncthreads();
   if (grp == 0 && c < w) {
-    const int l = threadIdx.x & 63;
-    part[(int64_t)blockIdx.y * w + c] = ((s[0][l] + s[1][l]) + s[2][l]) + s[3][l];
+#pragma unroll
+    for (int j = 0; j < NW; ++j)
+      part[j * pstride + (int64_t)blockIdx.x * w + c] =
+          ((s[j][0][l] + s[j][1][l]) + s[j][2][l]) + s[j][3][l];
   }
 }
 
+template <int NW>
 __global__ __launch_bounds__(256) void colsum_final_kernel(
-    int32_t nblk, int32_t w, const float* __restrict__ part,
-    float* __restrict__ out) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= w) return;
-  float acc = 0.f;
-  for (int b = 0; b < nblk; ++b) acc += part[(int64_t)b * w + c];
-  out[c] = acc;
+    int32_t nblk, int32_t w, const float* __restrict__ part, int64_t pstride,
+    float* __restrict__ out0, float* __restrict__ out1) {
+  __shared__ float s[NW][CS_FG][CS_FC];
+  const int l = threadIdx.x % CS_FC;
+  const int grp = threadIdx.x / CS_FC;
+  const int c = blockIdx.x * CS_FC + l;
+  const int q = (nblk + CS_FG - 1) / CS_FG;
+  const int b0 = min(nblk, grp * q), b1 = min(nblk, b0 + q);
+#pragma unroll
+  for (int j = 0; j < NW; ++j) {
+    float acc = 0.f;
+    if (c < w) {
+      const float* p = part + j * pstride + c;
+#pragma unroll 8
+      for (int b = b0; b < b1; ++b) acc += p[(int64_t)b * w];
+    }
+    s[j][grp][l] = acc;
+  }
+  __syncthreads();
+  if (threadIdx.x < CS_FC && c < w) {
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      float acc = s[j][0][l];
+      for (int g = 1; g < CS_FG; ++g) acc += s[j][g][l];
+      (j == 0 ? out0 : out1)[c] = acc;
+    }
+  }
 }
 
-size_t colsum_partials_bytes(int32_t n, int32_t w) {
-  return round_up((size_t)std::max<int64_t>(1, ceil_div(n, CS_ROWS)) * w * 4, 256);
+size_t colsum_partials_bytes(int32_t n, int32_t w, int nw) {
+  return round_up((size_t)nw * std::max<int64_t>(1, ceil_div(n, CS_ROWS)) * w * 4, 256);
 }
 
 hipError_t colsum_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
-                         float* out, float* partials, hipStream_t s) {
+                         float* out, float* partials, hipStream_t s,
+                         const float* row_weight) {
   if (w <= 0) return hipSuccess;
   const int nblk = (int)std::max<int64_t>(1, ceil_div(n, CS_ROWS));
-  dim3 grid((unsigned)ceil_div(w, 64), (unsigned)nblk);
+  const int64_t ps = (int64_t)nblk * w;
+  dim3 grid((unsigned)nblk, (unsigned)ceil_div(w, 64));
   timer_begin(GNN_K_COLSUM, s);
-  colsum_partial_kernel<<<grid, 256, 0, s>>>(n, w, G, ldg, partials);
-  colsum_final_kernel<<<(unsigned)ceil_div(w, 256), 256, 0, s>>>(nblk, w, partials, out);
+  colsum_partial_kernel<1><<<grid, 256, 0, s>>>(n, w, G, ldg, row_weight, nullptr,
+                                                partials, ps);
+  colsum_final_kernel<1><<<(unsigned)ceil_div(w, CS_FC), 256, 0, s>>>(nblk, w, partials, ps,
+                                                                       out, nullptr);
   timer_end(GNN_K_COLSUM, 4.0 * n * w, s);
+  return hipGetLastError();
+}
+
+hipError_t colsum2_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
+                          const float* w0, const float* w1, float* out0,
+                          float* out1, float* partials, hipStream_t s) {
+  if (w <= 0) return hipSuccess;
+  const int nblk = (int)std::max<int64_t>(1, ceil_div(n, CS_ROWS));
+  const int64_t ps = (int64_t)nblk * w;
+  dim3 grid((unsigned)nblk, (unsigned)ceil_div(w, 64));
+  timer_begin(GNN_K_COLSUM, s);
+  colsum_partial_kernel<2><<<grid, 256, 0, s>>>(n, w, G, ldg, w0, w1, partials, ps);
+  colsum_final_kernel<2><<<(unsigned)ceil_div(w, CS_FC), 256, 0, s>>>(nblk, w, partials, ps,
+                                                                       out0, out1);
+  timer_end(GNN_K_COLSUM, 4.0 * n * w + 8.0 * n, s);
   return hipGetLastError();
 }
 

@@ -16,7 +16,8 @@
 //     of the transposed values, Algorithm 6's permutation)
 //   dP = A_att^T G + ds a1^T + dt a2^T   (aggregation on the transposed
 //                                         attention, then a rank-2 update)
-//   [da1; da2] = [ds dt]^T P,  dW = X^T dP,  dX = dP W^T   (matrix cores)
+//   da1 = P^T ds, da2 = P^T dt (weighted column sums, fixed order),
+//   dW = X^T dP,  dX = dP W^T                             (matrix cores)
 #include <algorithm>
 
 #include "abi.hpp"
@@ -157,11 +158,11 @@ gnn_status check_gat(const gnn_csr* csr, const gnn_layer* L, float alpha) {
 
 // saved: P (n x ld_h), s, t (n), att (nnz).
 // workspace: G (n x ld_h), dP (n x ld_h), dz, dz_t, att_t (nnz), [ds; dt]
-// (2 x ld_n), GEMM partials.
+// (2 x ld_n), column-sum partials, GEMM partials.
 struct GatLayout {
   int64_t ld_h, ld_n;
   size_t s_p, s_s, s_t, s_att, saved;
-  size_t w_g, w_dp, w_dz, w_dzt, w_att_t, w_dsdt, w_gemm, total;
+  size_t w_g, w_dp, w_dz, w_dzt, w_att_t, w_dsdt, w_cs, w_gemm, total;
 };
 
 GatLayout gat_layout(const gnn_csr* csr, const gnn_layer* L) {
@@ -182,14 +183,14 @@ GatLayout gat_layout(const gnn_csr* csr, const gnn_layer* L) {
   g = std::max(g, gemm_workspace_bytes(gemm1(0, 0, n, h, f_in, 0, f_in, 0, h, 0, h, 0, L->flags)));
   g = std::max(g, gemm_workspace_bytes(gemm1(1, 0, f_in, h, n, 0, f_in, 0, h, 0, h, 0, L->flags)));
   g = std::max(g, gemm_workspace_bytes(gemm1(0, 1, n, f_in, h, 0, h, 0, h, 0, f_in, 0, L->flags)));
-  g = std::max(g, gemm_workspace_bytes(gemm1(0, 0, 2, h, n, 0, n, 0, h, 0, h, 0, L->flags)));
   o.w_g = 0;
   o.w_dp = nh;
   o.w_dz = o.w_dp + nh;
   o.w_dzt = o.w_dz + eb;
   o.w_att_t = o.w_dzt + eb;
   o.w_dsdt = o.w_att_t + eb;
-  o.w_gemm = o.w_dsdt + round_up((size_t)2 * o.ld_n * 4, 256);
+  o.w_cs = o.w_dsdt + round_up((size_t)2 * o.ld_n * 4, 256);
+  o.w_gemm = o.w_cs + colsum_partials_bytes(n, h, 2);
   o.total = o.w_gemm + round_up(g, 256);
   return o;
 }
@@ -300,8 +301,9 @@ gnn_status gnn_gat_bwd(const gnn_csr* csr, const gnn_layer* layer, const float* 
   if (n == 0) {  // no rows: zero gradients through empty products
     GNN_HIP(gemm_launch(gemm1(1, 0, f_in, h, 0, X, layer->ld_x, dY, layer->ld_y, dW, h, 0,
                               layer->flags), gws, gws_bytes, stream));
-    GNN_HIP(gemm_launch(gemm1(0, 0, 2, h, 0, X, 1, dY, layer->ld_y, da, h, 0,
-                              layer->flags), gws, gws_bytes, stream));
+    float* cspart = reinterpret_cast<float*>(ws + o.w_cs);
+    GNN_HIP(colsum_launch(0, h, dY, h, da, cspart, stream));
+    GNN_HIP(colsum_launch(0, h, dY, h, da + h, cspart, stream));
     return GNN_OK;
   }
   const char* sv = static_cast<const char*>(saved);
@@ -342,9 +344,10 @@ gnn_status gnn_gat_bwd(const gnn_csr* csr, const gnn_layer* layer, const float* 
   gat_rank2_kernel<<<(unsigned)ceil_div((int64_t)n * h, 256), 256, 0, stream>>>(
       n, h, ds, dt, a, dP, o.ld_h);
   GNN_HIP(hipGetLastError());
-  // [da1; da2] = [ds; dt] P (2 x h), dW = X^T dP, dX = dP W^T
-  GNN_HIP(gemm_launch(gemm1(0, 0, 2, h, n, ds, o.ld_n, P, o.ld_h, da, h, 0, layer->flags),
-                      gws, gws_bytes, stream));
+  // da1 = P^T ds, da2 = P^T dt (weighted column sums), dW = X^T dP,
+  // dX = dP W^T
+  float* cspart = reinterpret_cast<float*>(ws + o.w_cs);
+  GNN_HIP(colsum2_launch(n, h, P, o.ld_h, ds, dt, da, da + h, cspart, stream));
   GNN_HIP(gemm_launch(gemm1(1, 0, f_in, h, n, X, layer->ld_x, dP, o.ld_h, dW, h, 0,
                             layer->flags), gws, gws_bytes, stream));
   if (dX)

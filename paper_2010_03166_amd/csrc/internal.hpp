@@ -141,10 +141,16 @@ hipError_t mask_launch(int32_t n, int32_t width, int32_t split,
                        const float* Y, const float* dY, int64_t ld_y,
                        float* dst0, int64_t ld0, float* dst1, int64_t ld1,
                        hipStream_t s);
-// out[c] = sum over rows of G[r, c], rows in ascending blocks of 256 summed
-// in a fixed order.  partials: colsum_partials_bytes.
-size_t colsum_partials_bytes(int32_t n, int32_t w);
+// out[c] = sum over rows of G[r, c] in a fixed order (the same for every
+// call with the same n); with row_weight, out[c] = sum_r row_weight[r] G[r, c].
+// colsum2 forms out0 = G^T w0 and out1 = G^T w1 from one pass over G.
+// partials: colsum_partials_bytes(n, w, number of sums).
+size_t colsum_partials_bytes(int32_t n, int32_t w, int nw = 1);
 hipError_t colsum_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
-                         float* out, float* partials, hipStream_t s);
+                         float* out, float* partials, hipStream_t s,
+                         const float* row_weight = nullptr);
+hipError_t colsum2_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
+                          const float* w0, const float* w1, float* out0,
+                          float* out1, float* partials, hipStream_t s);
 
 }  // namespace gnnprop
