@@ -475,28 +475,39 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
 //
 // Same tiling, work split and epilogue as the fp32 kernel, with operands
 // rounded to bf16 (round to nearest even, v_cvt_pk_bf16_f32) as they are
-// staged into LDS, fp32 accumulation on v_mfma_f32_32x32x16_bf16, and
-// 32-deep K slices (two MFMA steps; small enough that the fp32 prefetch
-// registers leave room for two blocks per CU).  In MFMA step s (s = 0, 1)
-// lane half h supplies the 8 values k = 16 h + 8 s + j (j = 0..7).
-//   K-contiguous operand: LDS [x][k] rows of 32 + 8 bf16; one 128-bit read
-//     per fragment.
+// staged into LDS and fp32 accumulation on v_mfma_f32_32x32x16_bf16.  A
+// 32 x 32 x 16 bf16 MFMA takes a sixteenth of the cycles of the fp32 one, so
+// a K step here is 64 deep (four MFMA steps, 16 MFMAs per wavefront between
+// barriers) to amortise the per-step chain of waits, conversions, LDS
+// stores and the barrier.  In MFMA step s (s = 0..3) lane half h supplies
+// the 8 values k = 32 h + 8 s + j (j = 0..7); A and B use the same order,
+// so the contraction is unchanged.
+//   K-contiguous operand: LDS [x][k] rows of 64 + 8 bf16 (36 words); one
+//     128-bit read per fragment.
 //   X-contiguous operand: LDS rows of k pairs, each word = (k, k+1) of one
-//     x as bf16x2; a fragment is 4 words from 4 rows; the pair rows are
-//     stored in the order (kp mod 8) * 2 + kp / 8 (kp = k / 2) so the two
-//     lane halves read adjacent rows.
+//     x as bf16x2; a fragment is 4 words from 4 pair rows.  Pair kp lives
+//     in half kp / 16 (pairs of lane half 0, then of lane half 1), row
+//     kp mod 16, and the second half starts 32 words past the first's end,
+//     so the two lane halves of a read fall on different banks.
+// Interior tiles over full K steps run the fp32 kernel's pipeline: store the
+// next step (in registers) into the other LDS stage, issue the loads of the
+// step after it, compute, one barrier.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 
-constexpr int BK16 = 32;
-constexpr int KC16_STRIDE = 20;   // 32-bit words per [x][k] row (40 bf16)
-constexpr int XC16_STRIDE = 160;  // words per k-pair row
+constexpr int BK16 = 64;
+constexpr int KC16_STRIDE = BK16 / 2 + 4;          // words per [x][k] row
+constexpr int XC16_HALF = (BK16 / 4) * 128 + 32;   // words per half (16 pair rows + gap)
 constexpr int KC16_WORDS = 128 * KC16_STRIDE;
-constexpr int XC16_WORDS = (BK16 / 2) * XC16_STRIDE;
+constexpr int XC16_WORDS = 2 * XC16_HALF;
 
 __device__ inline uint32_t pack_bf16(float lo, float hi) {
   bf16x2v v = {(__bf16)lo, (__bf16)hi};
   return __builtin_bit_cast(uint32_t, v);
+}
+// LDS word of k pair kp, column x, in the x-contiguous bf16 layout.
+__device__ inline int xc16_word(int kp, int x) {
+  return (kp >> 4) * XC16_HALF + (kp & 15) * 128 + x;
 }
 
 template <bool AT, bool BT>
@@ -505,8 +516,10 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
   constexpr bool B_KC = BT;
   constexpr int A_WORDS = A_KC ? KC16_WORDS : XC16_WORDS;
   constexpr int B_WORDS = B_KC ? KC16_WORDS : XC16_WORDS;
-  __shared__ __attribute__((aligned(16))) uint32_t As[2][A_WORDS];
-  __shared__ __attribute__((aligned(16))) uint32_t Bs[2][B_WORDS];
+  __shared__ __attribute__((aligned(16))) uint32_t As0[A_WORDS];
+  __shared__ __attribute__((aligned(16))) uint32_t As1[A_WORDS];
+  __shared__ __attribute__((aligned(16))) uint32_t Bs0[B_WORDS];
+  __shared__ __attribute__((aligned(16))) uint32_t Bs1[B_WORDS];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -526,7 +539,6 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
     hi = block_lo(lb + 1, g.iters, g.nblocks);
   }
 
-  int buf = 0;
   int seg = 0;
   for (int64_t it = lo; it < hi; ++seg) {
     const int t = (int)(it / g.ktiles);
@@ -547,27 +559,29 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
     const int K0 = P.seg[0].K, K1 = P.seg[1].K;
     const bool a_in = va && m0 + BM <= M;
     const bool b_in = vb && n0 + BN <= N;
-    // KC: thread owns row x = (tid >> 2) + 64 p and k = 8 (tid & 3) .. + 7.
-    // XC: thread owns k-pair kp = (tid >> 5) + 8 p and x = 4 (tid & 31) .. + 3.
-    const int kx = tid >> 2, ky = 8 * (tid & 3);
+    // KC: thread owns k = 4 (tid & 15) .. + 3 of rows x = (tid >> 4) + 16 q
+    // (q = 0..7): 16 lanes read one 256-byte row, a wavefront 4 whole rows
+    // per instruction (8 cache lines per KiB).
+    // XC: thread owns k pair kp = (tid >> 5) + 8 p and x = 4 (tid & 31) .. + 3.
+    const int kx = tid >> 4, ky = 4 * (tid & 15);
     const int xk = tid >> 5, xy = 4 * (tid & 31);
 
-    float4 ra[4], rb[4];
-    // Loads of one operand's slice: `lo4`/`hi4` pairs per p (KC: k halves,
-    // XC: rows 2kp and 2kp+1).
-    auto load_op = [&](float4 (&r)[4], bool kc, const float* X, int64_t ld,
+    float4 ra[8], rb[8];
+    // One operand's K step: (KC) 4 consecutive k of 8 rows, or (XC) rows
+    // 2 kp and 2 kp + 1, for p = 0..3.
+    auto load_op = [&](float4 (&r)[8], bool kc, const float* X, int64_t ld,
                        int x0, int X_extent, int k0, int K, bool fast, bool vec) {
 #pragma unroll
-      for (int p = 0; p < 2; ++p) {
+      for (int p = 0; p < 4; ++p) {
         if (kc) {
-          const int x = x0 + kx + 64 * p, k = k0 + ky;
+          const int x = x0 + kx + 32 * p, k = k0 + ky;
           if (fast) {
             const float* q = X + (int64_t)x * ld + k;
             r[2 * p] = ld4(q);
-            r[2 * p + 1] = ld4(q + 4);
+            r[2 * p + 1] = ld4(q + 16 * ld);
           } else {
             r[2 * p] = load4(X, ld, x, k, X_extent, K, vec);
-            r[2 * p + 1] = load4(X, ld, x, k + 4, X_extent, K, vec);
+            r[2 * p + 1] = load4(X, ld, x + 16, k, X_extent, K, vec);
           }
         } else {
           const int k = k0 + 2 * (xk + 8 * p), x = x0 + xy;
@@ -590,25 +604,25 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
       load_op(ra, A_KC, s1 ? A1p : A0p, s1 ? lda1 : lda0, m0, M, k0, K, a_in && fk, va);
       load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, K, b_in && fk, vb);
     };
-    auto store_op = [&](uint32_t* L, const float4 (&r)[4], bool kc) {
+    auto store_op = [&](uint32_t* L, const float4 (&r)[8], bool kc) {
 #pragma unroll
-      for (int p = 0; p < 2; ++p) {
+      for (int p = 0; p < 4; ++p) {
         const float4 a = r[2 * p], b = r[2 * p + 1];
-        uint4 w;
-        if (kc) {  // 8 consecutive k of row x
-          w.x = pack_bf16(a.x, a.y);
-          w.y = pack_bf16(a.z, a.w);
-          w.z = pack_bf16(b.x, b.y);
-          w.w = pack_bf16(b.z, b.w);
-          *reinterpret_cast<uint4*>(&L[(kx + 64 * p) * KC16_STRIDE + ky / 2]) = w;
+        if (kc) {  // 4 consecutive k of rows x and x + 16
+          uint2 u, v;
+          u.x = pack_bf16(a.x, a.y);
+          u.y = pack_bf16(a.z, a.w);
+          v.x = pack_bf16(b.x, b.y);
+          v.y = pack_bf16(b.z, b.w);
+          *reinterpret_cast<uint2*>(&L[(kx + 32 * p) * KC16_STRIDE + ky / 2]) = u;
+          *reinterpret_cast<uint2*>(&L[(kx + 32 * p + 16) * KC16_STRIDE + ky / 2]) = v;
         } else {   // k pair (a: row 2kp, b: row 2kp+1) of 4 consecutive x
+          uint4 w;
           w.x = pack_bf16(a.x, b.x);
           w.y = pack_bf16(a.y, b.y);
           w.z = pack_bf16(a.z, b.z);
           w.w = pack_bf16(a.w, b.w);
-          const int kp = xk + 8 * p;
-          const int row = ((kp & 7) << 1) | (kp >> 3);
-          *reinterpret_cast<uint4*>(&L[row * XC16_STRIDE + xy]) = w;
+          *reinterpret_cast<uint4*>(&L[xc16_word(xk + 8 * p, xy)]) = w;
         }
       }
     };
@@ -621,31 +635,22 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    // fragment for block i of an operand at step s
+    // fragment for block i of an operand at MFMA step s
     auto frag = [&](const uint32_t* L, bool kc, int wbase, int i, int s) {
       uint4 w;
+      const int x = wbase + i * 32 + lr;
       if (kc) {
-        w = *reinterpret_cast<const uint4*>(
-            &L[(wbase + i * 32 + lr) * KC16_STRIDE + (16 * lh + 8 * s) / 2]);
+        w = *reinterpret_cast<const uint4*>(&L[x * KC16_STRIDE + 16 * lh + 4 * s]);
       } else {
-        const int x = wbase + i * 32 + lr;
-        // k pairs 8 lh + 4 s + j, stored at rows ((4 s + j) << 1) | lh
-        w.x = L[((((4 * s + 0) << 1) | lh)) * XC16_STRIDE + x];
-        w.y = L[((((4 * s + 1) << 1) | lh)) * XC16_STRIDE + x];
-        w.z = L[((((4 * s + 2) << 1) | lh)) * XC16_STRIDE + x];
-        w.w = L[((((4 * s + 3) << 1) | lh)) * XC16_STRIDE + x];
+        // k pairs 16 lh + 4 s + c
+        w.x = L[xc16_word(16 * lh + 4 * s + 0, x)];
+        w.y = L[xc16_word(16 * lh + 4 * s + 1, x)];
+        w.z = L[xc16_word(16 * lh + 4 * s + 2, x)];
+        w.w = L[xc16_word(16 * lh + 4 * s + 3, x)];
       }
       return __builtin_bit_cast(bf16x8, w);
     };
-
-    load_slice(kbeg);
-    for (int ks = kbeg; ks < kend; ++ks) {
-      store_op(As[buf], ra, A_KC);
-      store_op(Bs[buf], rb, B_KC);
-      __syncthreads();
-      if (ks + 1 < kend) load_slice(ks + 1);
-      const uint32_t* as = As[buf];
-      const uint32_t* bs = Bs[buf];
+    auto compute = [&](const uint32_t* as, const uint32_t* bs) {
 #pragma unroll
       for (int st = 0; st < BK16 / 16; ++st) {
         const bf16x8 a0 = frag(as, A_KC, wm * 64, 0, st);
@@ -656,9 +661,65 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
         acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
         acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
         acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+        // keep each MFMA step's fragment reads with it (hoisting all four
+        // steps' reads needs 64 more registers than two blocks per CU allow)
+        __builtin_amdgcn_sched_barrier(0);
       }
-      // (no scheduling hint here: it raises register pressure past 256)
-      buf ^= 1;
+    };
+
+    // Steps [kbeg, kf) are full and the tile is interior: pipelined path.
+    int kf = kbeg;
+    if (a_in && b_in) {
+      const int f0 = K0 / BK16, e1 = kt0 + K1 / BK16;
+      if (kbeg < f0)
+        kf = min(kend, f0 == kt0 ? e1 : f0);
+      else if (kbeg >= kt0 && kbeg < e1)
+        kf = min(kend, e1);
+    }
+    if (kf > kbeg) {
+      auto load_full = [&](int ks) {
+        ks = min(ks, kf - 1);  // past the end: repeat the last step (never read)
+        const bool s1 = ks >= kt0;
+        const int k0 = (s1 ? ks - kt0 : ks) * BK16;
+        load_op(ra, A_KC, s1 ? A1p : A0p, s1 ? lda1 : lda0, m0, M, k0, 0, true, true);
+        load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, 0, true, true);
+      };
+      auto step = [&](const uint32_t* as, const uint32_t* bs, uint32_t* as_n,
+                      uint32_t* bs_n, int kl) {
+        store_op(as_n, ra, A_KC);
+        store_op(bs_n, rb, B_KC);
+        load_full(kl);
+        compute(as, bs);
+        __syncthreads();
+      };
+      load_full(kbeg);
+      store_op(As0, ra, A_KC);
+      store_op(Bs0, rb, B_KC);
+      load_full(kbeg + 1);
+      __syncthreads();
+      for (int k = kbeg; k < kf; k += 2) {
+        step(As0, Bs0, As1, Bs1, k + 2);
+        if (k + 1 >= kf) break;
+        step(As1, Bs1, As0, Bs0, k + 3);
+      }
+    }
+
+    // Remaining steps (edge tiles, partial K steps): guarded loads, one step
+    // in registers ahead.
+    if (kf < kend) {
+      int buf = 0;
+      load_slice(kf);
+      for (int ks = kf; ks < kend; ++ks) {
+        uint32_t* as = buf ? As1 : As0;
+        uint32_t* bs = buf ? Bs1 : Bs0;
+        store_op(as, ra, A_KC);
+        store_op(bs, rb, B_KC);
+        __syncthreads();
+        if (ks + 1 < kend) load_slice(ks + 1);
+        compute(as, bs);
+        buf ^= 1;
+      }
+      __syncthreads();
     }
 
     const bool whole = kbeg == 0 && kend == g.ktiles;
