@@ -15,9 +15,10 @@
 // span all of them) is finished through LDS by the group holding its first
 // entry, adding the other groups' parts in group order.  One kernel, no
 // atomics, bit-reproducible, and work is balanced by entries, not rows.
-// Wide outputs are cut into 8 column slices, one per XCD (the GPU form of
-// the feature partition of Section 5.3, Theorem 2 / Algorithm 7, with each
-// XCD's L2 as the cache a slice must fit).
+// Outputs of 32 columns and more are cut into 8 (or 16) column slices, each
+// XCD gathering from its own (the GPU form of the feature partition of
+// Section 5.3, Theorem 2 / Algorithm 7, with each XCD's L2 as the cache a
+// slice should fit).
 #include "internal.hpp"
 
 namespace gnnprop {
@@ -245,14 +246,16 @@ struct SpmmArgs {
   int64_t ld_res;
   const float* mask;
   int64_t ld_mask;
-  int32_t nslices;  // column slices (blocks b with b % nslices == q own slice q)
+  int32_t nslices;  // column slices: 1, or a multiple of 8
   int32_t sw;       // slice width in columns
+  int32_t nwin;     // entry windows of the plan
 };
 
-// Block b works on column slice b % nslices of window b / nslices.  With 8
-// slices all the blocks of one slice run on one XCD (blocks are dispatched
-// round-robin over the 8 XCDs), so each XCD gathers from its own n x sw
-// slice of the input, which stays in that XCD's L2.
+// Column slices.  Blocks are dispatched round-robin over the 8 XCDs, so with
+// S = 8 P slices, block b = p (8 nwin) + 8 win + x works on slice 8 p + x of
+// window win: XCD x gathers only from slices x, x + 8, ..., one pass after
+// the other, and each n x sw slice is sized to stay in that XCD's L2 (the
+// cache-sized feature partitions of Theorem 2 / Algorithm 7).
 //
 // A group of G lanes covers G * W consecutive columns of the slice per pass
 // (W = 4: float4 per lane, so one gathered 256-byte row segment of a
@@ -343,8 +346,14 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
   __shared__ T tail[NG][G];     // part of a row that goes on past the group
   __shared__ int head_row[NG], tail_row[NG], starts[NG];
 
-  const int slice = blockIdx.x % a.nslices;
-  const int4 bi = a.binfo[blockIdx.x / a.nslices];
+  int slice = 0, win = blockIdx.x;
+  if (a.nslices >= 8) {
+    const int per = 8 * a.nwin;
+    const int r = (int)(blockIdx.x % per);
+    slice = 8 * (int)(blockIdx.x / per) + (r & 7);
+    win = r >> 3;
+  }
+  const int4 bi = a.binfo[win];
   const int r_lo = bi.x, r_hi = bi.y, B = bi.z, E = bi.w;
   const int gi = threadIdx.x / G, lane = threadIdx.x % G;
   const int gb = B + (int)((int64_t)(E - B) * gi / NG);
@@ -534,7 +543,9 @@ static void spmm_epi(const SpmmArgs& a, const PlanDims& d, bool off32,
 template <bool VEC, bool RAG>
 static void spmm_dispatch(const SpmmArgs& a, const PlanDims& d, bool off32,
                           hipStream_t s) {
-  const int units = VEC ? a.sw / 4 : a.sw;  // column vectors per slice row
+  const int units = VEC ? ceil_div(a.sw, 4) : a.sw;  // column vectors per slice row
+  if (units <= 4) return spmm_epi<4, VEC, RAG>(a, d, off32, s);
+  if (units <= 8) return spmm_epi<8, VEC, RAG>(a, d, off32, s);
   if (units <= 16) return spmm_epi<16, VEC, RAG>(a, d, off32, s);
   if (units <= 32) return spmm_epi<32, VEC, RAG>(a, d, off32, s);
   return spmm_epi<64, VEC, RAG>(a, d, off32, s);
@@ -569,8 +580,23 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   a.ld_res = c.ld_res;
   a.mask = c.mask;
   a.ld_mask = c.ld_mask;
-  a.nslices = c.w >= 256 ? 8 : 1;
+  // 8 slices (one per XCD) from 32 columns up.  A lane group covers a
+  // power of two of float4 columns; when 8 slices need groups of more than
+  // 16 lanes with over a quarter of them idle (602 columns: 76-column
+  // slices on 32 lanes), 16 slices on 16-lane groups are faster, having
+  // twice the groups, and so the gathers, in flight per block.
+  a.nwin = (int32_t)d.nblk;
+  a.nslices = c.w >= 32 ? 8 : 1;
   a.sw = (int32_t)round_up(ceil_div(c.w, a.nslices), 4);
+  if (a.nslices == 8 && a.sw > 64) {
+    const int units = a.sw / 4;
+    int g = 1;
+    while (g < units) g *= 2;
+    if (4 * units < 3 * g) {
+      a.nslices = 16;
+      a.sw = (int32_t)round_up(ceil_div(c.w, a.nslices), 4);
+    }
+  }
   // float4 lanes whenever rows start 16-byte aligned (the ragged end of a
   // width that is not a multiple of 4 is read and written per component)
   const bool vec = vec4_ok(c.in, c.ld_in) &&
