@@ -68,6 +68,8 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--skip-input-grad", action="store_true",
                     help="do not compute the first layer's input gradient")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the step replayed from a HIP graph")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the GCN and MixHop layer timings")
     ap.add_argument("--no-train", action="store_true",
@@ -232,6 +234,12 @@ def main():
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv)
                         for kk, vv in v.items()} for k, v in kernels.items()},
     }
+
+    # the same step replayed from a HIP graph: one host launch per step
+    # instead of one per kernel, which is what bounds the small workloads
+    if not args.no_graph:
+        out["graph_step"] = bench_graph(torch, step, st, wl, args, want_dx_first)
+        log("graph replay: %.4f ms per step" % out["graph_step"]["ms_per_step"])
 
     # the bf16 matrix-core variant of the same step (GEMM operands rounded to
     # bf16, fp32 accumulation; aggregation stays fp32), reported alongside
@@ -448,6 +456,40 @@ def bench_pipeline(G, runtime, synth, torch, np, args):
                          samp_ms, threads))
     del dev
     return res
+
+
+def bench_graph(torch, step, st, wl, args, want_dx_first):
+    """The propagation step captured once in a HIP graph and replayed; the
+    first replay's outputs and gradients are compared bit for bit with those
+    of the last eager step (every kernel is deterministic)."""
+    outs = [L[k] for i, L in enumerate(st.layers) for k in ("Y", "dW_self", "dW_neigh", "dX")
+            if k != "dX" or i > 0 or want_dx_first]
+    ref = [o.clone() for o in outs]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()  # warm-up outside the capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        step()
+    for o in outs:
+        o.fill_(float("nan"))
+    graph.replay()
+    torch.cuda.synchronize()
+    same = all(torch.equal(a, b) for a, b in zip(ref, outs))
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    del graph
+    return {"value": round(ms / wl.layers, 5), "unit": "ms", "ms_per_step": round(ms, 5),
+            "matches_eager": bool(same)}
 
 
 def bench_variants(G, runtime, synth, torch, np, g, x, wl, args):

@@ -829,13 +829,16 @@ static Shape gemm_shape(const GemmBatch& b) {
   // Otherwise, with few tiles and a long K (weight gradients, K = n), split
   // K into S ranges, one (tile, range) per block, ordered split-major so that
   // one XCD's blocks share a K slab of both operands in its L2; with more
-  // tiles, split all tile x K-slice iterations evenly over MAX_BLOCKS.
-  // resident blocks: 2 per CU
+  // tiles, split all tile x K-slice iterations evenly over MAX_BLOCKS
+  // (the resident slots, 2 per CU).  A launch of few tiles over 4 K slices
+  // or more is split even when all its iterations would fit the slots
+  // (small weight gradients: 2 tiles over K = 1000 would otherwise walk 32
+  // slices one after the other on 2 CUs).
   const int slots = MAX_BLOCKS;
   const int64_t rounds = ceil_div(s.tiles, slots);
   const double fill = (double)s.tiles / (double)(rounds * slots);
   s.splits = 1;
-  if (fill >= 0.85 || s.iters <= slots) {
+  if (fill >= 0.85 || (s.iters <= slots && (s.tiles > slots / 4 || s.ktiles < 4))) {
     s.nblocks = s.tiles;
   } else if (s.tiles <= slots / 4) {
     s.splits = (int)std::min<int64_t>(s.ktiles, slots / s.tiles);

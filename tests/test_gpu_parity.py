@@ -311,6 +311,50 @@ def test_tiny_workload_stack_end_to_end(fuse):
         assert maxrel(L["dX"], dx_ref) <= TOL, (l, "dX")
 
 
+def test_stack_step_graph_replay():
+    """One propagation step (plan, transposed values, forward and backward of
+    the whole stack) captured in a HIP graph: every replay, with eager steps
+    and synchronisations between replays, gives bit for bit the eager step's
+    outputs and gradients."""
+    wl = synth.WORKLOADS[synth.TINY_WORKLOAD]
+    inp = synth.workload_inputs(wl)
+    g, x, params, dy = inp["graph"], inp["x"], inp["params"], inp["dy"]
+    X, dY = to_dev(x, 64), to_dev(dy)
+    dg_cap, dg_eag = runtime.DeviceGraph(g), runtime.DeviceGraph(g)
+    cap = runtime.SageStack(dg_cap, params, wl.f_in)
+    eag = runtime.SageStack(dg_eag, params, wl.f_in)
+
+    def step(dg, st):
+        dg.prepare()
+        st.forward(X)
+        st.backward(dY)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(dg_cap, cap)  # warm-up outside the capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        step(dg_cap, cap)
+    keys = ("Y", "dW_self", "dW_neigh", "dX")
+    for it in range(3):
+        for L in cap.layers:  # stale results must not survive a replay
+            for k in keys:
+                L[k].fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        step(dg_eag, eag)
+        torch.cuda.synchronize()
+        for l in range(wl.layers):
+            for k in keys:
+                a = cap.layers[l][k].cpu().numpy()
+                b = eag.layers[l][k].cpu().numpy()
+                assert np.array_equal(a, b), (it, l, k)
+
+
 @pytest.mark.parametrize("order", [1, 2])
 @pytest.mark.parametrize("bias", [False, True])
 def test_layer_mask_flags_exact(order, bias):
