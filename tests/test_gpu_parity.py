@@ -121,7 +121,7 @@ def test_plan_exact(name):
 
 # ---------------------------------------------------------------- aggregation
 
-WIDTHS = [1, 3, 16, 50, 64, 128, 200, 300, 512, 1024, 1030]
+WIDTHS = [1, 3, 16, 50, 64, 128, 200, 300, 512, 602, 1024, 1030]
 
 
 @pytest.mark.parametrize("name", ["powerlaw", "star700", "no_self_loops",
@@ -490,7 +490,8 @@ TOL_BF16_LAYER = 2e-2    # vs the double-precision oracle on the fp32 inputs
 
 @pytest.mark.parametrize("M,N,K", [(37, 45, 29), (128, 128, 64), (130, 257, 70),
                                    (602, 512, 8000), (2001, 1300, 100),
-                                   (8000, 602, 1024), (64, 64, 0)])
+                                   (8000, 602, 1024), (64, 64, 0), (300, 96, 4099),
+                                   (1000, 128, 50)])
 @pytest.mark.parametrize("ta", [0, 1])
 @pytest.mark.parametrize("tb", [0, 1])
 def test_gemm_bf16_parity(M, N, K, ta, tb):
