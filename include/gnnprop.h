@@ -77,9 +77,10 @@ typedef enum gnn_status {
  *                  and by gnn_spmm with transpose = 1.  The transpose reuses
  *                  indptr/indices, so the pattern must be symmetric
  *                  (undirected subgraph, Section 5.2).
- *   plan           device buffer written by gnn_csr_build_plan: the
- *                  aggregation kernel's work lists (packed short rows, long
- *                  rows), a flagged copy of indices and each entry's row. */
+ *   plan           device buffer written by gnn_csr_build_plan (or
+ *                  gnn_csr_prepare): per window of 256 stored entries the
+ *                  rows whose first entry lies in it and their entry range,
+ *                  and the row of every entry. */
 typedef struct gnn_csr {
   int32_t n;
   int64_t nnz;
@@ -132,13 +133,25 @@ gnn_status gnn_csr_transpose_values(const gnn_csr* csr, float* values_t,
 size_t gnn_plan_bytes(int32_t n, int64_t nnz);
 
 /* Builds the aggregation work plan into `plan` (device memory of at least
- * gnn_plan_bytes(n, nnz) bytes).  Rows with at most 64 stored entries are
- * packed into items (runs of consecutive rows whose first entries share a
- * 64-entry window); longer rows are listed to be split across a whole
- * workgroup, with the parts added in a fixed order, so results are
- * deterministic.  Reads csr->n, nnz, indptr and indices. */
+ * gnn_plan_bytes(n, nnz) bytes).  The stored entries are cut into windows of
+ * 256; window k gets the rows whose first entry lies in it (so a row, hub
+ * rows included, is never shared between windows) and their entry range,
+ * and every entry its row.  The aggregation gives each window to one
+ * workgroup and splits its entries evenly over lane groups; the parts of a
+ * row cut between groups are added in a fixed order, so results are
+ * deterministic.  Reads csr->n, nnz and indptr. */
 gnn_status gnn_csr_build_plan(const gnn_csr* csr, void* plan,
                               size_t plan_bytes, hipStream_t stream);
+
+/* Both per-subgraph preparations (Section 5.2) in one launch: the plan of
+ * gnn_csr_build_plan into `plan` (plan_bytes >= gnn_plan_bytes) and the
+ * transposed values of gnn_csr_transpose_values into values_t (nnz floats).
+ * The results are bit for bit those of the two separate calls.  The
+ * pattern must be symmetric with ascending indices per row; csr->values_t
+ * and csr->plan are not read.  plan and values_t may not overlap each
+ * other or the CSR arrays (GNN_ERR_ALIAS). */
+gnn_status gnn_csr_prepare(const gnn_csr* csr, void* plan, size_t plan_bytes,
+                           float* values_t, hipStream_t stream);
 
 /* Checks the CSR on the device and synchronises `stream`: indptr
  * monotone with indptr[0] = 0 and indptr[n] = nnz, indices in range and

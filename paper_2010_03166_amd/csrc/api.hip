@@ -273,6 +273,25 @@ gnn_status gnn_csr_build_plan(const gnn_csr* csr, void* plan,
   return GNN_OK;
 }
 
+gnn_status gnn_csr_prepare(const gnn_csr* csr, void* plan, size_t plan_bytes,
+                           float* values_t, hipStream_t stream) {
+  gnn_status st = check_csr(csr, true, false);
+  if (st != GNN_OK) return st;
+  if (!plan) return GNN_ERR_NULL;
+  if (csr->nnz > 0 && !values_t) return GNN_ERR_NULL;
+  if (plan_bytes < gnn_plan_bytes(csr->n, csr->nnz)) return GNN_ERR_WORKSPACE;
+  const size_t vb = (size_t)csr->nnz * 4;
+  if (ranges_overlap(values_t, vb, csr->values, vb) ||
+      ranges_overlap(plan, plan_bytes, values_t, vb) ||
+      ranges_overlap(plan, plan_bytes, csr->values, vb) ||
+      ranges_overlap(plan, plan_bytes, csr->indptr, ((size_t)csr->n + 1) * 4) ||
+      ranges_overlap(plan, plan_bytes, csr->indices, (size_t)csr->nnz * 4))
+    return GNN_ERR_ALIAS;
+  GNN_HIP(prepare_launch(csr->n, csr->nnz, csr->indptr, csr->indices, csr->values,
+                         values_t, plan, stream));
+  return GNN_OK;
+}
+
 gnn_status gnn_csr_validate(const gnn_csr* csr, int32_t require_symmetric,
                             hipStream_t stream) {
   gnn_status st = check_csr(csr, false, false);

@@ -97,6 +97,10 @@ hipError_t transpose_values_launch(int32_t n, int64_t nnz,
                                    const int32_t* indices, const float* vals,
                                    float* vals_t, const void* plan,
                                    hipStream_t s);
+// Plan and transposed values of one graph in a single launch.
+hipError_t prepare_launch(int32_t n, int64_t nnz, const int32_t* indptr,
+                          const int32_t* indices, const float* vals,
+                          float* vals_t, void* plan, hipStream_t s);
 // Returns 0 if valid, else a nonzero code; synchronises.
 hipError_t validate_csr(int32_t n, int64_t nnz, const int32_t* indptr,
                         const int32_t* indices, int32_t symmetric,

@@ -174,6 +174,91 @@ hipError_t transpose_values_launch(int32_t n, int64_t nnz,
   return hipGetLastError();
 }
 
+// ------------------------------------------ plan + transposed values, fused
+//
+// Both per-subgraph preparations in one launch.  Blocks [0, nrow_blocks)
+// write the window records (one thread per row, as plan_blocks_kernel);
+// the others take 256 consecutive entries each: the block's first thread
+// finds the rows holding its first and last entry by binary search over
+// indptr, then every thread finds its own entry's row between those two
+// (a few steps), writes it to the plan and moves its value to the transposed
+// position (transpose_entry).  The two halves write disjoint parts of the
+// plan.
+__global__ __launch_bounds__(256) void prepare_kernel(
+    const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
+    const float* __restrict__ vals, float* __restrict__ vals_t, int32_t n,
+    int64_t nnz, int32_t nblk, int32_t nrow_blocks, int4* __restrict__ binfo,
+    PlanHeader* __restrict__ hdr, int32_t* __restrict__ erow) {
+  if ((int)blockIdx.x < nrow_blocks) {
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r > n) return;
+    const int p = indptr[r];
+    const int k_lo = r == 0 ? 0 : indptr[r - 1] / BLOCK_ENTRIES + 1;
+    const int k_hi = min(p / BLOCK_ENTRIES, nblk - 1);
+    for (int k = k_lo; k <= k_hi; ++k) {
+      binfo[k].x = r;
+      binfo[k].z = p;
+      if (k > 0) {
+        binfo[k - 1].y = r;
+        binfo[k - 1].w = p;
+      }
+    }
+    if (r == n) {
+      binfo[nblk - 1].y = n;
+      binfo[nblk - 1].w = (int)nnz;
+      PlanHeader h;
+      memset(&h, 0, sizeof(h));
+      h.nblk = nblk;
+      h.block_entries = BLOCK_ENTRIES;
+      h.n = n;
+      h.nnz = (int)nnz;
+      *hdr = h;
+    }
+    return;
+  }
+  // the last row r with indptr[r] <= j, searched in [lo, hi]
+  auto row_of = [&](int j, int lo, int hi) {
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (indptr[mid] <= j)
+        lo = mid;
+      else
+        hi = mid - 1;
+    }
+    return lo;
+  };
+  __shared__ int bounds[2];
+  const int64_t j0 = (int64_t)(blockIdx.x - nrow_blocks) * 256;
+  const int64_t j1 = min<int64_t>(j0 + 256, nnz) - 1;
+  if (threadIdx.x == 0) {
+    bounds[0] = row_of((int)j0, 0, n - 1);
+    bounds[1] = row_of((int)j1, bounds[0], n - 1);
+  }
+  __syncthreads();
+  const int64_t j = j0 + threadIdx.x;
+  if (j > j1) return;
+  const int v = row_of((int)j, bounds[0], bounds[1]);
+  erow[j] = v;
+  transpose_entry(v, (int)j, indptr, indices, vals, vals_t);
+}
+
+hipError_t prepare_launch(int32_t n, int64_t nnz, const int32_t* indptr,
+                          const int32_t* indices, const float* vals,
+                          float* vals_t, void* plan, hipStream_t s) {
+  const PlanDims d = plan_dims(n, nnz);
+  char* base = static_cast<char*>(plan);
+  const int rb = (int)ceil_div((int64_t)n + 1, 256);
+  const int eb = (n > 0 && nnz > 0) ? (int)ceil_div(nnz, 256) : 0;
+  timer_begin(GNN_K_PLAN, s);
+  prepare_kernel<<<(unsigned)(rb + eb), 256, 0, s>>>(
+      indptr, indices, vals, vals_t, n, nnz, (int32_t)d.nblk, rb,
+      reinterpret_cast<int4*>(base + d.binfo_offset),
+      reinterpret_cast<PlanHeader*>(base),
+      reinterpret_cast<int32_t*>(base + d.erow_offset));
+  timer_end(GNN_K_PLAN, 8.0 * (n + 1) + 16.0 * nnz, s);
+  return hipGetLastError();
+}
+
 // --------------------------------------------------------------- validate
 
 __global__ __launch_bounds__(256) void validate_kernel(

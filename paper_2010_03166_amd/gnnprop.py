@@ -63,6 +63,9 @@ EXPORTS = {
                                                   ctypes.c_void_p, ctypes.c_void_p]),
     "gnn_csr_build_plan": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.c_void_p,
                                             ctypes.c_size_t, ctypes.c_void_p]),
+    "gnn_csr_prepare": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.c_void_p,
+                                         ctypes.c_size_t, ctypes.c_void_p,
+                                         ctypes.c_void_p]),
     "gnn_csr_validate": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.c_int32,
                                           ctypes.c_void_p]),
     "gnn_prop_saved_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
@@ -228,6 +231,12 @@ def gnn_csr_build_plan(csr: gnn_csr, plan, stream=None):
     nbytes = plan.numel() * plan.element_size()
     _check(lib().gnn_csr_build_plan(ctypes.byref(csr), _ptr(plan), nbytes,
                                     _stream(stream)), "gnn_csr_build_plan")
+
+
+def gnn_csr_prepare(csr: gnn_csr, plan, values_t, stream=None):
+    nbytes = plan.numel() * plan.element_size()
+    _check(lib().gnn_csr_prepare(ctypes.byref(csr), _ptr(plan), nbytes, _ptr(values_t),
+                                 _stream(stream)), "gnn_csr_prepare")
 
 
 def gnn_csr_validate(csr: gnn_csr, require_symmetric: bool = True,

@@ -92,10 +92,9 @@ class DeviceGraph:
                           self.values_t, self.plan)
 
     def prepare(self, stream=None):
-        """Per-subgraph preparation: (A_s)^T values and the work plan."""
-        c = self.struct()
-        G.gnn_csr_build_plan(c, self.plan, stream)
-        G.gnn_csr_transpose_values(c, self.values_t, stream)
+        """Per-subgraph preparation: the work plan and (A_s)^T values, one
+        launch."""
+        G.gnn_csr_prepare(self.struct(), self.plan, self.values_t, stream)
 
     def validate(self, symmetric: bool = True) -> int:
         return G.gnn_csr_validate(self.struct(), symmetric)

@@ -86,6 +86,39 @@ def test_transpose_values_without_plan(name):
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
 
 
+EDGELESS = synth.symmetric_csr(5, np.zeros((0, 2), np.int64), self_loops=False)
+
+
+@pytest.mark.parametrize("name", list(GRAPHS) + ["edgeless"])
+def test_prepare_fused_equals_separate(name):
+    """gnn_csr_prepare (one launch) writes bit for bit the plan and the
+    transposed values of gnn_csr_build_plan + gnn_csr_transpose_values."""
+    g = EDGELESS if name == "edgeless" else GRAPHS[name]
+    a, b = runtime.DeviceGraph(g), runtime.DeviceGraph(g)
+    for dg in (a, b):  # stale bytes must not survive either path
+        dg.plan.fill_(0xA5)
+        dg.values_t.fill_(float("nan"))
+    G.gnn_csr_prepare(a.struct(), a.plan, a.values_t)
+    cb = b.struct()
+    G.gnn_csr_build_plan(cb, b.plan)
+    G.gnn_csr_transpose_values(cb, b.values_t)
+    torch.cuda.synchronize()
+    nb = G.gnn_plan_bytes(g.n, g.nnz)
+    assert np.array_equal(a.plan[:nb].cpu().numpy(), b.plan[:nb].cpu().numpy())
+    va = a.values_t[: g.nnz].cpu().numpy().view(np.uint32)
+    vb = b.values_t[: g.nnz].cpu().numpy().view(np.uint32)
+    assert np.array_equal(va, vb)
+
+
+def test_prepare_argument_errors():
+    g = GRAPHS["random"]
+    dg = runtime.DeviceGraph(g)
+    with pytest.raises(G.GnnError):  # plan too small
+        G.gnn_csr_prepare(dg.struct(), dg.plan[:16], dg.values_t)
+    with pytest.raises(G.GnnError):  # transposed values over the values
+        G.gnn_csr_prepare(dg.struct(), dg.plan, dg.values)
+
+
 def _ru(x, m=256):
     return (x + m - 1) // m * m
 
