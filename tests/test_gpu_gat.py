@@ -97,6 +97,29 @@ def test_gat_bf16_mode():
     check(g, r, O.GAT_ALPHA, tol=2e-2)
 
 
+def test_gat_zero_nodes():
+    """An empty subgraph: nothing to write forward, zero dW and da."""
+    g = synth.identity_graph(0)
+    dg = prepared(g)
+    c = dg.struct()
+    f_in, h = 6, 5
+    lay = G.make_layer(f_in, h, f_in, h, f_in, 0, 0)
+    saved = _buf(G.gnn_gat_saved_bytes(c, lay))
+    ws = _buf(G.gnn_gat_workspace_bytes(c, lay))
+    X = torch.empty((0, f_in), device="cuda")
+    Y = torch.empty((0, h), device="cuda")
+    W = to_dev(np.ones((f_in, h), np.float32))
+    A = to_dev(np.ones(2 * h, np.float32))
+    G.gnn_gat_fwd(c, lay, X, W, A, O.GAT_ALPHA, Y, None, saved, ws)
+    dW = torch.full((f_in, h), float("nan"), device="cuda")
+    da = torch.full((2 * h,), float("nan"), device="cuda")
+    G.gnn_gat_bwd(c, lay, X, W, A, O.GAT_ALPHA, Y, torch.empty((0, h), device="cuda"),
+                  saved, None, dW, da, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(dW.cpu().numpy(), np.zeros((f_in, h), np.float32))
+    assert np.array_equal(da.cpu().numpy(), np.zeros(2 * h, np.float32))
+
+
 def test_gat_argument_errors():
     g = GRAPHS["random"]
     c = prepared(g).struct()
