@@ -28,14 +28,15 @@
 // rows are stored in the order (k mod 16) * 2 + k / 16 so that the two lane
 // halves of a step read adjacent rows (different LDS banks).
 //
-// Work split (stream-K).  The launch's tiles x K-slices are cut into P
-// equal, contiguous ranges, one per block (P = 512 blocks = 2 per CU, or one
-// block per tile when the tiles already fill the machine).  A block writes a
-// tile it covers completely straight to C with the fused epilogue; a tile
-// shared by several blocks gets one partial tile per block, and a second
-// kernel adds them in block order (deterministic) before the epilogue.  This
-// keeps every CU busy for shapes whose tile count does not fill the chip
-// (weight gradients with K = n, f_in = 602 input gradients) without atomics.
+// Work split (gemm_shape).  One block per tile when the tiles fill the 512
+// resident slots (2 per CU), or come to about one per CU over a short K;
+// split-K (one (tile, K range) per block) for few tiles over a long K
+// (weight gradients, K = n); otherwise stream-K: the launch's tiles x
+// K-slices cut into 512 equal, contiguous ranges, one per block (f_in = 602
+// input gradients).  A block writes a tile it covers completely straight to
+// C with the fused epilogue; a tile shared by several blocks gets one
+// partial tile per block, and a second kernel adds them in block order
+// (deterministic) before the epilogue, so no atomics are involved.
 // Blocks are numbered so that each XCD (blocks are dispatched round-robin
 // over the 8 XCDs) works on a contiguous range of iterations: the tiles of a
 // row band (same A rows) or the same K range stay in one XCD's L2.
