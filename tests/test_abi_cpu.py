@@ -143,6 +143,31 @@ def test_argument_errors_are_synchronous(lib):
     assert L.gnn_csr_build_plan(ctypes.byref(c), P(0x10), 8, None) == -5
 
 
+def test_prepare_and_gat_argument_errors(lib):
+    L = G.lib()
+    P = ctypes.c_void_p
+    c = _fake_csr()
+    need = int(L.gnn_plan_bytes(c.n, c.nnz))
+    # fused preparation: plan too small, no plan, transposed values over the values
+    assert L.gnn_csr_prepare(ctypes.byref(c), P(0x10), need - 1, P(0x900000), None) == -5
+    assert L.gnn_csr_prepare(ctypes.byref(c), None, need, P(0x900000), None) == -1
+    assert L.gnn_csr_prepare(ctypes.byref(c), P(0x800000), need, P(c.values), None) == -7
+    assert L.gnn_csr_prepare(ctypes.byref(c), P(0x800000), need, None, None) == -1
+    # GAT: slope outside [0, 1] (and NaN), bad widths, workspace too small
+    lay = G.make_layer(8, 4, 8, 4, 8)
+    ws = 1 << 30
+    for alpha in (-0.1, 1.5, float("nan")):
+        assert L.gnn_gat_fwd(ctypes.byref(c), ctypes.byref(lay), P(0x10), P(0x20), P(0x30),
+                             ctypes.c_float(alpha), P(0x40), None, P(0x50), P(0x60), ws,
+                             None) == -2
+    bad = G.make_layer(8, 4, 8, 3, 8)  # ld_y < h
+    assert L.gnn_gat_fwd(ctypes.byref(c), ctypes.byref(bad), P(0x10), P(0x20), P(0x30),
+                         ctypes.c_float(0.2), P(0x40), None, P(0x50), P(0x60), ws, None) == -2
+    assert L.gnn_gat_fwd(ctypes.byref(c), ctypes.byref(lay), P(0x10), P(0x20), P(0x30),
+                         ctypes.c_float(0.2), P(0x40), None, P(0x50), P(0x60), 16, None) == -5
+    assert int(L.gnn_gat_workspace_bytes(ctypes.byref(c), ctypes.byref(bad))) == 0
+
+
 def test_empty_problems_need_no_launch(lib):
     L = G.lib()
     P = ctypes.c_void_p
