@@ -202,6 +202,13 @@ def main():
                      "bytes_per_launch": kernels["spmm"]["work"],
                      "avg_launch_us": round(kernels["spmm"]["avg_launch_us"], 2)}
 
+    # the streaming rate this GPU actually gives: a 512 MiB device-to-device
+    # copy (reads plus writes), the "achievable" line beside the 8 TB/s peak
+    copy_gbs = stream_copy_gbs(torch)
+    if roof_spmm is not None:
+        roof_spmm["copy_gbs"] = round(copy_gbs, 1)
+        roof_spmm["frac_of_copy"] = round(roof_spmm["achieved"] / copy_gbs, 4)
+
     traffic = measured_traffic(name, dtype)
     if traffic.get(dom) is not None:
         roof["traffic"] = traffic[dom]
@@ -456,6 +463,23 @@ def bench_pipeline(G, runtime, synth, torch, np, args):
                          samp_ms, threads))
     del dev
     return res
+
+
+def stream_copy_gbs(torch, mib: int = 512, reps: int = 5) -> float:
+    """GB/s (bytes read plus written) of a device-to-device copy."""
+    src = torch.ones((mib << 20) // 4, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2.0 * (mib << 20) / (ms * 1e6)
 
 
 def bench_graph(torch, step, st, wl, args, want_dx_first):
