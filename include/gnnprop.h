@@ -55,8 +55,17 @@ typedef enum gnn_status {
 } gnn_status;
 
 /* Layer flags. */
+/* GEMM products.  By default every fp32 operand of a weight transformation
+ * is split exactly into three bf16 pieces (x = hi + mid + lo, each rounded
+ * to nearest even) and the six piece products down to 2^-16 of hi x hi are
+ * accumulated in fp32 on the bf16 matrix cores: fp32 operands, results and
+ * accumulation, with a product error below 2^-24 relative (measured against
+ * fp64: no larger than that of the fp32 matrix-core instruction).  The two
+ * flags below select other arithmetic; setting both is GNN_ERR_UNSUPPORTED. */
 #define GNN_FLAG_BF16 0x1u /* GEMM operands rounded to bf16 (round to nearest
                               even), fp32 accumulation; aggregation stays fp32 */
+#define GNN_FLAG_F32_MFMA 0x8u /* GEMM products on the fp32 matrix-core
+                                  instruction (v_mfma_f32_32x32x2_f32) */
 /* Backward pass only (Algorithm 1's layer loop, backward direction): the
  * layers of a stack share their ReLU masks.  Layer l's input X is layer
  * l-1's output, so 1[X > 0] is layer l-1's mask and can be applied where

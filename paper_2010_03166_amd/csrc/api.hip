@@ -155,8 +155,8 @@ GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
   return b;
 }
 
-GemmBatch with_bf16(GemmBatch b, int32_t bf16) {
-  b.bf16 = bf16;
+GemmBatch with_mode(GemmBatch b, int32_t mode) {
+  b.mode = mode;
   return b;
 }
 
@@ -178,10 +178,10 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
     buf1 = (size_t)n * o.ld_v * 4;  // V
   }
   size_t gemm = 0;
-  const int32_t bf = (L->flags & GNN_FLAG_BF16) ? 1 : 0;
-  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
-  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 2 * h, 0, 2 * h, 0, 0), bf)));
-  gemm = std::max(gemm, gemm_workspace_bytes(with_bf16(dx_batch(o.order, n, f_in, h, 0, 2 * h, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
+  const int32_t bf = gemm_mode(L->flags);
+  gemm = std::max(gemm, gemm_workspace_bytes(with_mode(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
+  gemm = std::max(gemm, gemm_workspace_bytes(with_mode(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 2 * h, 0, 2 * h, 0, 0), bf)));
+  gemm = std::max(gemm, gemm_workspace_bytes(with_mode(dx_batch(o.order, n, f_in, h, 0, 2 * h, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
   o.off_buf0 = 0;
   o.off_buf1 = round_up(buf0, 256);
   o.off_gemm = o.off_buf1 + round_up(buf1, 256);
@@ -195,7 +195,8 @@ gnn_status check_layer(const gnn_layer* L) {
   if (L->f_in <= 0 || L->h <= 0) return GNN_ERR_SHAPE;
   if (L->ld_x < L->f_in || L->ld_y < 2 * (int64_t)L->h) return GNN_ERR_SHAPE;
   if (L->order < 0 || L->order > 2) return GNN_ERR_SHAPE;
-  if (L->flags & ~(GNN_FLAG_BF16 | GNN_FLAG_DY_MASKED | GNN_FLAG_DX_MASKED))
+  if ((L->flags & ~(GEMM_FLAGS | GNN_FLAG_DY_MASKED | GNN_FLAG_DX_MASKED)) ||
+      !gemm_flags_ok(L->flags))
     return GNN_ERR_UNSUPPORTED;
   return GNN_OK;
 }
@@ -348,7 +349,7 @@ size_t gnn_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
   b.p[0].N = N;
   b.p[0].seg[0].K = K;
   const size_t f32 = gemm_workspace_bytes(b);
-  b.bf16 = 1;
+  b.mode = GEMM_BF16;
   return std::max(f32, gemm_workspace_bytes(b));
 }
 
@@ -358,7 +359,7 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
                     void* workspace, size_t workspace_bytes,
                     hipStream_t stream) {
   if (M < 0 || N < 0 || K < 0) return GNN_ERR_SHAPE;
-  if (flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  if ((flags & ~GEMM_FLAGS) || !gemm_flags_ok(flags)) return GNN_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return GNN_OK;
   if (!C || (K > 0 && (!A || !B))) return GNN_ERR_NULL;
   if (ldc < N) return GNN_ERR_SHAPE;
@@ -371,7 +372,7 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
   b.nprob = 1;
   b.trans_a = trans_a != 0;
   b.trans_b = trans_b != 0;
-  b.bf16 = (flags & GNN_FLAG_BF16) != 0;
+  b.mode = gemm_mode(flags);
   b.p[0].nseg = 1;
   b.p[0].seg[0] = {A, B, lda, ldb, K};
   b.p[0].M = M;
@@ -436,13 +437,13 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
     GNN_HIP(spmm_launch(c, stream));
     GemmBatch b = fwd_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, W_self,
                             W_neigh, b_self, b_neigh, Y, layer->ld_y, nullptr, 0);
-    b.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
+    b.mode = gemm_mode(layer->flags);
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
   } else {
     float* P = reinterpret_cast<float*>(ws + o.off_buf0);
     GemmBatch b = fwd_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, W_self,
                             W_neigh, b_self, nullptr, Y, layer->ld_y, P, o.ld_p);
-    b.bf16 = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
+    b.mode = gemm_mode(layer->flags);
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
     SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y);
     c.epilogue = SPMM_BIAS_RELU;
@@ -491,7 +492,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   const size_t gws_bytes = o.off_cs - o.off_gemm;
   float* cspart = reinterpret_cast<float*>(ws + o.off_cs);
 
-  const int32_t bf = (layer->flags & GNN_FLAG_BF16) ? 1 : 0;
+  const int32_t bf = gemm_mode(layer->flags);
   const bool dy_masked = (layer->flags & GNN_FLAG_DY_MASKED) != 0;
   // dX masked by 1[X > 0]: the next layer down's G, in the epilogue that
   // writes the final dX
@@ -524,12 +525,12 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     GNN_HIP(spmm_launch(c, stream));
     GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, Gs,
                             ld_gs, T, ld_t, dW_self, dW_neigh);
-    bw.bf16 = bf;
+    bw.mode = bf;
     GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
     if (dX) {
       GemmBatch bx = dx_batch(2, n, f_in, h, Gs, ld_gs, T, ld_t, W_self,
                               W_neigh, dX, layer->ld_dx, nullptr, 0);
-      bx.bf16 = bf;
+      bx.mode = bf;
       bx.p[0].mask = dx_mask;
       bx.p[0].ld_mask = layer->ld_x;
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
@@ -552,12 +553,12 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     const float* S = static_cast<const float*>(saved);
     GemmBatch bw = dw_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, G, ld_g,
                             G + h, ld_g, dW_self, dW_neigh);
-    bw.bf16 = bf;
+    bw.mode = bf;
     GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
     if (dX) {
       GemmBatch bx = dx_batch(1, n, f_in, h, G, ld_g, G + h, ld_g, W_self,
                               W_neigh, dX, layer->ld_dx, V, o.ld_v);
-      bx.bf16 = bf;
+      bx.mode = bf;
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
       // dX = G_s W_s^T + A_s^T V, then the mask, in the aggregation epilogue
       SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx);

@@ -134,7 +134,7 @@ GemmBatch gemm1(int ta, int tb, int32_t M, int32_t N, int32_t K, const float* A,
   b.nprob = 1;
   b.trans_a = ta;
   b.trans_b = tb;
-  b.bf16 = (flags & GNN_FLAG_BF16) ? 1 : 0;
+  b.mode = gemm_mode(flags);
   b.p[0].nseg = 1;
   b.p[0].seg[0] = {A, B, lda, ldb, K};
   b.p[0].M = M;
@@ -151,7 +151,7 @@ gnn_status check_gat(const gnn_csr* csr, const gnn_layer* L, float alpha) {
   if (!L) return GNN_ERR_NULL;
   if (L->f_in <= 0 || L->h <= 0) return GNN_ERR_SHAPE;
   if (L->ld_x < L->f_in || L->ld_y < L->h) return GNN_ERR_SHAPE;
-  if (L->flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  if ((L->flags & ~GEMM_FLAGS) || !gemm_flags_ok(L->flags)) return GNN_ERR_UNSUPPORTED;
   if (!(alpha >= 0.f && alpha <= 1.f)) return GNN_ERR_SHAPE;
   return GNN_OK;
 }

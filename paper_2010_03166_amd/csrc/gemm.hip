@@ -1,8 +1,17 @@
 // Dense weight transformation on the gfx950 matrix cores (the second of the
 // three kernels of Section 5.1).
 //
-// C = sum_s op(A_s) op(B_s) (+ bias, ReLU), fp32 in and out, on
-// v_mfma_f32_32x32x2_f32.
+// C = sum_s op(A_s) op(B_s) (+ bias, ReLU), fp32 in and out.  Products, by
+// GemmBatch::mode:
+//   split (default): every fp32 operand value split exactly into bf16
+//     hi + mid + lo while its MFMA fragment is formed; the six piece products
+//     down to 2^-16 of hi x hi run on v_mfma_f32_32x32x16_bf16 with fp32
+//     accumulation (the bf16x6 scheme of Henry, Tang and Heinecke, 2019).
+//     Six 16-deep bf16 MFMAs take 192 cycles against 512 for the eight
+//     2-deep fp32 MFMAs that cover the same 16 k, and the result is as
+//     accurate (measured against fp64);
+//   fp32: v_mfma_f32_32x32x2_f32;
+//   bf16: operands rounded to bf16, one product (the kernel further down).
 //
 // Tiling.  A block of 256 threads (4 wavefronts in 2 x 2) computes a
 // 128 x 128 output tile; each wavefront holds a 64 x 64 sub-tile as 2 x 2
@@ -190,7 +199,44 @@ __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
     }
 }
 
-template <bool AT, bool BT>
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+
+// Two floats rounded to bf16 (round to nearest even), packed low, high.
+__device__ inline uint32_t pack_bf16(float lo, float hi) {
+  bf16x2v v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Eight floats as three bf16 vectors with x = hi + mid + lo exactly: hi is
+// x rounded to bf16, mid the remainder rounded, lo what is left.  Each
+// remainder is exact in fp32 (it has at most 16, then 8, significant bits),
+// and the last fits a bf16, so no information is lost.
+__device__ inline void split3_bf16(const float* x, bf16x8& hi, bf16x8& mid,
+                                   bf16x8& lo) {
+  uint4 h, m, l;
+  uint32_t* hp = &h.x;
+  uint32_t* mp = &m.x;
+  uint32_t* lp = &l.x;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const float x0 = x[2 * p], x1 = x[2 * p + 1];
+    const uint32_t a = pack_bf16(x0, x1);
+    const float r0 = x0 - __uint_as_float(a << 16);
+    const float r1 = x1 - __uint_as_float(a & 0xffff0000u);
+    const uint32_t b = pack_bf16(r0, r1);
+    const float s0 = r0 - __uint_as_float(b << 16);
+    const float s1 = r1 - __uint_as_float(b & 0xffff0000u);
+    hp[p] = a;
+    mp[p] = b;
+    lp[p] = pack_bf16(s0, s1);
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  mid = __builtin_bit_cast(bf16x8, m);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
+template <bool AT, bool BT, bool SPLIT>
 __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
   constexpr bool A_KC = !AT;  // A row-major M x K: k contiguous
   constexpr bool B_KC = BT;   // B stored N x K: k contiguous
@@ -336,7 +382,7 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
     const int a_xc_base = lh * XC_STRIDE + wm * 64 + lr;
     const int b_xc_base = lh * XC_STRIDE + wn * 64 + lr;
 
-    auto compute = [&](const float* as, const float* bs) {
+    auto compute_f32 = [&](const float* as, const float* bs) {
       // Operands of step s are fetched one step (XC) or one group (KC)
       // ahead of the MFMAs that consume them.
       float4 af[2], bf[2], afn[2], bfn[2];
@@ -390,6 +436,65 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
       }
     };
 
+    // Split products (SPLIT): each MFMA step contracts 16 k, lane half h
+    // supplying k = 16 h + 8 t + j (j = 0..7) at step t = 0, 1 of the slice,
+    // in both operands.  The fp32 fragments are read as for the fp32 MFMA,
+    // split into bf16 hi + mid + lo, and the products of the pieces whose
+    // weights are at least 2^-16 of hi x hi (hi hi, hi mid, mid hi, hi lo,
+    // lo hi, mid mid) accumulate in fp32, smallest first.  What is left out,
+    // mid lo + lo mid + lo lo, is below 2^-24 of |a b|.
+    auto frag8 = [&](const float* L, bool kc, int kc_base, int xc_base, int i,
+                     int t, float* f) {
+      if (kc) {
+        const float4 u = ld4(L + kc_base + i * 32 * KC_STRIDE + 8 * t);
+        const float4 v = ld4(L + kc_base + i * 32 * KC_STRIDE + 8 * t + 4);
+        f[0] = u.x; f[1] = u.y; f[2] = u.z; f[3] = u.w;
+        f[4] = v.x; f[5] = v.y; f[6] = v.z; f[7] = v.w;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = L[xc_base + (16 * t + 2 * j) * XC_STRIDE + i * 32];
+      }
+    };
+    auto compute_split = [&](const float* as, const float* bs) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        bf16x8 bh[2], bm[2], bl[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          float f[8];
+          frag8(bs, B_KC, b_kc_base, b_xc_base, j, t, f);
+          split3_bf16(f, bh[j], bm[j], bl[j]);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          float f[8];
+          frag8(as, A_KC, a_kc_base, a_xc_base, i, t, f);
+          bf16x8 ah, am, al;
+          split3_bf16(f, ah, am, al);
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            floatx16 c = acc[i][j];
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bm[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bh[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bm[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh[j], c, 0, 0, 0);
+            acc[i][j] = c;
+          }
+        }
+        // one MFMA step's reads, splits and products at a time (both steps
+        // at once need more registers than two blocks per CU allow)
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    auto compute = [&](const float* as, const float* bs) {
+      if constexpr (SPLIT)
+        compute_split(as, bs);
+      else
+        compute_f32(as, bs);
+    };
+
     // One pipelined step over a full slice: store the next slice (already
     // in registers) into the other stage, issue the global loads of the
     // slice after it, compute on the current stage, then one barrier.  The
@@ -401,25 +506,27 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
       store_slice(as_n, bs_n);
       load_full(kl);
       compute(as, bs);
-      // The stores go out with the first eight MFMAs, the loads with the
-      // next eight (a whole step ahead of the stores that consume them),
-      // and the fragment reads are spread over the rest.
+      if constexpr (!SPLIT) {
+        // The stores go out with the first eight MFMAs, the loads with the
+        // next eight (a whole step ahead of the stores that consume them),
+        // and the fragment reads are spread over the rest.
 #pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      }
+        for (int r = 0; r < 8; ++r) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        }
 #pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      }
+        for (int r = 0; r < 8; ++r) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS read
-        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // MFMA
+        for (int r = 0; r < 16; ++r) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // MFMA
+        }
       }
       __syncthreads();
     };
@@ -493,19 +600,12 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
 // Interior tiles over full K steps run the fp32 kernel's pipeline: store the
 // next step (in registers) into the other LDS stage, issue the loads of the
 // step after it, compute, one barrier.
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
-
 constexpr int BK16 = 64;
 constexpr int KC16_STRIDE = BK16 / 2 + 4;          // words per [x][k] row
 constexpr int XC16_HALF = (BK16 / 4) * 128 + 32;   // words per half (16 pair rows + gap)
 constexpr int KC16_WORDS = 128 * KC16_STRIDE;
 constexpr int XC16_WORDS = 2 * XC16_HALF;
 
-__device__ inline uint32_t pack_bf16(float lo, float hi) {
-  bf16x2v v = {(__bf16)lo, (__bf16)hi};
-  return __builtin_bit_cast(uint32_t, v);
-}
 // LDS word of k pair kp, column x, in the x-contiguous bf16 layout.
 __device__ inline int xc16_word(int kp, int x) {
   return (kp >> 4) * XC16_HALF + (kp & 15) * 128 + x;
@@ -812,7 +912,7 @@ struct Shape {
 static Shape gemm_shape(const GemmBatch& b) {
   Shape s;
   memset(&s, 0, sizeof(s));
-  const int BK = b.bf16 ? BK16 : gnnprop::BK;
+  const int BK = b.mode == GEMM_BF16 ? BK16 : gnnprop::BK;
   const int M = b.p[0].M;
   s.tiles_m = (int)ceil_div(M, BM);
   s.tiles_n0 = (int)ceil_div(b.p[0].N, BN);
@@ -857,7 +957,7 @@ static Shape gemm_shape(const GemmBatch& b) {
 
 static bool batch_ok(const GemmBatch& b) {
   if (b.nprob < 1 || b.nprob > 2) return false;
-  const int BK = b.bf16 ? BK16 : gnnprop::BK;
+  const int BK = b.mode == GEMM_BF16 ? BK16 : gnnprop::BK;
   if (b.nprob == 2) {
     if (b.p[0].M != b.p[1].M) return false;
     const auto kt = [BK](const GemmProblem& p) {
@@ -928,7 +1028,7 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
   const int kid = b.trans_a ? (b.trans_b ? GNN_K_GEMM_TT : GNN_K_GEMM_TN)
                             : (b.trans_b ? GNN_K_GEMM_NT : GNN_K_GEMM_NN);
   timer_begin(kid, s);
-  if (b.bf16) {
+  if (b.mode == GEMM_BF16) {
     if (!b.trans_a && !b.trans_b)
       gemm_bf16_kernel<false, false><<<grid, 256, 0, s>>>(g);
     else if (b.trans_a && !b.trans_b)
@@ -937,14 +1037,23 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
       gemm_bf16_kernel<false, true><<<grid, 256, 0, s>>>(g);
     else
       gemm_bf16_kernel<true, true><<<grid, 256, 0, s>>>(g);
+  } else if (b.mode == GEMM_F32) {
+    if (!b.trans_a && !b.trans_b)
+      gemm_f32_kernel<false, false, false><<<grid, 256, 0, s>>>(g);
+    else if (b.trans_a && !b.trans_b)
+      gemm_f32_kernel<true, false, false><<<grid, 256, 0, s>>>(g);
+    else if (!b.trans_a && b.trans_b)
+      gemm_f32_kernel<false, true, false><<<grid, 256, 0, s>>>(g);
+    else
+      gemm_f32_kernel<true, true, false><<<grid, 256, 0, s>>>(g);
   } else if (!b.trans_a && !b.trans_b) {
-    gemm_f32_kernel<false, false><<<grid, 256, 0, s>>>(g);
+    gemm_f32_kernel<false, false, true><<<grid, 256, 0, s>>>(g);
   } else if (b.trans_a && !b.trans_b) {
-    gemm_f32_kernel<true, false><<<grid, 256, 0, s>>>(g);
+    gemm_f32_kernel<true, false, true><<<grid, 256, 0, s>>>(g);
   } else if (!b.trans_a && b.trans_b) {
-    gemm_f32_kernel<false, true><<<grid, 256, 0, s>>>(g);
+    gemm_f32_kernel<false, true, true><<<grid, 256, 0, s>>>(g);
   } else {
-    gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g);
+    gemm_f32_kernel<true, true, true><<<grid, 256, 0, s>>>(g);
   }
   timer_end(kid, gemm_flops(b), s);
   hipError_t e = hipGetLastError();

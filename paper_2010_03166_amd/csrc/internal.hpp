@@ -126,11 +126,26 @@ struct GemmProblem {
   const float* mask;  // if set: C = mask[r, c] > 0 ? C : 0 (after bias/ReLU)
   int64_t ld_mask;
 };
+// How the products are formed (fp32 accumulation in every mode):
+//   GEMM_SPLIT  fp32 operands as three bf16 pieces each, six piece products
+//               on the bf16 matrix cores (the default; fp32 accuracy);
+//   GEMM_BF16   operands rounded to bf16, one product (GNN_FLAG_BF16);
+//   GEMM_F32    the fp32 matrix-core instruction (GNN_FLAG_F32_MFMA).
+enum GemmMode : int32_t { GEMM_SPLIT = 0, GEMM_BF16 = 1, GEMM_F32 = 2 };
+constexpr uint32_t GEMM_FLAGS = GNN_FLAG_BF16 | GNN_FLAG_F32_MFMA;
+inline int32_t gemm_mode(uint32_t flags) {
+  return (flags & GNN_FLAG_BF16) ? GEMM_BF16
+                                 : (flags & GNN_FLAG_F32_MFMA) ? GEMM_F32 : GEMM_SPLIT;
+}
+// Both product flags at once is not a mode.
+inline bool gemm_flags_ok(uint32_t flags) {
+  return (flags & GEMM_FLAGS) != GEMM_FLAGS;
+}
 struct GemmBatch {
   GemmProblem p[2];
   int32_t nprob;
   int32_t trans_a, trans_b;  // A stored K x M; B stored N x K
-  int32_t bf16;
+  int32_t mode;              // GemmMode
 };
 size_t gemm_workspace_bytes(const GemmBatch& b);
 hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,

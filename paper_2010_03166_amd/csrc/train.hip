@@ -193,7 +193,7 @@ GemmBatch prod(int ta, int tb, int32_t M, int32_t N, int32_t K, const float* A,
   b.nprob = 1;
   b.trans_a = ta;
   b.trans_b = tb;
-  b.bf16 = (flags & GNN_FLAG_BF16) ? 1 : 0;
+  b.mode = gemm_mode(flags);
   b.p[0].nseg = 1;
   b.p[0].seg[0] = {A, B, lda, ldb, K};
   b.p[0].M = M;
@@ -240,7 +240,7 @@ gnn_status gnn_classifier(int32_t n, int32_t f, int32_t C, int32_t kind,
                           hipStream_t stream) {
   if (n < 0 || f <= 0 || C <= 0) return GNN_ERR_SHAPE;
   if (kind != GNN_LOSS_SOFTMAX && kind != GNN_LOSS_SIGMOID) return GNN_ERR_UNSUPPORTED;
-  if (flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  if ((flags & ~GEMM_FLAGS) || !gemm_flags_ok(flags)) return GNN_ERR_UNSUPPORTED;
   if (!W || !loss || !dW) return GNN_ERR_NULL;
   if (n > 0 && (!X || !T)) return GNN_ERR_NULL;
   if (ld_x < f || ld_t < C || (xm && ld_xm < C) || (probs && ld_p < C) ||

@@ -34,7 +34,7 @@ GemmBatch gemm1(int trans_a, int trans_b, int32_t M, int32_t N, int32_t K,
   b.nprob = 1;
   b.trans_a = trans_a;
   b.trans_b = trans_b;
-  b.bf16 = (flags & GNN_FLAG_BF16) ? 1 : 0;
+  b.mode = gemm_mode(flags);
   GemmProblem& p = b.p[0];
   p.nseg = 1;
   p.seg[0] = {A, B, lda, ldb, K};
@@ -60,7 +60,7 @@ gnn_status check_variant_layer(const gnn_layer* L, int64_t width_y) {
   if (L->f_in <= 0 || L->h <= 0) return GNN_ERR_SHAPE;
   if (L->ld_x < L->f_in || L->ld_y < width_y) return GNN_ERR_SHAPE;
   if (L->order < 0 || L->order > 2) return GNN_ERR_SHAPE;
-  if (L->flags & ~GNN_FLAG_BF16) return GNN_ERR_UNSUPPORTED;
+  if ((L->flags & ~GEMM_FLAGS) || !gemm_flags_ok(L->flags)) return GNN_ERR_UNSUPPORTED;
   return GNN_OK;
 }
 

@@ -388,7 +388,7 @@ class Trainer:
             raise ValueError("optimizer must be 'sgd' or 'adam'")
         self.stack = SageStack(graph, params, f_in, order, flags, pad, fuse_masks, device)
         self.kind = G.GNN_LOSS_SIGMOID if multilabel else G.GNN_LOSS_SOFTMAX
-        self.flags = flags & G.GNN_FLAG_BF16
+        self.flags = flags & (G.GNN_FLAG_BF16 | G.GNN_FLAG_F32_MFMA)
         self.optimizer, self.lr, self.betas, self.eps = optimizer, lr, betas, eps
         self.device = device
         top = self.stack.layers[-1]

@@ -139,6 +139,11 @@ def test_argument_errors_are_synchronous(lib):
     assert L.gnn_gemm(0, 0, 4, 4, 4, P(0x10), 3, P(0x20), 4, P(0x30), 4, 0, None, 0, None) == -2
     assert L.gnn_gemm(0, 0, 4, 4, 4, P(0x10), 4, P(0x20), 4, P(0x30), 4, 0x80, None, 0, None) == -4
     assert L.gnn_gemm(0, 0, -1, 4, 4, P(0x10), 4, P(0x20), 4, P(0x30), 4, 0, None, 0, None) == -2
+    # bf16 and fp32-instruction products at once: not a mode
+    both = G.GNN_FLAG_BF16 | G.GNN_FLAG_F32_MFMA
+    assert L.gnn_gemm(0, 0, 4, 4, 4, P(0x10), 4, P(0x20), 4, P(0x30), 4, both, None, 0, None) == -4
+    bad = G.make_layer(8, 4, 8, 8, 8, flags=both)
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(bad), *([P(0x10)] * 8), ws, None) == -4
     # plan buffer too small
     assert L.gnn_csr_build_plan(ctypes.byref(c), P(0x10), 8, None) == -5
 

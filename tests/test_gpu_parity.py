@@ -203,11 +203,17 @@ GEMM_SHAPES = [(1, 1, 1), (37, 45, 29), (128, 128, 32), (130, 257, 70),
                (2001, 1300, 100), (8000, 602, 1024)]
 
 
+# the two fp32 product paths: three-piece bf16 split (default) and the
+# fp32 matrix-core instruction
+MODES = {"split": 0, "f32_mfma": G.GNN_FLAG_F32_MFMA}
+
+
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
 @pytest.mark.parametrize("ta", [0, 1])
 @pytest.mark.parametrize("tb", [0, 1])
 @pytest.mark.parametrize("layout", ["aligned", "unaligned"])
-def test_gemm_parity(M, N, K, ta, tb, layout):
+@pytest.mark.parametrize("mode", list(MODES))
+def test_gemm_parity(M, N, K, ta, tb, layout, mode):
     rng = np.random.default_rng(M * 7 + N * 3 + K)
     a = rng.standard_normal((K, M) if ta else (M, K)).astype(np.float32)
     b = rng.standard_normal((N, K) if tb else (K, N)).astype(np.float32)
@@ -222,12 +228,89 @@ def test_gemm_parity(M, N, K, ta, tb, layout):
     ws = torch.empty(max(G.gnn_gemm_workspace_bytes(M, N, K), 256),
                      dtype=torch.uint8, device="cuda")
     G.gnn_gemm(ta, tb, M, N, K, A, A.stride(0), B, B.stride(0), C, C.stride(0),
-               0, ws)
+               MODES[mode], ws)
     torch.cuda.synchronize()
     aa = a.T if ta else a
     bb = b.T if tb else b
     ref = O.mm_nn(aa, bb) if K > 0 else np.zeros((M, N))
     assert maxrel(C, ref) <= TOL
+
+
+def _gemm(a, b, flags):
+    M, K = a.shape
+    N = b.shape[1]
+    A, B = to_dev(a), to_dev(b)
+    C = empty_out(M, N, N)
+    ws = torch.empty(max(G.gnn_gemm_workspace_bytes(M, N, K), 256),
+                     dtype=torch.uint8, device="cuda")
+    G.gnn_gemm(0, 0, M, N, K, A, K, B, N, C, N, flags, ws)
+    torch.cuda.synchronize()
+    return C.cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("ta_tb", [(0, 0), (1, 0), (0, 1), (1, 1)])
+@pytest.mark.parametrize("full", ["a", "b"])
+def test_gemm_split_keeps_every_operand_bit(ta_tb, full):
+    """One operand has all 24 significand bits in use (1 + 2^-9 + 2^-18 +
+    2^-23, scaled by powers of two: hi, mid and lo pieces all nonzero), the
+    other selects one entry per output with a power-of-two weight, so every
+    exact result is an fp32 number.  The split path and the fp32 path must
+    return it bit for bit; the bf16 path, which keeps 8 bits, cannot."""
+    ta, tb = ta_tb
+    M, N, K = 96, 80, 64
+    rng = np.random.default_rng(5)
+    sig = 1.0 + 2.0 ** -9 + 2.0 ** -18 + 2.0 ** -23
+
+    def dense(r, c):
+        return (sig * rng.choice([1.0, -1.0], size=(r, c))
+                * np.ldexp(1.0, rng.integers(-3, 4, size=(r, c))))
+
+    def select(r, c, axis):
+        m = np.zeros((r, c))
+        if axis == 0:   # one nonzero per column
+            m[rng.integers(0, r, size=c), np.arange(c)] = np.ldexp(1.0, -rng.integers(0, 3, size=c))
+        else:           # one nonzero per row
+            m[np.arange(r), rng.integers(0, c, size=r)] = np.ldexp(1.0, -rng.integers(0, 3, size=r))
+        return m
+
+    if full == "a":
+        a, b = dense(M, K), select(K, N, 0)
+    else:
+        a, b = select(M, K, 1), dense(K, N)
+    a, b = a.astype(np.float32), b.astype(np.float32)
+    ref = a.astype(np.float64) @ b.astype(np.float64)
+    assert np.array_equal(ref.astype(np.float32).astype(np.float64), ref)
+    A = to_dev(np.ascontiguousarray(a.T) if ta else a)
+    B = to_dev(np.ascontiguousarray(b.T) if tb else b)
+    out = {}
+    for name, fl in (("split", 0), ("f32_mfma", G.GNN_FLAG_F32_MFMA),
+                     ("bf16", G.GNN_FLAG_BF16)):
+        C = empty_out(M, N, N)
+        ws = torch.empty(max(G.gnn_gemm_workspace_bytes(M, N, K), 256),
+                         dtype=torch.uint8, device="cuda")
+        G.gnn_gemm(ta, tb, M, N, K, A, A.stride(0), B, B.stride(0), C, C.stride(0),
+                   fl, ws)
+        torch.cuda.synchronize()
+        out[name] = C.cpu().numpy().astype(np.float64)
+    assert np.array_equal(out["split"], ref)
+    assert np.array_equal(out["f32_mfma"], ref)
+    assert not np.array_equal(out["bf16"], ref)
+
+
+@pytest.mark.parametrize("M,N,K", [(2000, 1024, 1024), (602, 512, 8000)])
+def test_gemm_split_accuracy_matches_f32_mfma(M, N, K):
+    """Against the double-precision product, the split path's error is of
+    the fp32 path's size (measured: 1.1e-6 against 1.5e-6 at 8000 x 1024 x
+    1024): no more than twice it, and far inside the layer tolerance."""
+    rng = np.random.default_rng(M + N + K)
+    a = rng.standard_normal((M, K)).astype(np.float32)
+    b = (rng.standard_normal((K, N)) * 0.05).astype(np.float32)
+    ref = O.mm_nn(a, b)
+    scale = np.abs(ref).max()
+    e_split = np.abs(_gemm(a, b, 0) - ref).max() / scale
+    e_f32 = np.abs(_gemm(a, b, G.GNN_FLAG_F32_MFMA) - ref).max() / scale
+    assert e_split <= 2 * e_f32 + 1e-7, (e_split, e_f32)
+    assert e_split <= 1e-5
 
 
 # --------------------------------------------------------------- one layer
@@ -244,10 +327,10 @@ def layer_inputs(n, f_in, h, seed, bias):
     return g, x, p, dy
 
 
-def run_layer(g, x, p, y_for_bwd, dy, order, pad=16, want_dx=True):
+def run_layer(g, x, p, y_for_bwd, dy, order, pad=16, want_dx=True, flags=0):
     f_in, h = p.w_self.shape
     dg = prepared(g)
-    st = runtime.SageStack(dg, [p], f_in, order=order, pad=pad)
+    st = runtime.SageStack(dg, [p], f_in, order=order, pad=pad, flags=flags)
     xd = to_dev(x, (f_in + pad - 1) // pad * pad)
     st.forward(xd)
     torch.cuda.synchronize()
@@ -273,11 +356,12 @@ LAYER_CASES = [(1, 7, 5), (37, 7, 5), (500, 50, 128), (400, 130, 64),
 @pytest.mark.parametrize("n,f_in,h", LAYER_CASES)
 @pytest.mark.parametrize("order", [1, 2])
 @pytest.mark.parametrize("bias", [False, True])
-def test_layer_parity(n, f_in, h, order, bias):
+@pytest.mark.parametrize("mode", list(MODES))
+def test_layer_parity(n, f_in, h, order, bias, mode):
     g, x, p, dy = layer_inputs(n, f_in, h, n + f_in + h, bias)
     y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh, p.b_self, p.b_neigh)
     y32 = y_ref.astype(np.float32)
-    got = run_layer(g, x, p, y32, dy, order)
+    got = run_layer(g, x, p, y32, dy, order, flags=MODES[mode])
     assert maxrel(got["Y"], y_ref) <= TOL
     r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy, want_db=bias)
     for k in ("dX", "dW_self", "dW_neigh") + (("db_self", "db_neigh") if bias else ()):
