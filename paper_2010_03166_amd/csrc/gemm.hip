@@ -3,15 +3,15 @@
 //
 // C = sum_s op(A_s) op(B_s) (+ bias, ReLU), fp32 in and out.  Products, by
 // GemmBatch::mode:
-//   split (default): every fp32 operand value split exactly into bf16
-//     hi + mid + lo while its MFMA fragment is formed; the six piece products
-//     down to 2^-16 of hi x hi run on v_mfma_f32_32x32x16_bf16 with fp32
-//     accumulation (the bf16x6 scheme of Henry, Tang and Heinecke, 2019).
-//     Six 16-deep bf16 MFMAs take 192 cycles against 512 for the eight
-//     2-deep fp32 MFMAs that cover the same 16 k, and the result is as
-//     accurate (measured against fp64);
-//   fp32: v_mfma_f32_32x32x2_f32;
-//   bf16: operands rounded to bf16, one product (the kernel further down).
+//   split (default, gemm_split_kernel further down): every fp32 operand
+//     value split exactly into bf16 hi + mid + lo as it is staged into LDS;
+//     the six piece products down to 2^-16 of hi x hi run on
+//     v_mfma_f32_32x32x16_bf16 with fp32 accumulation (the bf16x6 scheme of
+//     Henry, Tang and Heinecke, 2019).  Six 16-deep bf16 MFMAs take 192
+//     cycles against 512 for the eight 2-deep fp32 MFMAs that cover the same
+//     16 k, and the result is as accurate (measured against fp64);
+//   fp32 (gemm_f32_kernel): v_mfma_f32_32x32x2_f32, described below;
+//   bf16 (gemm_bf16_kernel): operands rounded to bf16, one product.
 //
 // Tiling.  A block of 256 threads (4 wavefronts in 2 x 2) computes a
 // 128 x 128 output tile; each wavefront holds a 64 x 64 sub-tile as 2 x 2
@@ -208,35 +208,7 @@ __device__ inline uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-// Eight floats as three bf16 vectors with x = hi + mid + lo exactly: hi is
-// x rounded to bf16, mid the remainder rounded, lo what is left.  Each
-// remainder is exact in fp32 (it has at most 16, then 8, significant bits),
-// and the last fits a bf16, so no information is lost.
-__device__ inline void split3_bf16(const float* x, bf16x8& hi, bf16x8& mid,
-                                   bf16x8& lo) {
-  uint4 h, m, l;
-  uint32_t* hp = &h.x;
-  uint32_t* mp = &m.x;
-  uint32_t* lp = &l.x;
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const float x0 = x[2 * p], x1 = x[2 * p + 1];
-    const uint32_t a = pack_bf16(x0, x1);
-    const float r0 = x0 - __uint_as_float(a << 16);
-    const float r1 = x1 - __uint_as_float(a & 0xffff0000u);
-    const uint32_t b = pack_bf16(r0, r1);
-    const float s0 = r0 - __uint_as_float(b << 16);
-    const float s1 = r1 - __uint_as_float(b & 0xffff0000u);
-    hp[p] = a;
-    mp[p] = b;
-    lp[p] = pack_bf16(s0, s1);
-  }
-  hi = __builtin_bit_cast(bf16x8, h);
-  mid = __builtin_bit_cast(bf16x8, m);
-  lo = __builtin_bit_cast(bf16x8, l);
-}
-
-template <bool AT, bool BT, bool SPLIT>
+template <bool AT, bool BT>
 __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
   constexpr bool A_KC = !AT;  // A row-major M x K: k contiguous
   constexpr bool B_KC = BT;   // B stored N x K: k contiguous
@@ -382,7 +354,7 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
     const int a_xc_base = lh * XC_STRIDE + wm * 64 + lr;
     const int b_xc_base = lh * XC_STRIDE + wn * 64 + lr;
 
-    auto compute_f32 = [&](const float* as, const float* bs) {
+    auto compute = [&](const float* as, const float* bs) {
       // Operands of step s are fetched one step (XC) or one group (KC)
       // ahead of the MFMAs that consume them.
       float4 af[2], bf[2], afn[2], bfn[2];
@@ -436,65 +408,6 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
       }
     };
 
-    // Split products (SPLIT): each MFMA step contracts 16 k, lane half h
-    // supplying k = 16 h + 8 t + j (j = 0..7) at step t = 0, 1 of the slice,
-    // in both operands.  The fp32 fragments are read as for the fp32 MFMA,
-    // split into bf16 hi + mid + lo, and the products of the pieces whose
-    // weights are at least 2^-16 of hi x hi (hi hi, hi mid, mid hi, hi lo,
-    // lo hi, mid mid) accumulate in fp32, smallest first.  What is left out,
-    // mid lo + lo mid + lo lo, is below 2^-24 of |a b|.
-    auto frag8 = [&](const float* L, bool kc, int kc_base, int xc_base, int i,
-                     int t, float* f) {
-      if (kc) {
-        const float4 u = ld4(L + kc_base + i * 32 * KC_STRIDE + 8 * t);
-        const float4 v = ld4(L + kc_base + i * 32 * KC_STRIDE + 8 * t + 4);
-        f[0] = u.x; f[1] = u.y; f[2] = u.z; f[3] = u.w;
-        f[4] = v.x; f[5] = v.y; f[6] = v.z; f[7] = v.w;
-      } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) f[j] = L[xc_base + (16 * t + 2 * j) * XC_STRIDE + i * 32];
-      }
-    };
-    auto compute_split = [&](const float* as, const float* bs) {
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        bf16x8 bh[2], bm[2], bl[2];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          float f[8];
-          frag8(bs, B_KC, b_kc_base, b_xc_base, j, t, f);
-          split3_bf16(f, bh[j], bm[j], bl[j]);
-        }
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          float f[8];
-          frag8(as, A_KC, a_kc_base, a_xc_base, i, t, f);
-          bf16x8 ah, am, al;
-          split3_bf16(f, ah, am, al);
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            floatx16 c = acc[i][j];
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bm[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bh[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bm[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh[j], c, 0, 0, 0);
-            acc[i][j] = c;
-          }
-        }
-        // one MFMA step's reads, splits and products at a time (both steps
-        // at once need more registers than two blocks per CU allow)
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-    auto compute = [&](const float* as, const float* bs) {
-      if constexpr (SPLIT)
-        compute_split(as, bs);
-      else
-        compute_f32(as, bs);
-    };
-
     // One pipelined step over a full slice: store the next slice (already
     // in registers) into the other stage, issue the global loads of the
     // slice after it, compute on the current stage, then one barrier.  The
@@ -506,27 +419,25 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
       store_slice(as_n, bs_n);
       load_full(kl);
       compute(as, bs);
-      if constexpr (!SPLIT) {
-        // The stores go out with the first eight MFMAs, the loads with the
-        // next eight (a whole step ahead of the stores that consume them),
-        // and the fragment reads are spread over the rest.
+      // The stores go out with the first eight MFMAs, the loads with the
+      // next eight (a whole step ahead of the stores that consume them),
+      // and the fragment reads are spread over the rest.
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        }
+      for (int r = 0; r < 8; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      }
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        }
+      for (int r = 0; r < 8; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS read
-          __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // MFMA
-        }
+      for (int r = 0; r < 16; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // MFMA
       }
       __syncthreads();
     };
@@ -831,6 +742,284 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
   }
 }
 
+// ----------------------------------------------- split-product kernel
+//
+// The default fp32 mode.  Each operand value is split once per block, as it
+// is staged into LDS, into bf16 hi + mid + lo (split3 below; exact), kept in
+// three LDS planes; the MFMAs read ready pieces, and the split of the next
+// stage does not wait for the current stage's products.  K advances 16 deep
+// per stage (one MFMA step: 24 MFMAs per wavefront), which keeps two
+// double-buffered stages of three planes per operand within half the LDS of
+// a CU (two blocks per CU).
+// Lane half h supplies k = 8 h + j (j = 0..7) in both operands.
+//   K-contiguous operand: plane [x][k] rows of 8 words (k pairs) + 4 words
+//     of padding (48 bytes: eight consecutive rows of a 128-bit fragment
+//     read fall on distinct banks); a fragment is one 128-bit read.
+//   X-contiguous operand: plane rows of k pairs, word (kp, x) = (k 2kp,
+//     2kp + 1) of column x; pairs 4..7 start 32 words past the end of pairs
+//     0..3 so that the two lane halves of a read use different banks; a
+//     fragment is 4 words from 4 pair rows.
+constexpr int BKS = 16;
+constexpr int KCS_ROW = 12;
+constexpr int KCS_PLANE = 128 * KCS_ROW;
+constexpr int XCS_HALF = 4 * 128 + 32;
+constexpr int XCS_PLANE = 2 * XCS_HALF;
+
+__device__ inline int xcs_word(int kp, int x) {
+  return (kp >> 2) * XCS_HALF + (kp & 3) * 128 + x;
+}
+
+// Pieces of the pair (x0, x1): hi, mid and lo packed as bf16x2 words with
+// x = hi + mid + lo exactly.
+__device__ inline void split3(float x0, float x1, uint32_t& h, uint32_t& m,
+                              uint32_t& l) {
+  // (the empty asm keeps each packed pair as one value: otherwise the
+  // compiler converts each half again to take it apart)
+  uint32_t a = pack_bf16(x0, x1);
+  asm volatile("" : "+v"(a));
+  const float r0 = x0 - __uint_as_float(a << 16);
+  const float r1 = x1 - __uint_as_float(a & 0xffff0000u);
+  uint32_t b = pack_bf16(r0, r1);
+  asm volatile("" : "+v"(b));
+  const float s0 = r0 - __uint_as_float(b << 16);
+  const float s1 = r1 - __uint_as_float(b & 0xffff0000u);
+  h = a;
+  m = b;
+  l = pack_bf16(s0, s1);
+}
+
+template <bool AT, bool BT>
+__global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
+  constexpr bool A_KC = !AT;
+  constexpr bool B_KC = BT;
+  constexpr int A_PLANE = A_KC ? KCS_PLANE : XCS_PLANE;
+  constexpr int B_PLANE = B_KC ? KCS_PLANE : XCS_PLANE;
+  __shared__ __attribute__((aligned(16))) uint32_t As0[3 * A_PLANE];
+  __shared__ __attribute__((aligned(16))) uint32_t As1[3 * A_PLANE];
+  __shared__ __attribute__((aligned(16))) uint32_t Bs0[3 * B_PLANE];
+  __shared__ __attribute__((aligned(16))) uint32_t Bs1[3 * B_PLANE];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int lr = lane & 31, lh = lane >> 5;
+  const bool va = g.vec_a != 0, vb = g.vec_b != 0;
+  const int M = g.M;
+
+  const int lb = logical_block(blockIdx.x, g.nblocks);
+  int64_t lo, hi;
+  if (g.splits > 1) {
+    const int sp = lb / g.tiles, t = lb % g.tiles;
+    lo = (int64_t)t * g.ktiles + (int64_t)sp * g.ktiles / g.splits;
+    hi = (int64_t)t * g.ktiles + (int64_t)(sp + 1) * g.ktiles / g.splits;
+  } else {
+    lo = block_lo(lb, g.iters, g.nblocks);
+    hi = block_lo(lb + 1, g.iters, g.nblocks);
+  }
+
+  int seg = 0;
+  for (int64_t it = lo; it < hi; ++seg) {
+    const int t = (int)(it / g.ktiles);
+    const int kbeg = (int)(it - (int64_t)t * g.ktiles);
+    const int kend = (int)min<int64_t>(g.ktiles, hi - (int64_t)t * g.ktiles);
+    it = (int64_t)t * g.ktiles + kend;
+    const TileInfo ti = tile_info(g, t);
+    const GemmProblem& P = ti.pi ? g.p[1] : g.p[0];
+    const int N = P.N;
+    const int m0 = ti.m0, n0 = ti.n0;
+    const int kt0 = ti.pi ? g.ktiles0[1] : g.ktiles0[0];
+    const float* const A0p = P.seg[0].A;
+    const float* const A1p = P.seg[1].A;
+    const float* const B0p = P.seg[0].B;
+    const float* const B1p = P.seg[1].B;
+    const int64_t lda0 = P.seg[0].lda, lda1 = P.seg[1].lda;
+    const int64_t ldb0 = P.seg[0].ldb, ldb1 = P.seg[1].ldb;
+    const int K0 = P.seg[0].K, K1 = P.seg[1].K;
+    const bool a_in = va && m0 + BM <= M;
+    const bool b_in = vb && n0 + BN <= N;
+    // KC: thread owns rows x = (tid >> 2) + 64 p (p = 0, 1), k = 4 (tid & 3)
+    // .. + 3 (4 lanes per 64-byte row segment).
+    // XC: thread owns k pair kp = tid >> 5 (rows 2 kp and 2 kp + 1) and
+    // x = 4 (tid & 31) .. + 3 (a wavefront reads 2 whole 512-byte rows).
+    const int kx = tid >> 2, ky = 4 * (tid & 3);
+    const int xk = tid >> 5, xy = 4 * (tid & 31);
+
+    float4 ra[2], rb[2];
+    auto load_op = [&](float4 (&r)[2], bool kc, const float* X, int64_t ld,
+                       int x0, int X_extent, int k0, int K, bool fast, bool vec) {
+      if (kc) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const int x = x0 + kx + 64 * p, k = k0 + ky;
+          r[p] = fast ? ld4(X + (int64_t)x * ld + k) : load4(X, ld, x, k, X_extent, K, vec);
+        }
+      } else {
+        const int k = k0 + 2 * xk, x = x0 + xy;
+        if (fast) {
+          const float* q = X + (int64_t)k * ld + x;
+          r[0] = ld4(q);
+          r[1] = ld4(q + ld);
+        } else {
+          r[0] = load4(X, ld, k, x, K, X_extent, vec);
+          r[1] = load4(X, ld, k + 1, x, K, X_extent, vec);
+        }
+      }
+    };
+    auto load_slice = [&](int ks) {
+      const bool s1 = ks >= kt0;
+      const int K = s1 ? K1 : K0;
+      const int k0 = (s1 ? ks - kt0 : ks) * BKS;
+      const bool fk = k0 + BKS <= K;
+      load_op(ra, A_KC, s1 ? A1p : A0p, s1 ? lda1 : lda0, m0, M, k0, K, a_in && fk, va);
+      load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, K, b_in && fk, vb);
+    };
+    // Split this thread's values and write the three pieces.
+    auto store_op = [&](uint32_t* L, const float4 (&r)[2], bool kc, int plane) {
+      if (kc) {  // 4 consecutive k of rows x and x + 64
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          uint2 h, m, l;
+          split3(r[p].x, r[p].y, h.x, m.x, l.x);
+          split3(r[p].z, r[p].w, h.y, m.y, l.y);
+          const int w = (kx + 64 * p) * KCS_ROW + ky / 2;
+          *reinterpret_cast<uint2*>(&L[w]) = h;
+          *reinterpret_cast<uint2*>(&L[plane + w]) = m;
+          *reinterpret_cast<uint2*>(&L[2 * plane + w]) = l;
+        }
+      } else {   // k pair (rows 2kp, 2kp + 1) of 4 consecutive x
+        uint4 h, m, l;
+        split3(r[0].x, r[1].x, h.x, m.x, l.x);
+        split3(r[0].y, r[1].y, h.y, m.y, l.y);
+        split3(r[0].z, r[1].z, h.z, m.z, l.z);
+        split3(r[0].w, r[1].w, h.w, m.w, l.w);
+        const int w = xcs_word(xk, xy);
+        *reinterpret_cast<uint4*>(&L[w]) = h;
+        *reinterpret_cast<uint4*>(&L[plane + w]) = m;
+        *reinterpret_cast<uint4*>(&L[2 * plane + w]) = l;
+      }
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // fragment of block i from one piece plane
+    auto frag = [&](const uint32_t* L, bool kc, int wbase, int i) {
+      uint4 w;
+      const int x = wbase + i * 32 + lr;
+      if (kc) {
+        w = *reinterpret_cast<const uint4*>(&L[x * KCS_ROW + 4 * lh]);
+      } else {
+        w.x = L[xcs_word(4 * lh + 0, x)];
+        w.y = L[xcs_word(4 * lh + 1, x)];
+        w.z = L[xcs_word(4 * lh + 2, x)];
+        w.w = L[xcs_word(4 * lh + 3, x)];
+      }
+      return __builtin_bit_cast(bf16x8, w);
+    };
+    // The six piece products down to 2^-16 of hi x hi, smallest first; what
+    // is left out (mid lo + lo mid + lo lo) is below 2^-24 of |a b|.
+    struct Frags {
+      bf16x8 a[3][2], b[3][2];
+    };
+    auto read_frags = [&](const uint32_t* as, const uint32_t* bs) {
+      Frags f;
+#pragma unroll
+      for (int q = 0; q < 3; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          f.a[q][i] = frag(as + q * A_PLANE, A_KC, wm * 64, i);
+          f.b[q][i] = frag(bs + q * B_PLANE, B_KC, wn * 64, i);
+        }
+      return f;
+    };
+    auto products = [&](const Frags& f) {
+      constexpr int terms[6][2] = {{1, 1}, {2, 0}, {0, 2}, {1, 0}, {0, 1}, {0, 0}};
+#pragma unroll
+      for (int u = 0; u < 6; ++u)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                f.a[terms[u][0]][i], f.b[terms[u][1]][j], acc[i][j], 0, 0, 0);
+    };
+    auto compute = [&](const uint32_t* as, const uint32_t* bs) {
+      products(read_frags(as, bs));
+    };
+
+    // Stages [kbeg, kf) are full and the tile is interior: pipelined path.
+    int kf = kbeg;
+    if (a_in && b_in) {
+      const int f0 = K0 / BKS, e1 = kt0 + K1 / BKS;
+      if (kbeg < f0)
+        kf = min(kend, f0 == kt0 ? e1 : f0);
+      else if (kbeg >= kt0 && kbeg < e1)
+        kf = min(kend, e1);
+    }
+    if (kf > kbeg) {
+      auto load_full = [&](int ks) {
+        ks = min(ks, kf - 1);  // past the end: repeat the last stage (never read)
+        const bool s1 = ks >= kt0;
+        const int k0 = (s1 ? ks - kt0 : ks) * BKS;
+        load_op(ra, A_KC, s1 ? A1p : A0p, s1 ? lda1 : lda0, m0, M, k0, 0, true, true);
+        load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, 0, true, true);
+      };
+      // Read this stage's fragments, split and store the next stage (in
+      // registers) into the other LDS buffer, issue the loads of the stage
+      // after it, the products, one barrier.  The fragment reads go first so
+      // that the next stage's LDS writes do not hold them up.
+      auto step = [&](const uint32_t* as, const uint32_t* bs, uint32_t* as_n,
+                      uint32_t* bs_n, int kl) {
+        const Frags f = read_frags(as, bs);
+        store_op(as_n, ra, A_KC, A_PLANE);
+        store_op(bs_n, rb, B_KC, B_PLANE);
+        load_full(kl);
+        products(f);
+        __syncthreads();
+      };
+      load_full(kbeg);
+      store_op(As0, ra, A_KC, A_PLANE);
+      store_op(Bs0, rb, B_KC, B_PLANE);
+      load_full(kbeg + 1);
+      __syncthreads();
+      for (int k = kbeg; k < kf; k += 2) {
+        step(As0, Bs0, As1, Bs1, k + 2);
+        if (k + 1 >= kf) break;
+        step(As1, Bs1, As0, Bs0, k + 3);
+      }
+    }
+
+    // Remaining stages (edge tiles, partial K): guarded loads, one stage in
+    // registers ahead.
+    if (kf < kend) {
+      int buf = 0;
+      load_slice(kf);
+      for (int ks = kf; ks < kend; ++ks) {
+        uint32_t* as = buf ? As1 : As0;
+        uint32_t* bs = buf ? Bs1 : Bs0;
+        store_op(as, ra, A_KC, A_PLANE);
+        store_op(bs, rb, B_KC, B_PLANE);
+        __syncthreads();
+        if (ks + 1 < kend) load_slice(ks + 1);
+        compute(as, bs);
+        buf ^= 1;
+      }
+      __syncthreads();
+    }
+
+    const bool whole = kbeg == 0 && kend == g.ktiles;
+    float* part = g.part + (g.splits > 1 ? (int64_t)lb
+                                         : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
+                               (BM * BN);
+    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh);
+  }
+}
+
 // Tiles shared by several blocks: add the blocks' partial tiles in block
 // order, then bias and ReLU.  Block (t, c) handles 1024 elements of tile t,
 // four consecutive columns per thread.
@@ -912,7 +1101,7 @@ struct Shape {
 static Shape gemm_shape(const GemmBatch& b) {
   Shape s;
   memset(&s, 0, sizeof(s));
-  const int BK = b.mode == GEMM_BF16 ? BK16 : gnnprop::BK;
+  const int BK = b.mode == GEMM_BF16 ? BK16 : b.mode == GEMM_SPLIT ? BKS : gnnprop::BK;
   const int M = b.p[0].M;
   s.tiles_m = (int)ceil_div(M, BM);
   s.tiles_n0 = (int)ceil_div(b.p[0].N, BN);
@@ -957,7 +1146,7 @@ static Shape gemm_shape(const GemmBatch& b) {
 
 static bool batch_ok(const GemmBatch& b) {
   if (b.nprob < 1 || b.nprob > 2) return false;
-  const int BK = b.mode == GEMM_BF16 ? BK16 : gnnprop::BK;
+  const int BK = b.mode == GEMM_BF16 ? BK16 : b.mode == GEMM_SPLIT ? BKS : gnnprop::BK;
   if (b.nprob == 2) {
     if (b.p[0].M != b.p[1].M) return false;
     const auto kt = [BK](const GemmProblem& p) {
@@ -1039,21 +1228,21 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
       gemm_bf16_kernel<true, true><<<grid, 256, 0, s>>>(g);
   } else if (b.mode == GEMM_F32) {
     if (!b.trans_a && !b.trans_b)
-      gemm_f32_kernel<false, false, false><<<grid, 256, 0, s>>>(g);
+      gemm_f32_kernel<false, false><<<grid, 256, 0, s>>>(g);
     else if (b.trans_a && !b.trans_b)
-      gemm_f32_kernel<true, false, false><<<grid, 256, 0, s>>>(g);
+      gemm_f32_kernel<true, false><<<grid, 256, 0, s>>>(g);
     else if (!b.trans_a && b.trans_b)
-      gemm_f32_kernel<false, true, false><<<grid, 256, 0, s>>>(g);
+      gemm_f32_kernel<false, true><<<grid, 256, 0, s>>>(g);
     else
-      gemm_f32_kernel<true, true, false><<<grid, 256, 0, s>>>(g);
+      gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g);
   } else if (!b.trans_a && !b.trans_b) {
-    gemm_f32_kernel<false, false, true><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<false, false><<<grid, 256, 0, s>>>(g);
   } else if (b.trans_a && !b.trans_b) {
-    gemm_f32_kernel<true, false, true><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<true, false><<<grid, 256, 0, s>>>(g);
   } else if (!b.trans_a && b.trans_b) {
-    gemm_f32_kernel<false, true, true><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<false, true><<<grid, 256, 0, s>>>(g);
   } else {
-    gemm_f32_kernel<true, true, true><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<true, true><<<grid, 256, 0, s>>>(g);
   }
   timer_end(kid, gemm_flops(b), s);
   hipError_t e = hipGetLastError();
