@@ -1127,13 +1127,17 @@ static Shape gemm_shape(const GemmBatch& b) {
   // 256 tiles) over at most 40 K slices runs one block per tile: measured
   // faster than stream-K plus its reduction (8000 x 512, K = 602: 65.5
   // against 61.3 + 12.2 us), slower from K = 2048 on.
+  // The rules count K in 32-deep slices whatever the kernel's stage depth
+  // (the split kernel's stages are 16 deep).
   const int slots = MAX_BLOCKS;
   const int64_t rounds = ceil_div(s.tiles, slots);
   const double fill = (double)s.tiles / (double)(rounds * slots);
-  const bool one_per_cu = s.tiles >= slots * 7 / 16 && s.tiles <= slots / 2 && s.ktiles <= 40;
+  const int kt32 = b.mode == GEMM_SPLIT ? (s.ktiles + 1) / 2 : s.ktiles;
+  const int64_t iters32 = (int64_t)s.tiles * kt32;
+  const bool one_per_cu = s.tiles >= slots * 7 / 16 && s.tiles <= slots / 2 && kt32 <= 40;
   s.splits = 1;
   if (fill >= 0.85 || one_per_cu ||
-      (s.iters <= slots && (s.tiles > slots / 4 || s.ktiles < 4))) {
+      (iters32 <= slots && (s.tiles > slots / 4 || kt32 < 4))) {
     s.nblocks = s.tiles;
   } else if (s.tiles <= slots / 4) {
     s.splits = (int)std::min<int64_t>(s.ktiles, slots / s.tiles);
