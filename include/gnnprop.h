@@ -60,8 +60,12 @@ typedef enum gnn_status {
  * to nearest even) and the six piece products down to 2^-16 of hi x hi are
  * accumulated in fp32 on the bf16 matrix cores: fp32 operands, results and
  * accumulation, with a product error below 2^-24 relative (measured against
- * fp64: no larger than that of the fp32 matrix-core instruction).  The two
- * flags below select other arithmetic; setting both is GNN_ERR_UNSUPPORTED. */
+ * fp64: no larger than that of the fp32 matrix-core instruction).  Operands
+ * must be finite and below bf16's largest finite value (about 3.39e38) in
+ * magnitude: an infinite operand makes its outputs NaN where the fp32
+ * instruction gives infinities (use GNN_FLAG_F32_MFMA for such data).  The
+ * two flags below select other arithmetic; setting both is
+ * GNN_ERR_UNSUPPORTED. */
 #define GNN_FLAG_BF16 0x1u /* GEMM operands rounded to bf16 (round to nearest
                               even), fp32 accumulation; aggregation stays fp32 */
 #define GNN_FLAG_F32_MFMA 0x8u /* GEMM products on the fp32 matrix-core
