@@ -78,6 +78,7 @@ struct GemmKArgs {
   int32_t splits;      // > 1: split-K mode, one (tile, K range) per block
   float* part;         // partial tiles (2 per block stream-K, 1 split-K)
   int32_t vec_a, vec_b;
+  int32_t vec_c[2];    // C (and mask, bias) of problem i take float4 accesses
 };
 
 __device__ inline float4 ld4(const float* p) {
@@ -148,14 +149,63 @@ __device__ inline TileInfo tile_info(const GemmKArgs& g, int t) {
 // block): straight to C with bias, ReLU and mask when the block covered the
 // whole K range, else to its partial tile.  Interior tiles take a path
 // without per-element guards, so the mask loads go out sixteen at a time.
+//
+// Whole interior tiles whose C (and mask, bias) take float4 accesses go
+// through LDS instead: each wavefront writes one 32 x 32 block at a time
+// into its own region (rows of 40 floats: the two lane halves' rows land 32
+// banks apart), reads it back as float4 along rows and stores 8 rows of
+// 128 bytes per instruction, with the same bias, ReLU and mask.  `lds0` and
+// `lds1` are two LDS arrays of at least 2 x 1280 floats that no wavefront
+// reads any more (the K loop ended with a barrier); the path ends with a
+// barrier, so the next tile may write them.  The condition is uniform over
+// the block.
+constexpr int EPI_ROW = 40;
+constexpr int EPI_REGION = 32 * EPI_ROW;
+
 __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
                                  int M, const floatx16 (&acc)[2][2],
                                  bool whole, float* part, int wm, int wn,
-                                 int lr, int lh) {
+                                 int lr, int lh, bool vec_c, float* lds0,
+                                 float* lds1) {
   const int N = P.N;
   // moved-back tiles take the guarded path, which skips what they do not own
   const bool interior = ti.m0 + BM <= M && ti.n0 + BN <= N && ti.m0 == ti.r0 &&
                         ti.n0 == ti.c0;
+  if (whole && interior && vec_c) {
+    const int wave = 2 * wn + wm, lane = lh * 32 + lr;
+    float* L = (wave < 2 ? lds0 : lds1) + (wave & 1) * EPI_REGION;
+    const int rr = lane >> 3, c4 = 4 * (lane & 7);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          L[(8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_ROW + lr] = acc[i][j][r];
+        const int row0 = ti.m0 + wm * 64 + i * 32, col = ti.n0 + wn * 64 + j * 32 + c4;
+        const float4 bc = P.bias ? ld4(P.bias + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = row0 + rr + 8 * q;
+          float4 v = ld4(&L[(rr + 8 * q) * EPI_ROW + c4]);
+          v.x += bc.x; v.y += bc.y; v.z += bc.z; v.w += bc.w;
+          if (P.relu) {
+            v.x = fmaxf(v.x, 0.f); v.y = fmaxf(v.y, 0.f);
+            v.z = fmaxf(v.z, 0.f); v.w = fmaxf(v.w, 0.f);
+          }
+          if (P.mask) {
+            const float4 m = ld4(P.mask + (int64_t)row * P.ld_mask + col);
+            if (!(m.x > 0.f)) v.x = 0.f;
+            if (!(m.y > 0.f)) v.y = 0.f;
+            if (!(m.z > 0.f)) v.z = 0.f;
+            if (!(m.w > 0.f)) v.w = 0.f;
+          }
+          *reinterpret_cast<float4*>(P.C + (int64_t)row * P.ldc + col) = v;
+        }
+      }
+    __syncthreads();
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -220,6 +270,7 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
   __shared__ __attribute__((aligned(16))) float As1[A_FLOATS];
   __shared__ __attribute__((aligned(16))) float Bs0[B_FLOATS];
   __shared__ __attribute__((aligned(16))) float Bs1[B_FLOATS];
+  static_assert(A_FLOATS >= 2 * EPI_REGION && B_FLOATS >= 2 * EPI_REGION, "epilogue regions");
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -486,7 +537,8 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
     float* part = g.part + (g.splits > 1 ? (int64_t)lb
                                          : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
                                (BM * BN);
-    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh);
+    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh, g.vec_c[ti.pi] != 0,
+              reinterpret_cast<float*>(As0), reinterpret_cast<float*>(Bs0));
   }
 }
 
@@ -532,6 +584,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
   __shared__ __attribute__((aligned(16))) uint32_t As1[A_WORDS];
   __shared__ __attribute__((aligned(16))) uint32_t Bs0[B_WORDS];
   __shared__ __attribute__((aligned(16))) uint32_t Bs1[B_WORDS];
+  static_assert(A_WORDS >= 2 * EPI_REGION && B_WORDS >= 2 * EPI_REGION, "epilogue regions");
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -738,7 +791,8 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
     float* part = g.part + (g.splits > 1 ? (int64_t)lb
                                          : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
                                (BM * BN);
-    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh);
+    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh, g.vec_c[ti.pi] != 0,
+              reinterpret_cast<float*>(As0), reinterpret_cast<float*>(Bs0));
   }
 }
 
@@ -798,6 +852,8 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
   __shared__ __attribute__((aligned(16))) uint32_t As1[3 * A_PLANE];
   __shared__ __attribute__((aligned(16))) uint32_t Bs0[3 * B_PLANE];
   __shared__ __attribute__((aligned(16))) uint32_t Bs1[3 * B_PLANE];
+  static_assert(3 * A_PLANE >= 2 * EPI_REGION && 3 * B_PLANE >= 2 * EPI_REGION,
+                "epilogue regions");
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -1016,7 +1072,8 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
     float* part = g.part + (g.splits > 1 ? (int64_t)lb
                                          : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
                                (BM * BN);
-    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh);
+    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh, g.vec_c[ti.pi] != 0,
+              reinterpret_cast<float*>(As0), reinterpret_cast<float*>(Bs0));
   }
 }
 
@@ -1208,6 +1265,11 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
       va = va && vec4_ok(p.seg[k].A, p.seg[k].lda);
       vb = vb && vec4_ok(p.seg[k].B, p.seg[k].ldb);
     }
+  }
+  for (int i = 0; i < b.nprob; ++i) {
+    const GemmProblem& p = g.p[i];
+    g.vec_c[i] = vec4_ok(p.C, p.ldc) && (!p.mask || vec4_ok(p.mask, p.ld_mask)) &&
+                 (!p.bias || aligned16(p.bias));
   }
   g.vec_a = va;
   g.vec_b = vb;
