@@ -297,6 +297,28 @@ def test_gemm_split_keeps_every_operand_bit(ta_tb, full):
     assert not np.array_equal(out["bf16"], ref)
 
 
+@pytest.mark.parametrize("M,N,K", [(2001, 1300, 100), (1000, 512, 64), (256, 384, 700)])
+@pytest.mark.parametrize("flags", [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16])
+def test_gemm_epilogue_paths_bit_identical(M, N, K, flags):
+    """Whole interior tiles of a float4-aligned C are written through LDS as
+    float4 rows; the same product into a C 4 bytes off alignment takes the
+    per-element path.  Both must hold the same bits everywhere."""
+    rng = np.random.default_rng(M + N + K + flags)
+    a = rng.standard_normal((M, K)).astype(np.float32)
+    b = rng.standard_normal((K, N)).astype(np.float32)
+    A, B = to_dev(a), to_dev(b)
+    ws = torch.empty(max(G.gnn_gemm_workspace_bytes(M, N, K), 256),
+                     dtype=torch.uint8, device="cuda")
+    outs = []
+    for shift in (False, True):
+        C = empty_out(M, N, N + 4, shift=shift)
+        G.gnn_gemm(0, 0, M, N, K, A, K, B, N, C, C.stride(0), flags, ws)
+        torch.cuda.synchronize()
+        outs.append(C.cpu().numpy().copy())
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    assert maxrel(outs[0], O.mm_nn(a, b)) <= (TOL if flags != G.GNN_FLAG_BF16 else 2e-2)
+
+
 @pytest.mark.parametrize("M,N,K", [(2000, 1024, 1024), (602, 512, 8000)])
 def test_gemm_split_accuracy_matches_f32_mfma(M, N, K):
     """Against the double-precision product, the split path's error is of
