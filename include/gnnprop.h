@@ -206,7 +206,8 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
  *   db_self, db_neigh = column sums of the two halves of G
  * dX may be NULL (not computed; e.g. the first layer).  db_* may be NULL.
  * layer->flags may add GNN_FLAG_DY_MASKED (dY already masked) and
- * GNN_FLAG_DX_MASKED (dX returned masked by 1[X > 0]).
+ * GNN_FLAG_DX_MASKED (dX returned masked by 1[X > 0]) to the product flags
+ * (GNN_FLAG_BF16 or GNN_FLAG_F32_MFMA, or neither: split products).
  * Needs csr->values, csr->values_t and csr->plan, and the `saved` buffer of
  * the matching gnn_prop_fwd call with the same layer (same order).  Outputs
  * must not overlap inputs. */
@@ -225,9 +226,9 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
  * csr->values must hold A_hat = (I + D)^-1/2 (I + A) (I + D)^-1/2 (the
  * pattern storing the self loops); it is symmetric, so csr->values_t may
  * point to csr->values.  layer->h is one path's output width; layer->flags
- * may hold GNN_FLAG_BF16 only.  Sizes of `saved` and workspace come from the
- * matching queries; ownership and aliasing rules are those of
- * gnn_prop_fwd / gnn_prop_bwd.
+ * may hold one product flag (GNN_FLAG_BF16 or GNN_FLAG_F32_MFMA) only.  Sizes
+ * of `saved` and workspace come from the matching queries; ownership and
+ * aliasing rules are those of gnn_prop_fwd / gnn_prop_bwd.
  *
  * GCN (Eq. "gcn forward"): Y = ReLU(A_hat X W + b), Y n x h (stride
  * ld_y >= h), W f_in x h row-major, b [h] or NULL; order as for GraphSAGE
@@ -278,8 +279,8 @@ gnn_status gnn_mixhop_bwd(const gnn_csr* csr, const gnn_layer* layer,
  *   P = X W,  att_uv = LeakyReLU(a1 . P_u + a2 . P_v)  (slope alpha in
  *   [0, 1] below 0),  Y = ReLU(A_att P)
  * with a = [a1; a2] (2h floats, device).  layer: f_in, h, ld_x, ld_y
- * (Y is n x h), ld_dx; order is ignored; flags: GNN_FLAG_BF16 for the
- * products.  att_out (nnz floats, may be NULL) receives the attention
+ * (Y is n x h), ld_dx; order is ignored; flags: GNN_FLAG_BF16 or
+ * GNN_FLAG_F32_MFMA for the products.  att_out (nnz floats, may be NULL) receives the attention
  * values in CSR order.  `saved` (gnn_gat_saved_bytes) carries P, the
  * scores and the attention values from the forward to the backward call.
  * Backward: dW (f_in x h), da (2h) and optionally dX, by the chain rule
@@ -310,7 +311,7 @@ gnn_status gnn_gat_bwd(const gnn_csr* csr, const gnn_layer* layer, const float* 
  *   G  = (Y - T) / n * 1[XM > 0];   dW = X^T G (f x C);   dX = G W^T
  * `loss` is one float of device memory.  Optional outputs (NULL to skip):
  * xm = X_MLP (n x C, stride ld_xm), probs = Y (stride ld_p), dX (stride
- * ld_dx).  flags: GNN_FLAG_BF16 for the three products.  The loss is summed
+ * ld_dx).  flags: GNN_FLAG_BF16 or GNN_FLAG_F32_MFMA for the three products.  The loss is summed
  * in a fixed order (bit-reproducible).  No output may overlap an input,
  * another output or the workspace.  Workspace:
  * gnn_classifier_workspace_bytes(n, f, C).  n = 0 gives loss 0 and dW = 0. */
@@ -440,7 +441,8 @@ gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
  *   C = op(A) op(B),  C is M x N (stride ldc),
  *   op(A) = A (M x K, stride lda)  or A^T with A stored K x M (trans_a = 1),
  *   op(B) = B (K x N, stride ldb)  or B^T with B stored N x K (trans_b = 1).
- * flags: GNN_FLAG_BF16.  `workspace` of gnn_gemm_workspace_bytes bytes. */
+ * flags: GNN_FLAG_BF16 or GNN_FLAG_F32_MFMA (neither: split products).
+ * `workspace` of gnn_gemm_workspace_bytes bytes. */
 size_t gnn_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
                     int32_t K, const float* A, int64_t lda, const float* B,
