@@ -97,6 +97,12 @@ def test_gat_bf16_mode():
     check(g, r, O.GAT_ALPHA, tol=2e-2)
 
 
+def test_gat_f32_mfma_mode():
+    g = GRAPHS["powerlaw"]
+    r = run_gat(g, 64, 48, seed=7, flags=G.GNN_FLAG_F32_MFMA)
+    check(g, r, O.GAT_ALPHA)
+
+
 def test_gat_zero_nodes():
     """An empty subgraph: nothing to write forward, zero dW and da."""
     g = synth.identity_graph(0)

@@ -94,6 +94,15 @@ def test_classifier_bf16_mode():
         assert maxrel(r[k], ref[k]) <= 2e-2, k
 
 
+def test_classifier_f32_mfma_mode():
+    x, w, t = _head_case(2000, 512, 41, False, seed=10)
+    r = run_head(x, w, t, G.GNN_LOSS_SOFTMAX, flags=G.GNN_FLAG_F32_MFMA)
+    ref = O.classifier(x, w, t, G.GNN_LOSS_SOFTMAX, relu_on=r["xm"] > 0)
+    assert abs(r["loss"] - ref["loss"]) <= TOL * ref["loss"]
+    for k in ("probs", "dW", "dX"):
+        assert maxrel(r[k], ref[k]) <= TOL, k
+
+
 def test_classifier_optional_outputs_and_empty():
     x, w, t = _head_case(200, 40, 17, True, seed=2)
     r = run_head(x, w, t, G.GNN_LOSS_SIGMOID, want_probs=False, want_dx=False)

@@ -101,6 +101,16 @@ def test_gcn_bf16_mode():
         assert maxrel(r[k], ref[k]) <= 2e-2, k
 
 
+def test_gcn_f32_mfma_mode():
+    """GNN_FLAG_F32_MFMA: the fp32 matrix-core products, fp32 tolerance."""
+    g = GRAPHS["powerlaw"]
+    r = run_gcn(g, 64, 48, 2, True, flags=G.GNN_FLAG_F32_MFMA)
+    assert maxrel(r["Y"], O.gcn_fwd(g, r["x"], r["w"], r["b"])) <= TOL
+    ref = O.gcn_bwd(g, r["x"], r["w"], r["Y"], r["dy"], want_db=True)
+    for k in ("dX", "dW", "db"):
+        assert maxrel(r[k], ref[k]) <= TOL, k
+
+
 def run_mixhop(g, K, f_in, h, bias, seed=0, pad=8, want_dx=True, flags=0):
     dg = prepared(g)
     c = dg.struct()
@@ -136,6 +146,15 @@ def test_mixhop_layer_parity(name, K):
     ref = O.mixhop_bwd(g, r["x"], r["w"], K, r["Y"], r["dy"], want_db=bias)
     for k in ("dX", "dW") + (("db",) if bias else ()):
         assert maxrel(r[k], ref[k]) <= TOL, (k, K)
+
+
+def test_mixhop_f32_mfma_mode():
+    g = GRAPHS["powerlaw"]
+    r = run_mixhop(g, 2, 36, 20, True, seed=4, flags=G.GNN_FLAG_F32_MFMA)
+    assert maxrel(r["Y"], O.mixhop_fwd(g, r["x"], r["w"], 2, r["b"])) <= TOL
+    ref = O.mixhop_bwd(g, r["x"], r["w"], 2, r["Y"], r["dy"], want_db=True)
+    for k in ("dX", "dW", "db"):
+        assert maxrel(r[k], ref[k]) <= TOL, k
 
 
 def test_mixhop_without_dx_and_unaligned_widths():
