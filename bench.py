@@ -72,6 +72,9 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--skip-input-grad", action="store_true",
                     help="do not compute the first layer's input gradient")
+    ap.add_argument("--fuse-masks", action="store_true",
+                    help="layers above the first write their dX already masked "
+                         "(the layer below skips its masking pass)")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the step replayed from a HIP graph")
     ap.add_argument("--no-variants", action="store_true",
@@ -125,7 +128,7 @@ def main():
 
     pad = 16
     dg = runtime.DeviceGraph(g)
-    st = runtime.SageStack(dg, params, wl.f_in, pad=pad)
+    st = runtime.SageStack(dg, params, wl.f_in, pad=pad, fuse_masks=args.fuse_masks)
     ld_x = (wl.f_in + pad - 1) // pad * pad
     X = runtime.padded(torch.from_numpy(x).cuda(), ld_x)
     dY = torch.from_numpy(dy).cuda()
