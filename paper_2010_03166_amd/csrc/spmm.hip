@@ -6,7 +6,8 @@
 // Aggregation design.  Row v of A_s . X is the weighted sum of the input
 // rows of v's neighbours.  The stored entries are cut into windows of
 // BLOCK_ENTRIES; workgroup i owns the rows whose first entry lies in window
-// i, i.e. a run of whole rows, so no row is shared between workgroups.  Its
+// i (in windows 2i and 2i + 1 for large launches), i.e. a run of whole rows,
+// so no row is shared between workgroups.  Its
 // entry range is split evenly over its groups of G lanes; a group streams
 // its entries (whatever their rows) with G-wide coalesced loads of index,
 // value and row, then gathers the neighbour rows' feature columns as float4
@@ -333,12 +334,14 @@ struct SpmmArgs {
   int64_t ld_mask;
   int32_t nslices;  // column slices: 1, or a multiple of 8
   int32_t sw;       // slice width in columns
-  int32_t nwin;     // entry windows of the plan
+  int32_t nwin;     // workgroups per slice: plan windows / wpb, rounded up
+  int32_t wpb;      // consecutive plan windows per workgroup (1 or 2)
+  int32_t nblk;     // plan windows
 };
 
 // Column slices.  Blocks are dispatched round-robin over the 8 XCDs, so with
 // S = 8 P slices, block b = p (8 nwin) + 8 win + x works on slice 8 p + x of
-// window win: XCD x gathers only from slices x, x + 8, ..., one pass after
+// window (group) win: XCD x gathers only from slices x, x + 8, ..., one pass after
 // the other, and each n x sw slice is sized to stay in that XCD's L2 (the
 // cache-sized feature partitions of Theorem 2 / Algorithm 7).
 //
@@ -438,8 +441,12 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
     slice = 8 * (int)(blockIdx.x / per) + (r & 7);
     win = r >> 3;
   }
-  const int4 bi = a.binfo[win];
-  const int r_lo = bi.x, r_hi = bi.y, B = bi.z, E = bi.w;
+  // Consecutive windows own consecutive rows and entries (an empty window
+  // inside a hub row starts and ends where the next row starts), so
+  // windows k .. k + wpb - 1 together are one run of whole rows.
+  const int k0 = win * a.wpb, k1 = min(k0 + a.wpb, a.nblk) - 1;
+  const int4 bi0 = a.binfo[k0], bi1 = a.binfo[k1];
+  const int r_lo = bi0.x, r_hi = bi1.y, B = bi0.z, E = bi1.w;
   const int gi = threadIdx.x / G, lane = threadIdx.x % G;
   const int gb = B + (int)((int64_t)(E - B) * gi / NG);
   const int ge = B + (int)((int64_t)(E - B) * (gi + 1) / NG);
@@ -606,7 +613,7 @@ static double spmm_bytes(int32_t n, int64_t nnz, int32_t w) {
 template <int G, bool VEC, int EPI, bool RAG>
 static void spmm_go(const SpmmArgs& a, const PlanDims& d, bool off32,
                     hipStream_t s) {
-  const unsigned grid = (unsigned)(d.nblk * a.nslices);
+  const unsigned grid = (unsigned)((int64_t)a.nwin * a.nslices);
   if (off32)
     spmm_kernel<G, SPMM_DEPTH, VEC, EPI, true, RAG><<<grid, 256, 0, s>>>(a);
   else
@@ -670,7 +677,6 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   // 16 lanes with over a quarter of them idle (602 columns: 76-column
   // slices on 32 lanes), 16 slices on 16-lane groups are faster, having
   // twice the groups, and so the gathers, in flight per block.
-  a.nwin = (int32_t)d.nblk;
   a.nslices = c.w >= 32 ? 8 : 1;
   a.sw = (int32_t)round_up(ceil_div(c.w, a.nslices), 4);
   if (a.nslices == 8 && a.sw > 64) {
@@ -682,6 +688,14 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
       a.sw = (int32_t)round_up(ceil_div(c.w, a.nslices), 4);
     }
   }
+  // Two windows per workgroup once the grid would pass 16,384 workgroups:
+  // each workgroup pays a chain of dependent loads (window record, entry
+  // metadata, first gathers) before its gathers stream, which a longer entry
+  // range amortises (50,000 nodes x 256 columns: 213 -> 175 us; 20,000 x
+  // 200: 80 -> 77 us); smaller launches keep one (8,000 x 512: even).
+  a.nblk = (int32_t)d.nblk;
+  a.wpb = d.nblk * a.nslices > 16384 ? 2 : 1;
+  a.nwin = (int32_t)ceil_div(d.nblk, (int64_t)a.wpb);
   // float4 lanes whenever rows start 16-byte aligned (the ragged end of a
   // width that is not a multiple of 4 is read and written per component)
   const bool vec = vec4_ok(c.in, c.ld_in) &&

@@ -182,6 +182,24 @@ def test_spmm_parity(name, w, transpose, layout):
     assert maxrel(out, ref) <= TOL_SPMM
 
 
+@pytest.mark.parametrize("w", [40, 200, 256])
+@pytest.mark.parametrize("transpose", [0, 1])
+def test_spmm_two_windows_per_workgroup(w, transpose):
+    """Launches of more than 16,384 workgroups give each workgroup two
+    consecutive plan windows: the 20,000-node workload graph (about 620 k
+    entries, 2,400 windows, 8 column slices), hubs spanning several windows,
+    checked against the oracle."""
+    g = synth.workload_graph(synth.WORKLOADS["cl2.1-n20000-f200-h512-L5"])
+    dg = prepared(g)
+    assert -(-g.nnz // 256) * 8 > 16384
+    x = np.random.default_rng(w + transpose).standard_normal((g.n, w)).astype(np.float32)
+    xin, out = to_dev(x, w), empty_out(g.n, w, w)
+    G.gnn_spmm(dg.struct(), transpose, w, xin, w, out, w, None)
+    torch.cuda.synchronize()
+    ref = O.spmm_transpose(g, x) if transpose else O.spmm(g, x)
+    assert maxrel(out, ref) <= TOL_SPMM
+
+
 def test_spmm_empty_graph_and_empty_rows():
     g = synth.symmetric_csr(6, np.array([[0, 1]]), self_loops=False)
     dg = prepared(g)
