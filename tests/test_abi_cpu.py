@@ -173,6 +173,27 @@ def test_prepare_and_gat_argument_errors(lib):
     assert int(L.gnn_gat_workspace_bytes(ctypes.byref(c), ctypes.byref(bad))) == 0
 
 
+def test_both_product_flags_rejected_everywhere(lib):
+    """GNN_FLAG_BF16 | GNN_FLAG_F32_MFMA is not a mode: every entry point with
+    GEMM products refuses it before touching its (fake) pointers."""
+    L = G.lib()
+    P = ctypes.c_void_p
+    c = _fake_csr()
+    both = G.GNN_FLAG_BF16 | G.GNN_FLAG_F32_MFMA
+    lay = G.make_layer(8, 4, 8, 8, 8, flags=both)
+    ws = 1 << 30
+    assert L.gnn_gcn_fwd(ctypes.byref(c), ctypes.byref(lay), P(0x10), P(0x20), None,
+                         P(0x30), P(0x40), P(0x50), ws, None) == -4
+    ml = G.make_layer(8, 4, 8, 12, 8, flags=both)  # (K + 1) h = 12 columns
+    assert L.gnn_mixhop_fwd(ctypes.byref(c), ctypes.byref(ml), 2, P(0x10), P(0x20), None,
+                            P(0x30), P(0x40), P(0x50), ws, None) == -4
+    gl = G.make_layer(8, 4, 8, 4, 8, flags=both)
+    assert L.gnn_gat_fwd(ctypes.byref(c), ctypes.byref(gl), P(0x10), P(0x20), P(0x30),
+                         ctypes.c_float(0.2), P(0x40), None, P(0x50), P(0x60), ws, None) == -4
+    assert L.gnn_classifier(16, 8, 4, G.GNN_LOSS_SOFTMAX, both, P(0x10), 8, P(0x20), P(0x30), 4,
+                            None, 4, None, 4, P(0x40), P(0x50), None, 8, P(0x60), ws, None) == -4
+
+
 def test_empty_problems_need_no_launch(lib):
     L = G.lib()
     P = ctypes.c_void_p
