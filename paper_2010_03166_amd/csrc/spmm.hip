@@ -228,12 +228,40 @@ __global__ __launch_bounds__(256) void prepare_kernel(
     }
     return lo;
   };
-  __shared__ int bounds[2];
   const int64_t j0 = (int64_t)(blockIdx.x - nrow_blocks) * 256;
   const int64_t j1 = min<int64_t>(j0 + 256, nnz) - 1;
+  // Rows of the block's first and last entry by a 128-way search each
+  // (threads 0-127 for j0, 128-255 for j1): every round probes 128 evenly
+  // spaced row starts at once and keeps the chunk holding the answer, so
+  // the chain of dependent loads is log_128 n long instead of log_2 n.
+  __shared__ int cnt[2], lo_s[2], hi_s[2];
+  const int half = threadIdx.x >> 7, t = threadIdx.x & 127;
+  const int jj = (int)(half ? j1 : j0);
+  int rounds = 0;
+  for (int64_t sz = n; sz > 1; sz = (sz + 127) / 128) ++rounds;
+  if (t == 0) {
+    lo_s[half] = 0;
+    hi_s[half] = n - 1;
+  }
+  for (int rd = 0; rd < rounds; ++rd) {
+    if (t == 0) cnt[half] = 0;
+    __syncthreads();
+    const int lo = lo_s[half], hi = hi_s[half];
+    const int c = (hi - lo + 128) / 128;  // chunk: ceil((hi - lo + 1) / 128)
+    const int pos = lo + t * c;
+    if (pos <= hi && indptr[pos] <= jj) atomicAdd(&cnt[half], 1);
+    __syncthreads();
+    if (t == 0) {
+      const int T = cnt[half];  // >= 1: indptr[lo] <= jj always holds
+      lo_s[half] = lo + (T - 1) * c;
+      hi_s[half] = min(hi, lo + T * c - 1);
+    }
+  }
+  __syncthreads();
+  __shared__ int bounds[2];
   if (threadIdx.x == 0) {
-    bounds[0] = row_of((int)j0, 0, n - 1);
-    bounds[1] = row_of((int)j1, bounds[0], n - 1);
+    bounds[0] = lo_s[0];
+    bounds[1] = lo_s[1];
   }
   __syncthreads();
   const int64_t j = j0 + threadIdx.x;
