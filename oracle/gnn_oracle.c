@@ -88,26 +88,33 @@ void oracle_spmm_transpose(int32_t n, const int32_t* indptr,
   }
 }
 
-/* Algorithm 6 (Section 5.2).  Walk rows v in order; the value of stored
- * entry (v,u) is appended to row u of the transposed data array at that
- * row's cursor.  With ascending indices, the entries of row u of the
- * transpose arrive in ascending v, i.e. in the order row u stores them. */
+/* Transposed values on the pattern of A_s (Section 5.2): the transpose
+ * holds A_s[v,u] at position (u,v), so each stored entry k = (u,v) of row u
+ * takes the value stored at (v,u), which a plain scan of row v finds.  This
+ * is the defining property itself; Algorithm 6 produces the same array in
+ * one pass.  Returns -1 if some (v,u) is not stored (the pattern is not
+ * symmetric and the transpose does not fit it). */
 int32_t oracle_transpose_values(int32_t n, const int32_t* indptr,
                                 const int32_t* indices, const double* values,
                                 double* values_t) {
-  int32_t* cursor = (int32_t*)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
-  if (!cursor) return -1;
-  for (int32_t u = 0; u < n; ++u) cursor[u] = indptr[u];
   int32_t status = 0;
-  for (int32_t v = 0; v < n && status == 0; ++v) {
-    for (int32_t j = indptr[v]; j < indptr[v + 1]; ++j) { /* half-open */
-      const int32_t u = indices[j];
-      if (cursor[u] >= indptr[u + 1]) { status = -1; break; }
-      values_t[cursor[u]] = values[j];
-      cursor[u] += 1;
+#pragma omp parallel for schedule(dynamic, 64) reduction(min : status)
+  for (int32_t u = 0; u < n; ++u) {
+    for (int32_t k = indptr[u]; k < indptr[u + 1]; ++k) {
+      const int32_t v = indices[k];
+      int32_t at = -1;
+      for (int32_t j = indptr[v]; j < indptr[v + 1]; ++j)
+        if (indices[j] == u) {
+          at = j;
+          break;
+        }
+      if (at < 0) {
+        status = -1;
+        continue;
+      }
+      values_t[k] = values[at];
     }
   }
-  free(cursor);
   return status;
 }
 

@@ -39,10 +39,10 @@ void oracle_spmm_transpose(int32_t n, const int32_t* indptr,
                            const int32_t* indices, const double* values,
                            int32_t w, const double* in, double* out);
 
-/* Section 5.2, Algorithm 6: values of (A_s)^T on the same indptr/indices,
- * by one pass with per-row append cursors.  Requires a symmetric pattern and
- * ascending indices within each row.  Returns 0, or -1 if a cursor would run
- * past its row (pattern not symmetric). */
+/* Section 5.2: values of (A_s)^T on the same indptr/indices (the array
+ * Algorithm 6 builds), written from its definition: entry (u,v) takes the
+ * value stored at (v,u).  Requires a symmetric pattern.  Returns 0, or -1
+ * if some (v,u) has no stored (u,v) counterpart. */
 int32_t oracle_transpose_values(int32_t n, const int32_t* indptr,
                                 const int32_t* indices, const double* values,
                                 double* values_t);
