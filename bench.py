@@ -77,6 +77,8 @@ def parse():
                          "(the layer below skips its masking pass)")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the step replayed from a HIP graph")
+    ap.add_argument("--no-rownorm", action="store_true",
+                    help="skip the step with GNN_FLAG_ROW_NORMALIZED")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the GCN and MixHop layer timings")
     ap.add_argument("--no-train", action="store_true",
@@ -276,6 +278,16 @@ def main():
             PEAK_TFLOPS["bf16"])
         log("bf16 variant: %.4f ms per step" % out["bf16_variant"]["ms_per_step"])
 
+    # the same step with A_s = D^-1 A taken from the pattern alone
+    # (GNN_FLAG_ROW_NORMALIZED: the aggregations read no value arrays)
+    if not args.no_rownorm:
+        out["row_normalized_variant"] = bench_mode(
+            G, runtime, torch, dg, params, wl, X, dY, args, want_dx_first, pad,
+            G.GNN_FLAG_ROW_NORMALIZED, "f32; A_s = D^-1 A from the row pointers "
+            "(GNN_FLAG_ROW_NORMALIZED), split products", PEAK_SPLIT)
+        log("row-normalized variant: %.4f ms per step" %
+            out["row_normalized_variant"]["ms_per_step"])
+
     # the GCN and MixHop layers (Section 2.1) on the same subgraph with the
     # symmetric normalisation, one layer each, forward + backward with dX
     if not args.no_variants:
@@ -345,6 +357,8 @@ def bench_mode(G, runtime, torch, dg, params, wl, X, dY, args, want_dx_first, pa
                          "avg_launch_us": round(1e3 * kms / launches, 2)}
             if kname.startswith("gemm_") and kname != "gemm_reduce":
                 kb[kname]["tflops"] = round(work / launches / (1e6 * kb[kname]["avg_launch_us"]), 1)
+            if kname == "spmm":
+                kb[kname]["gbs"] = round(work / launches / (1e3 * kb[kname]["avg_launch_us"]), 1)
     G.gnn_timer_reset()
     gb = [k for k in kb if "tflops" in kb[k]]
     dom = max(gb, key=lambda k: kb[k]["ms_per_step"])

@@ -70,6 +70,18 @@ typedef enum gnn_status {
                               even), fp32 accumulation; aggregation stays fp32 */
 #define GNN_FLAG_F32_MFMA 0x8u /* GEMM products on the fp32 matrix-core
                                   instruction (v_mfma_f32_32x32x2_f32) */
+/* GraphSAGE layers only (gnn_prop_fwd / gnn_prop_bwd).  Section 2.1 defines
+ * the layer's A_s as D^-1 A, D the diagonal of A's row sums; with this flag
+ * the aggregations take A_s from the pattern alone, A the 0/1 matrix of the
+ * stored entries (self loops as stored) and deg(v) = indptr[v+1] - indptr[v]:
+ * the forward sums each row's neighbour rows unweighted and scales the sum
+ * by 1/deg(v), the transposed aggregation weighs entry (u, v) by 1/deg(v)
+ * (the value (A_s)^T holds there when the pattern is symmetric, as the
+ * backward pass requires anyway).  csr->values and csr->values_t are then
+ * not read and may be NULL.  Results equal those of the same call with
+ * values = 1/deg in float (values_t from gnn_csr_transpose_values) up to
+ * rounding: the forward rounds the sum before the scaling. */
+#define GNN_FLAG_ROW_NORMALIZED 0x10u
 /* Backward pass only (Algorithm 1's layer loop, backward direction): the
  * layers of a stack share their ReLU masks.  Layer l's input X is layer
  * l-1's output, so 1[X > 0] is layer l-1's mask and can be applied where

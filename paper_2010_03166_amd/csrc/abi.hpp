@@ -34,15 +34,19 @@ inline gnn_status check_csr(const gnn_csr* c, bool need_vals, bool need_vals_t) 
   return GNN_OK;
 }
 
+// rownorm: A_s = D^-1 A taken from the pattern alone (GNN_FLAG_ROW_NORMALIZED);
+// the value arrays are then not read.
 inline SpmmCall spmm_call(const gnn_csr* c, bool transpose, int32_t w,
-                   const float* in, int64_t ld_in, float* out, int64_t ld_out) {
+                   const float* in, int64_t ld_in, float* out, int64_t ld_out,
+                   bool rownorm = false) {
   SpmmCall s;
   memset(&s, 0, sizeof(s));
   s.n = c->n;
   s.nnz = c->nnz;
   s.indptr = c->indptr;
   s.indices = c->indices;
-  s.vals = transpose ? c->values_t : c->values;
+  s.vals = rownorm ? nullptr : transpose ? c->values_t : c->values;
+  s.weights = !rownorm ? SPMM_W_VALUES : transpose ? SPMM_W_COL_DEG : SPMM_W_ROW_SCALE;
   s.plan = c->plan;
   s.w = w;
   s.in = in;

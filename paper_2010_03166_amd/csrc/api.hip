@@ -195,7 +195,8 @@ gnn_status check_layer(const gnn_layer* L) {
   if (L->f_in <= 0 || L->h <= 0) return GNN_ERR_SHAPE;
   if (L->ld_x < L->f_in || L->ld_y < 2 * (int64_t)L->h) return GNN_ERR_SHAPE;
   if (L->order < 0 || L->order > 2) return GNN_ERR_SHAPE;
-  if ((L->flags & ~(GEMM_FLAGS | GNN_FLAG_DY_MASKED | GNN_FLAG_DX_MASKED)) ||
+  if ((L->flags & ~(GEMM_FLAGS | GNN_FLAG_DY_MASKED | GNN_FLAG_DX_MASKED |
+                    GNN_FLAG_ROW_NORMALIZED)) ||
       !gemm_flags_ok(L->flags))
     return GNN_ERR_UNSUPPORTED;
   return GNN_OK;
@@ -411,9 +412,10 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
                         const float* b_neigh, float* Y, void* saved,
                         void* workspace, size_t workspace_bytes,
                         hipStream_t stream) {
-  gnn_status st = check_csr(csr, true, false);
+  gnn_status st = check_layer(layer);
   if (st != GNN_OK) return st;
-  if ((st = check_layer(layer)) != GNN_OK) return st;
+  const bool rn = (layer->flags & GNN_FLAG_ROW_NORMALIZED) != 0;
+  if ((st = check_csr(csr, !rn, false)) != GNN_OK) return st;
   const int32_t n = csr->n, f_in = layer->f_in, h = layer->h;
   if (n > 0 && (!X || !Y || !csr->plan)) return GNN_ERR_NULL;
   if (!W_self || !W_neigh) return GNN_ERR_NULL;
@@ -433,7 +435,7 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
   const size_t gws_bytes = o.off_cs - o.off_gemm;
   if (o.order == 1) {
     float* S = static_cast<float*>(saved);
-    SpmmCall c = spmm_call(csr, false, f_in, X, layer->ld_x, S, o.ld_s);
+    SpmmCall c = spmm_call(csr, false, f_in, X, layer->ld_x, S, o.ld_s, rn);
     GNN_HIP(spmm_launch(c, stream));
     GemmBatch b = fwd_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, W_self,
                             W_neigh, b_self, b_neigh, Y, layer->ld_y, nullptr, 0);
@@ -445,7 +447,7 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
                             W_neigh, b_self, nullptr, Y, layer->ld_y, P, o.ld_p);
     b.mode = gemm_mode(layer->flags);
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
-    SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y);
+    SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y, rn);
     c.epilogue = SPMM_BIAS_RELU;
     c.bias = b_neigh;
     GNN_HIP(spmm_launch(c, stream));
@@ -460,9 +462,10 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
                         float* dW_neigh, float* db_self, float* db_neigh,
                         void* workspace, size_t workspace_bytes,
                         hipStream_t stream) {
-  gnn_status st = check_csr(csr, true, true);
+  gnn_status st = check_layer(layer);
   if (st != GNN_OK) return st;
-  if ((st = check_layer(layer)) != GNN_OK) return st;
+  const bool rn = (layer->flags & GNN_FLAG_ROW_NORMALIZED) != 0;
+  if ((st = check_csr(csr, !rn, !rn)) != GNN_OK) return st;
   const int32_t n = csr->n, f_in = layer->f_in, h = layer->h;
   if (!W_self || !W_neigh || !dW_self || !dW_neigh) return GNN_ERR_NULL;
   if (n > 0 && (!X || !Y || !dY || !csr->plan)) return GNN_ERR_NULL;
@@ -521,7 +524,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       T = GT + h;
       ld_t = o.ld_g;
     }
-    SpmmCall c = spmm_call(csr, true, h, Gn, ld_gn, T, ld_t);
+    SpmmCall c = spmm_call(csr, true, h, Gn, ld_gn, T, ld_t, rn);
     GNN_HIP(spmm_launch(c, stream));
     GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, Gs,
                             ld_gs, T, ld_t, dW_self, dW_neigh);
@@ -561,7 +564,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       bx.mode = bf;
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
       // dX = G_s W_s^T + A_s^T V, then the mask, in the aggregation epilogue
-      SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx);
+      SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx, rn);
       c.epilogue = SPMM_ADD;
       c.res = dX;
       c.ld_res = layer->ld_dx;

@@ -66,6 +66,16 @@ enum SpmmEpilogue : int32_t {
   SPMM_ADD = 2,        // out = acc + res[row, c]         (res may alias out)
 };                     // with `mask` set: out = mask[row, c] > 0 ? out : 0
 
+// Where the weight of a stored entry comes from:
+//   SPMM_W_VALUES    the value array (vals);
+//   SPMM_W_ROW_SCALE A = D^-1 B with B the 0/1 pattern: the entries of a row
+//                    are summed unweighted and the sum is scaled by 1/deg of
+//                    that row (deg = its stored entries) when the row is
+//                    written; vals is not read;
+//   SPMM_W_COL_DEG   (D^-1 B)^T on a symmetric pattern: entry (u, v) weighs
+//                    1/deg(v), taken from the row pointers; vals is not read.
+enum SpmmWeights : int32_t { SPMM_W_VALUES = 0, SPMM_W_ROW_SCALE = 1, SPMM_W_COL_DEG = 2 };
+
 struct SpmmCall {
   int32_t n;
   int64_t nnz;
@@ -84,6 +94,7 @@ struct SpmmCall {
   int64_t ld_res;
   const float* mask;
   int64_t ld_mask;
+  int32_t weights;  // SpmmWeights
 };
 size_t spmm_partials_bytes(int32_t n, int64_t nnz, int32_t w);
 hipError_t spmm_launch(const SpmmCall& c, hipStream_t s);

@@ -365,6 +365,7 @@ struct SpmmArgs {
   int32_t nwin;     // workgroups per slice: plan windows / wpb, rounded up
   int32_t wpb;      // consecutive plan windows per workgroup (1 or 2)
   int32_t nblk;     // plan windows
+  int32_t weights;  // SpmmWeights
 };
 
 // Column slices.  Blocks are dispatched round-robin over the 8 XCDs, so with
@@ -406,6 +407,12 @@ struct Vec<true> {
     acc.z += x.z;
     acc.w += x.w;
   }
+  __device__ static void scale(T& acc, float s) {
+    acc.x *= s;
+    acc.y *= s;
+    acc.z *= s;
+    acc.w *= s;
+  }
   __device__ static T relu(T v) {
     v.x = fmaxf(v.x, 0.f);
     v.y = fmaxf(v.y, 0.f);
@@ -445,6 +452,7 @@ struct Vec<false> {
   __device__ static void store(float* p, T v) { *p = v; }
   __device__ static void fma(T& acc, float a, T x) { acc = fmaf(a, x, acc); }
   __device__ static void add(T& acc, T x) { acc += x; }
+  __device__ static void scale(T& acc, float s) { acc *= s; }
   __device__ static T relu(T v) { return fmaxf(v, 0.f); }
   __device__ static T select_pos(T m, T v) { return m > 0.f ? v : 0.f; }
   __device__ static T load_part(const float* p, int) { return *p; }
@@ -485,6 +493,15 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
   const int32_t* __restrict__ erow = a.erow;
   const float* __restrict__ vals = a.vals;
   const uint32_t ld_in = (uint32_t)a.ld_in;
+  const int32_t* __restrict__ indptr = a.indptr;
+  const int wmode = a.weights;
+  // weight of stored entry j (column idx); see SpmmWeights
+  auto weight = [&](int j, int idx) -> float {
+    if (wmode == SPMM_W_VALUES) return vals[j];
+    if (wmode == SPMM_W_ROW_SCALE) return 1.f;
+    const int d = indptr[idx + 1] - indptr[idx];
+    return d > 0 ? 1.f / (float)d : 0.f;
+  };
 
   // rows of the entries just outside this group's range (-1: none)
   int prev_row = -1, next_row = -1;
@@ -502,6 +519,8 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
     auto ld = [&](const float* p) { return part ? V::load_part(p, nv) : V::load(p); };
     auto finish = [&](int row, T acc) {
       if (!ok) return;
+      if (wmode == SPMM_W_ROW_SCALE)  // a row with entries: deg >= 1
+        V::scale(acc, 1.f / (float)(indptr[row + 1] - indptr[row]));
       if (EPI == SPMM_BIAS_RELU) {
         if (a.bias) V::add(acc, ld(a.bias + col));
         acc = V::relu(acc);
@@ -540,7 +559,7 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
       float nv = 0.f;
       if (lane < ge - gb) {
         ni = indices[gb + lane];
-        nv = vals[gb + lane];
+        nv = weight(gb + lane, ni);
         nr = erow[gb + lane];
       }
       for (int jb = gb; jb < ge; jb += G) {
@@ -551,7 +570,7 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
           const int j2 = jb + G + lane;
           const bool in_r = j2 < ge;
           ni = in_r ? indices[j2] : 0;
-          nv = in_r ? vals[j2] : 0.f;
+          nv = in_r ? weight(j2, ni) : 0.f;
           nr = in_r ? erow[j2] : 0;
         }
         for (int k = 0; k < cnt; k += D) {
@@ -700,6 +719,7 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   a.ld_res = c.ld_res;
   a.mask = c.mask;
   a.ld_mask = c.ld_mask;
+  a.weights = c.weights;
   // 8 slices (one per XCD) from 32 columns up.  A lane group covers a
   // power of two of float4 columns; when 8 slices need groups of more than
   // 16 lanes with over a quarter of them idle (602 columns: 76-column

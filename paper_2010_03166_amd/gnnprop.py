@@ -23,6 +23,7 @@ GNN_FLAG_BF16 = 0x1
 GNN_FLAG_DY_MASKED = 0x2
 GNN_FLAG_DX_MASKED = 0x4
 GNN_FLAG_F32_MFMA = 0x8
+GNN_FLAG_ROW_NORMALIZED = 0x10
 GNN_LOSS_SOFTMAX = 0
 GNN_LOSS_SIGMOID = 1
 KERNELS = {"spmm": 0, "spmm_reduce": 1, "gemm_nn": 2, "gemm_tn": 3,

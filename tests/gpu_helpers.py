@@ -69,3 +69,23 @@ def sample_rows(n, k, seed, must=()):
     rng = np.random.default_rng(seed)
     rows = list(must) + list(rng.choice(n, size=min(k, n), replace=False))
     return np.array(sorted(set(int(r) for r in rows if 0 <= r < n)), np.int64)
+
+
+def decision_flips(gpu_act, ref_act, bound=1e-4) -> int:
+    """Activation decisions (value > 0: a ReLU or LeakyReLU passes its input
+    unscaled) that the GPU took differently from the oracle's own forward
+    pass.  Asserts that every such decision lies at the kink, i.e. that both
+    activation values there are within bound * max|ref| of 0 (so rounding
+    alone decided it), and returns how many there were."""
+    if isinstance(gpu_act, torch.Tensor):
+        gpu_act = gpu_act.detach().cpu().numpy()
+    g = np.asarray(gpu_act, np.float64)
+    r = np.asarray(ref_act, np.float64)
+    assert g.shape == r.shape, (g.shape, r.shape)
+    flip = (g > 0) != (r > 0)
+    count = int(flip.sum())
+    if count:
+        lim = bound * max(float(np.abs(r).max()), 1e-300)
+        worst = float(np.maximum(np.abs(g[flip]), np.abs(r[flip])).max())
+        assert worst <= lim, ("decision far from the kink", count, worst, lim)
+    return count

@@ -194,6 +194,38 @@ def test_both_product_flags_rejected_everywhere(lib):
                             None, 4, None, 4, P(0x40), P(0x50), None, 8, P(0x60), ws, None) == -4
 
 
+def test_row_normalized_flag_arguments(lib):
+    """GNN_FLAG_ROW_NORMALIZED: the GraphSAGE layer needs no value arrays
+    (the checks pass NULL values / values_t and stop at the workspace size
+    instead); the other layers refuse the flag."""
+    L = G.lib()
+    P = ctypes.c_void_p
+    rn = G.GNN_FLAG_ROW_NORMALIZED
+    nov = G.make_csr(10, 30, 0x1000, 0x2000, None, None, 0x5000)
+    lay = G.make_layer(8, 4, 8, 8, 8, flags=rn)
+    plain = G.make_layer(8, 4, 8, 8, 8)
+    assert L.gnn_prop_fwd(ctypes.byref(nov), ctypes.byref(lay), *([P(0x10)] * 8), 16,
+                          None) == -5
+    assert L.gnn_prop_bwd(ctypes.byref(nov), ctypes.byref(lay), *([P(0x10)] * 12), 16,
+                          None) == -5
+    assert L.gnn_prop_fwd(ctypes.byref(nov), ctypes.byref(plain), *([P(0x10)] * 8), 16,
+                          None) == -1
+    assert L.gnn_prop_bwd(ctypes.byref(nov), ctypes.byref(plain), *([P(0x10)] * 12), 16,
+                          None) == -1
+    c = _fake_csr()
+    ws = 1 << 30
+    assert L.gnn_gcn_fwd(ctypes.byref(c), ctypes.byref(lay), P(0x10), P(0x20), None,
+                         P(0x30), P(0x40), P(0x50), ws, None) == -4
+    ml = G.make_layer(8, 4, 8, 12, 8, flags=rn)
+    assert L.gnn_mixhop_fwd(ctypes.byref(c), ctypes.byref(ml), 2, P(0x10), P(0x20), None,
+                            P(0x30), P(0x40), P(0x50), ws, None) == -4
+    gl = G.make_layer(8, 4, 8, 4, 8, flags=rn)
+    assert L.gnn_gat_fwd(ctypes.byref(c), ctypes.byref(gl), P(0x10), P(0x20), P(0x30),
+                         ctypes.c_float(0.2), P(0x40), None, P(0x50), P(0x60), ws, None) == -4
+    assert L.gnn_classifier(16, 8, 4, G.GNN_LOSS_SOFTMAX, rn, P(0x10), 8, P(0x20), P(0x30), 4,
+                            None, 4, None, 4, P(0x40), P(0x50), None, 8, P(0x60), ws, None) == -4
+
+
 def test_empty_problems_need_no_launch(lib):
     L = G.lib()
     P = ctypes.c_void_p

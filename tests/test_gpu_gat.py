@@ -1,10 +1,13 @@
 """GAT layer on the GPU against the CPU oracle (through the C ABI).
 
 Forward: Y and the attention values against the oracle's.  Backward:
-teacher-forced, the oracle gets the GPU's fp32 Y (its ReLU mask) and the
-sign of the GPU's attention values (its LeakyReLU decisions), so both sides
-take the same decisions; then dX, dW, da to max-normalised 1e-4 in fp32,
-2e-2 with bf16 products.
+teacher-forced so that both sides take the same decisions: the GPU backward
+receives the oracle's forward output Y (rounded to fp32) as its ReLU mask,
+and the oracle's backward the sign of the GPU's attention values (its
+LeakyReLU decisions, kept in the GPU's saved state); every ReLU and
+LeakyReLU decision of the GPU's forward that differs from the oracle's own
+must lie at the kink (gpu_helpers.decision_flips).  Then dX, dW, da to
+max-normalised 1e-4 in fp32, 2e-2 with bf16 products.
 """
 import numpy as np
 import pytest
@@ -14,7 +17,7 @@ from oracle import oracle as O
 from paper_2010_03166_amd import gnnprop as G
 from paper_2010_03166_amd import synth
 
-from gpu_helpers import maxrel, prepared, to_dev
+from gpu_helpers import decision_flips, maxrel, prepared, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -49,21 +52,27 @@ def run_gat(g, f_in, h, alpha=O.GAT_ALPHA, seed=0, pad=8, flags=0, want_dx=True,
     saved = _buf(G.gnn_gat_saved_bytes(c, lay))
     ws = _buf(G.gnn_gat_workspace_bytes(c, lay))
     G.gnn_gat_fwd(c, lay, X, W, A, alpha, Y, att, saved, ws)
+    torch.cuda.synchronize()
+    y_gpu, att_gpu = Y.cpu().numpy(), att.cpu().numpy()[: g.nnz]
+    y_ref, att_ref = O.gat_fwd(g, x, w, a, alpha, want_att=True)
+    y32 = y_ref.astype(np.float32)
+    Y.copy_(torch.from_numpy(y32).cuda())  # the oracle's ReLU mask for the backward
     dX = torch.full((g.n, ld_x), float("nan"), device="cuda")[:, :f_in] if want_dx else None
     dW = torch.full((f_in, h), float("nan"), device="cuda")
     da = torch.full((2 * h,), float("nan"), device="cuda")
     G.gnn_gat_bwd(c, lay, X, W, A, alpha, Y, to_dev(dy, ld_y), saved, dX, dW, da, ws)
     torch.cuda.synchronize()
-    return dict(x=x, w=w, a=a, dy=dy, Y=Y.cpu().numpy(), att=att.cpu().numpy()[: g.nnz],
-                dX=None if dX is None else dX.cpu().numpy(), dW=dW.cpu().numpy(),
+    return dict(x=x, w=w, a=a, dy=dy, Y=y_gpu, att=att_gpu, Y_ref=y_ref, att_ref=att_ref,
+                Y32=y32, dX=None if dX is None else dX.cpu().numpy(), dW=dW.cpu().numpy(),
                 da=da.cpu().numpy())
 
 
 def check(g, r, alpha, tol=TOL):
-    y_ref, att_ref = O.gat_fwd(g, r["x"], r["w"], r["a"], alpha, want_att=True)
-    assert maxrel(r["Y"], y_ref) <= tol
-    assert maxrel(r["att"], att_ref) <= tol
-    ref = O.gat_bwd(g, r["x"], r["w"], r["a"], r["Y"], r["dy"], alpha,
+    assert maxrel(r["Y"], r["Y_ref"]) <= tol
+    assert maxrel(r["att"], r["att_ref"]) <= tol
+    decision_flips(r["Y"], r["Y_ref"], tol)
+    decision_flips(r["att"], r["att_ref"], tol)
+    ref = O.gat_bwd(g, r["x"], r["w"], r["a"], r["Y32"], r["dy"], alpha,
                     want_dx=r["dX"] is not None, z_pos=r["att"] > 0)
     for k in ("dW", "da") + (("dX",) if r["dX"] is not None else ()):
         assert maxrel(r[k], ref[k]) <= tol, k

@@ -443,6 +443,90 @@ def test_layer_zero_nodes():
     assert float(st.layers[0]["dW_neigh"].abs().max()) == 0.0
 
 
+# ------------------------------------------- GNN_FLAG_ROW_NORMALIZED
+
+RN = G.GNN_FLAG_ROW_NORMALIZED
+
+
+def run_rn_pair(g, x, p, y32, dy, order, pad=16):
+    """The same layer through the general path (values = fp32(1/deg), the
+    transposed values from the preparation) and with GNN_FLAG_ROW_NORMALIZED,
+    for which the value arrays are overwritten with NaN first (a read of
+    them would show); both backward passes take y32 as Y."""
+    f_in, h = p.w_self.shape
+    outs = {}
+    for rn in (False, True):
+        dg = prepared(g)
+        if rn:
+            torch.cuda.synchronize()
+            dg.values.fill_(float("nan"))
+            dg.values_t.fill_(float("nan"))
+        st = runtime.SageStack(dg, [p], f_in, order=order, pad=pad,
+                               flags=RN if rn else 0)
+        st.forward(to_dev(x, (f_in + pad - 1) // pad * pad))
+        torch.cuda.synchronize()
+        o = {"Y": st.layers[0]["Y"].cpu().numpy().copy()}
+        st.layers[0]["Y"].copy_(torch.from_numpy(y32).cuda())
+        st.backward(to_dev(dy))
+        torch.cuda.synchronize()
+        for k in ("dX", "dW_self", "dW_neigh"):
+            o[k] = st.layers[0][k].cpu().numpy().copy()
+        outs[rn] = o
+        del st
+    return outs
+
+
+RN_GRAPHS = {k: GRAPHS[k] for k in ("powerlaw", "star700", "no_self_loops", "identity",
+                                    "path4", "single")}
+RN_GRAPHS["random_rownorm"] = synth.random_graph(300, 6.0, 1)  # values 1/deg
+
+
+@pytest.mark.parametrize("name", list(RN_GRAPHS))
+@pytest.mark.parametrize("order", [1, 2])
+def test_row_normalized_flag(name, order):
+    """Section 2.1's A_s = D^-1 A taken from the pattern alone: within 1e-5
+    of the general path on every output (forward and backward, both
+    orders; empty rows in no_self_loops), and within 1e-4 of the oracle."""
+    g = RN_GRAPHS[name]
+    assert np.array_equal(g.values, (1.0 / np.repeat(g.degrees(), g.degrees())
+                                     ).astype(np.float32))
+    f_in, h = (24, 40) if order == 1 else (40, 24)
+    rng = np.random.default_rng(order + g.n)
+    x = rng.standard_normal((g.n, f_in)).astype(np.float32)
+    p = synth.LayerParams(synth.glorot(f_in, h, rng), synth.glorot(f_in, h, rng))
+    dy = rng.standard_normal((g.n, 2 * h)).astype(np.float32)
+    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh)
+    y32 = y_ref.astype(np.float32)
+    outs = run_rn_pair(g, x, p, y32, dy, order)
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy)
+    for k in ("Y", "dX", "dW_self", "dW_neigh"):
+        assert maxrel(outs[True][k], outs[False][k]) <= TOL_SPMM, k
+        assert maxrel(outs[True][k], y_ref if k == "Y" else r[k]) <= TOL, k
+
+
+@pytest.mark.parametrize("name,layer", [("cl2.1-n8000-f602-h512-L2", 0),
+                                        ("cl2.1-n8000-f602-h512-L2", 1),
+                                        ("cl2.1-n20000-f200-h512-L5", 0)])
+def test_row_normalized_flag_full_size(name, layer):
+    """The benchmark's layer shapes at full size (8,000 nodes: 602 -> 2 x 512
+    and 1024 -> 2 x 512, order 2; 20,000 nodes: 200 -> 2 x 512, order 1 with
+    two plan windows per workgroup): every element within 1e-5 of the
+    general path."""
+    wl = synth.WORKLOADS[name]
+    g = synth.workload_graph(wl)
+    f_in, h = synth.layer_dims(wl)[layer]
+    rng = np.random.default_rng(77 + layer)
+    x = rng.standard_normal((g.n, f_in)).astype(np.float32)
+    if layer:
+        x = np.maximum(x, 0)
+    p = synth.LayerParams(synth.glorot(f_in, h, rng), synth.glorot(f_in, h, rng))
+    ysyn = np.maximum(rng.standard_normal((g.n, 2 * h)), 0).astype(np.float32)
+    dy = rng.standard_normal((g.n, 2 * h)).astype(np.float32)
+    outs = run_rn_pair(g, x, p, ysyn, dy, 0)
+    for k in ("Y", "dX", "dW_self", "dW_neigh"):
+        assert maxrel(outs[True][k], outs[False][k]) <= TOL_SPMM, k
+
+
 # ------------------------------------------------------ whole stacks, C ABI
 
 @pytest.mark.parametrize("fuse", [True, False])

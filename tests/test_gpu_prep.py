@@ -12,7 +12,7 @@ from oracle import oracle as O
 from paper_2010_03166_amd import gnnprop as G
 from paper_2010_03166_amd import runtime, synth
 
-from gpu_helpers import maxrel, to_dev
+from gpu_helpers import decision_flips, maxrel, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -175,8 +175,16 @@ def test_prepared_subgraph_trains_like_oracle():
     ys = [L["Y"].cpu().numpy() for L in tr.stack.layers]
     xm = tr.xm.cpu().numpy()
     sub.values = sub.values.astype(np.float32).astype(np.float64)
-    assert maxrel(ys[0], O.sage_fwd(sub, X[nodes], params[0].w_self,
-                                    params[0].w_neigh)) <= 1e-4
+    # the forward layer by layer on the GPU's own layer inputs, and every
+    # ReLU decision the oracle is then handed bounded to the kink
+    inp = [X[nodes]] + ys[:-1]
+    for l, p in enumerate(params):
+        y_ref = O.sage_fwd(sub, inp[l], p.w_self, p.w_neigh)
+        assert maxrel(ys[l], y_ref) <= 1e-4, l
+        decision_flips(ys[l], y_ref, 1e-4)
+    xm_ref = np.maximum(O.mm_nn(ys[-1], w_mlp), 0)
+    assert maxrel(xm, xm_ref) <= 1e-4
+    decision_flips(xm, xm_ref, 1e-4)
     ref = O.train_step(sub, X[nodes], params, w_mlp, Y[nodes], G.GNN_LOSS_SOFTMAX, "sgd",
                        lr=0.0, forced={"ys": ys, "relu_on": xm > 0})
     assert abs(float(tr.loss.item()) - ref["loss"]) <= 1e-5 * ref["loss"]

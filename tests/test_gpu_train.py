@@ -7,7 +7,9 @@ relative.  ReLU decisions are the GPU's: a logit or activation that rounding
 puts on the other side of 0 flips a whole gradient entry (for a sigmoid head
 by (1/2 - t)/n), so the oracle takes the GPU's X_MLP sign and layer outputs
 as its decisions (teacher forcing), and the forward values themselves are
-compared separately.  Adam divides by sqrt(v), so its update is likewise
+compared separately.  Every such decision that differs from the one the
+oracle takes on its own must lie at the kink: both values within the
+tolerance times the tensor's maximum of 0 (gpu_helpers.decision_flips).  Adam divides by sqrt(v), so its update is likewise
 checked on the GPU's own gradients.
 """
 import numpy as np
@@ -18,7 +20,7 @@ from oracle import oracle as O
 from paper_2010_03166_amd import gnnprop as G
 from paper_2010_03166_amd import runtime, synth
 
-from gpu_helpers import maxrel, prepared, to_dev
+from gpu_helpers import decision_flips, maxrel, prepared, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -76,7 +78,9 @@ def test_classifier_parity(case):
     kind = G.GNN_LOSS_SIGMOID if multi else G.GNN_LOSS_SOFTMAX
     x, w, t = _head_case(n, f, C, multi, seed=n + C)
     r = run_head(x, w, t, kind)
-    assert maxrel(r["xm"], np.maximum(O.mm_nn(x, w), 0)) <= TOL
+    xm_ref = np.maximum(O.mm_nn(x, w), 0)
+    assert maxrel(r["xm"], xm_ref) <= TOL
+    decision_flips(r["xm"], xm_ref, TOL)
     ref = O.classifier(x, w, t, kind, relu_on=r["xm"] > 0)
     assert abs(r["loss"] - ref["loss"]) <= TOL_LOSS * max(abs(ref["loss"]), 1e-30) or \
         abs(r["loss"] - ref["loss"]) < 1e-7
@@ -87,7 +91,9 @@ def test_classifier_parity(case):
 def test_classifier_bf16_mode():
     x, w, t = _head_case(2000, 512, 41, False, seed=9)
     r = run_head(x, w, t, G.GNN_LOSS_SOFTMAX, flags=G.GNN_FLAG_BF16)
-    assert maxrel(r["xm"], np.maximum(O.mm_nn(x, w), 0)) <= 2e-2
+    xm_ref = np.maximum(O.mm_nn(x, w), 0)
+    assert maxrel(r["xm"], xm_ref) <= 2e-2
+    decision_flips(r["xm"], xm_ref, 2e-2)
     ref = O.classifier(x, w, t, G.GNN_LOSS_SOFTMAX, relu_on=r["xm"] > 0)
     assert abs(r["loss"] - ref["loss"]) <= 2e-2 * ref["loss"]
     for k in ("probs", "dW", "dX"):
@@ -97,6 +103,9 @@ def test_classifier_bf16_mode():
 def test_classifier_f32_mfma_mode():
     x, w, t = _head_case(2000, 512, 41, False, seed=10)
     r = run_head(x, w, t, G.GNN_LOSS_SOFTMAX, flags=G.GNN_FLAG_F32_MFMA)
+    xm_ref = np.maximum(O.mm_nn(x, w), 0)
+    assert maxrel(r["xm"], xm_ref) <= TOL
+    decision_flips(r["xm"], xm_ref, TOL)
     ref = O.classifier(x, w, t, G.GNN_LOSS_SOFTMAX, relu_on=r["xm"] > 0)
     assert abs(r["loss"] - ref["loss"]) <= TOL * ref["loss"]
     for k in ("probs", "dW", "dX"):
@@ -106,6 +115,7 @@ def test_classifier_f32_mfma_mode():
 def test_classifier_optional_outputs_and_empty():
     x, w, t = _head_case(200, 40, 17, True, seed=2)
     r = run_head(x, w, t, G.GNN_LOSS_SIGMOID, want_probs=False, want_dx=False)
+    decision_flips(r["xm"], np.maximum(O.mm_nn(x, w), 0), TOL)
     ref = O.classifier(x, w, t, G.GNN_LOSS_SIGMOID, want_dx=False, relu_on=r["xm"] > 0)
     assert maxrel(r["dW"], ref["dW"]) <= TOL
     assert abs(r["loss"] - ref["loss"]) <= TOL_LOSS * ref["loss"]
@@ -206,11 +216,15 @@ def check_iteration(tr, g, x, t, kind, tol, before=None, rows=None):
         if rows is None:
             ref = O.sage_fwd(g, inp[l], p.w_self, p.w_neigh, p.b_self, p.b_neigh)
             assert maxrel(ys[l], ref) <= tol, ("Y", l)
+            decision_flips(ys[l], ref, tol)
         else:
             ref = O.sage_fwd_rows(g, inp[l], p.w_self, p.w_neigh, rows, p.b_self, p.b_neigh)
             assert maxrel(ys[l][rows], ref) <= tol, ("Y", l)
+            decision_flips(ys[l][rows], ref, tol)
     xm = tr.xm.cpu().numpy()
-    assert maxrel(xm, np.maximum(O.mm_nn(ys[-1], w_mlp), 0)) <= tol
+    xm_ref = np.maximum(O.mm_nn(ys[-1], w_mlp), 0)
+    assert maxrel(xm, xm_ref) <= tol
+    decision_flips(xm, xm_ref, tol)
     ref = O.train_step(g, x, params, w_mlp, t, kind, "sgd", lr=0.0,
                        forced={"ys": ys, "relu_on": xm > 0})
     loss = float(tr.loss.item())
