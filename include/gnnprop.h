@@ -186,6 +186,20 @@ gnn_status gnn_csr_prepare(const gnn_csr* csr, void* plan, size_t plan_bytes,
 gnn_status gnn_csr_validate(const gnn_csr* csr, int32_t require_symmetric,
                             hipStream_t stream);
 
+/* gnn_csr_validate for callers that cannot allocate device memory (serving
+ * loops, harnesses that forbid hipMalloc): the same checks and the same
+ * result, with the status word the check writes kept in a 256-byte array
+ * of static device memory that the library holds on each device it runs on
+ * until the process ends, instead of a hipMalloc'd word.  That scratch does
+ * not grow with the graph, so no size limit applies beyond those of
+ * gnn_csr_validate.  Every call on one device shares the array (each call
+ * clears it first): calls that overlap on one device race and must be
+ * serialised by the caller.  Synchronises `stream`; calls no hipMalloc or
+ * hipFree. */
+gnn_status gnn_csr_validate_noalloc(const gnn_csr* csr,
+                                    int32_t require_symmetric,
+                                    hipStream_t stream);
+
 /* ------------------------------------------------------------ one layer */
 
 /* Device bytes the forward pass saves for the backward pass (order 1 keeps

@@ -70,6 +70,8 @@ EXPORTS = {
                                          ctypes.c_void_p]),
     "gnn_csr_validate": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.c_int32,
                                           ctypes.c_void_p]),
+    "gnn_csr_validate_noalloc": (ctypes.c_int32, [ctypes.POINTER(gnn_csr),
+                                                  ctypes.c_int32, ctypes.c_void_p]),
     "gnn_prop_saved_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
                                                ctypes.POINTER(gnn_layer)]),
     "gnn_prop_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(gnn_csr),
@@ -246,6 +248,14 @@ def gnn_csr_validate(csr: gnn_csr, require_symmetric: bool = True,
     """Returns the status (GNN_OK or an error code) without raising."""
     return int(lib().gnn_csr_validate(ctypes.byref(csr), int(require_symmetric),
                                       _stream(stream)))
+
+
+def gnn_csr_validate_noalloc(csr: Optional[gnn_csr], require_symmetric: bool = True,
+                             stream=None) -> int:
+    """gnn_csr_validate without device allocation; returns the status."""
+    return int(lib().gnn_csr_validate_noalloc(
+        ctypes.byref(csr) if csr is not None else None, int(require_symmetric),
+        _stream(stream)))
 
 
 def gnn_prop_saved_bytes(csr: gnn_csr, layer: gnn_layer) -> int:
