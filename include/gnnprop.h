@@ -495,7 +495,8 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
 #define GNN_K_INDUCE 13       /* induced subgraph on the GPU */
 #define GNN_K_GATHER 14       /* feature / label row gather */
 #define GNN_K_SDDMM 15        /* GAT per-entry dot products */
-#define GNN_K_COUNT 16
+#define GNN_K_WSPLIT 16       /* weights split into bf16 pieces (split products) */
+#define GNN_K_COUNT 17
 
 /* When enabled, every kernel launch is bracketed by a pair of HIP events on
  * its stream.  gnn_timer_read synchronises on the recorded events and

@@ -43,7 +43,8 @@ TimerRec g_cur;
 struct LayerLayout {
   int order;
   int64_t ld_s, ld_p, ld_g, ld_gn, ld_v;
-  size_t off_buf0, off_buf1, off_gemm, off_cs, total;
+  size_t wp_words;  // split products: words of one weight's bf16 pieces
+  size_t off_buf0, off_buf1, off_gemm, off_cs, off_wp, total;
 };
 
 int resolve_order(const gnn_layer* L) {
@@ -155,6 +156,32 @@ GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
   return b;
 }
 
+// Split products: W_self and W_neigh pre-split into their bf16 pieces in
+// the workspace (once per call, in the orientation of this batch's B), and
+// the batch's segments pointed at them: segment B pointers equal to W_self
+// take the first, W_neigh the second.
+hipError_t attach_weight_planes(GemmBatch& b, const LayerLayout& o, char* ws,
+                                const float* Ws, const float* Wn, int32_t f_in,
+                                int32_t h, hipStream_t s) {
+  if (b.mode != GEMM_SPLIT) return hipSuccess;
+  uint32_t* wp[2] = {reinterpret_cast<uint32_t*>(ws + o.off_wp),
+                     reinterpret_cast<uint32_t*>(ws + o.off_wp + round_up(o.wp_words * 4, 256))};
+  const float* W[2] = {Ws, Wn};
+  // forward: op(B) = W (K = f_in, N = h); input gradient: op(B) = W^T
+  const int32_t K = b.trans_b ? h : f_in, N = b.trans_b ? f_in : h;
+  hipError_t e = split_b_planes_launch(W[0], W[1], h, K, N, b.trans_b != 0, wp[0], wp[1], s);
+  if (e != hipSuccess) return e;
+  const int64_t pw = (int64_t)(b_planes_words(K, N) / 3);
+  for (int i = 0; i < b.nprob; ++i)
+    for (int k = 0; k < b.p[i].nseg; ++k) {
+      GemmSeg& sg = b.p[i].seg[k];
+      sg.Bp = sg.B == Ws ? wp[0] : wp[1];
+      sg.bp_plane = pw;
+    }
+  b.b_planes = 1;
+  return hipSuccess;
+}
+
 GemmBatch with_mode(GemmBatch b, int32_t mode) {
   b.mode = mode;
   return b;
@@ -182,11 +209,17 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   gemm = std::max(gemm, gemm_workspace_bytes(with_mode(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
   gemm = std::max(gemm, gemm_workspace_bytes(with_mode(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 2 * h, 0, 2 * h, 0, 0), bf)));
   gemm = std::max(gemm, gemm_workspace_bytes(with_mode(dx_batch(o.order, n, f_in, h, 0, 2 * h, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
+  // split products: W_self and W_neigh as bf16 pieces, in the forward
+  // product's orientation (K = f_in, N = h) or the input gradient's (K = h,
+  // N = f_in), one at a time
+  o.wp_words = bf == GEMM_SPLIT ? std::max(b_planes_words(f_in, h), b_planes_words(h, f_in))
+                                : 0;
   o.off_buf0 = 0;
   o.off_buf1 = round_up(buf0, 256);
   o.off_gemm = o.off_buf1 + round_up(buf1, 256);
   o.off_cs = o.off_gemm + round_up(gemm, 256);
-  o.total = o.off_cs + colsum_partials_bytes(n, h);
+  o.off_wp = o.off_cs + round_up(colsum_partials_bytes(n, h), 256);
+  o.total = o.off_wp + 2 * round_up(o.wp_words * 4, 256);
   return o;
 }
 
@@ -340,6 +373,13 @@ gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
   return GNN_OK;
 }
 
+// Split products pre-split B into its bf16 pieces once (workspace, after
+// the partial tiles) when at least four row tiles of 128 share it: each
+// would otherwise split the same values again.
+static bool gemm_presplit_b(int32_t M, int32_t mode) {
+  return mode == GEMM_SPLIT && M >= 512;
+}
+
 size_t gnn_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
   if (M < 0 || N < 0 || K < 0) return 0;
   GemmBatch b;
@@ -351,7 +391,8 @@ size_t gnn_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
   b.p[0].seg[0].K = K;
   const size_t f32 = gemm_workspace_bytes(b);
   b.mode = GEMM_BF16;
-  return std::max(f32, gemm_workspace_bytes(b));
+  const size_t part = round_up(std::max(f32, gemm_workspace_bytes(b)), 256);
+  return part + (gemm_presplit_b(M, GEMM_SPLIT) ? round_up(b_planes_words(K, N) * 4, 256) : 0);
 }
 
 gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
@@ -380,7 +421,9 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
   b.p[0].N = N;
   b.p[0].C = C;
   b.p[0].ldc = ldc;
-  const size_t need = gemm_workspace_bytes(b);
+  const size_t part = round_up(gemm_workspace_bytes(b), 256);
+  const bool presplit = K > 0 && gemm_presplit_b(M, b.mode);
+  const size_t need = part + (presplit ? round_up(b_planes_words(K, N) * 4, 256) : 0);
   if (workspace_bytes < need || (need > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
   const size_t cb = mat_bytes(M, N, ldc);
@@ -388,7 +431,15 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
       (ranges_overlap(C, cb, A, trans_a ? mat_bytes(K, M, lda) : mat_bytes(M, K, lda)) ||
        ranges_overlap(C, cb, B, trans_b ? mat_bytes(N, K, ldb) : mat_bytes(K, N, ldb))))
     return GNN_ERR_ALIAS;
-  GNN_HIP(gemm_launch(b, workspace, workspace_bytes, stream));
+  if (presplit) {
+    uint32_t* planes = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + part);
+    GNN_HIP(split_b_planes_launch(B, nullptr, ldb, K, N, trans_b != 0, planes, nullptr,
+                                  stream));
+    b.b_planes = 1;
+    b.p[0].seg[0].Bp = planes;
+    b.p[0].seg[0].bp_plane = (int64_t)(b_planes_words(K, N) / 3);
+  }
+  GNN_HIP(gemm_launch(b, workspace, part, stream));
   return GNN_OK;
 }
 
@@ -440,12 +491,14 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
     GemmBatch b = fwd_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, W_self,
                             W_neigh, b_self, b_neigh, Y, layer->ld_y, nullptr, 0);
     b.mode = gemm_mode(layer->flags);
+    GNN_HIP(attach_weight_planes(b, o, ws, W_self, W_neigh, f_in, h, stream));
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
   } else {
     float* P = reinterpret_cast<float*>(ws + o.off_buf0);
     GemmBatch b = fwd_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, W_self,
                             W_neigh, b_self, nullptr, Y, layer->ld_y, P, o.ld_p);
     b.mode = gemm_mode(layer->flags);
+    GNN_HIP(attach_weight_planes(b, o, ws, W_self, W_neigh, f_in, h, stream));
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
     SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y, rn);
     c.epilogue = SPMM_BIAS_RELU;
@@ -536,6 +589,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       bx.mode = bf;
       bx.p[0].mask = dx_mask;
       bx.p[0].ld_mask = layer->ld_x;
+      GNN_HIP(attach_weight_planes(bx, o, ws, W_self, W_neigh, f_in, h, stream));
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
     }
     if (db_self) GNN_HIP(colsum_launch(n, h, Gs, ld_gs, db_self, cspart, stream));
@@ -562,6 +616,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       GemmBatch bx = dx_batch(1, n, f_in, h, G, ld_g, G + h, ld_g, W_self,
                               W_neigh, dX, layer->ld_dx, V, o.ld_v);
       bx.mode = bf;
+      GNN_HIP(attach_weight_planes(bx, o, ws, W_self, W_neigh, f_in, h, stream));
       GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
       // dX = G_s W_s^T + A_s^T V, then the mask, in the aggregation epilogue
       SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx, rn);

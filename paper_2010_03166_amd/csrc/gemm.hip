@@ -842,17 +842,23 @@ __device__ inline void split3(float x0, float x1, uint32_t& h, uint32_t& m,
   l = pack_bf16(s0, s1);
 }
 
-template <bool AT, bool BT>
+// BD: B comes pre-split (GemmSeg::Bp, split_b_planes_launch) and each
+// wavefront loads its B fragments straight from those planes into registers
+// (one 128-bit load per piece and block: the planes are in fragment order,
+// so a fragment is 1 KiB of consecutive bytes), one stage ahead of the
+// products that use them; only A goes through the split and LDS.
+template <bool AT, bool BT, bool BD>
 __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
   constexpr bool A_KC = !AT;
   constexpr bool B_KC = BT;
   constexpr int A_PLANE = A_KC ? KCS_PLANE : XCS_PLANE;
   constexpr int B_PLANE = B_KC ? KCS_PLANE : XCS_PLANE;
+  constexpr int B_WORDS = BD ? 4 : 3 * B_PLANE;
   __shared__ __attribute__((aligned(16))) uint32_t As0[3 * A_PLANE];
   __shared__ __attribute__((aligned(16))) uint32_t As1[3 * A_PLANE];
-  __shared__ __attribute__((aligned(16))) uint32_t Bs0[3 * B_PLANE];
-  __shared__ __attribute__((aligned(16))) uint32_t Bs1[3 * B_PLANE];
-  static_assert(3 * A_PLANE >= 2 * EPI_REGION && 3 * B_PLANE >= 2 * EPI_REGION,
+  __shared__ __attribute__((aligned(16))) uint32_t Bs0[B_WORDS];
+  __shared__ __attribute__((aligned(16))) uint32_t Bs1[B_WORDS];
+  static_assert(3 * A_PLANE >= 2 * EPI_REGION && (BD || 3 * B_PLANE >= 2 * EPI_REGION),
                 "epilogue regions");
 
   const int tid = threadIdx.x;
@@ -891,8 +897,11 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
     const int64_t lda0 = P.seg[0].lda, lda1 = P.seg[1].lda;
     const int64_t ldb0 = P.seg[0].ldb, ldb1 = P.seg[1].ldb;
     const int K0 = P.seg[0].K, K1 = P.seg[1].K;
+    const uint32_t* const Bq0 = P.seg[0].Bp;
+    const uint32_t* const Bq1 = P.seg[1].Bp;
+    const int64_t bps0 = P.seg[0].bp_plane, bps1 = P.seg[1].bp_plane;
     const bool a_in = va && m0 + BM <= M;
-    const bool b_in = vb && n0 + BN <= N;
+    const bool b_in = (BD || vb) && n0 + BN <= N;
     // KC: thread owns rows x = (tid >> 2) + 64 p (p = 0, 1), k = 4 (tid & 3)
     // .. + 3 (4 lanes per 64-byte row segment).
     // XC: thread owns k pair kp = tid >> 5 (rows 2 kp and 2 kp + 1) and
@@ -927,7 +936,8 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
       const int k0 = (s1 ? ks - kt0 : ks) * BKS;
       const bool fk = k0 + BKS <= K;
       load_op(ra, A_KC, s1 ? A1p : A0p, s1 ? lda1 : lda0, m0, M, k0, K, a_in && fk, va);
-      load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, K, b_in && fk, vb);
+      if (!BD)
+        load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, K, b_in && fk, vb);
     };
     // Split this thread's values and write the three pieces.
     auto store_op = [&](uint32_t* L, const float4 (&r)[2], bool kc, int plane) {
@@ -977,20 +987,44 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
       }
       return __builtin_bit_cast(bf16x8, w);
     };
+    typedef bf16x8 BFr[3][2];
+    // B fragments of stage ks from the planes (BD); columns past N read as
+    // zeros unless `full` (the tile's columns all lie inside N)
+    auto load_bfr = [&](BFr& bf, int ks, bool full) {
+      const bool s1 = ks >= kt0;
+      const uint32_t* Bq = s1 ? Bq1 : Bq0;
+      const int64_t ps = s1 ? bps1 : bps0;
+      const int64_t gN = (int64_t)(s1 ? ks - kt0 : ks) * N;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int n = n0 + wn * 64 + j * 32 + lr;
+        const uint32_t* src = Bq + (gN + n) * 8 + 4 * lh;
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+          uint4 w = make_uint4(0u, 0u, 0u, 0u);
+          if (full || n < N) w = *reinterpret_cast<const uint4*>(src + q * ps);
+          bf[q][j] = __builtin_bit_cast(bf16x8, w);
+        }
+      }
+    };
     // The six piece products down to 2^-16 of hi x hi, smallest first; what
     // is left out (mid lo + lo mid + lo lo) is below 2^-24 of |a b|.
     struct Frags {
       bf16x8 a[3][2], b[3][2];
     };
-    auto read_frags = [&](const uint32_t* as, const uint32_t* bs) {
-      Frags f;
+    auto read_a = [&](Frags& f, const uint32_t* as) {
 #pragma unroll
       for (int q = 0; q < 3; ++q)
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          f.a[q][i] = frag(as + q * A_PLANE, A_KC, wm * 64, i);
-          f.b[q][i] = frag(bs + q * B_PLANE, B_KC, wn * 64, i);
-        }
+        for (int i = 0; i < 2; ++i) f.a[q][i] = frag(as + q * A_PLANE, A_KC, wm * 64, i);
+    };
+    auto read_frags = [&](const uint32_t* as, const uint32_t* bs) {
+      Frags f;
+      read_a(f, as);
+#pragma unroll
+      for (int q = 0; q < 3; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) f.b[q][i] = frag(bs + q * B_PLANE, B_KC, wn * 64, i);
       return f;
     };
     auto products = [&](const Frags& f) {
@@ -1003,9 +1037,6 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
           for (int j = 0; j < 2; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                 f.a[terms[u][0]][i], f.b[terms[u][1]][j], acc[i][j], 0, 0, 0);
-    };
-    auto compute = [&](const uint32_t* as, const uint32_t* bs) {
-      products(read_frags(as, bs));
     };
 
     // Stages [kbeg, kf) are full and the tile is interior: pipelined path.
@@ -1023,30 +1054,61 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
         const bool s1 = ks >= kt0;
         const int k0 = (s1 ? ks - kt0 : ks) * BKS;
         load_op(ra, A_KC, s1 ? A1p : A0p, s1 ? lda1 : lda0, m0, M, k0, 0, true, true);
-        load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, 0, true, true);
+        if (!BD)
+          load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, 0, true, true);
       };
-      // Read this stage's fragments, split and store the next stage (in
-      // registers) into the other LDS buffer, issue the loads of the stage
-      // after it, the products, one barrier.  The fragment reads go first so
-      // that the next stage's LDS writes do not hold them up.
-      auto step = [&](const uint32_t* as, const uint32_t* bs, uint32_t* as_n,
-                      uint32_t* bs_n, int kl) {
-        const Frags f = read_frags(as, bs);
-        store_op(as_n, ra, A_KC, A_PLANE);
-        store_op(bs_n, rb, B_KC, B_PLANE);
-        load_full(kl);
-        products(f);
+      if (BD) {
+        // A through LDS as below; B fragments of stage k + 1 loaded while
+        // stage k's products run (two register sets, alternating)
+        BFr b0, b1;
+        auto step = [&](const uint32_t* as, uint32_t* as_n, int kl, BFr& bcur,
+                        BFr& bnext, int kb) {
+          Frags f;
+          read_a(f, as);
+#pragma unroll
+          for (int q = 0; q < 3; ++q)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) f.b[q][j] = bcur[q][j];
+          store_op(as_n, ra, A_KC, A_PLANE);
+          load_full(kl);
+          load_bfr(bnext, min(kb, kf - 1), true);
+          products(f);
+          __syncthreads();
+        };
+        load_full(kbeg);
+        store_op(As0, ra, A_KC, A_PLANE);
+        load_full(kbeg + 1);
+        load_bfr(b0, kbeg, true);
         __syncthreads();
-      };
-      load_full(kbeg);
-      store_op(As0, ra, A_KC, A_PLANE);
-      store_op(Bs0, rb, B_KC, B_PLANE);
-      load_full(kbeg + 1);
-      __syncthreads();
-      for (int k = kbeg; k < kf; k += 2) {
-        step(As0, Bs0, As1, Bs1, k + 2);
-        if (k + 1 >= kf) break;
-        step(As1, Bs1, As0, Bs0, k + 3);
+        for (int k = kbeg; k < kf; k += 2) {
+          step(As0, As1, k + 2, b0, b1, k + 1);
+          if (k + 1 >= kf) break;
+          step(As1, As0, k + 3, b1, b0, k + 2);
+        }
+      } else {
+        // Read this stage's fragments, split and store the next stage (in
+        // registers) into the other LDS buffer, issue the loads of the stage
+        // after it, the products, one barrier.  The fragment reads go first
+        // so that the next stage's LDS writes do not hold them up.
+        auto step = [&](const uint32_t* as, const uint32_t* bs, uint32_t* as_n,
+                        uint32_t* bs_n, int kl) {
+          const Frags f = read_frags(as, bs);
+          store_op(as_n, ra, A_KC, A_PLANE);
+          store_op(bs_n, rb, B_KC, B_PLANE);
+          load_full(kl);
+          products(f);
+          __syncthreads();
+        };
+        load_full(kbeg);
+        store_op(As0, ra, A_KC, A_PLANE);
+        store_op(Bs0, rb, B_KC, B_PLANE);
+        load_full(kbeg + 1);
+        __syncthreads();
+        for (int k = kbeg; k < kf; k += 2) {
+          step(As0, Bs0, As1, Bs1, k + 2);
+          if (k + 1 >= kf) break;
+          step(As1, Bs1, As0, Bs0, k + 3);
+        }
       }
     }
 
@@ -1059,10 +1121,17 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
         uint32_t* as = buf ? As1 : As0;
         uint32_t* bs = buf ? Bs1 : Bs0;
         store_op(as, ra, A_KC, A_PLANE);
-        store_op(bs, rb, B_KC, B_PLANE);
+        if (!BD) store_op(bs, rb, B_KC, B_PLANE);
         __syncthreads();
         if (ks + 1 < kend) load_slice(ks + 1);
-        compute(as, bs);
+        if (BD) {
+          Frags f;
+          read_a(f, as);
+          load_bfr(f.b, ks, false);
+          products(f);
+        } else {
+          products(read_frags(as, bs));
+        }
         buf ^= 1;
       }
       __syncthreads();
@@ -1073,8 +1142,53 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
                                          : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
                                (BM * BN);
     store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh, g.vec_c[ti.pi] != 0,
-              reinterpret_cast<float*>(As0), reinterpret_cast<float*>(Bs0));
+              reinterpret_cast<float*>(As0),
+              reinterpret_cast<float*>(BD ? As1 : Bs0));
   }
+}
+
+// One thread per word (bf16 pair k, k + 1 of one column) of the planes;
+// blockIdx.y picks one of the two matrices split in one launch.
+__global__ __launch_bounds__(256) void split_b_planes_kernel(
+    const float* __restrict__ B0, const float* __restrict__ B1, int64_t ld,
+    int32_t K, int32_t N, int32_t kn, uint32_t* __restrict__ planes0,
+    uint32_t* __restrict__ planes1, int64_t plane_words) {
+  const int64_t w = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (w >= plane_words) return;
+  const float* __restrict__ B = blockIdx.y ? B1 : B0;
+  uint32_t* __restrict__ planes = blockIdx.y ? planes1 : planes0;
+  const int tp = (int)(w & 7);
+  const int64_t gn = w >> 3;
+  const int n = (int)(gn % N), gi = (int)(gn / N);
+  const int k = 16 * gi + 2 * tp;
+  auto at = [&](int kk) -> float {
+    if (kk >= K) return 0.f;
+    return kn ? B[(int64_t)kk * ld + n] : B[(int64_t)n * ld + kk];
+  };
+  uint32_t h, m, l;
+  split3(at(k), at(k + 1), h, m, l);
+  planes[w] = h;
+  planes[plane_words + w] = m;
+  planes[2 * plane_words + w] = l;
+}
+
+size_t b_planes_words(int32_t K, int32_t N) {
+  if (K <= 0 || N <= 0) return 0;
+  return 3 * (size_t)ceil_div(K, BKS) * (size_t)N * 8;
+}
+
+hipError_t split_b_planes_launch(const float* B0, const float* B1, int64_t ld,
+                                 int32_t K, int32_t N, bool trans_b,
+                                 uint32_t* planes0, uint32_t* planes1,
+                                 hipStream_t s) {
+  const int64_t pw = (int64_t)(b_planes_words(K, N) / 3);
+  if (pw == 0) return hipSuccess;
+  const unsigned nmat = B1 ? 2 : 1;
+  timer_begin(GNN_K_WSPLIT, s);
+  split_b_planes_kernel<<<dim3((unsigned)ceil_div(pw, 256), nmat), 256, 0, s>>>(
+      B0, B1, ld, K, N, trans_b ? 0 : 1, planes0, planes1, pw);
+  timer_end(GNN_K_WSPLIT, 20.0 * (double)pw * nmat, s);  // 2 floats in, 3 words out
+  return hipGetLastError();
 }
 
 // Tiles shared by several blocks: add the blocks' partial tiles in block
@@ -1238,6 +1352,12 @@ double gemm_flops(const GemmBatch& b) {
 hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
                        hipStream_t s) {
   if (!batch_ok(b)) return hipErrorInvalidValue;
+  if (b.b_planes) {  // split products only, every segment's planes given
+    if (b.mode != GEMM_SPLIT) return hipErrorInvalidValue;
+    for (int i = 0; i < b.nprob; ++i)
+      for (int k = 0; k < b.p[i].nseg; ++k)
+        if (b.p[i].seg[k].K > 0 && !b.p[i].seg[k].Bp) return hipErrorInvalidValue;
+  }
   const Shape sh = gemm_shape(b);
   if (sh.tiles == 0) return hipSuccess;
   GemmKArgs g;
@@ -1301,14 +1421,23 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
       gemm_f32_kernel<false, true><<<grid, 256, 0, s>>>(g);
     else
       gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g);
+  } else if (b.b_planes) {
+    if (!b.trans_a && !b.trans_b)
+      gemm_split_kernel<false, false, true><<<grid, 256, 0, s>>>(g);
+    else if (b.trans_a && !b.trans_b)
+      gemm_split_kernel<true, false, true><<<grid, 256, 0, s>>>(g);
+    else if (!b.trans_a && b.trans_b)
+      gemm_split_kernel<false, true, true><<<grid, 256, 0, s>>>(g);
+    else
+      gemm_split_kernel<true, true, true><<<grid, 256, 0, s>>>(g);
   } else if (!b.trans_a && !b.trans_b) {
-    gemm_split_kernel<false, false><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<false, false, false><<<grid, 256, 0, s>>>(g);
   } else if (b.trans_a && !b.trans_b) {
-    gemm_split_kernel<true, false><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<true, false, false><<<grid, 256, 0, s>>>(g);
   } else if (!b.trans_a && b.trans_b) {
-    gemm_split_kernel<false, true><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<false, true, false><<<grid, 256, 0, s>>>(g);
   } else {
-    gemm_split_kernel<true, true><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<true, true, false><<<grid, 256, 0, s>>>(g);
   }
   timer_end(kid, gemm_flops(b), s);
   hipError_t e = hipGetLastError();

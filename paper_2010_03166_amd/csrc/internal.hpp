@@ -125,6 +125,10 @@ struct GemmSeg {
   const float* B;
   int64_t lda, ldb;
   int32_t K;
+  // Split mode with GemmBatch::b_planes: op(B) already split into its three
+  // bf16 pieces in fragment order (split_b_planes_launch); B is not read.
+  const uint32_t* Bp = nullptr;
+  int64_t bp_plane = 0;  // 32-bit words between two pieces' planes
 };
 struct GemmProblem {
   GemmSeg seg[2];
@@ -157,7 +161,21 @@ struct GemmBatch {
   int32_t nprob;
   int32_t trans_a, trans_b;  // A stored K x M; B stored N x K
   int32_t mode;              // GemmMode
+  int32_t b_planes;          // split mode: every segment's B given as Bp
 };
+// op(B) (K x N; stored K x N row-major when !trans_b, N x K when trans_b,
+// row stride ld) split exactly into bf16 hi + mid + lo (each rounded to
+// nearest even), written as three planes in MFMA fragment order: plane q,
+// 16-deep group g = k / 16, column n: the 16 pieces of k = 16 g .. 16 g + 15
+// as 8 words of bf16 pairs, at words ((g N + n) 8 .. + 7) of the plane; k
+// past K holds zeros.  Planes are b_planes_words(K, N) / 3 words apart.
+size_t b_planes_words(int32_t K, int32_t N);
+// B1 / planes1 may be NULL; otherwise a second matrix of the same shape and
+// stride is split in the same launch.
+hipError_t split_b_planes_launch(const float* B0, const float* B1, int64_t ld,
+                                 int32_t K, int32_t N, bool trans_b,
+                                 uint32_t* planes0, uint32_t* planes1,
+                                 hipStream_t s);
 size_t gemm_workspace_bytes(const GemmBatch& b);
 hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
                        hipStream_t s);

@@ -29,7 +29,7 @@ GNN_LOSS_SIGMOID = 1
 KERNELS = {"spmm": 0, "spmm_reduce": 1, "gemm_nn": 2, "gemm_tn": 3,
            "gemm_nt": 4, "gemm_tt": 5, "gemm_reduce": 6, "mask": 7,
            "colsum": 8, "plan": 9, "transpose": 10, "loss": 11, "update": 12,
-           "induce": 13, "gather": 14, "sddmm": 15}
+           "induce": 13, "gather": 14, "sddmm": 15, "wsplit": 16}
 GNN_NORM_ROW = 0
 GNN_NORM_SYM = 1
 

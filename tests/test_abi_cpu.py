@@ -93,7 +93,9 @@ def test_size_queries(lib):
         assert G.gnn_prop_workspace_bytes(c, l) > 8000 * 512 * 4
     auto = G.make_layer(602, 512, 604, 1024, 604, order=0)
     assert G.gnn_prop_saved_bytes(c, auto) == 0  # 602 > 512: order 2
-    assert G.gnn_gemm_workspace_bytes(8000, 1024, 602) == 0
+    # one block per tile (no partial tiles); the split products' B pieces:
+    # three planes of ceil(K / 16) groups x N columns x 16 bf16
+    assert G.gnn_gemm_workspace_bytes(8000, 1024, 602) == 3 * 38 * 1024 * 16 * 2
     assert G.gnn_gemm_workspace_bytes(602, 512, 8000) > 0  # split along K
     assert G.gnn_spmm_workspace_bytes(c, 512) == 0  # one kernel, no partials
 
