@@ -79,6 +79,10 @@ def parse():
                     help="skip the step replayed from a HIP graph")
     ap.add_argument("--no-rownorm", action="store_true",
                     help="skip the step with GNN_FLAG_ROW_NORMALIZED")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads (one line each in `configs`)")
+    ap.add_argument("--config-steps", type=int, default=10,
+                    help="timed steps per workload in `configs`")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the GCN and MixHop layer timings")
     ap.add_argument("--no-train", action="store_true",
@@ -303,6 +307,12 @@ def main():
     if not args.no_pipeline:
         out["pipeline"] = bench_pipeline(G, runtime, synth, torch, np, args)
 
+    # every other workload of the benchmark set, the same step timed the
+    # same way (fewer steps), with the bf16 variant beside the fp32 one for
+    # the 300-feature workload
+    if not args.no_configs:
+        out["configs"] = bench_configs(G, runtime, synth, torch, np, name, args)
+
     if not args.no_cpu_baseline:
         from oracle import oracle as O
         import numpy as np  # noqa: F811
@@ -321,6 +331,28 @@ def main():
                       % (reps, wl.layers)}
         log("cpu oracle %.1f ms/layer on %d threads" % (
             out["cpu_baseline"]["value"], out["cpu_baseline"]["cores"]))
+        # the oracle's own parallel speedup: the same step on one thread, for
+        # this workload and the 1,000-node one (results are the same for any
+        # thread count)
+        threads = O.num_threads()
+        single = {}
+        try:
+            O.set_num_threads(1)
+            for wname in (synth.TINY_WORKLOAD, name):
+                w = synth.WORKLOADS[wname]
+                d = inp if wname == name else synth.workload_inputs(w)
+                t = time.perf_counter()
+                O.transpose_values(d["graph"])
+                O.sage_stack(d["graph"], d["x"], d["params"], d["dy"],
+                             want_dx_first=want_dx_first)
+                ms1 = (time.perf_counter() - t) * 1e3 / w.layers
+                single[wname] = {"ms_per_layer_1_thread": round(ms1, 3)}
+                log("cpu oracle, 1 thread, %s: %.1f ms/layer" % (wname, ms1))
+        finally:
+            O.set_num_threads(threads)
+        single[name]["parallel_speedup"] = round(
+            single[name]["ms_per_layer_1_thread"] / out["cpu_baseline"]["value"], 2)
+        out["cpu_baseline"]["single_thread"] = single
     print(json.dumps(out), flush=True)
 
 
@@ -368,6 +400,97 @@ def bench_mode(G, runtime, torch, dg, params, wl, X, dY, args, want_dx_first, pa
                          "peak": peak, "unit": "TFLOP/s",
                          "frac": round(kb[dom]["tflops"] / peak, 4)},
             "kernels": kb}
+
+
+def time_stack(G, runtime, torch, dg, params, wl, X, dY, steps, warmup, flags):
+    """ms per step (wall, K steps after W warm-up) of prep + the stack forward
+    + backward with the first layer's dX, and the per-kernel event times of a
+    second pass of K steps."""
+    st = runtime.SageStack(dg, params, wl.f_in, pad=16, flags=flags)
+
+    def step():
+        dg.prepare()
+        st.forward(X)
+        st.backward(dY, want_dx_first=True)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    G.gnn_timer_reset()
+    G.gnn_timer_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    G.gnn_timer_enable(False)
+    kb = {}
+    for kname in G.KERNELS:
+        kms, launches, work = G.gnn_timer_read(kname)
+        if launches:
+            us = 1e3 * kms / launches
+            kb[kname] = {"ms_per_step": round(kms / steps, 4), "avg_launch_us": round(us, 2)}
+            if kname.startswith("gemm_") and kname != "gemm_reduce":
+                kb[kname]["tflops"] = round(work / launches / (1e6 * us), 1)
+            if kname == "spmm":
+                kb[kname]["gbs"] = round(work / launches / (1e3 * us), 1)
+    G.gnn_timer_reset()
+    del st
+    return ms, kb
+
+
+def bench_configs(G, runtime, synth, torch, np, skip, args):
+    """The other workloads (every configuration but the headline one): ms
+    per layer and per step, the dominant kernel (largest time per step among
+    the GEMMs and the aggregation) against its ceiling, and the aggregation's
+    algorithmic GB/s; for the 300-feature workload also the bf16-product
+    variant."""
+    res = {}
+    steps, warmup = max(2, args.config_steps), 2
+    for name, wl in synth.WORKLOADS.items():
+        if name == skip:
+            continue
+        inp = synth.workload_inputs(wl)
+        g, x, params, dy = inp["graph"], inp["x"], inp["params"], inp["dy"]
+        dg = runtime.DeviceGraph(g)
+        ld_x = (wl.f_in + 15) // 16 * 16
+        X = runtime.padded(torch.from_numpy(x).cuda(), ld_x)
+        dY = torch.from_numpy(dy).cuda()
+        modes = [("f32", 0, PEAK_SPLIT)]
+        if name == "cl2.3-n8000-f300-h512-L3":
+            modes.append(("bf16", G.GNN_FLAG_BF16, PEAK_TFLOPS["bf16"]))
+        entry = {"n": wl.n, "nnz": int(g.nnz), "f_in": wl.f_in, "hidden_per_half": wl.hidden,
+                 "layers": wl.layers}
+        for label, flags, peak in modes:
+            ms, kb = time_stack(G, runtime, torch, dg, params, wl, X, dY, steps, warmup,
+                                flags)
+            cands = [k for k in kb if "tflops" in kb[k] or k == "spmm"]
+            dom = max(cands, key=lambda k: kb[k]["ms_per_step"])
+            if dom == "spmm":
+                roof = {"kernel": dom, "bound": "hbm", "achieved": kb[dom]["gbs"],
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(kb[dom]["gbs"] / PEAK_HBM_GBS, 4)}
+            else:
+                roof = {"kernel": dom, "bound": "mfma", "achieved": kb[dom]["tflops"],
+                        "peak": round(peak, 1), "unit": "TFLOP/s",
+                        "frac": round(kb[dom]["tflops"] / peak, 4)}
+            e = {"ms_per_layer": round(ms / wl.layers, 5), "ms_per_step": round(ms, 5),
+                 "dominant": roof,
+                 "aggregation_gbs": kb.get("spmm", {}).get("gbs"),
+                 "kernels": kb}
+            if label == "f32":
+                entry.update(e)
+            else:
+                entry["bf16_variant"] = e
+            log("%s %s: %.4f ms/layer, dominant %s %.3f of its ceiling" % (
+                name, label, ms / wl.layers, dom, roof["frac"]))
+        res[name] = entry
+        del dg, X, dY
+        torch.cuda.empty_cache()
+    return res
 
 
 def bench_train(G, runtime, synth, torch, dg, X, params, wl, args, ms_prop):

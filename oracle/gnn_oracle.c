@@ -21,6 +21,15 @@ int32_t oracle_num_threads(void) {
 #endif
 }
 
+/* Threads of the following parallel regions (results do not depend on it). */
+void oracle_set_num_threads(int32_t n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* bfloat16 keeps the sign, the 8 exponent bits and the top 7 fraction bits
  * of a float.  Rounding to nearest, ties to even, adds 0x7fff plus the
  * lowest kept bit to the 32-bit pattern and truncates the low 16 bits. */

@@ -166,6 +166,7 @@ void oracle_round_bf16(int64_t count, const double* in, double* out);
 
 /* Number of OpenMP threads the oracle runs with. */
 int32_t oracle_num_threads(void);
+void oracle_set_num_threads(int32_t n);
 
 /* Induced subgraph of a full graph (int64 row pointers) on the sorted,
  * distinct node list `nodes` (node nodes[i] becomes i), self loops added,

@@ -94,6 +94,7 @@ def lib():
                                       _F64P, _F64P, _F64P, _F64P, _F64P, _F64P,
                                       _F64P],
                 "oracle_num_threads": [],
+                "oracle_set_num_threads": [i32],
             }
             for name, args in sigs.items():
                 fn = getattr(L, name)
@@ -138,6 +139,12 @@ def round_bf16(a) -> np.ndarray:
 
 def num_threads() -> int:
     return int(lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the oracle's later calls (results are identical for
+    any count)."""
+    lib().oracle_set_num_threads(int(n))
 
 
 def spmm(g, x: np.ndarray) -> np.ndarray:
