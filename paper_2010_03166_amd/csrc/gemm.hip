@@ -1297,7 +1297,10 @@ static Shape gemm_shape(const GemmBatch& b) {
   // slices one after the other on 2 CUs).  About one tile per CU (224 to
   // 256 tiles) over at most 40 K slices runs one block per tile: measured
   // faster than stream-K plus its reduction (8000 x 512, K = 602: 65.5
-  // against 61.3 + 12.2 us), slower from K = 2048 on.
+  // against 61.3 + 12.2 us), slower from K = 2048 on.  With split products
+  // the same holds up to one tile per slot over K = 2048 (8000 x 602, K =
+  // 1024, 315 tiles: 90.0 us against 89.1 for stream-K with its reduction),
+  // which then writes no partial tiles and needs no second launch.
   // The rules count K in 32-deep slices whatever the kernel's stage depth
   // (the split kernel's stages are 16 deep).
   const int slots = MAX_BLOCKS;
@@ -1305,7 +1308,9 @@ static Shape gemm_shape(const GemmBatch& b) {
   const double fill = (double)s.tiles / (double)(rounds * slots);
   const int kt32 = b.mode == GEMM_SPLIT ? (s.ktiles + 1) / 2 : s.ktiles;
   const int64_t iters32 = (int64_t)s.tiles * kt32;
-  const bool one_per_cu = s.tiles >= slots * 7 / 16 && s.tiles <= slots / 2 && kt32 <= 40;
+  const bool one_per_cu = s.tiles >= slots * 7 / 16 &&
+                          ((s.tiles <= slots / 2 && kt32 <= 40) ||
+                           (b.mode == GEMM_SPLIT && s.tiles <= slots && kt32 <= 64));
   s.splits = 1;
   if (fill >= 0.85 || one_per_cu ||
       (iters32 <= slots && (s.tiles > slots / 4 || kt32 < 4))) {

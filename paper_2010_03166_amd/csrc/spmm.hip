@@ -463,12 +463,18 @@ template <int G, int D, bool VEC, int EPI, bool OFF32, bool RAG>
 __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
   using V = Vec<VEC>;
   using T = typename V::T;
-  constexpr int NG = 256 / G;   // groups per block
-  constexpr int CW = G * V::W;  // columns per pass
   constexpr int EMPTY = -2;     // group range holds no entry
-  __shared__ T head[NG][G];     // part of a row begun in an earlier group
-  __shared__ T tail[NG][G];     // part of a row that goes on past the group
-  __shared__ int head_row[NG], tail_row[NG], starts[NG];
+  // Lane groups: G consecutive lanes of a wavefront (1 <= G <= 64), 64 / G
+  // groups per wavefront (the lanes past the last group take no part),
+  // groups numbered wavefront by wavefront.  A group's lane l is thread
+  // gtid(g) + l, so the per-lane LDS slots are indexed by thread.
+  constexpr int gpw = 64 / G;   // groups per wavefront
+  constexpr int NG = 4 * gpw;   // groups per block
+  constexpr int CW = G * V::W;  // columns per pass
+  __shared__ T head[256];       // part of a row begun in an earlier group
+  __shared__ T tail[256];       // part of a row that goes on past the group
+  __shared__ int head_row[256], tail_row[256], starts[256];
+  auto gtid = [&](int g) { return (g / gpw) * 64 + (g % gpw) * G; };
 
   int slice = 0, win = blockIdx.x;
   if (a.nslices >= 8) {
@@ -483,9 +489,14 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
   const int k0 = win * a.wpb, k1 = min(k0 + a.wpb, a.nblk) - 1;
   const int4 bi0 = a.binfo[k0], bi1 = a.binfo[k1];
   const int r_lo = bi0.x, r_hi = bi1.y, B = bi0.z, E = bi1.w;
-  const int gi = threadIdx.x / G, lane = threadIdx.x % G;
-  const int gb = B + (int)((int64_t)(E - B) * gi / NG);
-  const int ge = B + (int)((int64_t)(E - B) * (gi + 1) / NG);
+  const int tid = threadIdx.x;
+  const int wl = tid & 63, lg = wl / G;
+  const bool member = lg < gpw;            // lane belongs to a group
+  const int gi = (tid >> 6) * gpw + lg;    // group id (member lanes)
+  const int lane = wl - lg * G;            // lane within the group
+  const int base = lg * G;                 // the group's first lane in the wavefront
+  const int gb = member ? B + (int)((int64_t)(E - B) * gi / NG) : 0;
+  const int ge = member ? B + (int)((int64_t)(E - B) * (gi + 1) / NG) : 0;
   const int c_lo = slice * a.sw;
   const int c_hi = min(a.w, c_lo + a.sw);
   const float* __restrict__ in = a.in;
@@ -512,7 +523,7 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
 
   for (int c0 = c_lo; c0 < c_hi; c0 += CW) {
     const int col = c0 + lane * V::W;
-    const bool ok = col < c_hi;
+    const bool ok = member && col < c_hi;
     // a lane holding the ragged end of the row (fewer than W columns left)
     const int nv = c_hi - col;
     const bool part = RAG && ok && nv < V::W;
@@ -546,10 +557,10 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
         const bool opened_before = cur == first_row && prev_row == cur;
         const bool goes_on = last && next_row == cur;
         if (goes_on && !opened_before) {
-          tail[gi][lane] = acc;
+          tail[tid] = acc;
           tr = cur;
         } else if (opened_before) {
-          head[gi][lane] = acc;
+          head[tid] = acc;
           hr = cur;
         } else {
           finish(cur, acc);
@@ -577,7 +588,7 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
           T x[D];
 #pragma unroll
           for (int u = 0; u < D; ++u) {
-            const int idx = __shfl(fi, k + u, G);
+            const int idx = __shfl(fi, base + k + u);
             if (k + u < cnt && ok) {
               if (OFF32)
                 x[u] = ld(reinterpret_cast<const float*>(
@@ -592,8 +603,8 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
 #pragma unroll
           for (int u = 0; u < D; ++u) {
             if (k + u < cnt) {
-              const int rw = __shfl(fr, k + u, G);
-              const float val = __shfl(fv, k + u, G);
+              const int rw = __shfl(fr, base + k + u);
+              const float val = __shfl(fv, base + k + u);
               if (rw != cur) {
                 if (cur >= 0) close(false);
                 if (cur < 0) first_row = rw;
@@ -608,19 +619,19 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
       }
       close(true);
     }
-    if (lane == 0) {
+    if (member && lane == 0) {
       head_row[gi] = hr;
       tail_row[gi] = tr;
       starts[gi] = nstart;
     }
     __syncthreads();
     if (tr >= 0) {  // this group holds the first entry of a shared row
-      T s = tail[gi][lane];
+      T s = tail[tid];
       for (int g = gi + 1; g < NG; ++g) {
         const int h = head_row[g];
         if (h == EMPTY) continue;
         if (h != tr) break;
-        V::add(s, head[g][lane]);
+        V::add(s, head[gtid(g) + lane]);
       }
       finish(tr, s);
     }
@@ -628,7 +639,7 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
     int owned = 0;
     for (int g = 0; g < NG; ++g) owned += starts[g];
     if (owned < r_hi - r_lo) {
-      for (int r = r_lo + (int)threadIdx.x; r < r_hi; r += 256) {
+      for (int r = r_lo + tid; r < r_hi; r += 256) {
         if (a.indptr[r] == a.indptr[r + 1]) {
           for (int c = c0; c < min(c_hi, c0 + CW); ++c) {
             float v = 0.f;
@@ -658,8 +669,7 @@ static double spmm_bytes(int32_t n, int64_t nnz, int32_t w) {
 #endif
 
 template <int G, bool VEC, int EPI, bool RAG>
-static void spmm_go(const SpmmArgs& a, const PlanDims& d, bool off32,
-                    hipStream_t s) {
+static void spmm_go(const SpmmArgs& a, bool off32, hipStream_t s) {
   const unsigned grid = (unsigned)((int64_t)a.nwin * a.nslices);
   if (off32)
     spmm_kernel<G, SPMM_DEPTH, VEC, EPI, true, RAG><<<grid, 256, 0, s>>>(a);
@@ -668,26 +678,30 @@ static void spmm_go(const SpmmArgs& a, const PlanDims& d, bool off32,
 }
 
 template <int G, bool VEC, bool RAG>
-static void spmm_epi(const SpmmArgs& a, const PlanDims& d, bool off32,
-                     hipStream_t s) {
+static void spmm_epi(const SpmmArgs& a, bool off32, hipStream_t s) {
   switch (a.epilogue) {
-    case SPMM_BIAS_RELU: return spmm_go<G, VEC, SPMM_BIAS_RELU, RAG>(a, d, off32, s);
-    case SPMM_ADD: return spmm_go<G, VEC, SPMM_ADD, RAG>(a, d, off32, s);
-    default: return spmm_go<G, VEC, SPMM_STORE, RAG>(a, d, off32, s);
+    case SPMM_BIAS_RELU: return spmm_go<G, VEC, SPMM_BIAS_RELU, RAG>(a, off32, s);
+    case SPMM_ADD: return spmm_go<G, VEC, SPMM_ADD, RAG>(a, off32, s);
+    default: return spmm_go<G, VEC, SPMM_STORE, RAG>(a, off32, s);
   }
 }
 
-// RAG: float4 lanes on a width that is not a multiple of 4 (the lane at the
-// row's end reads and writes its 1..3 columns one by one).
+// Lane group width for a slice row of `units` float4s (or floats): a power
+// of two covering it, or 10 lanes for the 10-unit rows of 8 slices (300
+// columns: six groups to a wavefront instead of four 16-lane groups with 6
+// idle lanes each, 8,000 x 300 aggregation 39.6 -> 35.8 us; with 16 slices,
+// 602 columns, 16 lanes stay faster: 44.4 against 45.8 us).  RAG: float4
+// lanes on a width that is not a multiple of 4 (the lane at the row's end
+// reads and writes its 1..3 columns one by one).
 template <bool VEC, bool RAG>
-static void spmm_dispatch(const SpmmArgs& a, const PlanDims& d, bool off32,
-                          hipStream_t s) {
+static void spmm_dispatch(const SpmmArgs& a, bool off32, hipStream_t s) {
   const int units = VEC ? ceil_div(a.sw, 4) : a.sw;  // column vectors per slice row
-  if (units <= 4) return spmm_epi<4, VEC, RAG>(a, d, off32, s);
-  if (units <= 8) return spmm_epi<8, VEC, RAG>(a, d, off32, s);
-  if (units <= 16) return spmm_epi<16, VEC, RAG>(a, d, off32, s);
-  if (units <= 32) return spmm_epi<32, VEC, RAG>(a, d, off32, s);
-  return spmm_epi<64, VEC, RAG>(a, d, off32, s);
+  if (units <= 4) return spmm_epi<4, VEC, RAG>(a, off32, s);
+  if (units <= 8) return spmm_epi<8, VEC, RAG>(a, off32, s);
+  if (units == 10 && a.nslices == 8) return spmm_epi<10, VEC, RAG>(a, off32, s);
+  if (units <= 16) return spmm_epi<16, VEC, RAG>(a, off32, s);
+  if (units <= 32) return spmm_epi<32, VEC, RAG>(a, off32, s);
+  return spmm_epi<64, VEC, RAG>(a, off32, s);
 }
 
 size_t spmm_partials_bytes(int32_t n, int64_t nnz, int32_t w) {
@@ -720,10 +734,10 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   a.mask = c.mask;
   a.ld_mask = c.ld_mask;
   a.weights = c.weights;
-  // 8 slices (one per XCD) from 32 columns up.  A lane group covers a
-  // power of two of float4 columns; when 8 slices need groups of more than
-  // 16 lanes with over a quarter of them idle (602 columns: 76-column
-  // slices on 32 lanes), 16 slices on 16-lane groups are faster, having
+  // 8 slices (one per XCD) from 32 columns up.  A lane group covers the
+  // float4 columns of a slice row (spmm_dispatch); when 8 slices need
+  // groups of more than 16 lanes with over a quarter of them idle (602
+  // columns: 76-column slices on 32 lanes), 16 slices are faster, having
   // twice the groups, and so the gathers, in flight per block.
   a.nslices = c.w >= 32 ? 8 : 1;
   a.sw = (int32_t)round_up(ceil_div(c.w, a.nslices), 4);
@@ -755,11 +769,11 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   const bool off32 = ((int64_t)(c.n - 1) * c.ld_in + c.w) * 4 < (int64_t(1) << 32);
   timer_begin(GNN_K_SPMM, s);
   if (vec && c.w % 4 != 0)
-    spmm_dispatch<true, true>(a, d, off32, s);
+    spmm_dispatch<true, true>(a, off32, s);
   else if (vec)
-    spmm_dispatch<true, false>(a, d, off32, s);
+    spmm_dispatch<true, false>(a, off32, s);
   else
-    spmm_dispatch<false, false>(a, d, off32, s);
+    spmm_dispatch<false, false>(a, off32, s);
   timer_end(GNN_K_SPMM, spmm_bytes(c.n, c.nnz, c.w), s);
   return hipGetLastError();
 }

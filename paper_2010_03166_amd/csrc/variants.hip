@@ -113,8 +113,14 @@ MixLayout mix_layout(const gnn_csr* csr, const gnn_layer* L, int32_t K) {
   size_t g = 0;
   const GemmBatch f = gemm1(0, 0, n, h, f_in, 0, f_in, 0, wy, 0, wy, 0, 1, L->flags);
   const GemmBatch w = gemm1(1, 0, f_in, h, n, 0, f_in, 0, wy, 0, wy, 0, 0, L->flags);
-  g = std::max(g, gemm_ws(K > 0 ? gemm2(f, f) : f));
-  g = std::max(g, gemm_ws(K > 0 ? gemm2(w, w) : w));
+  // hops go two per launch, the last one alone when K + 1 is odd; the work
+  // split (and so the workspace) differs between the two shapes
+  g = std::max(g, gemm_ws(f));
+  g = std::max(g, gemm_ws(w));
+  if (K > 0) {
+    g = std::max(g, gemm_ws(gemm2(f, f)));
+    g = std::max(g, gemm_ws(gemm2(w, w)));
+  }
   g = std::max(g, gemm_ws(gemm1(0, 1, n, f_in, h, 0, wy, 0, wy, 0, f_in, 0, 0, L->flags)));
   o.off_g = 0;
   o.off_r0 = round_up((size_t)n * o.ld_g * 4, 256);
