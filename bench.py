@@ -226,6 +226,9 @@ def main():
         roof_spmm["copy_gbs"] = round(copy_gbs, 1)
         roof_spmm["frac_of_copy"] = round(roof_spmm["achieved"] / copy_gbs, 4)
 
+    if roof_spmm is not None:
+        roof_spmm.update(gather_floor(torch, G, dg, wl.hidden, kernels["spmm"]["work"]))
+
     traffic = measured_traffic(name, dtype)
     if traffic.get(dom) is not None:
         roof["traffic"] = traffic[dom]
@@ -626,6 +629,36 @@ def bench_pipeline(G, runtime, synth, torch, np, args):
                          samp_ms, threads))
     del dev
     return res
+
+
+def gather_floor(torch, G, dg, w, bytes_per_launch, reps=50):
+    """The aggregation's gather order on this GPU without its row
+    bookkeeping (gnn_spmm_gather_floor: same grid, slices, lane groups,
+    entry order and loads, one sum per lane), timed beside gnn_spmm on the
+    same graph and width with events on the stream both run on: the floor
+    for this access pattern against which the aggregation is measured."""
+    x = torch.randn(dg.n, w, device="cuda")
+    out = torch.empty(dg.n, w, device="cuda")
+    csr = dg.struct()
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return 1e3 * e0.elapsed_time(e1) / reps
+
+    us_floor = timed(lambda: G.gnn_spmm_gather_floor(csr, 0, w, x, w, out, w))
+    us_spmm = timed(lambda: G.gnn_spmm(csr, 0, w, x, w, out, w, None))
+    del x, out
+    return {"gather_floor_us": round(us_floor, 2),
+            "spmm_same_call_us": round(us_spmm, 2),
+            "frac_of_gather_floor": round(us_floor / us_spmm, 4),
+            "gather_floor_gbs": round(bytes_per_launch / (us_floor * 1e3), 1)}
 
 
 def stream_copy_gbs(torch, mib: int = 512, reps: int = 5) -> float:

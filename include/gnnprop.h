@@ -463,6 +463,21 @@ gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
                     int64_t ld_out, void* workspace, size_t workspace_bytes,
                     hipStream_t stream);
 
+/* Measurement aid, not part of the method: the gathers of gnn_spmm alone.
+ * It runs gnn_spmm's grid, column slices, lane groups, entry order and
+ * loads (index, value, neighbour row slice) but keeps one sum per lane for
+ * all of its entries instead of one per row: no per-entry row reads, no row
+ * closing, no finishing of rows shared between lane groups.  Each plan
+ * window's column totals (in a fixed order) go to the window's first row,
+ * zeros to its other rows, so every row of `out` is written once and the
+ * column sums of `out` equal those of A_s . in (resp. (A_s)^T . in).  Its
+ * time bounds from below what the aggregation's gather order costs on the
+ * device.  Same arguments and checks as gnn_spmm (no workspace); rows of
+ * `in` and `out` must start 16-byte aligned (else GNN_ERR_UNSUPPORTED). */
+gnn_status gnn_spmm_gather_floor(const gnn_csr* csr, int32_t transpose,
+                                 int32_t w, const float* in, int64_t ld_in,
+                                 float* out, int64_t ld_out, hipStream_t stream);
+
 /* Dense weight transformation alone (Section 5.1's second kernel):
  *   C = op(A) op(B),  C is M x N (stride ldc),
  *   op(A) = A (M x K, stride lda)  or A^T with A stored K x M (trans_a = 1),

@@ -373,6 +373,23 @@ gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
   return GNN_OK;
 }
 
+gnn_status gnn_spmm_gather_floor(const gnn_csr* csr, int32_t transpose,
+                                 int32_t w, const float* in, int64_t ld_in,
+                                 float* out, int64_t ld_out, hipStream_t stream) {
+  gnn_status st = check_csr(csr, !transpose, transpose != 0);
+  if (st != GNN_OK) return st;
+  if (w < 0 || ld_in < w || ld_out < w) return GNN_ERR_SHAPE;
+  if (csr->n == 0 || w == 0) return GNN_OK;
+  if (!in || !out || !csr->plan) return GNN_ERR_NULL;
+  if (!vec4_ok(in, ld_in) || !vec4_ok(out, ld_out)) return GNN_ERR_UNSUPPORTED;
+  if (ranges_overlap(in, mat_bytes(csr->n, w, ld_in), out,
+                     mat_bytes(csr->n, w, ld_out)))
+    return GNN_ERR_ALIAS;
+  SpmmCall c = spmm_call(csr, transpose != 0, w, in, ld_in, out, ld_out);
+  GNN_HIP(spmm_floor_launch(c, stream));
+  return GNN_OK;
+}
+
 // Split products pre-split B into its bf16 pieces once (workspace, after
 // the partial tiles) when at least four row tiles of 128 share it: each
 // would otherwise split the same values again.

@@ -98,6 +98,9 @@ struct SpmmCall {
 };
 size_t spmm_partials_bytes(int32_t n, int64_t nnz, int32_t w);
 hipError_t spmm_launch(const SpmmCall& c, hipStream_t s);
+// The aggregation's loads and gathers alone (a measurement floor; float4
+// lanes only: hipErrorInvalidValue when rows are not 16-byte aligned).
+hipError_t spmm_floor_launch(const SpmmCall& c, hipStream_t s);
 
 hipError_t plan_build_launch(int32_t n, int64_t nnz, const int32_t* indptr,
                              const int32_t* indices, void* plan, hipStream_t s);

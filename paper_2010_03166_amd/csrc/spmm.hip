@@ -658,6 +658,117 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
   }
 }
 
+// Gather floor.  The aggregation's own loads in its own order, and nothing
+// else: the same grid, column slices, lane groups, entry ranges, batches of
+// G index / value loads and D gathers in flight, but one accumulator per
+// lane for all of the group's entries instead of one per row, no entry rows
+// read, no row closing and no LDS finish of shared rows.  The block's total
+// per column (summed over its groups in group order) is written to the
+// window's first row and zeros to its other rows, so that every output row
+// is still written once and the column sums of `out` equal those of
+// A_s . in.  Its time is what this gather order costs on the chip: the
+// floor against which the aggregation's own bookkeeping is measured.
+template <int G, int D, bool OFF32, bool RAG>
+__global__ __launch_bounds__(256) void spmm_floor_kernel(SpmmArgs a) {
+  using V = Vec<true>;
+  using T = typename V::T;
+  constexpr int gpw = 64 / G;
+  constexpr int NG = 4 * gpw;
+  constexpr int CW = G * V::W;
+  __shared__ T part[256];
+  auto gtid = [&](int g) { return (g / gpw) * 64 + (g % gpw) * G; };
+
+  int slice = 0, win = blockIdx.x;
+  if (a.nslices >= 8) {
+    const int per = 8 * a.nwin;
+    const int r = (int)(blockIdx.x % per);
+    slice = 8 * (int)(blockIdx.x / per) + (r & 7);
+    win = r >> 3;
+  }
+  const int k0 = win * a.wpb, k1 = min(k0 + a.wpb, a.nblk) - 1;
+  const int4 bi0 = a.binfo[k0], bi1 = a.binfo[k1];
+  const int r_lo = bi0.x, r_hi = bi1.y, B = bi0.z, E = bi1.w;
+  const int tid = threadIdx.x;
+  const int wl = tid & 63, lg = wl / G;
+  const bool member = lg < gpw;
+  const int gi = (tid >> 6) * gpw + lg;
+  const int lane = wl - lg * G;
+  const int base = lg * G;
+  const int gb = member ? B + (int)((int64_t)(E - B) * gi / NG) : 0;
+  const int ge = member ? B + (int)((int64_t)(E - B) * (gi + 1) / NG) : 0;
+  const int c_lo = slice * a.sw;
+  const int c_hi = min(a.w, c_lo + a.sw);
+  const float* __restrict__ in = a.in;
+  const int32_t* __restrict__ indices = a.indices;
+  const float* __restrict__ vals = a.vals;
+  const uint32_t ld_in = (uint32_t)a.ld_in;
+
+  for (int c0 = c_lo; c0 < c_hi; c0 += CW) {
+    const int col = c0 + lane * V::W;
+    const bool ok = member && col < c_hi;
+    const int nv = c_hi - col;
+    const bool prt = RAG && ok && nv < V::W;
+    auto ld = [&](const float* p) { return prt ? V::load_part(p, nv) : V::load(p); };
+    T acc = V::zero();
+    int ni = 0;
+    float nw = 0.f;
+    if (gb < ge && lane < ge - gb) {
+      ni = indices[gb + lane];
+      nw = vals[gb + lane];
+    }
+    for (int jb = gb; jb < ge; jb += G) {
+      const int cnt = min(G, ge - jb);
+      const int fi = ni;
+      const float fv = nw;
+      if (jb + G < ge) {
+        const int j2 = jb + G + lane;
+        const bool in_r = j2 < ge;
+        ni = in_r ? indices[j2] : 0;
+        nw = in_r ? vals[j2] : 0.f;
+      }
+      for (int k = 0; k < cnt; k += D) {
+        T x[D];
+#pragma unroll
+        for (int u = 0; u < D; ++u) {
+          const int idx = __shfl(fi, base + k + u);
+          if (k + u < cnt && ok) {
+            if (OFF32)
+              x[u] = ld(reinterpret_cast<const float*>(
+                  reinterpret_cast<const char*>(in) +
+                  (((uint32_t)idx * ld_in + (uint32_t)col) << 2)));
+            else
+              x[u] = ld(in + (int64_t)idx * a.ld_in + col);
+          } else {
+            x[u] = V::zero();
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < D; ++u) {
+          const float val = __shfl(fv, base + k + u);
+          if (k + u < cnt) V::fma(acc, val, x[u]);
+        }
+      }
+    }
+    part[tid] = acc;
+    __syncthreads();
+    if (member) {
+      for (int r = r_lo + gi; r < r_hi; r += NG) {
+        T v = V::zero();
+        if (r == r_lo)
+          for (int g = 0; g < NG; ++g) V::add(v, part[gtid(g) + lane]);
+        if (ok) {
+          float* dst = a.out + (int64_t)r * a.ld_out + col;
+          if (prt)
+            V::store_part(dst, v, nv);
+          else
+            V::store(dst, v);
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // Algorithmic bytes of one aggregation: row pointers, an index and a value
 // per stored entry, the n x w input read once and the output written once.
 static double spmm_bytes(int32_t n, int64_t nnz, int32_t w) {
@@ -711,8 +822,10 @@ size_t spmm_partials_bytes(int32_t n, int64_t nnz, int32_t w) {
   return 0;
 }
 
-hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
-  if (c.n <= 0 || c.w <= 0) return hipSuccess;
+// Launch arguments of an aggregation call: column slices, lane groups and
+// windows per workgroup; *vec: float4 lanes possible, *off32: 32-bit
+// gather offsets.
+static SpmmArgs spmm_args(const SpmmCall& c, bool* vec_out, bool* off32_out) {
   const PlanDims d = plan_dims(c.n, c.nnz);
   const char* base = static_cast<const char*>(c.plan);
   SpmmArgs a;
@@ -767,6 +880,15 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
                    (!c.mask || vec4_ok(c.mask, c.ld_mask));
   // Gather offsets in 32 bits when the input spans less than 4 GiB.
   const bool off32 = ((int64_t)(c.n - 1) * c.ld_in + c.w) * 4 < (int64_t(1) << 32);
+  *vec_out = vec;
+  *off32_out = off32;
+  return a;
+}
+
+hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
+  if (c.n <= 0 || c.w <= 0) return hipSuccess;
+  bool vec = false, off32 = false;
+  const SpmmArgs a = spmm_args(c, &vec, &off32);
   timer_begin(GNN_K_SPMM, s);
   if (vec && c.w % 4 != 0)
     spmm_dispatch<true, true>(a, off32, s);
@@ -775,6 +897,38 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   else
     spmm_dispatch<false, false>(a, off32, s);
   timer_end(GNN_K_SPMM, spmm_bytes(c.n, c.nnz, c.w), s);
+  return hipGetLastError();
+}
+
+template <int G, bool RAG>
+static void spmm_floor_go(const SpmmArgs& a, bool off32, hipStream_t s) {
+  const unsigned grid = (unsigned)((int64_t)a.nwin * a.nslices);
+  if (off32)
+    spmm_floor_kernel<G, SPMM_DEPTH, true, RAG><<<grid, 256, 0, s>>>(a);
+  else
+    spmm_floor_kernel<G, SPMM_DEPTH, false, RAG><<<grid, 256, 0, s>>>(a);
+}
+
+template <bool RAG>
+static void spmm_floor_dispatch(const SpmmArgs& a, bool off32, hipStream_t s) {
+  const int units = ceil_div(a.sw, 4);  // the lane groups of spmm_dispatch
+  if (units <= 4) return spmm_floor_go<4, RAG>(a, off32, s);
+  if (units <= 8) return spmm_floor_go<8, RAG>(a, off32, s);
+  if (units == 10 && a.nslices == 8) return spmm_floor_go<10, RAG>(a, off32, s);
+  if (units <= 16) return spmm_floor_go<16, RAG>(a, off32, s);
+  if (units <= 32) return spmm_floor_go<32, RAG>(a, off32, s);
+  return spmm_floor_go<64, RAG>(a, off32, s);
+}
+
+hipError_t spmm_floor_launch(const SpmmCall& c, hipStream_t s) {
+  if (c.n <= 0 || c.w <= 0) return hipSuccess;
+  bool vec = false, off32 = false;
+  const SpmmArgs a = spmm_args(c, &vec, &off32);
+  if (!vec) return hipErrorInvalidValue;
+  if (c.w % 4 != 0)
+    spmm_floor_dispatch<true>(a, off32, s);
+  else
+    spmm_floor_dispatch<false>(a, off32, s);
   return hipGetLastError();
 }
 

@@ -86,6 +86,10 @@ EXPORTS = {
                                   ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                   ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t,
                                   ctypes.c_void_p]),
+    "gnn_spmm_gather_floor": (ctypes.c_int32, [ctypes.POINTER(gnn_csr), ctypes.c_int32,
+                                               ctypes.c_int32, ctypes.c_void_p,
+                                               ctypes.c_int64, ctypes.c_void_p,
+                                               ctypes.c_int64, ctypes.c_void_p]),
     "gnn_gemm_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32] * 3),
     "gnn_gemm": (ctypes.c_int32, [ctypes.c_int32] * 5 + [
         ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
@@ -487,6 +491,13 @@ def gnn_spmm(csr: gnn_csr, transpose: bool, w: int, inp, ld_in: int, out,
     _check(lib().gnn_spmm(ctypes.byref(csr), int(transpose), int(w), _ptr(inp),
                           int(ld_in), _ptr(out), int(ld_out), _ptr(workspace),
                           _nbytes(workspace), _stream(stream)), "gnn_spmm")
+
+
+def gnn_spmm_gather_floor(csr: gnn_csr, transpose: bool, w: int, inp, ld_in: int,
+                          out, ld_out: int, stream=None):
+    _check(lib().gnn_spmm_gather_floor(ctypes.byref(csr), int(transpose), int(w),
+                                       _ptr(inp), int(ld_in), _ptr(out), int(ld_out),
+                                       _stream(stream)), "gnn_spmm_gather_floor")
 
 
 def gnn_gemm_workspace_bytes(M: int, N: int, K: int) -> int:

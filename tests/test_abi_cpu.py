@@ -138,6 +138,13 @@ def test_argument_errors_are_synchronous(lib):
                           None, None, P(xs + 8), P(0x40), P(0x50), ws, None) == -7
     # spmm / gemm
     assert L.gnn_spmm(ctypes.byref(c), 0, 8, P(0x10), 4, P(0x20), 8, None, 0, None) == -2
+    # gather floor: the same checks, plus 16-byte aligned rows
+    assert L.gnn_spmm_gather_floor(ctypes.byref(c), 0, 8, P(0x10), 4, P(0x20), 8, None) == -2
+    assert L.gnn_spmm_gather_floor(None, 0, 8, P(0x10), 8, P(0x20), 8, None) == -1
+    assert L.gnn_spmm_gather_floor(ctypes.byref(c), 0, 8, P(0x14), 8, P(0x20), 8, None) == -4
+    assert L.gnn_spmm_gather_floor(ctypes.byref(c), 0, 8, P(0x10), 9, P(0x20), 8, None) == -4
+    assert L.gnn_spmm_gather_floor(ctypes.byref(c), 0, 8, P(0x1000), 8, P(0x1010), 8,
+                                   None) == -7
     assert L.gnn_gemm(0, 0, 4, 4, 4, P(0x10), 3, P(0x20), 4, P(0x30), 4, 0, None, 0, None) == -2
     assert L.gnn_gemm(0, 0, 4, 4, 4, P(0x10), 4, P(0x20), 4, P(0x30), 4, 0x80, None, 0, None) == -4
     assert L.gnn_gemm(0, 0, -1, 4, 4, P(0x10), 4, P(0x20), 4, P(0x30), 4, 0, None, 0, None) == -2
@@ -235,3 +242,4 @@ def test_empty_problems_need_no_launch(lib):
     assert L.gnn_gemm(0, 0, 0, 4, 4, None, 4, None, 4, None, 4, 0, None, 0, None) == 0
     c = G.make_csr(0, 0, 0x1000, None, None, None, None)
     assert L.gnn_spmm(ctypes.byref(c), 0, 8, P(0x10), 8, P(0x20), 8, None, 0, None) == 0
+    assert L.gnn_spmm_gather_floor(ctypes.byref(c), 0, 8, P(0x10), 8, P(0x20), 8, None) == 0

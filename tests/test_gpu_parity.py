@@ -200,6 +200,38 @@ def test_spmm_two_windows_per_workgroup(w, transpose):
     assert maxrel(out, ref) <= TOL_SPMM
 
 
+FLOOR_CASES = [("powerlaw", 16), ("powerlaw", 300), ("star700", 512), ("boundary", 602),
+               ("random", 64), ("identity", 1030)]
+
+
+@pytest.mark.parametrize("name,w", FLOOR_CASES + [("workload", 512), ("workload", 602)])
+@pytest.mark.parametrize("transpose", [0, 1])
+def test_spmm_gather_floor_column_sums(name, w, transpose):
+    """The gather floor (a measurement aid) writes every output row once and
+    keeps the column sums of the aggregation: sum_v out[v, :] equals
+    1^T (A_s X) (resp. 1^T (A_s^T X)), up to fp32 summation error measured
+    against the column sums of |A_s| |X|."""
+    g = (synth.workload_graph(synth.WORKLOADS["cl2.1-n8000-f602-h512-L2"])
+         if name == "workload" else GRAPHS[name])
+    if g.n * w > 3_000_000 and name != "workload":
+        w = max(4, 3_000_000 // g.n // 4 * 4)
+    dg = prepared(g)
+    x = np.random.default_rng(w + 7).standard_normal((g.n, w)).astype(np.float32)
+    ld = (w + 3) // 4 * 4
+    xin, out = to_dev(x, ld), empty_out(g.n, w, ld)
+    G.gnn_spmm_gather_floor(dg.struct(), transpose, w, xin, ld, out, ld)
+    torch.cuda.synchronize()
+    o = out.cpu().numpy().astype(np.float64)
+    assert np.isfinite(o).all()
+    ref = (O.spmm_transpose(g, x) if transpose else O.spmm(g, x)).sum(axis=0)
+    # |A| |X| column sums (the transpose has the same entries, moved)
+    rows = np.repeat(np.arange(g.n), np.diff(g.indptr.astype(np.int64)))
+    src = rows if transpose else g.indices
+    absx = np.abs(x.astype(np.float64))
+    scale = (np.abs(g.values.astype(np.float64))[:, None] * absx[src]).sum(axis=0)
+    assert np.all(np.abs(o.sum(axis=0) - ref) <= 1e-5 * scale + 1e-30)
+
+
 def test_spmm_empty_graph_and_empty_rows():
     g = synth.symmetric_csr(6, np.array([[0, 1]]), self_loops=False)
     dg = prepared(g)
