@@ -44,7 +44,10 @@ struct LayerLayout {
   int order;
   int64_t ld_s, ld_p, ld_g, ld_gn, ld_v;
   size_t wp_words;  // split products: words of one weight's bf16 pieces
-  size_t off_buf0, off_buf1, off_gemm, off_cs, off_wp, total;
+  // GEMM workspace: [off_gemm, off_gemm_x) holds the weight gradients'
+  // partial tiles, which stay there until the input-gradient launch that
+  // follows sums them; [off_gemm_x, off_cs) serves every other launch
+  size_t off_buf0, off_buf1, off_gemm, off_gemm_x, off_cs, off_wp, total;
 };
 
 int resolve_order(const gnn_layer* L) {
@@ -204,11 +207,11 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
     buf0 = (size_t)n * o.ld_g * 4;  // G
     buf1 = (size_t)n * o.ld_v * 4;  // V
   }
-  size_t gemm = 0;
   const int32_t bf = gemm_mode(L->flags);
-  gemm = std::max(gemm, gemm_workspace_bytes(with_mode(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)));
-  gemm = std::max(gemm, gemm_workspace_bytes(with_mode(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 2 * h, 0, 2 * h, 0, 0), bf)));
-  gemm = std::max(gemm, gemm_workspace_bytes(with_mode(dx_batch(o.order, n, f_in, h, 0, 2 * h, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
+  const size_t gemm_w = gemm_workspace_bytes(with_mode(dw_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 2 * h, 0, 2 * h, 0, 0), bf));
+  const size_t gemm = std::max(
+      gemm_workspace_bytes(with_mode(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)),
+      gemm_workspace_bytes(with_mode(dx_batch(o.order, n, f_in, h, 0, 2 * h, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
   // split products: W_self and W_neigh as bf16 pieces, in the forward
   // product's orientation (K = f_in, N = h) or the input gradient's (K = h,
   // N = f_in), one at a time
@@ -217,7 +220,8 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   o.off_buf0 = 0;
   o.off_buf1 = round_up(buf0, 256);
   o.off_gemm = o.off_buf1 + round_up(buf1, 256);
-  o.off_cs = o.off_gemm + round_up(gemm, 256);
+  o.off_gemm_x = o.off_gemm + round_up(gemm_w, 256);
+  o.off_cs = o.off_gemm_x + round_up(gemm, 256);
   o.off_wp = o.off_cs + round_up(colsum_partials_bytes(n, h), 256);
   o.total = o.off_wp + 2 * round_up(o.wp_words * 4, 256);
   return o;
@@ -561,8 +565,13 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   char* ws = static_cast<char*>(workspace);
   float* buf0 = reinterpret_cast<float*>(ws + o.off_buf0);
   float* buf1 = reinterpret_cast<float*>(ws + o.off_buf1);
-  void* gws = ws + o.off_gemm;
-  const size_t gws_bytes = o.off_cs - o.off_gemm;
+  // weight gradients in one region; their reduction, if any, is held and
+  // run by the input-gradient launch, which uses the other region
+  void* wws = ws + o.off_gemm;
+  const size_t wws_bytes = o.off_gemm_x - o.off_gemm;
+  void* xws = ws + o.off_gemm_x;
+  const size_t xws_bytes = o.off_cs - o.off_gemm_x;
+  GemmFixup held;
   float* cspart = reinterpret_cast<float*>(ws + o.off_cs);
 
   const int32_t bf = gemm_mode(layer->flags);
@@ -599,7 +608,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, Gs,
                             ld_gs, T, ld_t, dW_self, dW_neigh);
     bw.mode = bf;
-    GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
+    GNN_HIP(gemm_launch(bw, wws, wws_bytes, stream, dX ? &held : nullptr));
     if (dX) {
       GemmBatch bx = dx_batch(2, n, f_in, h, Gs, ld_gs, T, ld_t, W_self,
                               W_neigh, dX, layer->ld_dx, nullptr, 0);
@@ -607,7 +616,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       bx.p[0].mask = dx_mask;
       bx.p[0].ld_mask = layer->ld_x;
       GNN_HIP(attach_weight_planes(bx, o, ws, W_self, W_neigh, f_in, h, stream));
-      GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
+      GNN_HIP(gemm_launch(bx, xws, xws_bytes, stream, nullptr, &held));
     }
     if (db_self) GNN_HIP(colsum_launch(n, h, Gs, ld_gs, db_self, cspart, stream));
     if (db_neigh) GNN_HIP(colsum_launch(n, h, Gn, ld_gn, db_neigh, cspart, stream));
@@ -628,13 +637,13 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     GemmBatch bw = dw_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, G, ld_g,
                             G + h, ld_g, dW_self, dW_neigh);
     bw.mode = bf;
-    GNN_HIP(gemm_launch(bw, gws, gws_bytes, stream));
+    GNN_HIP(gemm_launch(bw, wws, wws_bytes, stream, dX ? &held : nullptr));
     if (dX) {
       GemmBatch bx = dx_batch(1, n, f_in, h, G, ld_g, G + h, ld_g, W_self,
                               W_neigh, dX, layer->ld_dx, V, o.ld_v);
       bx.mode = bf;
       GNN_HIP(attach_weight_planes(bx, o, ws, W_self, W_neigh, f_in, h, stream));
-      GNN_HIP(gemm_launch(bx, gws, gws_bytes, stream));
+      GNN_HIP(gemm_launch(bx, xws, xws_bytes, stream, nullptr, &held));
       // dX = G_s W_s^T + A_s^T V, then the mask, in the aggregation epilogue
       SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx, rn);
       c.epilogue = SPMM_ADD;

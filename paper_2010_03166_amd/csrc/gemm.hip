@@ -252,6 +252,89 @@ __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 
+// Tiles shared by several blocks: add the blocks' partial tiles in block
+// order, then bias and ReLU.  Chunk c of tile t is 1024 elements, four
+// consecutive columns per thread of a 256-thread block.  Run by
+// gemm_fixup_kernel, or by extra blocks at the end of the next GEMM launch
+// on the stream (which reads the partials the earlier launch wrote).
+constexpr int FIX_CHUNKS = BM * BN / 1024;
+
+__device__ inline void fixup_chunk(const GemmKArgs& g, int t, int chunk) {
+  const int64_t first = (int64_t)t * g.ktiles, last = first + g.ktiles - 1;
+  int b0 = 0, b1 = 0;
+  if (g.splits <= 1) {
+    b0 = block_of(first, g.iters, g.nblocks);
+    b1 = block_of(last, g.iters, g.nblocks);
+    if (b0 == b1) return;  // written directly by its only block
+  }
+  const TileInfo ti = tile_info(g, t);
+  const GemmProblem& P = ti.pi ? g.p[1] : g.p[0];
+  const int e = chunk * 1024 + threadIdx.x * 4;
+  const int rl = e / BN, cl = e % BN;
+  const int row = ti.m0 + rl, col = ti.n0 + cl;
+  if (row >= g.M || col >= P.N || row < ti.r0) return;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (g.splits > 1) {
+    const float* src = g.part + (int64_t)t * (BM * BN) + e;
+    const int64_t st = (int64_t)g.tiles * (BM * BN);
+    int sp = 0;
+    for (; sp + 4 <= g.splits; sp += 4) {  // four partials in flight, in order
+      float4 p[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) p[u] = ld4(src + (sp + u) * st);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        v.x += p[u].x;
+        v.y += p[u].y;
+        v.z += p[u].z;
+        v.w += p[u].w;
+      }
+    }
+    for (; sp < g.splits; ++sp) {
+      const float4 p = ld4(src + sp * st);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+  } else {
+    for (int b = b0; b <= b1; ++b) {
+      // the tile is block b's first tile iff b's range starts inside it
+      const int slot = block_lo(b, g.iters, g.nblocks) >= first ? 0 : 1;
+      const float4 p = ld4(g.part + ((int64_t)b * 2 + slot) * (BM * BN) + e);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+  }
+  float o[4] = {v.x, v.y, v.z, v.w};
+  float* dst = P.C + (int64_t)row * P.ldc + col;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (col + u >= P.N) break;
+    if (col + u < ti.c0) continue;  // its neighbour's column
+    float x = o[u];
+    if (P.bias) x += P.bias[col + u];
+    if (P.relu) x = fmaxf(x, 0.f);
+    if (P.mask && !(P.mask[(int64_t)row * P.ld_mask + col + u] > 0.f)) x = 0.f;
+    dst[u] = x;
+  }
+}
+
+__global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
+  fixup_chunk(g, blockIdx.x, blockIdx.y);
+}
+
+// Blocks past the GEMM's own run the chunks of a reduction left by the
+// previous launch (`fx`, fx.tiles x FIX_CHUNKS of them); true for those.
+__device__ inline bool run_pending_fixup(const GemmKArgs& g, const GemmKArgs& fx) {
+  if ((int)blockIdx.x < g.nblocks) return false;
+  const int f = (int)blockIdx.x - g.nblocks;
+  fixup_chunk(fx, f / FIX_CHUNKS, f % FIX_CHUNKS);
+  return true;
+}
+
 // Two floats rounded to bf16 (round to nearest even), packed low, high.
 __device__ inline uint32_t pack_bf16(float lo, float hi) {
   bf16x2v v = {(__bf16)lo, (__bf16)hi};
@@ -259,7 +342,8 @@ __device__ inline uint32_t pack_bf16(float lo, float hi) {
 }
 
 template <bool AT, bool BT>
-__global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g) {
+__global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g, GemmKArgs fx) {
+  if (run_pending_fixup(g, fx)) return;
   constexpr bool A_KC = !AT;  // A row-major M x K: k contiguous
   constexpr bool B_KC = BT;   // B stored N x K: k contiguous
   constexpr int A_FLOATS = A_KC ? KC_FLOATS : XC_FLOATS;
@@ -575,7 +659,8 @@ __device__ inline int xc16_word(int kp, int x) {
 }
 
 template <bool AT, bool BT>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g) {
+__global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g, GemmKArgs fx) {
+  if (run_pending_fixup(g, fx)) return;
   constexpr bool A_KC = !AT;
   constexpr bool B_KC = BT;
   constexpr int A_WORDS = A_KC ? KC16_WORDS : XC16_WORDS;
@@ -848,7 +933,8 @@ __device__ inline void split3(float x0, float x1, uint32_t& h, uint32_t& m,
 // so a fragment is 1 KiB of consecutive bytes), one stage ahead of the
 // products that use them; only A goes through the split and LDS.
 template <bool AT, bool BT, bool BD>
-__global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g) {
+__global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKArgs fx) {
+  if (run_pending_fixup(g, fx)) return;
   constexpr bool A_KC = !AT;
   constexpr bool B_KC = BT;
   constexpr int A_PLANE = A_KC ? KCS_PLANE : XCS_PLANE;
@@ -1191,75 +1277,6 @@ hipError_t split_b_planes_launch(const float* B0, const float* B1, int64_t ld,
   return hipGetLastError();
 }
 
-// Tiles shared by several blocks: add the blocks' partial tiles in block
-// order, then bias and ReLU.  Block (t, c) handles 1024 elements of tile t,
-// four consecutive columns per thread.
-constexpr int FIX_CHUNKS = BM * BN / 1024;
-
-__global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
-  const int t = blockIdx.x;
-  const int64_t first = (int64_t)t * g.ktiles, last = first + g.ktiles - 1;
-  int b0 = 0, b1 = 0;
-  if (g.splits <= 1) {
-    b0 = block_of(first, g.iters, g.nblocks);
-    b1 = block_of(last, g.iters, g.nblocks);
-    if (b0 == b1) return;  // written directly by its only block
-  }
-  const TileInfo ti = tile_info(g, t);
-  const GemmProblem& P = ti.pi ? g.p[1] : g.p[0];
-  const int e = blockIdx.y * 1024 + threadIdx.x * 4;
-  const int rl = e / BN, cl = e % BN;
-  const int row = ti.m0 + rl, col = ti.n0 + cl;
-  if (row >= g.M || col >= P.N || row < ti.r0) return;
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (g.splits > 1) {
-    const float* src = g.part + (int64_t)t * (BM * BN) + e;
-    const int64_t st = (int64_t)g.tiles * (BM * BN);
-    int sp = 0;
-    for (; sp + 4 <= g.splits; sp += 4) {  // four partials in flight, in order
-      float4 p[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) p[u] = ld4(src + (sp + u) * st);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        v.x += p[u].x;
-        v.y += p[u].y;
-        v.z += p[u].z;
-        v.w += p[u].w;
-      }
-    }
-    for (; sp < g.splits; ++sp) {
-      const float4 p = ld4(src + sp * st);
-      v.x += p.x;
-      v.y += p.y;
-      v.z += p.z;
-      v.w += p.w;
-    }
-  } else {
-    for (int b = b0; b <= b1; ++b) {
-      // the tile is block b's first tile iff b's range starts inside it
-      const int slot = block_lo(b, g.iters, g.nblocks) >= first ? 0 : 1;
-      const float4 p = ld4(g.part + ((int64_t)b * 2 + slot) * (BM * BN) + e);
-      v.x += p.x;
-      v.y += p.y;
-      v.z += p.z;
-      v.w += p.w;
-    }
-  }
-  float o[4] = {v.x, v.y, v.z, v.w};
-  float* dst = P.C + (int64_t)row * P.ldc + col;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    if (col + u >= P.N) break;
-    if (col + u < ti.c0) continue;  // its neighbour's column
-    float x = o[u];
-    if (P.bias) x += P.bias[col + u];
-    if (P.relu) x = fmaxf(x, 0.f);
-    if (P.mask && !(P.mask[(int64_t)row * P.ld_mask + col + u] > 0.f)) x = 0.f;
-    dst[u] = x;
-  }
-}
-
 // ------------------------------------------------------------------ host
 
 struct Shape {
@@ -1354,8 +1371,25 @@ double gemm_flops(const GemmBatch& b) {
   return f;
 }
 
+// The reduction of a launch's shared tiles as its own kernel.
+static hipError_t fixup_launch(const GemmKArgs& g, hipStream_t s) {
+  timer_begin(GNN_K_GEMM_REDUCE, s);
+  gemm_fixup_kernel<<<dim3((unsigned)g.tiles, FIX_CHUNKS), 256, 0, s>>>(g);
+  timer_end(GNN_K_GEMM_REDUCE, 0.0, s);
+  return hipGetLastError();
+}
+
+hipError_t gemm_flush(const GemmFixup& fx, hipStream_t s) {
+  if (!fx.pending) return hipSuccess;
+  GemmKArgs g;
+  memcpy(&g, fx.args, sizeof(g));
+  return fixup_launch(g, s);
+}
+
 hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
-                       hipStream_t s) {
+                       hipStream_t s, GemmFixup* defer, const GemmFixup* pending) {
+  static_assert(sizeof(GemmKArgs) <= sizeof(GemmFixup::args), "GemmFixup size");
+  if (defer) defer->pending = 0;
   if (!batch_ok(b)) return hipErrorInvalidValue;
   if (b.b_planes) {  // split products only, every segment's planes given
     if (b.mode != GEMM_SPLIT) return hipErrorInvalidValue;
@@ -1364,7 +1398,7 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
         if (b.p[i].seg[k].K > 0 && !b.p[i].seg[k].Bp) return hipErrorInvalidValue;
   }
   const Shape sh = gemm_shape(b);
-  if (sh.tiles == 0) return hipSuccess;
+  if (sh.tiles == 0) return pending ? gemm_flush(*pending, s) : hipSuccess;
   GemmKArgs g;
   memset(&g, 0, sizeof(g));
   g.nprob = b.nprob;
@@ -1404,53 +1438,63 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
       return hipErrorInvalidValue;
     g.part = static_cast<float*>(workspace);
   }
-  const unsigned grid = (unsigned)sh.nblocks;
+  // a reduction left by the previous launch: its chunks as extra blocks
+  GemmKArgs fx;
+  memset(&fx, 0, sizeof(fx));
+  int extra = 0;
+  if (pending && pending->pending) {
+    memcpy(&fx, pending->args, sizeof(fx));
+    extra = fx.tiles * FIX_CHUNKS;
+  }
+  const unsigned grid = (unsigned)(sh.nblocks + extra);
   const int kid = b.trans_a ? (b.trans_b ? GNN_K_GEMM_TT : GNN_K_GEMM_TN)
                             : (b.trans_b ? GNN_K_GEMM_NT : GNN_K_GEMM_NN);
   timer_begin(kid, s);
   if (b.mode == GEMM_BF16) {
     if (!b.trans_a && !b.trans_b)
-      gemm_bf16_kernel<false, false><<<grid, 256, 0, s>>>(g);
+      gemm_bf16_kernel<false, false><<<grid, 256, 0, s>>>(g, fx);
     else if (b.trans_a && !b.trans_b)
-      gemm_bf16_kernel<true, false><<<grid, 256, 0, s>>>(g);
+      gemm_bf16_kernel<true, false><<<grid, 256, 0, s>>>(g, fx);
     else if (!b.trans_a && b.trans_b)
-      gemm_bf16_kernel<false, true><<<grid, 256, 0, s>>>(g);
+      gemm_bf16_kernel<false, true><<<grid, 256, 0, s>>>(g, fx);
     else
-      gemm_bf16_kernel<true, true><<<grid, 256, 0, s>>>(g);
+      gemm_bf16_kernel<true, true><<<grid, 256, 0, s>>>(g, fx);
   } else if (b.mode == GEMM_F32) {
     if (!b.trans_a && !b.trans_b)
-      gemm_f32_kernel<false, false><<<grid, 256, 0, s>>>(g);
+      gemm_f32_kernel<false, false><<<grid, 256, 0, s>>>(g, fx);
     else if (b.trans_a && !b.trans_b)
-      gemm_f32_kernel<true, false><<<grid, 256, 0, s>>>(g);
+      gemm_f32_kernel<true, false><<<grid, 256, 0, s>>>(g, fx);
     else if (!b.trans_a && b.trans_b)
-      gemm_f32_kernel<false, true><<<grid, 256, 0, s>>>(g);
+      gemm_f32_kernel<false, true><<<grid, 256, 0, s>>>(g, fx);
     else
-      gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g);
+      gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g, fx);
   } else if (b.b_planes) {
     if (!b.trans_a && !b.trans_b)
-      gemm_split_kernel<false, false, true><<<grid, 256, 0, s>>>(g);
+      gemm_split_kernel<false, false, true><<<grid, 256, 0, s>>>(g, fx);
     else if (b.trans_a && !b.trans_b)
-      gemm_split_kernel<true, false, true><<<grid, 256, 0, s>>>(g);
+      gemm_split_kernel<true, false, true><<<grid, 256, 0, s>>>(g, fx);
     else if (!b.trans_a && b.trans_b)
-      gemm_split_kernel<false, true, true><<<grid, 256, 0, s>>>(g);
+      gemm_split_kernel<false, true, true><<<grid, 256, 0, s>>>(g, fx);
     else
-      gemm_split_kernel<true, true, true><<<grid, 256, 0, s>>>(g);
+      gemm_split_kernel<true, true, true><<<grid, 256, 0, s>>>(g, fx);
   } else if (!b.trans_a && !b.trans_b) {
-    gemm_split_kernel<false, false, false><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<false, false, false><<<grid, 256, 0, s>>>(g, fx);
   } else if (b.trans_a && !b.trans_b) {
-    gemm_split_kernel<true, false, false><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<true, false, false><<<grid, 256, 0, s>>>(g, fx);
   } else if (!b.trans_a && b.trans_b) {
-    gemm_split_kernel<false, true, false><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<false, true, false><<<grid, 256, 0, s>>>(g, fx);
   } else {
-    gemm_split_kernel<true, true, false><<<grid, 256, 0, s>>>(g);
+    gemm_split_kernel<true, true, false><<<grid, 256, 0, s>>>(g, fx);
   }
   timer_end(kid, gemm_flops(b), s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !streamk) return e;
-  timer_begin(GNN_K_GEMM_REDUCE, s);
-  gemm_fixup_kernel<<<dim3((unsigned)sh.tiles, FIX_CHUNKS), 256, 0, s>>>(g);
-  timer_end(GNN_K_GEMM_REDUCE, 0.0, s);
-  return hipGetLastError();
+  if (defer) {  // the next launch (or gemm_flush) sums the shared tiles
+    memcpy(defer->args, &g, sizeof(g));
+    defer->pending = 1;
+    return hipSuccess;
+  }
+  return fixup_launch(g, s);
 }
 
 }  // namespace gnnprop

@@ -180,8 +180,23 @@ hipError_t split_b_planes_launch(const float* B0, const float* B1, int64_t ld,
                                  uint32_t* planes0, uint32_t* planes1,
                                  hipStream_t s);
 size_t gemm_workspace_bytes(const GemmBatch& b);
+// The reduction of a stream-K or split-K launch's shared tiles, held back so
+// that the next GEMM launch on the stream runs it in extra blocks of its own
+// grid instead of a kernel of its own.  The held launch's partial tiles
+// (its workspace) must stay untouched until then: the next launch takes
+// another workspace region.
+struct GemmFixup {
+  int32_t pending = 0;
+  alignas(16) unsigned char args[512];  // the held launch's kernel arguments
+};
+// `defer`: if the launch needs a reduction, hold it in *defer instead of
+// running it.  `pending`: a held reduction to run in this launch (or alone
+// when this launch has no tiles).
 hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
-                       hipStream_t s);
+                       hipStream_t s, GemmFixup* defer = nullptr,
+                       const GemmFixup* pending = nullptr);
+// Runs a held reduction as a kernel of its own (no-op if none is held).
+hipError_t gemm_flush(const GemmFixup& fx, hipStream_t s);
 double gemm_flops(const GemmBatch& b);
 
 // ----------------------------------------------------- elementwise
