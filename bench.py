@@ -77,6 +77,9 @@ def parse():
                          "(the layer below skips its masking pass)")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the step replayed from a HIP graph")
+    ap.add_argument("--no-floor", action="store_true",
+                    help="skip the aggregation's gather floor (keeps a profile of the "
+                         "step free of its standalone launches)")
     ap.add_argument("--no-rownorm", action="store_true",
                     help="skip the step with GNN_FLAG_ROW_NORMALIZED")
     ap.add_argument("--no-configs", action="store_true",
@@ -226,7 +229,7 @@ def main():
         roof_spmm["copy_gbs"] = round(copy_gbs, 1)
         roof_spmm["frac_of_copy"] = round(roof_spmm["achieved"] / copy_gbs, 4)
 
-    if roof_spmm is not None:
+    if roof_spmm is not None and not args.no_floor:
         roof_spmm.update(gather_floor(torch, G, dg, wl.hidden, kernels["spmm"]["work"]))
 
     traffic = measured_traffic(name, dtype)

@@ -162,7 +162,9 @@ gnn_status check_gat(const gnn_csr* csr, const gnn_layer* L, float alpha) {
 struct GatLayout {
   int64_t ld_h, ld_n;
   size_t s_p, s_s, s_t, s_att, saved;
-  size_t w_g, w_dp, w_dz, w_dzt, w_att_t, w_dsdt, w_cs, w_gemm, total;
+  // GEMM workspace: [w_gemm, w_gemm_x) the weight gradient's partial tiles,
+  // summed by the input-gradient launch; [w_gemm_x, total) the rest
+  size_t w_g, w_dp, w_dz, w_dzt, w_att_t, w_dsdt, w_cs, w_gemm, w_gemm_x, total;
 };
 
 GatLayout gat_layout(const gnn_csr* csr, const gnn_layer* L) {
@@ -179,10 +181,11 @@ GatLayout gat_layout(const gnn_csr* csr, const gnn_layer* L) {
   o.s_t = o.s_s + nb;
   o.s_att = o.s_t + nb;
   o.saved = o.s_att + eb;
-  size_t g = 0;
-  g = std::max(g, gemm_workspace_bytes(gemm1(0, 0, n, h, f_in, 0, f_in, 0, h, 0, h, 0, L->flags)));
-  g = std::max(g, gemm_workspace_bytes(gemm1(1, 0, f_in, h, n, 0, f_in, 0, h, 0, h, 0, L->flags)));
-  g = std::max(g, gemm_workspace_bytes(gemm1(0, 1, n, f_in, h, 0, h, 0, h, 0, f_in, 0, L->flags)));
+  const size_t gw =
+      gemm_workspace_bytes(gemm1(1, 0, f_in, h, n, 0, f_in, 0, h, 0, h, 0, L->flags));
+  const size_t g = std::max(
+      gemm_workspace_bytes(gemm1(0, 0, n, h, f_in, 0, f_in, 0, h, 0, h, 0, L->flags)),
+      gemm_workspace_bytes(gemm1(0, 1, n, f_in, h, 0, h, 0, h, 0, f_in, 0, L->flags)));
   o.w_g = 0;
   o.w_dp = nh;
   o.w_dz = o.w_dp + nh;
@@ -191,7 +194,8 @@ GatLayout gat_layout(const gnn_csr* csr, const gnn_layer* L) {
   o.w_dsdt = o.w_att_t + eb;
   o.w_cs = o.w_dsdt + round_up((size_t)2 * o.ld_n * 4, 256);
   o.w_gemm = o.w_cs + colsum_partials_bytes(n, h, 2);
-  o.total = o.w_gemm + round_up(g, 256);
+  o.w_gemm_x = o.w_gemm + round_up(gw, 256);
+  o.total = o.w_gemm_x + round_up(g, 256);
   return o;
 }
 
@@ -348,11 +352,16 @@ gnn_status gnn_gat_bwd(const gnn_csr* csr, const gnn_layer* layer, const float* 
   // dX = dP W^T
   float* cspart = reinterpret_cast<float*>(ws + o.w_cs);
   GNN_HIP(colsum2_launch(n, h, P, o.ld_h, ds, dt, da, da + h, cspart, stream));
+  // the weight gradient's reduction, if any, runs in the input-gradient
+  // launch, which takes the other workspace region
+  GemmFixup held;
   GNN_HIP(gemm_launch(gemm1(1, 0, f_in, h, n, X, layer->ld_x, dP, o.ld_h, dW, h, 0,
-                            layer->flags), gws, gws_bytes, stream));
+                            layer->flags), ws + o.w_gemm, o.w_gemm_x - o.w_gemm, stream,
+                      dX ? &held : nullptr));
   if (dX)
     GNN_HIP(gemm_launch(gemm1(0, 1, n, f_in, h, dP, o.ld_h, W, h, dX, layer->ld_dx, 0,
-                              layer->flags), gws, gws_bytes, stream));
+                              layer->flags), ws + o.w_gemm_x, o.total - o.w_gemm_x, stream,
+                        nullptr, &held));
   return GNN_OK;
 }
 

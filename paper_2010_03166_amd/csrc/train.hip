@@ -182,7 +182,9 @@ inline unsigned update_grid(int64_t count) {
 struct ClsLayout {
   int64_t ld_c;
   int nblk;
-  size_t off_m, off_g, off_part, off_gemm, total;
+  // GEMM workspace: [off_gemm, off_gemm_x) the weight gradient's partial
+  // tiles, summed by the input-gradient launch; [off_gemm_x, total) the rest
+  size_t off_m, off_g, off_part, off_gemm, off_gemm_x, total;
 };
 
 GemmBatch prod(int ta, int tb, int32_t M, int32_t N, int32_t K, const float* A,
@@ -208,15 +210,16 @@ ClsLayout cls_layout(int32_t n, int32_t f, int32_t C, uint32_t flags) {
   ClsLayout o;
   o.ld_c = round_up(C, 4);
   o.nblk = (int)std::max<int64_t>(1, ceil_div(n, LOSS_ROWS));
-  size_t g = 0;
-  g = std::max(g, gemm_workspace_bytes(prod(0, 0, n, C, f, 0, f, 0, C, 0, C, 1, flags)));
-  g = std::max(g, gemm_workspace_bytes(prod(1, 0, f, C, n, 0, f, 0, C, 0, C, 0, flags)));
-  g = std::max(g, gemm_workspace_bytes(prod(0, 1, n, f, C, 0, C, 0, C, 0, f, 0, flags)));
+  const size_t gw = gemm_workspace_bytes(prod(1, 0, f, C, n, 0, f, 0, C, 0, C, 0, flags));
+  const size_t g =
+      std::max(gemm_workspace_bytes(prod(0, 0, n, C, f, 0, f, 0, C, 0, C, 1, flags)),
+               gemm_workspace_bytes(prod(0, 1, n, f, C, 0, C, 0, C, 0, f, 0, flags)));
   o.off_m = 0;
   o.off_g = round_up((size_t)n * o.ld_c * 4, 256);
   o.off_part = o.off_g + round_up((size_t)n * o.ld_c * 4, 256);
   o.off_gemm = o.off_part + round_up((size_t)o.nblk * 4, 256);
-  o.total = o.off_gemm + round_up(g, 256);
+  o.off_gemm_x = o.off_gemm + round_up(gw, 256);
+  o.total = o.off_gemm_x + round_up(g, 256);
   return o;
 }
 
@@ -290,11 +293,14 @@ gnn_status gnn_classifier(int32_t n, int32_t f, int32_t C, int32_t kind,
     GNN_HIP(hipGetLastError());
     return GNN_OK;
   }
+  // the weight gradient's reduction, if any, runs in the input-gradient
+  // launch, which takes the other workspace region
+  GemmFixup held;
   GNN_HIP(gemm_launch(prod(1, 0, f, C, n, X, ld_x, G, o.ld_c, dW, C, 0, flags), gws,
-                      gws_bytes, stream));
+                      o.off_gemm_x - o.off_gemm, stream, dX ? &held : nullptr));
   if (dX)
-    GNN_HIP(gemm_launch(prod(0, 1, n, f, C, G, o.ld_c, W, C, dX, ld_dx, 0, flags), gws,
-                        gws_bytes, stream));
+    GNN_HIP(gemm_launch(prod(0, 1, n, f, C, G, o.ld_c, W, C, dX, ld_dx, 0, flags),
+                        ws + o.off_gemm_x, o.total - o.off_gemm_x, stream, nullptr, &held));
   return GNN_OK;
 }
 

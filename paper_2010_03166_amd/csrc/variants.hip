@@ -71,7 +71,9 @@ size_t gemm_ws(const GemmBatch& b) { return gemm_workspace_bytes(b); }
 struct GcnLayout {
   int order;
   int64_t ld_s, ld_h, ld_b;
-  size_t off_a, off_b, off_gemm, off_cs, total;
+  // GEMM workspace: [off_gemm, off_gemm_x) the weight gradient's partial
+  // tiles, summed by the input-gradient launch; [off_gemm_x, off_cs) the rest
+  size_t off_a, off_b, off_gemm, off_gemm_x, off_cs, total;
 };
 
 GcnLayout gcn_layout(const gnn_csr* csr, const gnn_layer* L) {
@@ -83,14 +85,15 @@ GcnLayout gcn_layout(const gnn_csr* csr, const gnn_layer* L) {
   o.ld_b = std::max(o.ld_h, o.ld_s);
   const size_t a = (size_t)n * o.ld_h * 4;  // P or G
   const size_t b = (size_t)n * o.ld_b * 4;  // T or V
-  size_t g = 0;
-  g = std::max(g, gemm_ws(gemm1(0, 0, n, h, f_in, 0, f_in, 0, h, 0, h, 0, 0, L->flags)));
-  g = std::max(g, gemm_ws(gemm1(1, 0, f_in, h, n, 0, f_in, 0, h, 0, h, 0, 0, L->flags)));
-  g = std::max(g, gemm_ws(gemm1(0, 1, n, f_in, h, 0, h, 0, h, 0, f_in, 0, 0, L->flags)));
+  const size_t gw = gemm_ws(gemm1(1, 0, f_in, h, n, 0, f_in, 0, h, 0, h, 0, 0, L->flags));
+  const size_t g =
+      std::max(gemm_ws(gemm1(0, 0, n, h, f_in, 0, f_in, 0, h, 0, h, 0, 0, L->flags)),
+               gemm_ws(gemm1(0, 1, n, f_in, h, 0, h, 0, h, 0, f_in, 0, 0, L->flags)));
   o.off_a = 0;
   o.off_b = round_up(a, 256);
   o.off_gemm = o.off_b + round_up(b, 256);
-  o.off_cs = o.off_gemm + round_up(g, 256);
+  o.off_gemm_x = o.off_gemm + round_up(gw, 256);
+  o.off_cs = o.off_gemm_x + round_up(g, 256);
   o.total = o.off_cs + colsum_partials_bytes(n, h);
   return o;
 }
@@ -99,7 +102,11 @@ GcnLayout gcn_layout(const gnn_csr* csr, const gnn_layer* L) {
 
 struct MixLayout {
   int64_t ld_s, ld_g, ld_r;
-  size_t saved, off_g, off_r0, off_r1, off_gemm, off_cs, total;
+  // GEMM workspace: the weight-gradient launches' partial tiles alternate
+  // between [off_gemm, off_gemm + gw) and the gw bytes after it (each
+  // launch sums its predecessor's, the first input-gradient launch the
+  // last's); [off_gemm_x, off_cs) serves the other launches
+  size_t saved, off_g, off_r0, off_r1, off_gemm, gw, off_gemm_x, off_cs, total;
 };
 
 MixLayout mix_layout(const gnn_csr* csr, const gnn_layer* L, int32_t K) {
@@ -110,23 +117,25 @@ MixLayout mix_layout(const gnn_csr* csr, const gnn_layer* L, int32_t K) {
   o.ld_g = round_up(wy, 4);
   o.ld_r = round_up(f_in, 4);
   o.saved = (size_t)K * n * o.ld_s * 4;
-  size_t g = 0;
+  size_t g = 0, gw = 0;
   const GemmBatch f = gemm1(0, 0, n, h, f_in, 0, f_in, 0, wy, 0, wy, 0, 1, L->flags);
   const GemmBatch w = gemm1(1, 0, f_in, h, n, 0, f_in, 0, wy, 0, wy, 0, 0, L->flags);
   // hops go two per launch, the last one alone when K + 1 is odd; the work
   // split (and so the workspace) differs between the two shapes
   g = std::max(g, gemm_ws(f));
-  g = std::max(g, gemm_ws(w));
+  gw = std::max(gw, gemm_ws(w));
   if (K > 0) {
     g = std::max(g, gemm_ws(gemm2(f, f)));
-    g = std::max(g, gemm_ws(gemm2(w, w)));
+    gw = std::max(gw, gemm_ws(gemm2(w, w)));
   }
   g = std::max(g, gemm_ws(gemm1(0, 1, n, f_in, h, 0, wy, 0, wy, 0, f_in, 0, 0, L->flags)));
+  o.gw = round_up(gw, 256);
   o.off_g = 0;
   o.off_r0 = round_up((size_t)n * o.ld_g * 4, 256);
   o.off_r1 = o.off_r0 + round_up((size_t)n * o.ld_r * 4, 256);
   o.off_gemm = o.off_r1 + round_up((size_t)n * o.ld_r * 4, 256);
-  o.off_cs = o.off_gemm + round_up(g, 256);
+  o.off_gemm_x = o.off_gemm + (K >= 2 ? 2 : 1) * o.gw;  // K >= 2: several dW launches
+  o.off_cs = o.off_gemm_x + round_up(g, 256);
   o.total = o.off_cs + colsum_partials_bytes(n, wy);
   return o;
 }
@@ -215,28 +224,34 @@ gnn_status gnn_gcn_bwd(const gnn_csr* csr, const gnn_layer* layer,
   char* ws = static_cast<char*>(workspace);
   float* G = reinterpret_cast<float*>(ws + o.off_a);
   float* B = reinterpret_cast<float*>(ws + o.off_b);
-  void* gws = ws + o.off_gemm;
-  const size_t gws_bytes = o.off_cs - o.off_gemm;
+  // the weight gradient's reduction, if any, is held for the input-gradient
+  // launch, which takes the other workspace region
+  void* wws = ws + o.off_gemm;
+  const size_t wws_bytes = o.off_gemm_x - o.off_gemm;
+  void* xws = ws + o.off_gemm_x;
+  const size_t xws_bytes = o.off_cs - o.off_gemm_x;
+  GemmFixup held;
   float* cspart = reinterpret_cast<float*>(ws + o.off_cs);
   GNN_HIP(mask_launch(n, h, h, Y, dY, layer->ld_y, G, o.ld_h, nullptr, 0, stream));
   if (o.order == 1) {
     const float* S = static_cast<const float*>(saved);
     GNN_HIP(gemm_launch(gemm1(1, 0, f_in, h, n, S, o.ld_s, G, o.ld_h, dW, h, nullptr, 0,
-                              layer->flags), gws, gws_bytes, stream));
+                              layer->flags), wws, wws_bytes, stream, dX ? &held : nullptr));
     if (dX) {
       float* V = B;
       GNN_HIP(gemm_launch(gemm1(0, 1, n, f_in, h, G, o.ld_h, W, h, V, o.ld_b, nullptr, 0,
-                                layer->flags), gws, gws_bytes, stream));
+                                layer->flags), xws, xws_bytes, stream, nullptr, &held));
       GNN_HIP(spmm_launch(spmm_call(csr, true, f_in, V, o.ld_b, dX, layer->ld_dx), stream));
     }
   } else {
     float* T = B;
     GNN_HIP(spmm_launch(spmm_call(csr, true, h, G, o.ld_h, T, o.ld_b), stream));
     GNN_HIP(gemm_launch(gemm1(1, 0, f_in, h, n, X, layer->ld_x, T, o.ld_b, dW, h, nullptr,
-                              0, layer->flags), gws, gws_bytes, stream));
+                              0, layer->flags), wws, wws_bytes, stream, dX ? &held : nullptr));
     if (dX)
       GNN_HIP(gemm_launch(gemm1(0, 1, n, f_in, h, T, o.ld_b, W, h, dX, layer->ld_dx,
-                                nullptr, 0, layer->flags), gws, gws_bytes, stream));
+                                nullptr, 0, layer->flags), xws, xws_bytes, stream, nullptr,
+                          &held));
   }
   if (db) GNN_HIP(colsum_launch(n, h, G, o.ld_h, db, cspart, stream));
   return GNN_OK;
@@ -334,8 +349,8 @@ gnn_status gnn_mixhop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   float* G = reinterpret_cast<float*>(ws + o.off_g);
   float* R[2] = {reinterpret_cast<float*>(ws + o.off_r0),
                  reinterpret_cast<float*>(ws + o.off_r1)};
-  void* gws = ws + o.off_gemm;
-  const size_t gws_bytes = o.off_cs - o.off_gemm;
+  void* xws = ws + o.off_gemm_x;
+  const size_t xws_bytes = o.off_cs - o.off_gemm_x;
   float* cspart = reinterpret_cast<float*>(ws + o.off_cs);
   const float* Sv = static_cast<const float*>(saved);
   auto S = [&](int k) -> const float* {
@@ -343,15 +358,22 @@ gnn_status gnn_mixhop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   };
   auto ldS = [&](int k) { return k == 0 ? layer->ld_x : o.ld_s; };
   GNN_HIP(mask_launch(n, wy, wy, Y, dY, layer->ld_y, G, o.ld_g, nullptr, 0, stream));
-  // dW_k = S_k^T G_k, two hops per launch
+  // dW_k = S_k^T G_k, two hops per launch; each launch's reduction is held
+  // and summed by extra blocks of the next GEMM launch (the partial tiles
+  // alternate between two regions)
   auto dw = [&](int k) {
     return gemm1(1, 0, f_in, h, n, S(k), ldS(k), G + (size_t)k * h, o.ld_g,
                  dW + (size_t)k * h, wy, nullptr, 0, layer->flags);
   };
-  for (int k = 0; k <= K; k += 2) {
+  GemmFixup held[2];
+  const GemmFixup* pend = nullptr;
+  for (int k = 0, i = 0; k <= K; k += 2, ++i) {
     const GemmBatch bt = k + 1 <= K ? gemm2(dw(k), dw(k + 1)) : dw(k);
-    GNN_HIP(gemm_launch(bt, gws, gws_bytes, stream));
+    GNN_HIP(gemm_launch(bt, ws + o.off_gemm + (i & 1) * o.gw, o.gw, stream, &held[i & 1],
+                        pend));
+    pend = &held[i & 1];
   }
+  if (!dX && pend) GNN_HIP(gemm_flush(*pend, stream));
   if (db) GNN_HIP(colsum_launch(n, wy, G, o.ld_g, db, cspart, stream));
   if (dX) {
     // Horner: R = G_K W_K^T;  R = G_k W_k^T + A_hat^T R for k = K-1 .. 0,
@@ -363,11 +385,11 @@ gnn_status gnn_mixhop_bwd(const gnn_csr* csr, const gnn_layer* layer,
     int cur = 0;
     float* r = K == 0 ? dX : R[cur];
     int64_t ld_r = K == 0 ? layer->ld_dx : o.ld_r;
-    GNN_HIP(gemm_launch(vk(K, r, ld_r), gws, gws_bytes, stream));
+    GNN_HIP(gemm_launch(vk(K, r, ld_r), xws, xws_bytes, stream, nullptr, pend));
     for (int k = K - 1; k >= 0; --k) {
       float* nx = k == 0 ? dX : R[cur ^ 1];
       const int64_t ld_nx = k == 0 ? layer->ld_dx : o.ld_r;
-      GNN_HIP(gemm_launch(vk(k, nx, ld_nx), gws, gws_bytes, stream));
+      GNN_HIP(gemm_launch(vk(k, nx, ld_nx), xws, xws_bytes, stream));
       SpmmCall c = spmm_call(csr, true, f_in, r, ld_r, nx, ld_nx);
       c.epilogue = SPMM_ADD;
       c.res = nx;

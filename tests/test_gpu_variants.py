@@ -155,7 +155,7 @@ def run_mixhop(g, K, f_in, h, bias, seed=0, pad=8, want_dx=True, flags=0):
 
 
 @pytest.mark.parametrize("name", list(GRAPHS))
-@pytest.mark.parametrize("K", [0, 1, 2, 3])
+@pytest.mark.parametrize("K", [0, 1, 2, 3, 4])
 def test_mixhop_layer_parity(name, K):
     g = GRAPHS[name]
     bias = K % 2 == 1
@@ -177,12 +177,15 @@ def test_mixhop_f32_mfma_mode():
         assert maxrel(r[k], ref[k]) <= TOL, k
 
 
-def test_mixhop_without_dx_and_unaligned_widths():
+@pytest.mark.parametrize("K", [2, 4])
+def test_mixhop_without_dx_and_unaligned_widths(K):
+    """Without dX the last weight-gradient launch's reduction runs on its
+    own (K = 4: three launches, each summing its predecessor's tiles)."""
     g = GRAPHS["random"]
-    r = run_mixhop(g, 2, 13, 7, True, pad=1, want_dx=False)
+    r = run_mixhop(g, K, 13, 7, True, pad=1, want_dx=False)
     assert maxrel(r["Y"], r["Y_ref"]) <= TOL
     decision_flips(r["Y"], r["Y_ref"], TOL)
-    ref = O.mixhop_bwd(g, r["x"], r["w"], 2, r["Y32"], r["dy"], want_dx=False, want_db=True)
+    ref = O.mixhop_bwd(g, r["x"], r["w"], K, r["Y32"], r["dy"], want_dx=False, want_db=True)
     assert maxrel(r["dW"], ref["dW"]) <= TOL and maxrel(r["db"], ref["db"]) <= TOL
 
 
