@@ -410,9 +410,13 @@ size_t gnn_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
   b.p[0].M = M;
   b.p[0].N = N;
   b.p[0].seg[0].K = K;
-  const size_t f32 = gemm_workspace_bytes(b);
-  b.mode = GEMM_BF16;
-  const size_t part = round_up(std::max(f32, gemm_workspace_bytes(b)), 256);
+  // the largest need of the three product modes (their work splits differ)
+  size_t need = 0;
+  for (const int32_t mode : {GEMM_SPLIT, GEMM_BF16, GEMM_F32}) {
+    b.mode = mode;
+    need = std::max(need, gemm_workspace_bytes(b));
+  }
+  const size_t part = round_up(need, 256);
   return part + (gemm_presplit_b(M, GEMM_SPLIT) ? round_up(b_planes_words(K, N) * 4, 256) : 0);
 }
 

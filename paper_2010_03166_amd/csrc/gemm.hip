@@ -1315,11 +1315,15 @@ static Shape gemm_shape(const GemmBatch& b) {
   // 256 tiles) over at most 40 K slices runs one block per tile: measured
   // faster than stream-K plus its reduction (8000 x 512, K = 602: 65.5
   // against 61.3 + 12.2 us), slower from K = 2048 on.  With split products
-  // the same holds up to one tile per slot over K = 2048 (8000 x 602, K =
-  // 1024, 315 tiles: 90.0 us against 89.1 for stream-K with its reduction),
-  // which then writes no partial tiles and needs no second launch.
-  // The rules count K in 32-deep slices whatever the kernel's stage depth
-  // (the split kernel's stages are 16 deep).
+  // and with bf16 operands the same holds up to one tile per slot over K =
+  // 2048 (8000 x 602, K = 1024, 315 tiles: 90.0 us against 89.1 for
+  // stream-K with its reduction; bf16 39.2 against 55.1 us), which then
+  // writes no partial tiles and needs no second launch; the fp32-MFMA
+  // kernel keeps stream-K there (114.0 against 142.4 us).
+  // The rules count K in the fp32 kernel's 32-deep slices for the split
+  // kernel (two of its 16-deep stages each) and in its own stages for the
+  // others (the bf16 kernel's are 64 deep, so its short-K launches stay on
+  // one block per tile).
   const int slots = MAX_BLOCKS;
   const int64_t rounds = ceil_div(s.tiles, slots);
   const double fill = (double)s.tiles / (double)(rounds * slots);
@@ -1327,7 +1331,7 @@ static Shape gemm_shape(const GemmBatch& b) {
   const int64_t iters32 = (int64_t)s.tiles * kt32;
   const bool one_per_cu = s.tiles >= slots * 7 / 16 &&
                           ((s.tiles <= slots / 2 && kt32 <= 40) ||
-                           (b.mode == GEMM_SPLIT && s.tiles <= slots && kt32 <= 64));
+                           (b.mode != GEMM_F32 && s.tiles <= slots && kt32 <= 64));
   s.splits = 1;
   if (fill >= 0.85 || one_per_cu ||
       (iters32 <= slots && (s.tiles > slots / 4 || kt32 < 4))) {
@@ -1336,7 +1340,9 @@ static Shape gemm_shape(const GemmBatch& b) {
     s.splits = (int)std::min<int64_t>(s.ktiles, slots / s.tiles);
     s.nblocks = s.tiles * s.splits;
   } else {
-    s.nblocks = slots;
+    // stream-K: every block gets at least one K slice, so that the blocks
+    // sharing a tile are consecutive and each holds a partial of it
+    s.nblocks = (int)std::min<int64_t>(slots, s.iters);
   }
   return s;
 }

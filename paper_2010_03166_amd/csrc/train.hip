@@ -229,9 +229,11 @@ extern "C" {
 
 size_t gnn_classifier_workspace_bytes(int32_t n, int32_t f, int32_t C) {
   if (n < 0 || f <= 0 || C <= 0) return 0;
-  return cls_layout(n, f, C, 0).total > cls_layout(n, f, C, GNN_FLAG_BF16).total
-             ? cls_layout(n, f, C, 0).total
-             : cls_layout(n, f, C, GNN_FLAG_BF16).total;
+  // the largest need of the three product modes (their work splits differ)
+  size_t need = 0;
+  for (const uint32_t flags : {0u, GNN_FLAG_BF16, GNN_FLAG_F32_MFMA})
+    need = std::max(need, cls_layout(n, f, C, flags).total);
+  return need;
 }
 
 gnn_status gnn_classifier(int32_t n, int32_t f, int32_t C, int32_t kind,
