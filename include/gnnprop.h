@@ -67,7 +67,11 @@ typedef enum gnn_status {
  * two flags below select other arithmetic; setting both is
  * GNN_ERR_UNSUPPORTED. */
 #define GNN_FLAG_BF16 0x1u /* GEMM operands rounded to bf16 (round to nearest
-                              even), fp32 accumulation; aggregation stays fp32 */
+                              even), fp32 accumulation; the aggregation sums
+                              in fp32 (in the backward pass its output T and
+                              the mask's G_s are kept in the workspace already
+                              rounded, as only the GEMMs read them); all
+                              outputs fp32 */
 #define GNN_FLAG_F32_MFMA 0x8u /* GEMM products on the fp32 matrix-core
                                   instruction (v_mfma_f32_32x32x2_f32) */
 /* GraphSAGE layers only (gnn_prop_fwd / gnn_prop_bwd).  Section 2.1 defines

@@ -43,6 +43,10 @@ TimerRec g_cur;
 struct LayerLayout {
   int order;
   int64_t ld_s, ld_p, ld_g, ld_gn, ld_v;
+  // bf16 products, order 2: G_s and T as bf16 (row stride ld_h16) in buf0,
+  // T at off_t16 bytes past G_s
+  int64_t ld_h16;
+  size_t off_t16;
   size_t wp_words;  // split products: words of one weight's bf16 pieces
   // GEMM workspace: [off_gemm, off_gemm_x) holds the weight gradients'
   // partial tiles, which stay there until the input-gradient launch that
@@ -200,8 +204,11 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   o.ld_gn = round_up(h, 4);
   o.ld_v = round_up(f_in, 4);
   size_t buf0, buf1;
+  o.ld_h16 = round_up(h, 4);
+  o.off_t16 = round_up((size_t)n * o.ld_h16 * 2, 256);
   if (o.order == 2) {
     buf0 = std::max((size_t)n * o.ld_p, (size_t)n * o.ld_g) * 4;  // P | GT
+    if (gemm_mode(L->flags) == GEMM_BF16) buf0 = std::max(buf0, 2 * o.off_t16);  // G_s, T bf16
     buf1 = (size_t)n * o.ld_gn * 4;                               // G_n
   } else {
     buf0 = (size_t)n * o.ld_g * 4;  // G
@@ -583,7 +590,39 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   // dX masked by 1[X > 0]: the next layer down's G, in the epilogue that
   // writes the final dX
   const float* dx_mask = (layer->flags & GNN_FLAG_DX_MASKED) ? X : nullptr;
-  if (o.order == 2) {
+  if (o.order == 2 && bf == GEMM_BF16 && !dy_masked) {
+    // bf16 products: the masking pass writes G_s rounded to bf16 and G_n in
+    // fp32 (the aggregation's input), the transposed aggregation writes T
+    // rounded to bf16; both products read them as bf16 operands (half the
+    // bytes, no conversion in the GEMM).  db_self comes from Y and dY.
+    uint16_t* Gs16 = reinterpret_cast<uint16_t*>(buf0);
+    uint16_t* T16 = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(buf0) + o.off_t16);
+    float* G_n = buf1;
+    GNN_HIP(mask_launch(n, 2 * h, h, Y, dY, layer->ld_y, Gs16, o.ld_h16, G_n, o.ld_gn, stream,
+                        true));
+    SpmmCall c = spmm_call(csr, true, h, G_n, o.ld_gn, reinterpret_cast<float*>(T16),
+                           o.ld_h16, rn);
+    c.epilogue = SPMM_STORE_BF16;
+    GNN_HIP(spmm_launch(c, stream));
+    const float* gs = reinterpret_cast<const float*>(Gs16);
+    const float* t = reinterpret_cast<const float*>(T16);
+    GemmBatch bw = dw_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, gs, o.ld_h16, t,
+                            o.ld_h16, dW_self, dW_neigh);
+    bw.mode = bf;
+    bw.b16 = 1;
+    GNN_HIP(gemm_launch(bw, wws, wws_bytes, stream, dX ? &held : nullptr));
+    if (dX) {
+      GemmBatch bx = dx_batch(2, n, f_in, h, gs, o.ld_h16, t, o.ld_h16, W_self, W_neigh, dX,
+                              layer->ld_dx, nullptr, 0);
+      bx.mode = bf;
+      bx.a16 = 1;
+      bx.p[0].mask = dx_mask;
+      bx.p[0].ld_mask = layer->ld_x;
+      GNN_HIP(gemm_launch(bx, xws, xws_bytes, stream, nullptr, &held));
+    }
+    if (db_self) GNN_HIP(colsum_masked_launch(n, h, Y, dY, layer->ld_y, db_self, cspart, stream));
+    if (db_neigh) GNN_HIP(colsum_launch(n, h, G_n, o.ld_gn, db_neigh, cspart, stream));
+  } else if (o.order == 2) {
     // G_s and G_n: dY itself when already masked, else a masking pass
     // writes them into [G_s | T] (n x ld_g) and G_n (n x ld_gn).
     const float *Gs, *Gn;

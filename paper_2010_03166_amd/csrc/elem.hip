@@ -8,11 +8,11 @@ namespace gnnprop {
 // G = dY * 1[Y > 0] over n x width; columns [0, split) go to dst0, the rest
 // to dst1 (the self and neighbour halves of a GraphSAGE output, or one block
 // when split = width).  One thread per 4 columns when every row start is
-// 16-byte aligned.
-template <bool VEC>
+// aligned for them.  H0: dst0 holds bf16 (rounded to nearest even).
+template <bool VEC, bool H0>
 __global__ __launch_bounds__(256) void mask_kernel(
     int32_t n, int32_t width, int32_t split, const float* __restrict__ Y,
-    const float* __restrict__ dY, int64_t ld_y, float* __restrict__ dst0,
+    const float* __restrict__ dY, int64_t ld_y, void* __restrict__ dst0,
     int64_t ld0, float* __restrict__ dst1, int64_t ld1) {
   constexpr int W = VEC ? 4 : 1;
   const int per_row = width / W;
@@ -22,8 +22,8 @@ __global__ __launch_bounds__(256) void mask_kernel(
     const int row = (int)(e / per_row);
     const int col = (int)(e % per_row) * W;
     const int64_t src = (int64_t)row * ld_y + col;
-    float* dst = col < split ? dst0 + (int64_t)row * ld0 + col
-                             : dst1 + (int64_t)row * ld1 + (col - split);
+    const bool first = col < split;
+    const int64_t at = first ? (int64_t)row * ld0 + col : (int64_t)row * ld1 + (col - split);
     if (VEC) {
       const float4 y = *reinterpret_cast<const float4*>(Y + src);
       const float4 d = *reinterpret_cast<const float4*>(dY + src);
@@ -32,29 +32,42 @@ __global__ __launch_bounds__(256) void mask_kernel(
       g.y = y.y > 0.f ? d.y : 0.f;
       g.z = y.z > 0.f ? d.z : 0.f;
       g.w = y.w > 0.f ? d.w : 0.f;
-      *reinterpret_cast<float4*>(dst) = g;
+      if (H0 && first)
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(dst0) + at) =
+            make_uint2(pack_bf16(g.x, g.y), pack_bf16(g.z, g.w));
+      else
+        *reinterpret_cast<float4*>((first ? static_cast<float*>(dst0) : dst1) + at) = g;
     } else {
-      *dst = Y[src] > 0.f ? dY[src] : 0.f;
+      const float g = Y[src] > 0.f ? dY[src] : 0.f;
+      if (H0 && first)
+        static_cast<uint16_t*>(dst0)[at] = (uint16_t)(pack_bf16(g, 0.f) & 0xffffu);
+      else
+        (first ? static_cast<float*>(dst0) : dst1)[at] = g;
     }
   }
 }
 
 hipError_t mask_launch(int32_t n, int32_t width, int32_t split,
                        const float* Y, const float* dY, int64_t ld_y,
-                       float* dst0, int64_t ld0, float* dst1, int64_t ld1,
-                       hipStream_t s) {
+                       void* dst0, int64_t ld0, float* dst1, int64_t ld1,
+                       hipStream_t s, bool dst0_bf16) {
   if (n <= 0 || width <= 0) return hipSuccess;
+  const bool d0_ok = dst0_bf16 ? (reinterpret_cast<uintptr_t>(dst0) % 8 == 0 && ld0 % 4 == 0)
+                               : vec4_ok(dst0, ld0);
   const bool vec = (width % 4 == 0) && (split % 4 == 0) && vec4_ok(Y, ld_y) &&
-                   vec4_ok(dY, ld_y) && vec4_ok(dst0, ld0) &&
-                   (split == width || vec4_ok(dst1, ld1));
+                   vec4_ok(dY, ld_y) && d0_ok && (split == width || vec4_ok(dst1, ld1));
   const int64_t units = (int64_t)n * width / (vec ? 4 : 1);
   const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(units, 256), 8192);
   timer_begin(GNN_K_MASK, s);
-  if (vec)
-    mask_kernel<true><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
+  if (vec && dst0_bf16)
+    mask_kernel<true, true><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
+  else if (vec)
+    mask_kernel<true, false><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
+  else if (dst0_bf16)
+    mask_kernel<false, true><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
   else
-    mask_kernel<false><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
-  timer_end(GNN_K_MASK, 12.0 * n * width, s);
+    mask_kernel<false, false><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
+  timer_end(GNN_K_MASK, (dst0_bf16 ? 10.0 : 12.0) * n * width, s);
   return hipGetLastError();
 }
 
@@ -70,11 +83,13 @@ constexpr int CS_RPT = 16;
 constexpr int CS_ROWS = 4 * CS_RPT;
 constexpr int CS_FC = 16, CS_FG = 256 / CS_FC;
 
-template <int NW>
+// MASKED: the summed value is G[r, c] where Ym[r, c] > 0, else 0 (Ym has
+// G's row stride).
+template <int NW, bool MASKED>
 __global__ __launch_bounds__(256) void colsum_partial_kernel(
     int32_t n, int32_t w, const float* __restrict__ G, int64_t ldg,
     const float* __restrict__ w0, const float* __restrict__ w1,
-    float* __restrict__ part, int64_t pstride) {
+    float* __restrict__ part, int64_t pstride, const float* __restrict__ Ym) {
   __shared__ float s[NW][4][64];
   const int l = threadIdx.x & 63;
   const int grp = threadIdx.x >> 6;
@@ -86,8 +101,10 @@ __global__ __launch_bounds__(256) void colsum_partial_kernel(
   if (c < w) {
     float v[CS_RPT];
 #pragma unroll
-    for (int k = 0; k < CS_RPT; ++k)
+    for (int k = 0; k < CS_RPT; ++k) {
       v[k] = r0 + k < n ? G[(int64_t)(r0 + k) * ldg + c] : 0.f;
+      if (MASKED && r0 + k < n && !(Ym[(int64_t)(r0 + k) * ldg + c] > 0.f)) v[k] = 0.f;
+    }
 #pragma unroll
     for (int k = 0; k < CS_RPT; ++k) {
       if (r0 + k >= n) break;
@@ -149,8 +166,8 @@ hipError_t colsum_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
   const int64_t ps = (int64_t)nblk * w;
   dim3 grid((unsigned)nblk, (unsigned)ceil_div(w, 64));
   timer_begin(GNN_K_COLSUM, s);
-  colsum_partial_kernel<1><<<grid, 256, 0, s>>>(n, w, G, ldg, row_weight, nullptr,
-                                                partials, ps);
+  colsum_partial_kernel<1, false><<<grid, 256, 0, s>>>(n, w, G, ldg, row_weight, nullptr,
+                                                       partials, ps, nullptr);
   colsum_final_kernel<1><<<(unsigned)ceil_div(w, CS_FC), 256, 0, s>>>(nblk, w, partials, ps,
                                                                        out, nullptr);
   timer_end(GNN_K_COLSUM, 4.0 * n * w, s);
@@ -165,10 +182,26 @@ hipError_t colsum2_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
   const int64_t ps = (int64_t)nblk * w;
   dim3 grid((unsigned)nblk, (unsigned)ceil_div(w, 64));
   timer_begin(GNN_K_COLSUM, s);
-  colsum_partial_kernel<2><<<grid, 256, 0, s>>>(n, w, G, ldg, w0, w1, partials, ps);
+  colsum_partial_kernel<2, false><<<grid, 256, 0, s>>>(n, w, G, ldg, w0, w1, partials, ps,
+                                                       nullptr);
   colsum_final_kernel<2><<<(unsigned)ceil_div(w, CS_FC), 256, 0, s>>>(nblk, w, partials, ps,
                                                                        out0, out1);
   timer_end(GNN_K_COLSUM, 4.0 * n * w + 8.0 * n, s);
+  return hipGetLastError();
+}
+
+hipError_t colsum_masked_launch(int32_t n, int32_t w, const float* Y, const float* dY,
+                                int64_t ld, float* out, float* partials, hipStream_t s) {
+  if (w <= 0) return hipSuccess;
+  const int nblk = (int)std::max<int64_t>(1, ceil_div(n, CS_ROWS));
+  const int64_t ps = (int64_t)nblk * w;
+  dim3 grid((unsigned)nblk, (unsigned)ceil_div(w, 64));
+  timer_begin(GNN_K_COLSUM, s);
+  colsum_partial_kernel<1, true><<<grid, 256, 0, s>>>(n, w, dY, ld, nullptr, nullptr, partials,
+                                                      ps, Y);
+  colsum_final_kernel<1><<<(unsigned)ceil_div(w, CS_FC), 256, 0, s>>>(nblk, w, partials, ps,
+                                                                       out, nullptr);
+  timer_end(GNN_K_COLSUM, 8.0 * n * w, s);
   return hipGetLastError();
 }
 

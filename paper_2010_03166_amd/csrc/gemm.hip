@@ -250,7 +250,6 @@ __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 
 // Tiles shared by several blocks: add the blocks' partial tiles in block
 // order, then bias and ReLU.  Chunk c of tile t is 1024 elements, four
@@ -335,11 +334,6 @@ __device__ inline bool run_pending_fixup(const GemmKArgs& g, const GemmKArgs& fx
   return true;
 }
 
-// Two floats rounded to bf16 (round to nearest even), packed low, high.
-__device__ inline uint32_t pack_bf16(float lo, float hi) {
-  bf16x2v v = {(__bf16)lo, (__bf16)hi};
-  return __builtin_bit_cast(uint32_t, v);
-}
 
 template <bool AT, bool BT>
 __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g, GemmKArgs fx) {
@@ -658,7 +652,58 @@ __device__ inline int xc16_word(int kp, int x) {
   return (kp >> 4) * XC16_HALF + (kp & 15) * 128 + x;
 }
 
-template <bool AT, bool BT>
+// Operand storage of the bf16 kernel: fp32 values rounded to bf16 as they
+// are staged, or bf16 values already (written so by the kernel that
+// produced them), moved unchanged.  R holds 4 consecutive elements of one
+// row; kc() gives them as the two k-pair words of the [x][k] layout, xc()
+// the four (k, k+1) words of rows a (k) and b (k + 1).
+template <bool H>
+struct Bf16Op;
+template <>
+struct Bf16Op<false> {
+  using E = float;
+  using R = float4;
+  __device__ static R fast(const float* p) { return ld4(p); }
+  __device__ static R guarded(const float* base, int64_t ld, int r, int c, int Rn,
+                              int Cn, bool vec) {
+    return load4(base, ld, r, c, Rn, Cn, vec);
+  }
+  __device__ static uint2 kc(R a) { return make_uint2(pack_bf16(a.x, a.y), pack_bf16(a.z, a.w)); }
+  __device__ static uint4 xc(R a, R b) {
+    return make_uint4(pack_bf16(a.x, b.x), pack_bf16(a.y, b.y), pack_bf16(a.z, b.z),
+                      pack_bf16(a.w, b.w));
+  }
+};
+template <>
+struct Bf16Op<true> {
+  using E = uint16_t;
+  using R = uint2;  // elements c, c + 1 in .x (low, high), c + 2, c + 3 in .y
+  __device__ static R fast(const uint16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+  __device__ static R guarded(const uint16_t* base, int64_t ld, int r, int c, int Rn,
+                              int Cn, bool vec) {
+    R v = make_uint2(0u, 0u);
+    if (r < Rn && c < Cn) {
+      const uint16_t* p = base + (int64_t)r * ld + c;
+      if (vec && c + 3 < Cn) {
+        v = fast(p);
+      } else {
+        const uint32_t e0 = p[0], e1 = c + 1 < Cn ? p[1] : 0u;
+        const uint32_t e2 = c + 2 < Cn ? p[2] : 0u, e3 = c + 3 < Cn ? p[3] : 0u;
+        v.x = e0 | (e1 << 16);
+        v.y = e2 | (e3 << 16);
+      }
+    }
+    return v;
+  }
+  __device__ static uint2 kc(R a) { return a; }
+  __device__ static uint4 xc(R a, R b) {
+    return make_uint4((a.x & 0xffffu) | (b.x << 16), (a.x >> 16) | (b.x & 0xffff0000u),
+                      (a.y & 0xffffu) | (b.y << 16), (a.y >> 16) | (b.y & 0xffff0000u));
+  }
+};
+
+// A16 / B16: that operand is stored as bf16 (GemmBatch::a16 / b16).
+template <bool AT, bool BT, bool A16, bool B16>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g, GemmKArgs fx) {
   if (run_pending_fixup(g, fx)) return;
   constexpr bool A_KC = !AT;
@@ -700,10 +745,12 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g, GemmKArg
     const int N = P.N;
     const int m0 = ti.m0, n0 = ti.n0;
     const int kt0 = ti.pi ? g.ktiles0[1] : g.ktiles0[0];
-    const float* const A0p = P.seg[0].A;
-    const float* const A1p = P.seg[1].A;
-    const float* const B0p = P.seg[0].B;
-    const float* const B1p = P.seg[1].B;
+    using OA = Bf16Op<A16>;
+    using OB = Bf16Op<B16>;
+    const auto* const A0p = reinterpret_cast<const typename OA::E*>(P.seg[0].A);
+    const auto* const A1p = reinterpret_cast<const typename OA::E*>(P.seg[1].A);
+    const auto* const B0p = reinterpret_cast<const typename OB::E*>(P.seg[0].B);
+    const auto* const B1p = reinterpret_cast<const typename OB::E*>(P.seg[1].B);
     const int64_t lda0 = P.seg[0].lda, lda1 = P.seg[1].lda;
     const int64_t ldb0 = P.seg[0].ldb, ldb1 = P.seg[1].ldb;
     const int K0 = P.seg[0].K, K1 = P.seg[1].K;
@@ -716,32 +763,34 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g, GemmKArg
     const int kx = tid >> 4, ky = 4 * (tid & 15);
     const int xk = tid >> 5, xy = 4 * (tid & 31);
 
-    float4 ra[8], rb[8];
+    typename OA::R ra[8];
+    typename OB::R rb[8];
     // One operand's K step: (KC) 4 consecutive k of 8 rows, or (XC) rows
-    // 2 kp and 2 kp + 1, for p = 0..3.
-    auto load_op = [&](float4 (&r)[8], bool kc, const float* X, int64_t ld,
-                       int x0, int X_extent, int k0, int K, bool fast, bool vec) {
+    // 2 kp and 2 kp + 1, for p = 0..3 (Op: the operand's storage).
+    auto load_op = [&](auto& r, bool kc, const auto* X, int64_t ld, int x0, int X_extent,
+                       int k0, int K, bool fast, bool vec) {
+      using Op = Bf16Op<sizeof(*X) == 2>;
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
         if (kc) {
           const int x = x0 + kx + 32 * p, k = k0 + ky;
           if (fast) {
-            const float* q = X + (int64_t)x * ld + k;
-            r[2 * p] = ld4(q);
-            r[2 * p + 1] = ld4(q + 16 * ld);
+            const auto* q = X + (int64_t)x * ld + k;
+            r[2 * p] = Op::fast(q);
+            r[2 * p + 1] = Op::fast(q + 16 * ld);
           } else {
-            r[2 * p] = load4(X, ld, x, k, X_extent, K, vec);
-            r[2 * p + 1] = load4(X, ld, x + 16, k, X_extent, K, vec);
+            r[2 * p] = Op::guarded(X, ld, x, k, X_extent, K, vec);
+            r[2 * p + 1] = Op::guarded(X, ld, x + 16, k, X_extent, K, vec);
           }
         } else {
           const int k = k0 + 2 * (xk + 8 * p), x = x0 + xy;
           if (fast) {
-            const float* q = X + (int64_t)k * ld + x;
-            r[2 * p] = ld4(q);
-            r[2 * p + 1] = ld4(q + ld);
+            const auto* q = X + (int64_t)k * ld + x;
+            r[2 * p] = Op::fast(q);
+            r[2 * p + 1] = Op::fast(q + ld);
           } else {
-            r[2 * p] = load4(X, ld, k, x, K, X_extent, vec);
-            r[2 * p + 1] = load4(X, ld, k + 1, x, K, X_extent, vec);
+            r[2 * p] = Op::guarded(X, ld, k, x, K, X_extent, vec);
+            r[2 * p + 1] = Op::guarded(X, ld, k + 1, x, K, X_extent, vec);
           }
         }
       }
@@ -754,25 +803,17 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g, GemmKArg
       load_op(ra, A_KC, s1 ? A1p : A0p, s1 ? lda1 : lda0, m0, M, k0, K, a_in && fk, va);
       load_op(rb, B_KC, s1 ? B1p : B0p, s1 ? ldb1 : ldb0, n0, N, k0, K, b_in && fk, vb);
     };
-    auto store_op = [&](uint32_t* L, const float4 (&r)[8], bool kc) {
+    auto store_op = [&](uint32_t* L, const auto& r, bool kc) {
+      using Op = Bf16Op<sizeof(r[0]) == 8>;
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
-        const float4 a = r[2 * p], b = r[2 * p + 1];
         if (kc) {  // 4 consecutive k of rows x and x + 16
-          uint2 u, v;
-          u.x = pack_bf16(a.x, a.y);
-          u.y = pack_bf16(a.z, a.w);
-          v.x = pack_bf16(b.x, b.y);
-          v.y = pack_bf16(b.z, b.w);
-          *reinterpret_cast<uint2*>(&L[(kx + 32 * p) * KC16_STRIDE + ky / 2]) = u;
-          *reinterpret_cast<uint2*>(&L[(kx + 32 * p + 16) * KC16_STRIDE + ky / 2]) = v;
-        } else {   // k pair (a: row 2kp, b: row 2kp+1) of 4 consecutive x
-          uint4 w;
-          w.x = pack_bf16(a.x, b.x);
-          w.y = pack_bf16(a.y, b.y);
-          w.z = pack_bf16(a.z, b.z);
-          w.w = pack_bf16(a.w, b.w);
-          *reinterpret_cast<uint4*>(&L[xc16_word(xk + 8 * p, xy)]) = w;
+          *reinterpret_cast<uint2*>(&L[(kx + 32 * p) * KC16_STRIDE + ky / 2]) = Op::kc(r[2 * p]);
+          *reinterpret_cast<uint2*>(&L[(kx + 32 * p + 16) * KC16_STRIDE + ky / 2]) =
+              Op::kc(r[2 * p + 1]);
+        } else {   // k pair (row 2kp, row 2kp+1) of 4 consecutive x
+          *reinterpret_cast<uint4*>(&L[xc16_word(xk + 8 * p, xy)]) =
+              Op::xc(r[2 * p], r[2 * p + 1]);
         }
       }
     };
@@ -1397,6 +1438,13 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
   static_assert(sizeof(GemmKArgs) <= sizeof(GemmFixup::args), "GemmFixup size");
   if (defer) defer->pending = 0;
   if (!batch_ok(b)) return hipErrorInvalidValue;
+  // bf16-stored operands: the bf16 mode's weight-gradient (B) and
+  // input-gradient (A) launches only
+  if (b.a16 || b.b16) {
+    if (b.mode != GEMM_BF16 || (b.a16 && b.b16)) return hipErrorInvalidValue;
+    if (b.b16 && !(b.trans_a && !b.trans_b)) return hipErrorInvalidValue;
+    if (b.a16 && !(!b.trans_a && b.trans_b)) return hipErrorInvalidValue;
+  }
   if (b.b_planes) {  // split products only, every segment's planes given
     if (b.mode != GEMM_SPLIT) return hipErrorInvalidValue;
     for (int i = 0; i < b.nprob; ++i)
@@ -1418,6 +1466,10 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
   g.nblocks = sh.nblocks;
   g.splits = sh.splits;
   bool va = true, vb = true;
+  // 4 consecutive elements per load: 16 bytes (fp32) or 8 (bf16 storage)
+  auto vec_ok = [](const void* p, int64_t ld, bool h) {
+    return h ? (reinterpret_cast<uintptr_t>(p) % 8 == 0 && ld % 4 == 0) : vec4_ok(p, ld);
+  };
   for (int i = 0; i < b.nprob; ++i) {
     g.p[i] = b.p[i];
     if (g.p[i].nseg < 2) {
@@ -1427,8 +1479,8 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
     g.ktiles0[i] = sh.kt0[i];
     const GemmProblem& p = g.p[i];
     for (int k = 0; k < p.nseg; ++k) {
-      va = va && vec4_ok(p.seg[k].A, p.seg[k].lda);
-      vb = vb && vec4_ok(p.seg[k].B, p.seg[k].ldb);
+      va = va && vec_ok(p.seg[k].A, p.seg[k].lda, b.a16 != 0);
+      vb = vb && vec_ok(p.seg[k].B, p.seg[k].ldb, b.b16 != 0);
     }
   }
   for (int i = 0; i < b.nprob; ++i) {
@@ -1456,15 +1508,19 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
   const int kid = b.trans_a ? (b.trans_b ? GNN_K_GEMM_TT : GNN_K_GEMM_TN)
                             : (b.trans_b ? GNN_K_GEMM_NT : GNN_K_GEMM_NN);
   timer_begin(kid, s);
-  if (b.mode == GEMM_BF16) {
+  if (b.mode == GEMM_BF16 && b.b16) {  // (checked above: trans_a, !trans_b, !a16)
+    gemm_bf16_kernel<true, false, false, true><<<grid, 256, 0, s>>>(g, fx);
+  } else if (b.mode == GEMM_BF16 && b.a16) {  // (!trans_a, trans_b)
+    gemm_bf16_kernel<false, true, true, false><<<grid, 256, 0, s>>>(g, fx);
+  } else if (b.mode == GEMM_BF16) {
     if (!b.trans_a && !b.trans_b)
-      gemm_bf16_kernel<false, false><<<grid, 256, 0, s>>>(g, fx);
+      gemm_bf16_kernel<false, false, false, false><<<grid, 256, 0, s>>>(g, fx);
     else if (b.trans_a && !b.trans_b)
-      gemm_bf16_kernel<true, false><<<grid, 256, 0, s>>>(g, fx);
+      gemm_bf16_kernel<true, false, false, false><<<grid, 256, 0, s>>>(g, fx);
     else if (!b.trans_a && b.trans_b)
-      gemm_bf16_kernel<false, true><<<grid, 256, 0, s>>>(g, fx);
+      gemm_bf16_kernel<false, true, false, false><<<grid, 256, 0, s>>>(g, fx);
     else
-      gemm_bf16_kernel<true, true><<<grid, 256, 0, s>>>(g, fx);
+      gemm_bf16_kernel<true, true, false, false><<<grid, 256, 0, s>>>(g, fx);
   } else if (b.mode == GEMM_F32) {
     if (!b.trans_a && !b.trans_b)
       gemm_f32_kernel<false, false><<<grid, 256, 0, s>>>(g, fx);

@@ -64,6 +64,8 @@ enum SpmmEpilogue : int32_t {
   SPMM_STORE = 0,      // out = acc
   SPMM_BIAS_RELU = 1,  // out = max(acc + bias[c], 0)   (bias may be null)
   SPMM_ADD = 2,        // out = acc + res[row, c]         (res may alias out)
+  SPMM_STORE_BF16 = 3, // out = acc rounded to bf16 (uint16 storage; rows
+                       // 8-byte aligned, ld_out a multiple of 4 elements)
 };                     // with `mask` set: out = mask[row, c] > 0 ? out : 0
 
 // Where the weight of a stored entry comes from:
@@ -165,6 +167,10 @@ struct GemmBatch {
   int32_t trans_a, trans_b;  // A stored K x M; B stored N x K
   int32_t mode;              // GemmMode
   int32_t b_planes;          // split mode: every segment's B given as Bp
+  // bf16 mode: every segment's A (a16) or B (b16) holds bf16 values (the
+  // float pointer points at them, ld in elements); supported for the weight
+  // gradients' B (trans_a, !trans_b) and the input gradient's A (trans_b)
+  int32_t a16, b16;
 };
 // op(B) (K x N; stored K x N row-major when !trans_b, N x K when trans_b,
 // row stride ld) split exactly into bf16 hi + mid + lo (each rounded to
@@ -201,12 +207,20 @@ double gemm_flops(const GemmBatch& b);
 
 // ----------------------------------------------------- elementwise
 
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+// Two floats rounded to bf16 (round to nearest even), packed low, high.
+__device__ inline uint32_t pack_bf16(float lo, float hi) {
+  bf16x2v v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 // G = dY * 1[Y > 0] over an n x width block; columns [0, split) -> dst0,
-// [split, width) -> dst1 (dst1 unused when split = width).
+// [split, width) -> dst1 (dst1 unused when split = width).  dst0_bf16:
+// dst0 receives G rounded to bf16 (uint16 storage, ld0 in elements).
 hipError_t mask_launch(int32_t n, int32_t width, int32_t split,
                        const float* Y, const float* dY, int64_t ld_y,
-                       float* dst0, int64_t ld0, float* dst1, int64_t ld1,
-                       hipStream_t s);
+                       void* dst0, int64_t ld0, float* dst1, int64_t ld1,
+                       hipStream_t s, bool dst0_bf16 = false);
 // out[c] = sum over rows of G[r, c] in a fixed order (the same for every
 // call with the same n); with row_weight, out[c] = sum_r row_weight[r] G[r, c].
 // colsum2 forms out0 = G^T w0 and out1 = G^T w1 from one pass over G.
@@ -218,5 +232,10 @@ hipError_t colsum_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
 hipError_t colsum2_launch(int32_t n, int32_t w, const float* G, int64_t ldg,
                           const float* w0, const float* w1, float* out0,
                           float* out1, float* partials, hipStream_t s);
+// out[c] = sum over rows of (Y[r, c] > 0 ? dY[r, c] : 0), the bias gradient
+// taken from the layer's output and its gradient directly (same order as
+// colsum_launch of the masked G).
+hipError_t colsum_masked_launch(int32_t n, int32_t w, const float* Y, const float* dY,
+                                int64_t ld, float* out, float* partials, hipStream_t s);
 
 }  // namespace gnnprop

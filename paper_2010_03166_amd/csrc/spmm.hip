@@ -434,6 +434,16 @@ struct Vec<true> {
     if (k > 1) p[1] = v.y;
     if (k > 2) p[2] = v.z;
   }
+  // rounded to bf16: all four values, or the first k (1..3)
+  __device__ static void store_h(uint16_t* p, T v) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf16(v.x, v.y), pack_bf16(v.z, v.w));
+  }
+  __device__ static void store_h_part(uint16_t* p, T v, int k) {
+    const uint32_t a = pack_bf16(v.x, v.y), b = pack_bf16(v.z, v.w);
+    p[0] = (uint16_t)(a & 0xffffu);
+    if (k > 1) p[1] = (uint16_t)(a >> 16);
+    if (k > 2) p[2] = (uint16_t)(b & 0xffffu);
+  }
   // v where m > 0, else 0 (a selection: NaN or infinite v is not spread)
   __device__ static T select_pos(T m, T v) {
     v.x = m.x > 0.f ? v.x : 0.f;
@@ -457,6 +467,8 @@ struct Vec<false> {
   __device__ static T select_pos(T m, T v) { return m > 0.f ? v : 0.f; }
   __device__ static T load_part(const float* p, int) { return *p; }
   __device__ static void store_part(float* p, T v, int) { *p = v; }
+  __device__ static void store_h(uint16_t* p, T v) { *p = (uint16_t)(pack_bf16(v, 0.f) & 0xffffu); }
+  __device__ static void store_h_part(uint16_t* p, T v, int) { store_h(p, v); }
 };
 
 template <int G, int D, bool VEC, int EPI, bool OFF32, bool RAG>
@@ -538,6 +550,14 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
       } else if (EPI == SPMM_ADD) {
         V::add(acc, ld(a.res + (int64_t)row * a.ld_res + col));
         if (a.mask) acc = V::select_pos(ld(a.mask + (int64_t)row * a.ld_mask + col), acc);
+      }
+      if (EPI == SPMM_STORE_BF16) {
+        uint16_t* dst = reinterpret_cast<uint16_t*>(a.out) + (int64_t)row * a.ld_out + col;
+        if (part)
+          V::store_h_part(dst, acc, nv);
+        else
+          V::store_h(dst, acc);
+        return;
       }
       float* dst = a.out + (int64_t)row * a.ld_out + col;
       if (part)
@@ -649,7 +669,10 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
               v = a.res[(int64_t)r * a.ld_res + c];
               if (a.mask && !(a.mask[(int64_t)r * a.ld_mask + c] > 0.f)) v = 0.f;
             }
-            a.out[(int64_t)r * a.ld_out + c] = v;
+            if (EPI == SPMM_STORE_BF16)
+              reinterpret_cast<uint16_t*>(a.out)[(int64_t)r * a.ld_out + c] = 0;
+            else
+              a.out[(int64_t)r * a.ld_out + c] = v;
           }
         }
       }
@@ -771,8 +794,8 @@ __global__ __launch_bounds__(256) void spmm_floor_kernel(SpmmArgs a) {
 
 // Algorithmic bytes of one aggregation: row pointers, an index and a value
 // per stored entry, the n x w input read once and the output written once.
-static double spmm_bytes(int32_t n, int64_t nnz, int32_t w) {
-  return 4.0 * (n + 1) + 8.0 * (double)nnz + 8.0 * (double)n * w;
+static double spmm_bytes(int32_t n, int64_t nnz, int32_t w, int out_bytes = 4) {
+  return 4.0 * (n + 1) + 8.0 * (double)nnz + (4.0 + out_bytes) * (double)n * w;
 }
 
 #ifndef SPMM_DEPTH
@@ -793,6 +816,9 @@ static void spmm_epi(const SpmmArgs& a, bool off32, hipStream_t s) {
   switch (a.epilogue) {
     case SPMM_BIAS_RELU: return spmm_go<G, VEC, SPMM_BIAS_RELU, RAG>(a, off32, s);
     case SPMM_ADD: return spmm_go<G, VEC, SPMM_ADD, RAG>(a, off32, s);
+    case SPMM_STORE_BF16:  // aligned rows only (spmm_launch checks)
+      if constexpr (VEC) return spmm_go<G, VEC, SPMM_STORE_BF16, RAG>(a, off32, s);
+      return;
     default: return spmm_go<G, VEC, SPMM_STORE, RAG>(a, off32, s);
   }
 }
@@ -873,8 +899,10 @@ static SpmmArgs spmm_args(const SpmmCall& c, bool* vec_out, bool* off32_out) {
   a.nwin = (int32_t)ceil_div(d.nblk, (int64_t)a.wpb);
   // float4 lanes whenever rows start 16-byte aligned (the ragged end of a
   // width that is not a multiple of 4 is read and written per component)
-  const bool vec = vec4_ok(c.in, c.ld_in) &&
-                   vec4_ok(c.out, c.ld_out) &&
+  const bool out_ok = c.epilogue == SPMM_STORE_BF16
+                          ? (reinterpret_cast<uintptr_t>(c.out) % 8 == 0 && c.ld_out % 4 == 0)
+                          : vec4_ok(c.out, c.ld_out);
+  const bool vec = vec4_ok(c.in, c.ld_in) && out_ok &&
                    (c.epilogue != SPMM_BIAS_RELU || !c.bias || aligned16(c.bias)) &&
                    (c.epilogue != SPMM_ADD || vec4_ok(c.res, c.ld_res)) &&
                    (!c.mask || vec4_ok(c.mask, c.ld_mask));
@@ -889,6 +917,7 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
   if (c.n <= 0 || c.w <= 0) return hipSuccess;
   bool vec = false, off32 = false;
   const SpmmArgs a = spmm_args(c, &vec, &off32);
+  if (c.epilogue == SPMM_STORE_BF16 && !vec) return hipErrorInvalidValue;
   timer_begin(GNN_K_SPMM, s);
   if (vec && c.w % 4 != 0)
     spmm_dispatch<true, true>(a, off32, s);
@@ -896,7 +925,7 @@ hipError_t spmm_launch(const SpmmCall& c, hipStream_t s) {
     spmm_dispatch<true, false>(a, off32, s);
   else
     spmm_dispatch<false, false>(a, off32, s);
-  timer_end(GNN_K_SPMM, spmm_bytes(c.n, c.nnz, c.w), s);
+  timer_end(GNN_K_SPMM, spmm_bytes(c.n, c.nnz, c.w, c.epilogue == SPMM_STORE_BF16 ? 2 : 4), s);
   return hipGetLastError();
 }
 
