@@ -630,12 +630,20 @@ def test_stack_step_graph_replay():
 
 @pytest.mark.parametrize("order", [1, 2])
 @pytest.mark.parametrize("bias", [False, True])
-def test_layer_mask_flags_exact(order, bias):
+@pytest.mark.parametrize("mode,f_in,h", [("split", 40, 24), ("bf16", 40, 24),
+                                         ("bf16", 37, 16)])
+def test_layer_mask_flags_exact(order, bias, mode, f_in, h):
     """GNN_FLAG_DY_MASKED with a pre-masked dY, plus GNN_FLAG_DX_MASKED,
     gives bit for bit the plain backward's weight and bias gradients and its
-    dX with the input's sign mask applied."""
+    dX with the input's sign mask applied.  In bf16 mode (order 2) the plain
+    backward keeps G_s and T as bf16 in its workspace and the GEMMs read
+    them as bf16 operands, while the pre-masked path hands them over in
+    fp32 and the GEMMs round them: the same values, so the same bits.  (h is
+    a multiple of 4 so that the pre-masked dY's neighbour half, G_n = dY + h,
+    is aggregated with the same lane groups and summation order as the
+    masking pass's aligned G_n.)"""
     g = GRAPHS["powerlaw"]
-    f_in, h = 40, 24
+    base = G.GNN_FLAG_BF16 if mode == "bf16" else 0
     rng = np.random.default_rng(7)
     p = synth.LayerParams(synth.glorot(f_in, h, rng), synth.glorot(f_in, h, rng),
                           rng.standard_normal(h) if bias else None,
@@ -645,15 +653,15 @@ def test_layer_mask_flags_exact(order, bias):
     dy = rng.standard_normal((g.n, 2 * h)).astype(np.float32)
     dg = prepared(g)
     outs = {}
-    for mode in ("plain", "fused"):
-        st = runtime.SageStack(dg, [p], f_in, order=order)
+    for how in ("plain", "fused"):
+        st = runtime.SageStack(dg, [p], f_in, order=order, flags=base)
         xin = to_dev(x, 48)
         y = st.forward(xin)
         torch.cuda.synchronize()
         L = st.layers[0]
         d = to_dev(dy, L["Y"].stride(0))
         flags = 0
-        if mode == "fused":
+        if how == "fused":
             d = to_dev(np.where(y.cpu().numpy() > 0, dy, 0), L["Y"].stride(0))
             flags = G.GNN_FLAG_DY_MASKED | G.GNN_FLAG_DX_MASKED
         lay = st._layer(0, xin.stride(0), flags)
@@ -661,8 +669,8 @@ def test_layer_mask_flags_exact(order, bias):
                        L["saved"], L["dX"], L["dW_self"], L["dW_neigh"],
                        L["db_self"], L["db_neigh"], st.workspace)
         torch.cuda.synchronize()
-        outs[mode] = {k: L[k].cpu().numpy().copy() for k in
-                      ("dX", "dW_self", "dW_neigh") + (("db_self", "db_neigh") if bias else ())}
+        outs[how] = {k: L[k].cpu().numpy().copy() for k in
+                     ("dX", "dW_self", "dW_neigh") + (("db_self", "db_neigh") if bias else ())}
     a, b = outs["plain"], outs["fused"]
     for k in a:
         exp = a[k] if k != "dX" else np.where(x > 0, a[k], 0).astype(np.float32)
@@ -786,11 +794,16 @@ def test_gemm_bf16_parity(M, N, K, ta, tb):
     assert maxrel(C, ref) <= TOL_BF16_KERNEL
 
 
-@pytest.mark.parametrize("n,f_in,h", [(500, 50, 128), (400, 130, 64), (300, 602, 40)])
+@pytest.mark.parametrize("n,f_in,h,bias", [(500, 50, 128, False), (400, 130, 64, True),
+                                           (300, 602, 40, False), (300, 37, 13, True)])
 @pytest.mark.parametrize("order", [1, 2])
-def test_layer_bf16(n, f_in, h, order):
-    g, x, p, dy = layer_inputs(n, f_in, h, 77 + n, False)
-    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh)
+def test_layer_bf16(n, f_in, h, bias, order):
+    """bf16 products against the double-precision oracle at the bf16
+    tolerance; h = 13 takes the per-element mask and the ragged bf16 stores
+    of the transposed aggregation, the bias cases the bias gradients summed
+    from Y and dY."""
+    g, x, p, dy = layer_inputs(n, f_in, h, 77 + n, bias)
+    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh, p.b_self, p.b_neigh)
     y32 = y_ref.astype(np.float32)
     dg = prepared(g)
     st = runtime.SageStack(dg, [p], f_in, order=order, flags=G.GNN_FLAG_BF16)
@@ -800,8 +813,8 @@ def test_layer_bf16(n, f_in, h, order):
     st.layers[0]["Y"].copy_(torch.from_numpy(y32).cuda())
     st.backward(to_dev(dy))
     torch.cuda.synchronize()
-    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy)
-    for k in ("dX", "dW_self", "dW_neigh"):
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy, want_db=bias)
+    for k in ("dX", "dW_self", "dW_neigh") + (("db_self", "db_neigh") if bias else ()):
         assert maxrel(st.layers[0][k], r[k]) <= TOL_BF16_LAYER, k
 
 
