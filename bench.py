@@ -105,7 +105,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the path runs one subgraph per GPU and "
-              "this build has no multi-GPU leg (requested --gpus %d, WORLD_SIZE %d)"
+              "has no multi-GPU leg (requested --gpus %d, WORLD_SIZE %d)"
               % (args.gpus, world), file=sys.stderr)
         sys.exit(2)
 
