@@ -59,6 +59,27 @@ def measured_traffic(workload: str, dtype: str) -> dict:
     return out
 
 
+def measured_mfma_util(workload: str, dtype: str) -> dict:
+    """rocprofv3 MfmaUtil (percent) per GEMM kind from the committed counter
+    summary, only where the kernel's source file is unchanged since."""
+    import glob
+    import hashlib
+    out = {}
+    for path in glob.glob(os.path.join(ROOT, "profiles", "mfma_util_*.json")):
+        try:
+            d = json.load(open(path))
+        except (OSError, ValueError):
+            continue
+        if d.get("workload") != workload or d.get("dtype") != dtype:
+            continue
+        for k, v in d.get("kernels", {}).items():
+            src = os.path.join(ROOT, v["source"])
+            ok = os.path.exists(src) and hashlib.sha256(
+                open(src, "rb").read()).hexdigest() == v["source_sha256"]
+            out[k] = v["mfma_util_pct"] if ok else None
+    return out
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -235,8 +256,15 @@ def main():
     traffic = measured_traffic(name, dtype)
     if traffic.get(dom) is not None:
         roof["traffic"] = traffic[dom]
+        # the counters' bytes over the same launch time (HBM plus MALL)
+        roof["traffic_gbs"] = round(traffic[dom] / (kernels[dom]["avg_launch_us"] * 1e3), 1)
     if roof_spmm is not None:
         roof_spmm["traffic"] = traffic.get("spmm")
+        if traffic.get("spmm") is not None:
+            roof_spmm["traffic_gbs"] = round(
+                traffic["spmm"] / (kernels["spmm"]["avg_launch_us"] * 1e3), 1)
+    if dom in gemm_names:
+        roof["mfma_util_pct"] = measured_mfma_util(name, dtype).get(dom)
 
     out = {
         "metric": METRIC,
