@@ -362,7 +362,10 @@ def main():
             "cores": O.num_threads(), "kind": "oracle",
             "sample": "%d full step(s) of the same workload (Algorithm 6 + %d "
                       "layers forward + backward), double precision, plain loops"
-                      % (reps, wl.layers)}
+                      % (reps, wl.layers),
+            "cpu_model": cpu_model(),
+            "gpu_speedup": None}
+        out["cpu_baseline"]["gpu_speedup"] = round(out["cpu_baseline"]["value"] / out["value"], 1)
         log("cpu oracle %.1f ms/layer on %d threads" % (
             out["cpu_baseline"]["value"], out["cpu_baseline"]["cores"]))
         # the oracle's own parallel speedup: the same step on one thread, for
@@ -690,6 +693,17 @@ def gather_floor(torch, G, dg, w, bytes_per_launch, reps=50):
             "spmm_same_call_us": round(us_spmm, 2),
             "frac_of_gather_floor": round(us_floor / us_spmm, 4),
             "gather_floor_gbs": round(bytes_per_launch / (us_floor * 1e3), 1)}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (as /proc/cpuinfo gives it), or ""."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
 
 
 def stream_copy_gbs(torch, mib: int = 512, reps: int = 5) -> float:
