@@ -199,10 +199,11 @@ def chung_lu_weights(n: int, gamma: float, mean_deg: float,
 
 def chung_lu_edges(n: int, gamma: float, mean_deg: float,
                    kmax: Optional[float], rng: np.random.Generator) -> np.ndarray:
-    """round(n*mean/2) distinct undirected non-loop edges, both endpoints
-    drawn independently with probability proportional to the weights; the
-    first distinct pairs in draw order are kept."""
-    target = int(round(n * mean_deg / 2.0))
+    """round(n*mean/2) distinct undirected non-loop edges (at most all
+    n(n-1)/2 of them, for tiny n), both endpoints drawn independently with
+    probability proportional to the weights; the first distinct pairs in
+    draw order are kept."""
+    target = min(int(round(n * mean_deg / 2.0)), n * (n - 1) // 2)
     w = chung_lu_weights(n, gamma, mean_deg, kmax)
     cdf = np.cumsum(w)
     cdf /= cdf[-1]

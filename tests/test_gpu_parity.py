@@ -440,6 +440,39 @@ def test_layer_parity(n, f_in, h, order, bias, mode):
         assert maxrel(got[k], r[k]) <= TOL, k
 
 
+def _random_layer_cases(count=24, seed=2024):
+    """Seeded random layer shapes and options: odd and aligned widths,
+    padded strides, with or without bias and dX, all three product modes
+    (the split-K and stream-K launches, held reductions and bf16 operand
+    storage all come up across them)."""
+    rng = np.random.default_rng(seed)
+    modes = [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16]
+    cases = []
+    for i in range(count):
+        n = int(rng.integers(2, 900))
+        f_in = int(rng.choice([int(rng.integers(1, 160)), int(rng.integers(1, 40)) * 8]))
+        h = int(rng.choice([int(rng.integers(1, 140)), int(rng.integers(1, 32)) * 8]))
+        cases.append((i, n, f_in, h, int(rng.integers(1, 3)), bool(rng.integers(0, 2)),
+                      bool(rng.integers(0, 2)), modes[i % 3], int(rng.choice([1, 4, 16]))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_layer_cases(), ids=lambda c: "case%d" % c[0])
+def test_layer_random_shapes(case):
+    _, n, f_in, h, order, bias, want_dx, flags, pad = case
+    g, x, p, dy = layer_inputs(n, f_in, h, 1000 + n + f_in + h, bias)
+    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh, p.b_self, p.b_neigh)
+    y32 = y_ref.astype(np.float32)
+    got = run_layer(g, x, p, y32, dy, order, pad=pad, want_dx=want_dx, flags=flags)
+    tol = 2e-2 if flags == G.GNN_FLAG_BF16 else TOL
+    assert maxrel(got["Y"], y_ref) <= tol
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy, want_dx=want_dx, want_db=bias)
+    keys = ("dW_self", "dW_neigh") + (("dX",) if want_dx else ()) + \
+        (("db_self", "db_neigh") if bias else ())
+    for k in keys:
+        assert maxrel(got[k], r[k]) <= tol, k
+
+
 @pytest.mark.parametrize("flags", [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16])
 @pytest.mark.parametrize("order", [1, 2])
 def test_layer_zero_nodes(flags, order):
