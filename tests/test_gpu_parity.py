@@ -286,6 +286,53 @@ def test_gemm_parity(M, N, K, ta, tb, layout, mode):
     assert maxrel(C, ref) <= TOL
 
 
+def _random_gemm_cases(count=30, seed=77):
+    """Seeded random shapes over the work-split regimes (one block per tile,
+    split-K for few tiles over a long K, stream-K in between), all four
+    transposes, aligned or shifted layouts and the three product modes."""
+    rng = np.random.default_rng(seed)
+    modes = [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16]
+    cases = []
+    for i in range(count):
+        kind = i % 3
+        if kind == 0:    # many tiles
+            M, N, K = int(rng.integers(1500, 6000)), int(rng.integers(200, 1100)), \
+                int(rng.integers(1, 700))
+        elif kind == 1:  # few tiles, long K
+            M, N, K = int(rng.integers(1, 700)), int(rng.integers(1, 600)), \
+                int(rng.integers(1000, 9000))
+        else:            # in between
+            M, N, K = int(rng.integers(300, 3000)), int(rng.integers(100, 1400)), \
+                int(rng.integers(20, 3000))
+        cases.append((i, M, N, K, int(rng.integers(0, 2)), int(rng.integers(0, 2)),
+                      bool(rng.integers(0, 2)), modes[int(rng.integers(0, 3))]))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_gemm_cases(), ids=lambda c: "case%d" % c[0])
+def test_gemm_random_shapes(case):
+    _, M, N, K, ta, tb, aligned, flags = case
+    rng = np.random.default_rng(M + 5 * N + 11 * K)
+    a = rng.standard_normal((K, M) if ta else (M, K)).astype(np.float32)
+    b = rng.standard_normal((N, K) if tb else (K, N)).astype(np.float32)
+    if aligned:
+        A = to_dev(a, (a.shape[1] + 3) // 4 * 4)
+        B = to_dev(b, (b.shape[1] + 3) // 4 * 4)
+        C = empty_out(M, N, (N + 3) // 4 * 4)
+    else:
+        A = unaligned(a, a.shape[1] + 1)
+        B = unaligned(b, b.shape[1] + 3)
+        C = empty_out(M, N, N + 1, shift=True)
+    ws = torch.empty(max(G.gnn_gemm_workspace_bytes(M, N, K), 256),
+                     dtype=torch.uint8, device="cuda")
+    G.gnn_gemm(ta, tb, M, N, K, A, A.stride(0), B, B.stride(0), C, C.stride(0), flags, ws)
+    torch.cuda.synchronize()
+    if flags == G.GNN_FLAG_BF16:   # exact products of the rounded operands
+        a, b = O.round_bf16(a), O.round_bf16(b)
+    ref = O.mm_nn(a.T if ta else a, b.T if tb else b)
+    assert maxrel(C, ref) <= (TOL_BF16_KERNEL if flags == G.GNN_FLAG_BF16 else TOL)
+
+
 def _gemm(a, b, flags):
     M, K = a.shape
     N = b.shape[1]
