@@ -30,6 +30,9 @@
  *     must not overlap unless an entry point says otherwise.
  *   - gnn_prop_fwd / gnn_prop_bwd / gnn_spmm / gnn_gemm allocate no device
  *     memory: scratch comes from the caller's `workspace`.
+ *   - `workspace`, `saved` and plan buffers (csr->plan included) must start
+ *     16-byte aligned, as hipMalloc memory does; any other address is
+ *     GNN_ERR_UNSUPPORTED.
  */
 #ifndef GNNPROP_H
 #define GNNPROP_H

@@ -19,6 +19,10 @@ inline bool ranges_overlap(const void* a, size_t an, const void* b, size_t bn) {
   return pa < pb + bn && pb < pa + an;
 }
 
+// Workspace, saved and plan buffers: the kernels access them 16 bytes at a
+// time (NULL passes; whether one is required is checked separately).
+inline bool buf16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 inline size_t mat_bytes(int64_t rows, int64_t cols, int64_t ld) {
   if (rows <= 0 || cols <= 0) return 0;
   return (size_t)(((rows - 1) * ld + cols) * 4);
@@ -31,6 +35,7 @@ inline gnn_status check_csr(const gnn_csr* c, bool need_vals, bool need_vals_t) 
   if (c->nnz > 0 && !c->indices) return GNN_ERR_NULL;
   if (need_vals && c->nnz > 0 && !c->values) return GNN_ERR_NULL;
   if (need_vals_t && c->nnz > 0 && !c->values_t) return GNN_ERR_NULL;
+  if (!buf16(c->plan)) return GNN_ERR_UNSUPPORTED;
   return GNN_OK;
 }
 

@@ -313,6 +313,7 @@ gnn_status gnn_csr_build_plan(const gnn_csr* csr, void* plan,
   gnn_status st = check_csr(csr, false, false);
   if (st != GNN_OK) return st;
   if (!plan) return GNN_ERR_NULL;
+  if (!buf16(plan)) return GNN_ERR_UNSUPPORTED;
   if (plan_bytes < gnn_plan_bytes(csr->n, csr->nnz)) return GNN_ERR_WORKSPACE;
   GNN_HIP(plan_build_launch(csr->n, csr->nnz, csr->indptr, csr->indices,
                             plan, stream));
@@ -325,6 +326,7 @@ gnn_status gnn_csr_prepare(const gnn_csr* csr, void* plan, size_t plan_bytes,
   if (st != GNN_OK) return st;
   if (!plan) return GNN_ERR_NULL;
   if (csr->nnz > 0 && !values_t) return GNN_ERR_NULL;
+  if (!buf16(plan)) return GNN_ERR_UNSUPPORTED;
   if (plan_bytes < gnn_plan_bytes(csr->n, csr->nnz)) return GNN_ERR_WORKSPACE;
   const size_t vb = (size_t)csr->nnz * 4;
   if (ranges_overlap(values_t, vb, csr->values, vb) ||
@@ -373,6 +375,7 @@ gnn_status gnn_spmm(const gnn_csr* csr, int32_t transpose, int32_t w,
   if (w < 0 || ld_in < w || ld_out < w) return GNN_ERR_SHAPE;
   if (csr->n == 0 || w == 0) return GNN_OK;
   if (!in || !out || !csr->plan) return GNN_ERR_NULL;
+  if (!buf16(workspace)) return GNN_ERR_UNSUPPORTED;
   const size_t need = spmm_partials_bytes(csr->n, csr->nnz, w);
   if (workspace_bytes < need || (need > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
@@ -441,6 +444,7 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
     if (trans_a ? lda < M : lda < K) return GNN_ERR_SHAPE;
     if (trans_b ? ldb < K : ldb < N) return GNN_ERR_SHAPE;
   }
+  if (!buf16(workspace)) return GNN_ERR_UNSUPPORTED;
   GemmBatch b;
   memset(&b, 0, sizeof(b));
   b.nprob = 1;
@@ -504,6 +508,7 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
   if (!W_self || !W_neigh) return GNN_ERR_NULL;
   const LayerLayout o = layer_layout(csr, layer);
   if (o.order == 1 && n > 0 && !saved) return GNN_ERR_NULL;
+  if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || (o.total > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
   if (n == 0) return GNN_OK;
@@ -557,6 +562,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   if (dX && layer->ld_dx < f_in) return GNN_ERR_SHAPE;
   const LayerLayout o = layer_layout(csr, layer);
   if (o.order == 1 && n > 0 && !saved) return GNN_ERR_NULL;
+  if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || (o.total > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
   {

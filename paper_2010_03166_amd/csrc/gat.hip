@@ -230,6 +230,7 @@ gnn_status gnn_gat_fwd(const gnn_csr* csr, const gnn_layer* layer, const float* 
   if (!W || !a) return GNN_ERR_NULL;
   if (n > 0 && (!X || !Y || !saved || !csr->plan)) return GNN_ERR_NULL;
   const GatLayout o = gat_layout(csr, layer);
+  if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || !workspace) return GNN_ERR_WORKSPACE;
   {
     const void* ins[] = {X, W, a};
@@ -282,6 +283,7 @@ gnn_status gnn_gat_bwd(const gnn_csr* csr, const gnn_layer* layer, const float* 
   if (n > 0 && (!X || !Y || !dY || !saved || !csr->plan)) return GNN_ERR_NULL;
   if (dX && layer->ld_dx < f_in) return GNN_ERR_SHAPE;
   const GatLayout o = gat_layout(csr, layer);
+  if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || !workspace) return GNN_ERR_WORKSPACE;
   {
     const size_t wb = (size_t)f_in * h * 4;

@@ -436,6 +436,7 @@ gnn_status gnn_induce_subgraph(int64_t n_full, int64_t nnz_full,
     return GNN_ERR_SHAPE;
   if (norm != GNN_NORM_ROW && norm != GNN_NORM_SYM) return GNN_ERR_UNSUPPORTED;
   if (!sub_indptr || !nnz_out || !status_out) return GNN_ERR_NULL;
+  if (!buf16(workspace)) return GNN_ERR_UNSUPPORTED;
   if (n_s > 0 && (!indptr || !nodes || !map || !sub_indices || !sub_values || !workspace))
     return GNN_ERR_NULL;
   if (n_s > 0 && nnz_full > 0 && !indices) return GNN_ERR_NULL;

@@ -251,6 +251,7 @@ gnn_status gnn_classifier(int32_t n, int32_t f, int32_t C, int32_t kind,
   if (ld_x < f || ld_t < C || (xm && ld_xm < C) || (probs && ld_p < C) ||
       (dX && ld_dx < f))
     return GNN_ERR_SHAPE;
+  if (!buf16(workspace)) return GNN_ERR_UNSUPPORTED;
   const ClsLayout o = cls_layout(n, f, C, flags);
   if (workspace_bytes < o.total || !workspace) return GNN_ERR_WORKSPACE;
   {

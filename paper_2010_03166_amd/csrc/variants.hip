@@ -167,6 +167,7 @@ gnn_status gnn_gcn_fwd(const gnn_csr* csr, const gnn_layer* layer,
   if (n > 0 && (!X || !Y || !csr->plan)) return GNN_ERR_NULL;
   const GcnLayout o = gcn_layout(csr, layer);
   if (o.order == 1 && n > 0 && !saved) return GNN_ERR_NULL;
+  if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || (o.total > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
   if (n == 0) return GNN_OK;
@@ -208,6 +209,7 @@ gnn_status gnn_gcn_bwd(const gnn_csr* csr, const gnn_layer* layer,
   if (dX && layer->ld_dx < f_in) return GNN_ERR_SHAPE;
   const GcnLayout o = gcn_layout(csr, layer);
   if (o.order == 1 && n > 0 && !saved) return GNN_ERR_NULL;
+  if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || (o.total > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
   {
@@ -286,6 +288,7 @@ gnn_status gnn_mixhop_fwd(const gnn_csr* csr, const gnn_layer* layer,
   if (!W) return GNN_ERR_NULL;
   if (n > 0 && (!X || !Y || !csr->plan || (K > 0 && !saved))) return GNN_ERR_NULL;
   const MixLayout o = mix_layout(csr, layer, K);
+  if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || (o.total > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
   if (n == 0) return GNN_OK;
@@ -332,6 +335,7 @@ gnn_status gnn_mixhop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   if (n > 0 && (!X || !Y || !dY || !csr->plan || (K > 0 && !saved))) return GNN_ERR_NULL;
   if (dX && layer->ld_dx < f_in) return GNN_ERR_SHAPE;
   const MixLayout o = mix_layout(csr, layer, K);
+  if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || (o.total > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
   {

@@ -157,6 +157,44 @@ def test_argument_errors_are_synchronous(lib):
     assert L.gnn_csr_build_plan(ctypes.byref(c), P(0x10), 8, None) == -5
 
 
+def test_misaligned_buffers_rejected(lib):
+    """Workspace, saved and plan buffers must start 16-byte aligned (the
+    kernels access them 16 bytes at a time): any other address is refused
+    before anything is enqueued."""
+    L = G.lib()
+    P = ctypes.c_void_p
+    ws = 1 << 30
+    c = _fake_csr()
+    odd_plan = G.make_csr(10, 30, 0x1000, 0x2000, 0x3000, 0x4000, 0x5004)
+    lay = G.make_layer(8, 4, 8, 8, 8)
+    args = [P(0x10)] * 8
+    assert L.gnn_prop_fwd(ctypes.byref(odd_plan), ctypes.byref(lay), *args, ws, None) == -4
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(lay), *args[:6], P(0x18), P(0x10),
+                          ws, None) == -4  # saved
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(lay), *args[:7], P(0x14), ws,
+                          None) == -4  # workspace
+    assert L.gnn_prop_bwd(ctypes.byref(c), ctypes.byref(lay), *([P(0x10)] * 11), P(0x14), ws,
+                          None) == -4
+    assert L.gnn_csr_build_plan(ctypes.byref(c), P(0x14), 1 << 20, None) == -4
+    need = int(L.gnn_plan_bytes(c.n, c.nnz))
+    assert L.gnn_csr_prepare(ctypes.byref(c), P(0x800004), need, P(0x900000), None) == -4
+    assert L.gnn_spmm(ctypes.byref(odd_plan), 0, 8, P(0x10), 8, P(0x20), 8, None, 0,
+                      None) == -4
+    assert L.gnn_gemm(0, 0, 4, 4, 4, P(0x10), 4, P(0x20), 4, P(0x30), 4, 0, P(0x44), ws,
+                      None) == -4
+    assert L.gnn_gcn_fwd(ctypes.byref(c), ctypes.byref(lay), P(0x10), P(0x20), None,
+                         P(0x30), P(0x40), P(0x54), ws, None) == -4
+    ml = G.make_layer(8, 4, 8, 12, 8)
+    assert L.gnn_mixhop_fwd(ctypes.byref(c), ctypes.byref(ml), 2, P(0x10), P(0x20), None,
+                            P(0x30), P(0x48), P(0x50), ws, None) == -4
+    gl = G.make_layer(8, 4, 8, 4, 8)
+    assert L.gnn_gat_fwd(ctypes.byref(c), ctypes.byref(gl), P(0x10), P(0x20), P(0x30),
+                         ctypes.c_float(0.2), P(0x40), None, P(0x50), P(0x64), ws, None) == -4
+    assert L.gnn_classifier(16, 8, 4, G.GNN_LOSS_SOFTMAX, 0, P(0x10), 8, P(0x20), P(0x30), 4,
+                            None, 4, None, 4, P(0x40), P(0x50), None, 8, P(0x6c), ws,
+                            None) == -4
+
+
 def test_prepare_and_gat_argument_errors(lib):
     L = G.lib()
     P = ctypes.c_void_p
