@@ -392,8 +392,12 @@ struct Vec<true> {
   __device__ static T load(const float* p) {
     return *reinterpret_cast<const float4*>(p);
   }
+  // output rows are stored nontemporal: written once, read by the next
+  // kernel, they would otherwise take L2 lines from the gathered rows
   __device__ static void store(float* p, T v) {
-    *reinterpret_cast<float4*>(p) = v;
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    const f4v x = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(x, reinterpret_cast<f4v*>(p));
   }
   __device__ static void fma(T& acc, float a, T x) {
     acc.x = fmaf(a, x.x, acc.x);
