@@ -545,6 +545,37 @@ def test_layer_zero_nodes(flags, order):
         assert np.array_equal(L[k].cpu().numpy(), np.zeros(L[k].shape, np.float32)), k
 
 
+@pytest.mark.parametrize("flags", [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16])
+@pytest.mark.parametrize("order", [1, 2])
+def test_layer_edgeless_subgraph(flags, order):
+    """A subgraph whose nodes hold no stored entries at all (no self loops:
+    every row empty, one window owning all of them).  Section 2.1's
+    aggregation of an empty row is zero, so Y's neighbour half is
+    ReLU(b_neigh), the weight gradient dW_neigh is exactly zero and the
+    transposed aggregation adds nothing to dX; forward and backward against
+    the oracle in every product mode and both orders."""
+    n, f_in, h = 37, 12, 10
+    g = synth.symmetric_csr(n, np.zeros((0, 2), np.int64), self_loops=False)
+    assert g.nnz == 0
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((n, f_in)).astype(np.float32)
+    p = synth.LayerParams(synth.glorot(f_in, h, rng), synth.glorot(f_in, h, rng),
+                          rng.standard_normal(h).astype(np.float32) * 0.1,
+                          rng.standard_normal(h).astype(np.float32) * 0.1)
+    dy = rng.standard_normal((n, 2 * h)).astype(np.float32)
+    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh, p.b_self, p.b_neigh)
+    y32 = y_ref.astype(np.float32)
+    got = run_layer(g, x, p, y32, dy, order, flags=flags)
+    tol = TOL_BF16_LAYER if flags == G.GNN_FLAG_BF16 else TOL
+    assert maxrel(got["Y"], y_ref) <= tol
+    nb = np.broadcast_to(np.maximum(p.b_neigh, 0), (n, h))
+    assert np.array_equal(got["Y"][:, h:], nb.astype(np.float32))
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy, want_db=True)
+    assert not np.any(r["dW_neigh"])
+    for k in ("dX", "dW_self", "dW_neigh", "db_self", "db_neigh"):
+        assert maxrel(got[k], r[k]) <= tol, k
+
+
 @pytest.mark.parametrize("order", [1, 2])
 def test_layer_without_input_gradient(order):
     g, x, p, dy = layer_inputs(200, 40, 24, 5, False)
