@@ -209,10 +209,15 @@ gnn_status gnn_csr_validate_noalloc(const gnn_csr* csr,
 
 /* ------------------------------------------------------------ one layer */
 
-/* Device bytes the forward pass saves for the backward pass (order 1 keeps
- * A_s X, n x f_in floats; order 2 keeps nothing), and the scratch bytes
- * forward and backward need.  Both depend only on csr->n, csr->nnz and the
- * layer shape. */
+/* Device bytes the forward pass saves for the backward pass, and the
+ * scratch bytes forward and backward need.  Order 1 saves A_s X (n x f_in
+ * floats).  With split products (neither product flag) the forward's weight
+ * split also writes the bf16 pieces of W_self^T and W_neigh^T that the input
+ * gradient's product uses (3 x 2 x ceil(h / 16) x 16 x f_in bytes each), so
+ * that the backward pass does not split the weights again; with
+ * GNN_FLAG_BF16 or GNN_FLAG_F32_MFMA order 2 saves nothing.  Both sizes
+ * depend only on csr->n, csr->nnz, the layer shape, its order and its
+ * product flag. */
 size_t gnn_prop_saved_bytes(const gnn_csr* csr, const gnn_layer* layer);
 size_t gnn_prop_workspace_bytes(const gnn_csr* csr, const gnn_layer* layer);
 
@@ -221,8 +226,8 @@ size_t gnn_prop_workspace_bytes(const gnn_csr* csr, const gnn_layer* layer);
  *   Y[:, h:2h] = ReLU(A_s X W_neigh + b_neigh)
  * b_self / b_neigh may be NULL (no bias: the paper's form).  Needs
  * csr->values and csr->plan.  `saved` (gnn_prop_saved_bytes, may be NULL
- * when that is 0) receives what gnn_prop_bwd needs and must be passed to it
- * unchanged.  Y must not overlap X. */
+ * when that is 0 or csr->n is 0) receives what gnn_prop_bwd needs and must
+ * be passed to it unchanged.  Y must not overlap X. */
 gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
                         const float* X, const float* W_self,
                         const float* W_neigh, const float* b_self,
@@ -242,7 +247,10 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
  * GNN_FLAG_DX_MASKED (dX returned masked by 1[X > 0]) to the product flags
  * (GNN_FLAG_BF16 or GNN_FLAG_F32_MFMA, or neither: split products).
  * Needs csr->values, csr->values_t and csr->plan, and the `saved` buffer of
- * the matching gnn_prop_fwd call with the same layer (same order).  Outputs
+ * the matching gnn_prop_fwd call with the same layer (same order and product
+ * flag) and the same weights: with split products the input gradient takes
+ * the weights' pieces saved by that call (as in training, where the
+ * backward pass follows the forward pass that used the weights).  Outputs
  * must not overlap inputs. */
 gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
                         const float* X, const float* W_self,

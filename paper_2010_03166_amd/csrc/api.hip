@@ -52,6 +52,11 @@ struct LayerLayout {
   // partial tiles, which stay there until the input-gradient launch that
   // follows sums them; [off_gemm_x, off_cs) serves every other launch
   size_t off_buf0, off_buf1, off_gemm, off_gemm_x, off_cs, off_wp, total;
+  // saved buffer: order 1's A_s X (n x ld_s floats) at 0; with split
+  // products the input gradient's pieces of W_self^T and W_neigh^T (sp_words
+  // words each, K = h, N = f_in), written by the forward's weight split, at
+  // off_sp and off_sp + sp_stride
+  size_t sp_words, off_sp, sp_stride, saved_total;
 };
 
 int resolve_order(const gnn_layer* L) {
@@ -167,25 +172,42 @@ GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
 // the workspace (once per call, in the orientation of this batch's B), and
 // the batch's segments pointed at them: segment B pointers equal to W_self
 // take the first, W_neigh the second.
-hipError_t attach_weight_planes(GemmBatch& b, const LayerLayout& o, char* ws,
+// Points the batch's weight segments at bf16 pieces: planes[0] for W_self,
+// planes[1] for W_neigh, pw words per plane.
+void use_weight_planes(GemmBatch& b, const float* Ws, uint32_t* const planes[2], int64_t pw) {
+  for (int i = 0; i < b.nprob; ++i)
+    for (int k = 0; k < b.p[i].nseg; ++k) {
+      GemmSeg& sg = b.p[i].seg[k];
+      sg.Bp = sg.B == Ws ? planes[0] : planes[1];
+      sg.bp_plane = pw;
+    }
+  b.b_planes = 1;
+}
+
+uint32_t* const* saved_planes(const LayerLayout& o, const void* saved, uint32_t* out[2]) {
+  char* sv = static_cast<char*>(const_cast<void*>(saved));
+  out[0] = reinterpret_cast<uint32_t*>(sv + o.off_sp);
+  out[1] = reinterpret_cast<uint32_t*>(sv + o.off_sp + o.sp_stride);
+  return out;
+}
+
+// Forward product (split products): W_self and W_neigh split once into the
+// workspace in the forward orientation (op(B) = W, K = f_in, N = h) and, in
+// the same launch, into the saved buffer in the input gradient's (op(B) =
+// W^T, K = h, N = f_in), which gnn_prop_bwd reads instead of splitting.
+hipError_t attach_weight_planes(GemmBatch& b, const LayerLayout& o, char* ws, void* saved,
                                 const float* Ws, const float* Wn, int32_t f_in,
                                 int32_t h, hipStream_t s) {
   if (b.mode != GEMM_SPLIT) return hipSuccess;
   uint32_t* wp[2] = {reinterpret_cast<uint32_t*>(ws + o.off_wp),
                      reinterpret_cast<uint32_t*>(ws + o.off_wp + round_up(o.wp_words * 4, 256))};
-  const float* W[2] = {Ws, Wn};
-  // forward: op(B) = W (K = f_in, N = h); input gradient: op(B) = W^T
-  const int32_t K = b.trans_b ? h : f_in, N = b.trans_b ? f_in : h;
-  hipError_t e = split_b_planes_launch(W[0], W[1], h, K, N, b.trans_b != 0, wp[0], wp[1], s);
+  uint32_t* sp[2];
+  saved_planes(o, saved, sp);
+  const SplitJob jobs[4] = {{Ws, h, f_in, h, 0, wp[0]}, {Wn, h, f_in, h, 0, wp[1]},
+                            {Ws, h, h, f_in, 1, sp[0]}, {Wn, h, h, f_in, 1, sp[1]}};
+  hipError_t e = split_b_planes_launch(jobs, 4, s);
   if (e != hipSuccess) return e;
-  const int64_t pw = (int64_t)(b_planes_words(K, N) / 3);
-  for (int i = 0; i < b.nprob; ++i)
-    for (int k = 0; k < b.p[i].nseg; ++k) {
-      GemmSeg& sg = b.p[i].seg[k];
-      sg.Bp = sg.B == Ws ? wp[0] : wp[1];
-      sg.bp_plane = pw;
-    }
-  b.b_planes = 1;
+  use_weight_planes(b, Ws, wp, (int64_t)(b_planes_words(f_in, h) / 3));
   return hipSuccess;
 }
 
@@ -219,11 +241,14 @@ LayerLayout layer_layout(const gnn_csr* csr, const gnn_layer* L) {
   const size_t gemm = std::max(
       gemm_workspace_bytes(with_mode(fwd_batch(o.order, n, f_in, h, 0, f_in, 0, 0, 0, 0, 0, 0, 0, 2 * h, 0, 0), bf)),
       gemm_workspace_bytes(with_mode(dx_batch(o.order, n, f_in, h, 0, 2 * h, 0, 2 * h, 0, 0, 0, f_in, 0, f_in), bf)));
-  // split products: W_self and W_neigh as bf16 pieces, in the forward
-  // product's orientation (K = f_in, N = h) or the input gradient's (K = h,
-  // N = f_in), one at a time
-  o.wp_words = bf == GEMM_SPLIT ? std::max(b_planes_words(f_in, h), b_planes_words(h, f_in))
-                                : 0;
+  // split products: W_self and W_neigh as bf16 pieces in the forward
+  // product's orientation (K = f_in, N = h) in the workspace; the input
+  // gradient's (K = h, N = f_in) in the saved buffer
+  o.wp_words = bf == GEMM_SPLIT ? b_planes_words(f_in, h) : 0;
+  o.sp_words = bf == GEMM_SPLIT ? b_planes_words(h, f_in) : 0;
+  o.off_sp = o.order == 1 ? round_up((size_t)n * o.ld_s * 4, 256) : 0;
+  o.sp_stride = round_up(o.sp_words * 4, 256);
+  o.saved_total = o.off_sp + 2 * o.sp_stride;
   o.off_buf0 = 0;
   o.off_buf1 = round_up(buf0, 256);
   o.off_gemm = o.off_buf1 + round_up(buf1, 256);
@@ -469,8 +494,8 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
     return GNN_ERR_ALIAS;
   if (presplit) {
     uint32_t* planes = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + part);
-    GNN_HIP(split_b_planes_launch(B, nullptr, ldb, K, N, trans_b != 0, planes, nullptr,
-                                  stream));
+    const SplitJob job = {B, ldb, K, N, trans_b != 0, planes};
+    GNN_HIP(split_b_planes_launch(&job, 1, stream));
     b.b_planes = 1;
     b.p[0].seg[0].Bp = planes;
     b.p[0].seg[0].bp_plane = (int64_t)(b_planes_words(K, N) / 3);
@@ -480,10 +505,9 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
 }
 
 size_t gnn_prop_saved_bytes(const gnn_csr* csr, const gnn_layer* layer) {
-  if (!csr || !layer || csr->n < 0 || layer->f_in <= 0 || layer->h <= 0)
+  if (!csr || !layer || csr->n < 0 || csr->nnz < 0 || layer->f_in <= 0 || layer->h <= 0)
     return 0;
-  if (resolve_order(layer) != 1) return 0;
-  return round_up((size_t)csr->n * round_up(layer->f_in, 4) * 4, 256);
+  return layer_layout(csr, layer).saved_total;
 }
 
 size_t gnn_prop_workspace_bytes(const gnn_csr* csr, const gnn_layer* layer) {
@@ -507,7 +531,7 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
   if (n > 0 && (!X || !Y || !csr->plan)) return GNN_ERR_NULL;
   if (!W_self || !W_neigh) return GNN_ERR_NULL;
   const LayerLayout o = layer_layout(csr, layer);
-  if (o.order == 1 && n > 0 && !saved) return GNN_ERR_NULL;
+  if (o.saved_total > 0 && n > 0 && !saved) return GNN_ERR_NULL;
   if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || (o.total > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
@@ -528,14 +552,14 @@ gnn_status gnn_prop_fwd(const gnn_csr* csr, const gnn_layer* layer,
     GemmBatch b = fwd_batch(1, n, f_in, h, X, layer->ld_x, S, o.ld_s, W_self,
                             W_neigh, b_self, b_neigh, Y, layer->ld_y, nullptr, 0);
     b.mode = gemm_mode(layer->flags);
-    GNN_HIP(attach_weight_planes(b, o, ws, W_self, W_neigh, f_in, h, stream));
+    GNN_HIP(attach_weight_planes(b, o, ws, saved, W_self, W_neigh, f_in, h, stream));
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
   } else {
     float* P = reinterpret_cast<float*>(ws + o.off_buf0);
     GemmBatch b = fwd_batch(2, n, f_in, h, X, layer->ld_x, nullptr, 0, W_self,
                             W_neigh, b_self, nullptr, Y, layer->ld_y, P, o.ld_p);
     b.mode = gemm_mode(layer->flags);
-    GNN_HIP(attach_weight_planes(b, o, ws, W_self, W_neigh, f_in, h, stream));
+    GNN_HIP(attach_weight_planes(b, o, ws, saved, W_self, W_neigh, f_in, h, stream));
     GNN_HIP(gemm_launch(b, gws, gws_bytes, stream));
     SpmmCall c = spmm_call(csr, false, h, P, o.ld_p, Y + h, layer->ld_y, rn);
     c.epilogue = SPMM_BIAS_RELU;
@@ -561,7 +585,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
   if (n > 0 && (!X || !Y || !dY || !csr->plan)) return GNN_ERR_NULL;
   if (dX && layer->ld_dx < f_in) return GNN_ERR_SHAPE;
   const LayerLayout o = layer_layout(csr, layer);
-  if (o.order == 1 && n > 0 && !saved) return GNN_ERR_NULL;
+  if (o.saved_total > 0 && n > 0 && !saved) return GNN_ERR_NULL;
   if (!buf16(workspace) || !buf16(saved)) return GNN_ERR_UNSUPPORTED;
   if (workspace_bytes < o.total || (o.total > 0 && !workspace))
     return GNN_ERR_WORKSPACE;
@@ -664,7 +688,12 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       bx.mode = bf;
       bx.p[0].mask = dx_mask;
       bx.p[0].ld_mask = layer->ld_x;
-      GNN_HIP(attach_weight_planes(bx, o, ws, W_self, W_neigh, f_in, h, stream));
+      if (bx.mode == GEMM_SPLIT && saved) {  // the pieces the forward call saved
+        // (saved is NULL only for n = 0, where the product has no tiles)
+        uint32_t* sp[2];
+        use_weight_planes(bx, W_self, saved_planes(o, saved, sp),
+                          (int64_t)(b_planes_words(h, f_in) / 3));
+      }
       GNN_HIP(gemm_launch(bx, xws, xws_bytes, stream, nullptr, &held));
     }
     if (db_self) GNN_HIP(colsum_launch(n, h, Gs, ld_gs, db_self, cspart, stream));
@@ -691,7 +720,12 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       GemmBatch bx = dx_batch(1, n, f_in, h, G, ld_g, G + h, ld_g, W_self,
                               W_neigh, dX, layer->ld_dx, V, o.ld_v);
       bx.mode = bf;
-      GNN_HIP(attach_weight_planes(bx, o, ws, W_self, W_neigh, f_in, h, stream));
+      if (bx.mode == GEMM_SPLIT && saved) {  // the pieces the forward call saved
+        // (saved is NULL only for n = 0, where the product has no tiles)
+        uint32_t* sp[2];
+        use_weight_planes(bx, W_self, saved_planes(o, saved, sp),
+                          (int64_t)(b_planes_words(h, f_in) / 3));
+      }
       GNN_HIP(gemm_launch(bx, xws, xws_bytes, stream, nullptr, &held));
       // dX = G_s W_s^T + A_s^T V, then the mask, in the aggregation epilogue
       SpmmCall c = spmm_call(csr, true, f_in, V, o.ld_v, dX, layer->ld_dx, rn);

@@ -1275,15 +1275,21 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
 }
 
 // One thread per word (bf16 pair k, k + 1 of one column) of the planes;
-// blockIdx.y picks one of the two matrices split in one launch.
-__global__ __launch_bounds__(256) void split_b_planes_kernel(
-    const float* __restrict__ B0, const float* __restrict__ B1, int64_t ld,
-    int32_t K, int32_t N, int32_t kn, uint32_t* __restrict__ planes0,
-    uint32_t* __restrict__ planes1, int64_t plane_words) {
+// blockIdx.y picks the matrix (job) of the launch.
+struct SplitJobs {
+  SplitJob j[MAX_SPLIT_JOBS];
+  int64_t pw[MAX_SPLIT_JOBS];  // words of one plane of job i
+};
+__global__ __launch_bounds__(256) void split_b_planes_kernel(SplitJobs jobs) {
+  const SplitJob& J = jobs.j[blockIdx.y];
+  const int64_t plane_words = jobs.pw[blockIdx.y];
   const int64_t w = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (w >= plane_words) return;
-  const float* __restrict__ B = blockIdx.y ? B1 : B0;
-  uint32_t* __restrict__ planes = blockIdx.y ? planes1 : planes0;
+  const float* __restrict__ B = J.B;
+  uint32_t* __restrict__ planes = J.planes;
+  const int K = J.K, N = J.N;
+  const int64_t ld = J.ld;
+  const bool kn = !J.trans_b;
   const int tp = (int)(w & 7);
   const int64_t gn = w >> 3;
   const int n = (int)(gn % N), gi = (int)(gn / N);
@@ -1304,17 +1310,23 @@ size_t b_planes_words(int32_t K, int32_t N) {
   return 3 * (size_t)ceil_div(K, BKS) * (size_t)N * 8;
 }
 
-hipError_t split_b_planes_launch(const float* B0, const float* B1, int64_t ld,
-                                 int32_t K, int32_t N, bool trans_b,
-                                 uint32_t* planes0, uint32_t* planes1,
-                                 hipStream_t s) {
-  const int64_t pw = (int64_t)(b_planes_words(K, N) / 3);
-  if (pw == 0) return hipSuccess;
-  const unsigned nmat = B1 ? 2 : 1;
+hipError_t split_b_planes_launch(const SplitJob* jobs, int njobs, hipStream_t s) {
+  if (njobs < 1 || njobs > MAX_SPLIT_JOBS) return hipErrorInvalidValue;
+  SplitJobs a;
+  memset(&a, 0, sizeof(a));
+  int64_t pw_max = 0;
+  double words = 0;
+  for (int i = 0; i < njobs; ++i) {
+    a.j[i] = jobs[i];
+    const int64_t pw = (int64_t)(b_planes_words(jobs[i].K, jobs[i].N) / 3);
+    a.pw[i] = pw;
+    pw_max = std::max(pw_max, pw);
+    words += (double)pw;
+  }
+  if (pw_max == 0) return hipSuccess;
   timer_begin(GNN_K_WSPLIT, s);
-  split_b_planes_kernel<<<dim3((unsigned)ceil_div(pw, 256), nmat), 256, 0, s>>>(
-      B0, B1, ld, K, N, trans_b ? 0 : 1, planes0, planes1, pw);
-  timer_end(GNN_K_WSPLIT, 20.0 * (double)pw * nmat, s);  // 2 floats in, 3 words out
+  split_b_planes_kernel<<<dim3((unsigned)ceil_div(pw_max, 256), (unsigned)njobs), 256, 0, s>>>(a);
+  timer_end(GNN_K_WSPLIT, 20.0 * words, s);  // per word: 2 floats in, 3 words out
   return hipGetLastError();
 }
 

@@ -179,12 +179,18 @@ struct GemmBatch {
 // as 8 words of bf16 pairs, at words ((g N + n) 8 .. + 7) of the plane; k
 // past K holds zeros.  Planes are b_planes_words(K, N) / 3 words apart.
 size_t b_planes_words(int32_t K, int32_t N);
-// B1 / planes1 may be NULL; otherwise a second matrix of the same shape and
-// stride is split in the same launch.
-hipError_t split_b_planes_launch(const float* B0, const float* B1, int64_t ld,
-                                 int32_t K, int32_t N, bool trans_b,
-                                 uint32_t* planes0, uint32_t* planes1,
-                                 hipStream_t s);
+// One matrix to split: op(B) (K x N) of B with row stride ld, into the
+// planes at `planes` (b_planes_words(K, N) words, 16-byte aligned).
+struct SplitJob {
+  const float* B;
+  int64_t ld;
+  int32_t K, N;
+  int32_t trans_b;
+  uint32_t* planes;
+};
+constexpr int MAX_SPLIT_JOBS = 4;
+// Up to MAX_SPLIT_JOBS matrices split in one launch.
+hipError_t split_b_planes_launch(const SplitJob* jobs, int njobs, hipStream_t s);
 size_t gemm_workspace_bytes(const GemmBatch& b);
 // The reduction of a stream-K or split-K launch's shared tiles, held back so
 // that the next GEMM launch on the stream runs it in extra blocks of its own

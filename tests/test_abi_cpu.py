@@ -87,12 +87,21 @@ def test_size_queries(lib):
     c = _fake_csr(8000, 128000)
     l1 = G.make_layer(602, 512, 604, 1024, 604, order=1)
     l2 = G.make_layer(602, 512, 604, 1024, 604, order=2)
-    assert G.gnn_prop_saved_bytes(c, l1) >= 8000 * 604 * 4
-    assert G.gnn_prop_saved_bytes(c, l2) == 0
+    # split products: the forward also saves the input gradient's bf16
+    # pieces of W_self^T and W_neigh^T (three planes of ceil(h / 16) groups
+    # x f_in columns x 16 bf16 each)
+    pieces = 2 * (3 * 32 * 602 * 16 * 2)
+    assert G.gnn_prop_saved_bytes(c, l1) >= 8000 * 604 * 4 + pieces
+    assert G.gnn_prop_saved_bytes(c, l2) == pieces
+    for flag in (G.GNN_FLAG_BF16, G.GNN_FLAG_F32_MFMA):  # no pieces
+        l2f = G.make_layer(602, 512, 604, 1024, 604, order=2, flags=flag)
+        assert G.gnn_prop_saved_bytes(c, l2f) == 0
+        l1f = G.make_layer(602, 512, 604, 1024, 604, order=1, flags=flag)
+        assert 8000 * 604 * 4 <= G.gnn_prop_saved_bytes(c, l1f) < 8000 * 604 * 4 + 256
     for l in (l1, l2):
         assert G.gnn_prop_workspace_bytes(c, l) > 8000 * 512 * 4
     auto = G.make_layer(602, 512, 604, 1024, 604, order=0)
-    assert G.gnn_prop_saved_bytes(c, auto) == 0  # 602 > 512: order 2
+    assert G.gnn_prop_saved_bytes(c, auto) == pieces  # 602 > 512: order 2
     # one block per tile (no partial tiles); the split products' B pieces:
     # three planes of ceil(K / 16) groups x N columns x 16 bf16
     assert G.gnn_gemm_workspace_bytes(8000, 1024, 602) == 3 * 38 * 1024 * 16 * 2
