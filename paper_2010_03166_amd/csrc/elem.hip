@@ -67,7 +67,11 @@ hipError_t mask_launch(int32_t n, int32_t width, int32_t split,
     mask_kernel<false, true><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
   else
     mask_kernel<false, false><<<grid, 256, 0, s>>>(n, width, split, Y, dY, ld_y, dst0, ld0, dst1, ld1);
-  timer_end(GNN_K_MASK, (dst0_bf16 ? 10.0 : 12.0) * n * width, s);
+  // Y and dY read (8 bytes per element), G written: columns [0, split) as
+  // bf16 when dst0_bf16, the rest as fp32
+  timer_end(GNN_K_MASK,
+            8.0 * n * width + (dst0_bf16 ? 2.0 : 4.0) * n * split + 4.0 * n * (width - split),
+            s);
   return hipGetLastError();
 }
 
