@@ -204,6 +204,27 @@ def test_misaligned_buffers_rejected(lib):
                             None) == -4
 
 
+def test_saved_buffer_required_where_it_holds_something(lib):
+    """Order 2 saves the input gradient's weight pieces with split products,
+    so forward and backward then need `saved`; with GNN_FLAG_BF16 or
+    GNN_FLAG_F32_MFMA order 2 saves nothing and NULL is accepted (the calls
+    below stop at the workspace size instead)."""
+    L = G.lib()
+    P = ctypes.c_void_p
+    c = _fake_csr()
+    split = G.make_layer(8, 4, 8, 8, 8, order=2)
+    assert G.gnn_prop_saved_bytes(c, split) > 0
+    fwd = [P(0x10)] * 6 + [None, P(0x20)]   # X .. Y, saved = NULL, workspace
+    bwd = [P(0x10)] * 5 + [None] + [P(0x30)] * 5 + [P(0x20)]
+    assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(split), *fwd, 1 << 30, None) == -1
+    assert L.gnn_prop_bwd(ctypes.byref(c), ctypes.byref(split), *bwd, 1 << 30, None) == -1
+    for flag in (G.GNN_FLAG_BF16, G.GNN_FLAG_F32_MFMA):
+        lay = G.make_layer(8, 4, 8, 8, 8, order=2, flags=flag)
+        assert G.gnn_prop_saved_bytes(c, lay) == 0
+        assert L.gnn_prop_fwd(ctypes.byref(c), ctypes.byref(lay), *fwd, 16, None) == -5
+        assert L.gnn_prop_bwd(ctypes.byref(c), ctypes.byref(lay), *bwd, 16, None) == -5
+
+
 def test_prepare_and_gat_argument_errors(lib):
     L = G.lib()
     P = ctypes.c_void_p
