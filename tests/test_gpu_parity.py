@@ -286,7 +286,7 @@ def test_gemm_parity(M, N, K, ta, tb, layout, mode):
     assert maxrel(C, ref) <= TOL
 
 
-def _random_gemm_cases(count=30, seed=77):
+def _random_gemm_cases(count=90, seed=77):
     """Seeded random shapes over the work-split regimes (one block per tile,
     split-K for few tiles over a long K, stream-K in between), all four
     transposes, aligned or shifted layouts and the three product modes."""
@@ -487,7 +487,7 @@ def test_layer_parity(n, f_in, h, order, bias, mode):
         assert maxrel(got[k], r[k]) <= TOL, k
 
 
-def _random_layer_cases(count=24, seed=2024):
+def _random_layer_cases(count=96, seed=2024):
     """Seeded random layer shapes and options: odd and aligned widths,
     padded strides, with or without bias and dX, all three product modes
     (the split-K and stream-K launches, held reductions and bf16 operand
