@@ -182,6 +182,45 @@ def test_spmm_parity(name, w, transpose, layout):
     assert maxrel(out, ref) <= TOL_SPMM
 
 
+def _random_spmm_cases(count=48, seed=555):
+    """Seeded random aggregations: uniform or power-law degrees (hub rows
+    over several windows), with or without self loops, random values;
+    widths from 1 to 1100 (narrow slices, the 10-lane groups, ragged
+    ends), padded or odd row strides, both directions."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(count):
+        n = int(rng.integers(1, 4000))
+        w = int(rng.choice([int(rng.integers(1, 1100)), int(rng.integers(1, 128)) * 8]))
+        w = max(1, min(w, 3_000_000 // n))
+        cases.append((i, n, w, float(rng.uniform(0.3, 40.0)), bool(rng.integers(0, 2)),
+                      bool(rng.integers(0, 2)), int(rng.integers(0, 2)),
+                      int(rng.integers(0, 8)), bool(rng.integers(0, 2))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_spmm_cases(), ids=lambda c: "case%d" % c[0])
+def test_spmm_random_graphs(case):
+    i, n, w, mean, powerlaw, loops, transpose, pad, shift = case
+    if powerlaw and n > 2:
+        g = synth.power_law_graph(n, 2.1, min(mean, n - 1.0), seed=100 + i)
+    else:
+        g = synth.random_graph(n, min(mean, max(n - 1.0, 0.0)), 200 + i,
+                               self_loops=loops, values="random")
+    dg = prepared(g)
+    x = np.random.default_rng(300 + i).standard_normal((g.n, w)).astype(np.float32)
+    ld = w + pad
+    if shift:
+        xin, out = unaligned(x, ld), empty_out(g.n, w, ld, shift=True)
+    else:
+        ld = (ld + 3) // 4 * 4
+        xin, out = to_dev(x, ld), empty_out(g.n, w, ld)
+    G.gnn_spmm(dg.struct(), transpose, w, xin, xin.stride(0), out, out.stride(0), None)
+    torch.cuda.synchronize()
+    ref = O.spmm_transpose(g, x) if transpose else O.spmm(g, x)
+    assert maxrel(out, ref) <= TOL_SPMM
+
+
 @pytest.mark.parametrize("w", [40, 200, 256])
 @pytest.mark.parametrize("transpose", [0, 1])
 def test_spmm_two_windows_per_workgroup(w, transpose):
