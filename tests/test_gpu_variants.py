@@ -200,6 +200,57 @@ def test_mixhop_full_size_bench_graph():
         assert maxrel(r[k], ref[k]) <= TOL, k
 
 
+def _random_variant_cases(count=30, seed=808):
+    """Seeded random GCN / MixHop layers: graph size and density (uniform or
+    power-law), widths, order (GCN) or hop count (MixHop), bias, product
+    mode, row-stride padding and, for MixHop, whether dX is wanted."""
+    rng = np.random.default_rng(seed)
+    modes = [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16]
+    cases = []
+    for i in range(count):
+        cases.append((i, int(rng.integers(1, 1500)), float(rng.uniform(0.5, 20.0)),
+                      bool(rng.integers(0, 2)), int(rng.integers(1, 200)),
+                      int(rng.integers(1, 160)), int(rng.integers(0, 3)),
+                      int(rng.integers(0, 5)), bool(rng.integers(0, 2)), modes[i % 3],
+                      int(rng.integers(0, 9)), bool(rng.integers(0, 2))))
+    return cases
+
+
+def _random_graph(i, n, mean, powerlaw):
+    if powerlaw and n > 2:
+        return synth.sym_normalized(synth.power_law_graph(n, 2.1, min(mean, n - 1.0),
+                                                          seed=400 + i))
+    return synth.random_graph(n, min(mean, max(n - 1.0, 0.0)), 500 + i,
+                              values="sym-normalized")
+
+
+@pytest.mark.parametrize("case", _random_variant_cases(), ids=lambda c: "case%d" % c[0])
+def test_gcn_random_shapes(case):
+    i, n, mean, powerlaw, f_in, h, order, _, bias, flags, pad, _ = case
+    g = _random_graph(i, n, mean, powerlaw)
+    tol = 2e-2 if flags == G.GNN_FLAG_BF16 else TOL
+    r = run_gcn(g, f_in, h, order, bias, flags=flags, seed=i, pad=pad)
+    assert maxrel(r["Y"], r["Y_ref"]) <= tol
+    decision_flips(r["Y"], r["Y_ref"], tol)
+    ref = O.gcn_bwd(g, r["x"], r["w"], r["Y32"], r["dy"], want_db=bias)
+    for k in ("dX", "dW") + (("db",) if bias else ()):
+        assert maxrel(r[k], ref[k]) <= tol, k
+
+
+@pytest.mark.parametrize("case", _random_variant_cases(seed=909), ids=lambda c: "case%d" % c[0])
+def test_mixhop_random_shapes(case):
+    i, n, mean, powerlaw, f_in, h, _, K, bias, flags, pad, want_dx = case
+    g = _random_graph(i + 1000, n, mean, powerlaw)
+    tol = 2e-2 if flags == G.GNN_FLAG_BF16 else TOL
+    r = run_mixhop(g, K, f_in, h, bias, seed=i, pad=pad, want_dx=want_dx, flags=flags)
+    assert maxrel(r["Y"], r["Y_ref"]) <= tol
+    decision_flips(r["Y"], r["Y_ref"], tol)
+    ref = O.mixhop_bwd(g, r["x"], r["w"], K, r["Y32"], r["dy"], want_dx=want_dx,
+                       want_db=bias)
+    for k in (("dX",) if want_dx else ()) + ("dW",) + (("db",) if bias else ()):
+        assert maxrel(r[k], ref[k]) <= tol, (k, K)
+
+
 def test_variant_argument_errors():
     g = GRAPHS["random"]
     dg = prepared(g)
