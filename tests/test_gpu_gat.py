@@ -112,6 +112,29 @@ def test_gat_f32_mfma_mode():
     check(g, r, O.GAT_ALPHA)
 
 
+def _random_gat_cases(count=30, seed=1212):
+    """Seeded random GAT layers: graph size and density (uniform or
+    power-law), widths, LeakyReLU slope in [0, 1], product mode, row-stride
+    padding, with and without dX."""
+    rng = np.random.default_rng(seed)
+    modes = [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16]
+    return [(i, int(rng.integers(1, 1500)), float(rng.uniform(0.5, 20.0)),
+             bool(rng.integers(0, 2)), int(rng.integers(1, 200)), int(rng.integers(1, 160)),
+             float(rng.uniform(0.0, 1.0)), modes[i % 3], int(rng.integers(0, 9)),
+             bool(rng.integers(0, 2))) for i in range(count)]
+
+
+@pytest.mark.parametrize("case", _random_gat_cases(), ids=lambda c: "case%d" % c[0])
+def test_gat_random_shapes(case):
+    i, n, mean, powerlaw, f_in, h, alpha, flags, pad, want_dx = case
+    if powerlaw and n > 2:
+        g = synth.power_law_graph(n, 2.1, min(mean, n - 1.0), seed=600 + i)
+    else:
+        g = synth.random_graph(n, min(mean, max(n - 1.0, 0.0)), 700 + i)
+    r = run_gat(g, f_in, h, alpha, seed=i, pad=pad, flags=flags, want_dx=want_dx)
+    check(g, r, alpha, tol=2e-2 if flags == G.GNN_FLAG_BF16 else TOL)
+
+
 def test_gat_zero_nodes():
     """An empty subgraph: nothing to write forward, zero dW and da."""
     g = synth.identity_graph(0)
