@@ -125,6 +125,37 @@ def test_classifier_optional_outputs_and_empty():
     assert e["loss"] == 0.0 and np.all(e["dW"] == 0)
 
 
+def _random_head_cases(count=30, seed=3131):
+    """Seeded random classifier heads: rows, features, classes, softmax or
+    sigmoid, product mode, row-stride padding, optional outputs."""
+    rng = np.random.default_rng(seed)
+    modes = [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16]
+    return [(i, int(rng.integers(1, 2500)), int(rng.integers(1, 600)),
+             int(rng.integers(1, 200)), bool(rng.integers(0, 2)), modes[i % 3],
+             int(rng.integers(0, 6)), bool(rng.integers(0, 2)), bool(rng.integers(0, 2)))
+            for i in range(count)]
+
+
+@pytest.mark.parametrize("case", _random_head_cases(), ids=lambda c: "case%d" % c[0])
+def test_classifier_random_shapes(case):
+    i, n, f, C, multi, flags, pad, want_probs, want_dx = case
+    kind = G.GNN_LOSS_SIGMOID if multi else G.GNN_LOSS_SOFTMAX
+    tol = 2e-2 if flags == G.GNN_FLAG_BF16 else TOL
+    x, w, t = _head_case(n, f, C, multi, seed=900 + i)
+    r = run_head(x, w, t, kind, flags=flags, pad=pad, want_probs=want_probs,
+                 want_dx=want_dx)
+    xm_ref = np.maximum(O.mm_nn(x, w), 0)
+    assert maxrel(r["xm"], xm_ref) <= tol
+    decision_flips(r["xm"], xm_ref, tol)
+    ref = O.classifier(x, w, t, kind, want_dx=want_dx, relu_on=r["xm"] > 0)
+    loss_tol = 2e-2 if flags == G.GNN_FLAG_BF16 else TOL_LOSS
+    assert abs(r["loss"] - ref["loss"]) <= loss_tol * abs(ref["loss"]) or \
+        abs(r["loss"] - ref["loss"]) < 1e-7
+    keys = ("dW",) + (("probs",) if want_probs else ()) + (("dX",) if want_dx else ())
+    for k in keys:
+        assert maxrel(r[k], ref[k]) <= tol, k
+
+
 def test_classifier_deterministic():
     x, w, t = _head_case(5000, 128, 41, False, seed=4)
     a = run_head(x, w, t, G.GNN_LOSS_SOFTMAX)
