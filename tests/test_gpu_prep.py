@@ -88,6 +88,31 @@ def test_induce_parity(name, norm):
         check_parity(full, nodes, norm, r)
 
 
+def _random_induce_cases(count=24, seed=4545):
+    """Seeded random inductions: Kronecker full graphs of random scale and
+    density, node sets of random size drawn uniformly or in proportion to
+    degree, both normalisations."""
+    rng = np.random.default_rng(seed)
+    return [(i, int(rng.integers(8, 14)), float(rng.uniform(2.0, 24.0)),
+             float(rng.uniform(0.0, 1.0)), bool(rng.integers(0, 2)),
+             [G.GNN_NORM_ROW, G.GNN_NORM_SYM][int(rng.integers(0, 2))])
+            for i in range(count)]
+
+
+@pytest.mark.parametrize("case", _random_induce_cases(), ids=lambda c: "case%d" % c[0])
+def test_induce_random_sets(case):
+    i, scale, deg, frac, biased, norm = case
+    full = synth.kronecker_graph(scale, deg, 50 + i)
+    rng = np.random.default_rng(60 + i)
+    size = max(1, int(frac * min(full.n, 5000)))
+    if biased and full.nnz > 0:
+        p = full.degrees() + 1.0
+        nodes = np.unique(rng.choice(full.n, size=size, p=p / p.sum())).astype(np.int32)
+    else:
+        nodes = np.sort(rng.choice(full.n, size=size, replace=False)).astype(np.int32)
+    check_parity(full, nodes, norm, run_induce(full, nodes, norm))
+
+
 def test_induce_frontier_like_large_set():
     """8,000 nodes drawn with probability proportional to degree (the bias
     of the frontier sampler) from a 2^15-node graph: hub rows spread over
