@@ -559,6 +559,30 @@ def test_layer_random_shapes(case):
         assert maxrel(got[k], r[k]) <= tol, k
 
 
+@pytest.mark.parametrize("case", _random_layer_cases(count=24, seed=3033),
+                         ids=lambda c: "case%d" % c[0])
+def test_layer_random_shapes_row_normalized(case):
+    """The random layer cases with GNN_FLAG_ROW_NORMALIZED added to the
+    product mode: A_s = D^-1 A taken from the pattern (the graphs store
+    1/deg, so the oracle's value-based layer is the same operator)."""
+    _random_row_normalized_layer(case[:7] + (case[7] | G.GNN_FLAG_ROW_NORMALIZED, case[8]))
+
+
+def _random_row_normalized_layer(case):
+    _, n, f_in, h, order, bias, want_dx, flags, pad = case
+    g, x, p, dy = layer_inputs(n, f_in, h, 4000 + n + f_in + h, bias)
+    y_ref = O.sage_fwd(g, x, p.w_self, p.w_neigh, p.b_self, p.b_neigh)
+    y32 = y_ref.astype(np.float32)
+    got = run_layer(g, x, p, y32, dy, order, pad=pad, want_dx=want_dx, flags=flags)
+    tol = 2e-2 if flags & G.GNN_FLAG_BF16 else TOL
+    assert maxrel(got["Y"], y_ref) <= tol
+    r = O.sage_bwd(g, x, p.w_self, p.w_neigh, y32, dy, want_dx=want_dx, want_db=bias)
+    keys = ("dW_self", "dW_neigh") + (("dX",) if want_dx else ()) + \
+        (("db_self", "db_neigh") if bias else ())
+    for k in keys:
+        assert maxrel(got[k], r[k]) <= tol, k
+
+
 @pytest.mark.parametrize("flags", [0, G.GNN_FLAG_F32_MFMA, G.GNN_FLAG_BF16])
 @pytest.mark.parametrize("order", [1, 2])
 def test_layer_zero_nodes(flags, order):
