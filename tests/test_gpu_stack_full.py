@@ -118,3 +118,68 @@ def test_stack_whole_tensors_with_bias(mode):
     """The 3-layer 8,000-node stack with per-half biases: db_self and
     db_neigh of every layer as well."""
     run_and_check("cl2.3-n8000-f300-h512-L3", mode, bias=True)
+
+
+def _random_stack_cases(count=16, seed=6060):
+    """Seeded random small stacks: 2 to 5 layers with random widths per
+    layer, product mode, bias, and the cross-layer mask fusion on or off."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(count):
+        L = int(rng.integers(2, 6))
+        cases.append((i, int(rng.integers(2, 1500)), int(rng.integers(1, 200)),
+                      [int(rng.integers(1, 128)) for _ in range(L)], list(MODES)[i % 3],
+                      bool(rng.integers(0, 2)), bool(rng.integers(0, 2))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_stack_cases(), ids=lambda c: "case%d" % c[0])
+def test_stack_random_shapes(case):
+    """Chained stacks of random shapes, checked the same way as the full-size
+    ones (forward free, backward teacher-forced from the oracle's fp32 layer
+    outputs, every element of every layer); with the mask fusion, dX of the
+    layers above the first comes back masked by the sign of their input."""
+    i, n, f_in, hs, mode, bias, fuse = case
+    flags, tol = MODES[mode]
+    rng = np.random.default_rng(7000 + i)
+    g = synth.power_law_graph(n, 2.1, min(10.0, n - 1.0), seed=7100 + i)
+    x = rng.standard_normal((n, f_in)).astype(np.float32)
+    params, f = [], f_in
+    for h in hs:
+        p = synth.LayerParams(synth.glorot(f, h, rng), synth.glorot(f, h, rng))
+        if bias:
+            p.b_self = (0.1 * rng.standard_normal(h)).astype(np.float32)
+            p.b_neigh = (0.1 * rng.standard_normal(h)).astype(np.float32)
+        params.append(p)
+        f = 2 * h
+    dy = rng.standard_normal((n, f)).astype(np.float32)
+    xs, ys = [x], []
+    for p in params:
+        y = O.sage_fwd(g, xs[-1], p.w_self, p.w_neigh, p.b_self, p.b_neigh)
+        ys.append(y)
+        xs.append(y.astype(np.float32))
+    grads = [None] * len(params)
+    d = dy.astype(np.float64)
+    for l in reversed(range(len(params))):
+        p = params[l]
+        grads[l] = O.sage_bwd(g, xs[l], p.w_self, p.w_neigh, xs[l + 1], d, want_dx=True,
+                              want_db=bias)
+        d = grads[l]["dX"]
+    st = runtime.SageStack(prepared(g), params, f_in, flags=flags, fuse_masks=fuse)
+    st.forward(to_dev(x, (f_in + 15) // 16 * 16))
+    torch.cuda.synchronize()
+    for l, L in enumerate(st.layers):
+        y = L["Y"].cpu().numpy()
+        assert maxrel(y, ys[l]) <= tol, ("Y", l)
+        decision_flips(y, ys[l], bound=tol)
+    for l, L in enumerate(st.layers):
+        L["Y"].copy_(torch.from_numpy(xs[l + 1]).cuda())
+    st.backward(to_dev(dy), want_dx_first=True)
+    torch.cuda.synchronize()
+    keys = ("dX", "dW_self", "dW_neigh") + (("db_self", "db_neigh") if bias else ())
+    for l, L in enumerate(st.layers):
+        for k in keys:
+            ref = grads[l][k]
+            if k == "dX" and fuse and l > 0:
+                ref = ref * (xs[l] > 0)
+            assert maxrel(L[k].cpu().numpy(), ref) <= tol, (k, l)
