@@ -172,23 +172,26 @@ GemmBatch dx_batch(int order, int32_t n, int32_t f_in, int32_t h,
 // the workspace (once per call, in the orientation of this batch's B), and
 // the batch's segments pointed at them: segment B pointers equal to W_self
 // take the first, W_neigh the second.
-// Points the batch's weight segments at bf16 pieces: planes[0] for W_self,
-// planes[1] for W_neigh, pw words per plane.
-void use_weight_planes(GemmBatch& b, const float* Ws, uint32_t* const planes[2], int64_t pw) {
+// Points the batch's weight segments at bf16 pieces: p_self for W_self's,
+// p_neigh for W_neigh's, pw words per plane.
+void use_weight_planes(GemmBatch& b, const float* Ws, const uint32_t* p_self,
+                       const uint32_t* p_neigh, int64_t pw) {
   for (int i = 0; i < b.nprob; ++i)
     for (int k = 0; k < b.p[i].nseg; ++k) {
       GemmSeg& sg = b.p[i].seg[k];
-      sg.Bp = sg.B == Ws ? planes[0] : planes[1];
+      sg.Bp = sg.B == Ws ? p_self : p_neigh;
       sg.bp_plane = pw;
     }
   b.b_planes = 1;
 }
 
-uint32_t* const* saved_planes(const LayerLayout& o, const void* saved, uint32_t* out[2]) {
-  char* sv = static_cast<char*>(const_cast<void*>(saved));
-  out[0] = reinterpret_cast<uint32_t*>(sv + o.off_sp);
-  out[1] = reinterpret_cast<uint32_t*>(sv + o.off_sp + o.sp_stride);
-  return out;
+// The input gradient's pieces in the saved buffer: i = 0 W_self's, 1 W_neigh's.
+uint32_t* saved_plane(const LayerLayout& o, void* saved, int i) {
+  return reinterpret_cast<uint32_t*>(static_cast<char*>(saved) + o.off_sp + i * o.sp_stride);
+}
+const uint32_t* saved_plane(const LayerLayout& o, const void* saved, int i) {
+  return reinterpret_cast<const uint32_t*>(static_cast<const char*>(saved) + o.off_sp +
+                                           i * o.sp_stride);
 }
 
 // Forward product (split products): W_self and W_neigh split once into the
@@ -201,13 +204,13 @@ hipError_t attach_weight_planes(GemmBatch& b, const LayerLayout& o, char* ws, vo
   if (b.mode != GEMM_SPLIT) return hipSuccess;
   uint32_t* wp[2] = {reinterpret_cast<uint32_t*>(ws + o.off_wp),
                      reinterpret_cast<uint32_t*>(ws + o.off_wp + round_up(o.wp_words * 4, 256))};
-  uint32_t* sp[2];
-  saved_planes(o, saved, sp);
-  const SplitJob jobs[4] = {{Ws, h, f_in, h, 0, wp[0]}, {Wn, h, f_in, h, 0, wp[1]},
-                            {Ws, h, h, f_in, 1, sp[0]}, {Wn, h, h, f_in, 1, sp[1]}};
+  const SplitJob jobs[4] = {{Ws, h, f_in, h, 0, wp[0]},
+                            {Wn, h, f_in, h, 0, wp[1]},
+                            {Ws, h, h, f_in, 1, saved_plane(o, saved, 0)},
+                            {Wn, h, h, f_in, 1, saved_plane(o, saved, 1)}};
   hipError_t e = split_b_planes_launch(jobs, 4, s);
   if (e != hipSuccess) return e;
-  use_weight_planes(b, Ws, wp, (int64_t)(b_planes_words(f_in, h) / 3));
+  use_weight_planes(b, Ws, wp[0], wp[1], (int64_t)(b_planes_words(f_in, h) / 3));
   return hipSuccess;
 }
 
@@ -690,8 +693,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       bx.p[0].ld_mask = layer->ld_x;
       if (bx.mode == GEMM_SPLIT && saved) {  // the pieces the forward call saved
         // (saved is NULL only for n = 0, where the product has no tiles)
-        uint32_t* sp[2];
-        use_weight_planes(bx, W_self, saved_planes(o, saved, sp),
+        use_weight_planes(bx, W_self, saved_plane(o, saved, 0), saved_plane(o, saved, 1),
                           (int64_t)(b_planes_words(h, f_in) / 3));
       }
       GNN_HIP(gemm_launch(bx, xws, xws_bytes, stream, nullptr, &held));
@@ -722,8 +724,7 @@ gnn_status gnn_prop_bwd(const gnn_csr* csr, const gnn_layer* layer,
       bx.mode = bf;
       if (bx.mode == GEMM_SPLIT && saved) {  // the pieces the forward call saved
         // (saved is NULL only for n = 0, where the product has no tiles)
-        uint32_t* sp[2];
-        use_weight_planes(bx, W_self, saved_planes(o, saved, sp),
+        use_weight_planes(bx, W_self, saved_plane(o, saved, 0), saved_plane(o, saved, 1),
                           (int64_t)(b_planes_words(h, f_in) / 3));
       }
       GNN_HIP(gemm_launch(bx, xws, xws_bytes, stream, nullptr, &held));
