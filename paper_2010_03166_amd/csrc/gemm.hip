@@ -162,8 +162,11 @@ __device__ inline TileInfo tile_info(const GemmKArgs& g, int t) {
 constexpr int EPI_ROW = 40;
 constexpr int EPI_REGION = 32 * EPI_ROW;
 
+// NJ: 32-column blocks per wavefront (2: 4 wavefronts of 64 x 64; 1: 8 of
+// 64 x 32); WPH wavefronts share each of lds0 and lds1.
+template <int NJ = 2, int WPH = 2>
 __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
-                                 int M, const floatx16 (&acc)[2][2],
+                                 int M, const floatx16 (&acc)[2][NJ],
                                  bool whole, float* part, int wm, int wn,
                                  int lr, int lh, bool vec_c, float* lds0,
                                  float* lds1) {
@@ -173,16 +176,17 @@ __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
                         ti.n0 == ti.c0;
   if (whole && interior && vec_c) {
     const int wave = 2 * wn + wm, lane = lh * 32 + lr;
-    float* L = (wave < 2 ? lds0 : lds1) + (wave & 1) * EPI_REGION;
+    float* L = (wave < WPH ? lds0 : lds1) + (wave % WPH) * EPI_REGION;
     const int rr = lane >> 3, c4 = 4 * (lane & 7);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < NJ; ++j) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           L[(8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_ROW + lr] = acc[i][j][r];
-        const int row0 = ti.m0 + wm * 64 + i * 32, col = ti.n0 + wn * 64 + j * 32 + c4;
+        const int row0 = ti.m0 + wm * 64 + i * 32,
+                  col = ti.n0 + wn * 32 * NJ + j * 32 + c4;
         const float4 bc = P.bias ? ld4(P.bias + col) : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -209,8 +213,8 @@ __device__ inline void store_acc(const GemmProblem& P, const TileInfo& ti,
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int cl = wn * 64 + j * 32 + lr;
+    for (int j = 0; j < NJ; ++j) {
+      const int cl = wn * 32 * NJ + j * 32 + lr;
       const int col = ti.n0 + cl;
       const int rl0 = wm * 64 + i * 32 + lh * 4;
       if (!whole) {
@@ -329,6 +333,7 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmKArgs g) {
 // previous launch (`fx`, fx.tiles x FIX_CHUNKS of them); true for those.
 __device__ inline bool run_pending_fixup(const GemmKArgs& g, const GemmKArgs& fx) {
   if ((int)blockIdx.x < g.nblocks) return false;
+  if (threadIdx.x >= 256) return true;  // a chunk takes 256 threads
   const int f = (int)blockIdx.x - g.nblocks;
   fixup_chunk(fx, f / FIX_CHUNKS, f % FIX_CHUNKS);
   return true;
@@ -973,20 +978,28 @@ __device__ inline void split3(float x0, float x1, uint32_t& h, uint32_t& m,
 // (one 128-bit load per piece and block: the planes are in fragment order,
 // so a fragment is 1 KiB of consecutive bytes), one stage ahead of the
 // products that use them; only A goes through the split and LDS.
-template <bool AT, bool BT, bool BD>
-__global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKArgs fx) {
+// NW: wavefronts per block.  4: each computes 64 x 64 of the 128 x 128
+// tile.  8 (k-contiguous A, pre-split B only): each computes 64 x 32, four
+// wavefronts per SIMD at two blocks per CU, each thread staging one float4
+// of A per stage.
+template <bool AT, bool BT, bool BD, int NW = 4>
+__global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g, GemmKArgs fx) {
+  static_assert(NW == 4 || (NW == 8 && !AT && BD), "8 wavefronts: k-contiguous A, split B");
+  constexpr int NJ = NW == 8 ? 1 : 2;  // 32-column blocks per wavefront
+  constexpr int AP = 8 / NW;           // 64-row groups of A staged per thread
   if (run_pending_fixup(g, fx)) return;
   constexpr bool A_KC = !AT;
   constexpr bool B_KC = BT;
   constexpr int A_PLANE = A_KC ? KCS_PLANE : XCS_PLANE;
   constexpr int B_PLANE = B_KC ? KCS_PLANE : XCS_PLANE;
   constexpr int B_WORDS = BD ? 4 : 3 * B_PLANE;
-  __shared__ __attribute__((aligned(16))) uint32_t As0[3 * A_PLANE];
-  __shared__ __attribute__((aligned(16))) uint32_t As1[3 * A_PLANE];
+  constexpr int A_WORDS =
+      3 * A_PLANE > (NW / 2) * EPI_REGION ? 3 * A_PLANE : (NW / 2) * EPI_REGION;
+  __shared__ __attribute__((aligned(16))) uint32_t As0[A_WORDS];
+  __shared__ __attribute__((aligned(16))) uint32_t As1[A_WORDS];
   __shared__ __attribute__((aligned(16))) uint32_t Bs0[B_WORDS];
   __shared__ __attribute__((aligned(16))) uint32_t Bs1[B_WORDS];
-  static_assert(3 * A_PLANE >= 2 * EPI_REGION && (BD || 3 * B_PLANE >= 2 * EPI_REGION),
-                "epilogue regions");
+  static_assert(BD || 3 * B_PLANE >= 2 * EPI_REGION, "epilogue regions");
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -1041,7 +1054,7 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
                        int x0, int X_extent, int k0, int K, bool fast, bool vec) {
       if (kc) {
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
+        for (int p = 0; p < AP; ++p) {
           const int x = x0 + kx + 64 * p, k = k0 + ky;
           r[p] = fast ? ld4(X + (int64_t)x * ld + k) : load4(X, ld, x, k, X_extent, K, vec);
         }
@@ -1070,7 +1083,7 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
     auto store_op = [&](uint32_t* L, const float4 (&r)[2], bool kc, int plane) {
       if (kc) {  // 4 consecutive k of rows x and x + 64
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
+        for (int p = 0; p < AP; ++p) {
           uint2 h, m, l;
           split3(r[p].x, r[p].y, h.x, m.x, l.x);
           split3(r[p].z, r[p].w, h.y, m.y, l.y);
@@ -1092,11 +1105,11 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
       }
     };
 
-    floatx16 acc[2][2];
+    floatx16 acc[2][NJ];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
@@ -1114,7 +1127,7 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
       }
       return __builtin_bit_cast(bf16x8, w);
     };
-    typedef bf16x8 BFr[3][2];
+    typedef bf16x8 BFr[3][NJ];
     // B fragments of stage ks from the planes (BD); columns past N read as
     // zeros unless `full` (the tile's columns all lie inside N)
     auto load_bfr = [&](BFr& bf, int ks, bool full) {
@@ -1123,8 +1136,8 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
       const int64_t ps = s1 ? bps1 : bps0;
       const int64_t gN = (int64_t)(s1 ? ks - kt0 : ks) * N;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int n = n0 + wn * 64 + j * 32 + lr;
+      for (int j = 0; j < NJ; ++j) {
+        const int n = n0 + wn * 32 * NJ + j * 32 + lr;
         const uint32_t* src = Bq + (gN + n) * 8 + 4 * lh;
 #pragma unroll
         for (int q = 0; q < 3; ++q) {
@@ -1137,7 +1150,7 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
     // The six piece products down to 2^-16 of hi x hi, smallest first; what
     // is left out (mid lo + lo mid + lo lo) is below 2^-24 of |a b|.
     struct Frags {
-      bf16x8 a[3][2], b[3][2];
+      bf16x8 a[3][2], b[3][NJ];
     };
     auto read_a = [&](Frags& f, const uint32_t* as) {
 #pragma unroll
@@ -1151,7 +1164,7 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
 #pragma unroll
       for (int q = 0; q < 3; ++q)
 #pragma unroll
-        for (int i = 0; i < 2; ++i) f.b[q][i] = frag(bs + q * B_PLANE, B_KC, wn * 64, i);
+        for (int j = 0; j < NJ; ++j) f.b[q][j] = frag(bs + q * B_PLANE, B_KC, wn * 32 * NJ, j);
       return f;
     };
     auto products = [&](const Frags& f) {
@@ -1161,7 +1174,7 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
+          for (int j = 0; j < NJ; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                 f.a[terms[u][0]][i], f.b[terms[u][1]][j], acc[i][j], 0, 0, 0);
     };
@@ -1195,7 +1208,7 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
 #pragma unroll
           for (int q = 0; q < 3; ++q)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) f.b[q][j] = bcur[q][j];
+            for (int j = 0; j < NJ; ++j) f.b[q][j] = bcur[q][j];
           store_op(as_n, ra, A_KC, A_PLANE);
           load_full(kl);
           load_bfr(bnext, min(kb, kf - 1), true);
@@ -1268,9 +1281,9 @@ __global__ __launch_bounds__(256, 2) void gemm_split_kernel(GemmKArgs g, GemmKAr
     float* part = g.part + (g.splits > 1 ? (int64_t)lb
                                          : (int64_t)lb * 2 + (seg > 0 ? 1 : 0)) *
                                (BM * BN);
-    store_acc(P, ti, M, acc, whole, part, wm, wn, lr, lh, g.vec_c[ti.pi] != 0,
-              reinterpret_cast<float*>(As0),
-              reinterpret_cast<float*>(BD ? As1 : Bs0));
+    store_acc<NJ, NW / 2>(P, ti, M, acc, whole, part, wm, wn, lr, lh,
+                          g.vec_c[ti.pi] != 0, reinterpret_cast<float*>(As0),
+                          reinterpret_cast<float*>(BD ? As1 : Bs0));
   }
 }
 
@@ -1542,6 +1555,11 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
       gemm_f32_kernel<false, true><<<grid, 256, 0, s>>>(g, fx);
     else
       gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g, fx);
+  } else if (b.b_planes && !b.trans_a) {
+    if (!b.trans_b)
+      gemm_split_kernel<false, false, true, 8><<<grid, 512, 0, s>>>(g, fx);
+    else
+      gemm_split_kernel<false, true, true, 8><<<grid, 512, 0, s>>>(g, fx);
   } else if (b.b_planes) {
     if (!b.trans_a && !b.trans_b)
       gemm_split_kernel<false, false, true><<<grid, 256, 0, s>>>(g, fx);
