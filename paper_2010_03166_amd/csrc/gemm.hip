@@ -984,7 +984,7 @@ __device__ inline void split3(float x0, float x1, uint32_t& h, uint32_t& m,
 // of A per stage.
 template <bool AT, bool BT, bool BD, int NW = 4>
 __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g, GemmKArgs fx) {
-  static_assert(NW == 4 || (NW == 8 && !AT && BD), "8 wavefronts: k-contiguous A, split B");
+  static_assert(NW == 4 || (NW == 8 && !AT && (BD || BT)), "8 wavefronts: k-contiguous operands");
   constexpr int NJ = NW == 8 ? 1 : 2;  // 32-column blocks per wavefront
   constexpr int AP = 8 / NW;           // 64-row groups of A staged per thread
   if (run_pending_fixup(g, fx)) return;
@@ -999,7 +999,7 @@ __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g
   __shared__ __attribute__((aligned(16))) uint32_t As1[A_WORDS];
   __shared__ __attribute__((aligned(16))) uint32_t Bs0[B_WORDS];
   __shared__ __attribute__((aligned(16))) uint32_t Bs1[B_WORDS];
-  static_assert(BD || 3 * B_PLANE >= 2 * EPI_REGION, "epilogue regions");
+  static_assert(BD || NW == 8 || 3 * B_PLANE >= 2 * EPI_REGION, "epilogue regions");
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -1283,7 +1283,7 @@ __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g
                                (BM * BN);
     store_acc<NJ, NW / 2>(P, ti, M, acc, whole, part, wm, wn, lr, lh,
                           g.vec_c[ti.pi] != 0, reinterpret_cast<float*>(As0),
-                          reinterpret_cast<float*>(BD ? As1 : Bs0));
+                          reinterpret_cast<float*>(BD || NW == 8 ? As1 : Bs0));
   }
 }
 
@@ -1574,7 +1574,7 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
   } else if (b.trans_a && !b.trans_b) {
     gemm_split_kernel<true, false, false><<<grid, 256, 0, s>>>(g, fx);
   } else if (!b.trans_a && b.trans_b) {
-    gemm_split_kernel<false, true, false><<<grid, 256, 0, s>>>(g, fx);
+    gemm_split_kernel<false, true, false, 8><<<grid, 512, 0, s>>>(g, fx);
   } else {
     gemm_split_kernel<true, true, false><<<grid, 256, 0, s>>>(g, fx);
   }
