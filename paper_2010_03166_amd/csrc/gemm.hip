@@ -107,6 +107,23 @@ __device__ inline float4 load4(const float* base, int64_t ld, int r, int c,
   return v;
 }
 
+// Element (r, c..c+1) of a row-major R x C matrix, zeros outside; `vec`
+// (8-byte aligned rows, c even) allows one 8-byte load.
+__device__ inline float2 load2(const float* base, int64_t ld, int r, int c, int R, int C,
+                               bool vec) {
+  float2 v = make_float2(0.f, 0.f);
+  if (r < R && c < C) {
+    const float* p = base + (int64_t)r * ld + c;
+    if (vec && c + 1 < C) {
+      v = *reinterpret_cast<const float2*>(p);
+    } else {
+      v.x = p[0];
+      if (c + 1 < C) v.y = p[1];
+    }
+  }
+  return v;
+}
+
 __device__ inline int64_t block_lo(int b, int64_t iters, int nblocks) {
   return (int64_t)b * iters / nblocks;
 }
@@ -979,12 +996,12 @@ __device__ inline void split3(float x0, float x1, uint32_t& h, uint32_t& m,
 // so a fragment is 1 KiB of consecutive bytes), one stage ahead of the
 // products that use them; only A goes through the split and LDS.
 // NW: wavefronts per block.  4: each computes 64 x 64 of the 128 x 128
-// tile.  8 (k-contiguous A, pre-split B only): each computes 64 x 32, four
-// wavefronts per SIMD at two blocks per CU, each thread staging one float4
-// of A per stage.
+// tile.  8 (k-contiguous A): each computes 64 x 32, four wavefronts per
+// SIMD at two blocks per CU; a thread stages one float4 of a k-contiguous
+// operand, or two columns of one k pair of an x-contiguous one, per stage.
 template <bool AT, bool BT, bool BD, int NW = 4>
 __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g, GemmKArgs fx) {
-  static_assert(NW == 4 || (NW == 8 && !AT && (BD || BT)), "8 wavefronts: k-contiguous operands");
+  static_assert(NW == 4 || (NW == 8 && !AT), "8 wavefronts: k-contiguous A");
   constexpr int NJ = NW == 8 ? 1 : 2;  // 32-column blocks per wavefront
   constexpr int AP = 8 / NW;           // 64-row groups of A staged per thread
   if (run_pending_fixup(g, fx)) return;
@@ -1047,7 +1064,9 @@ __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g
     // XC: thread owns k pair kp = tid >> 5 (rows 2 kp and 2 kp + 1) and
     // x = 4 (tid & 31) .. + 3 (a wavefront reads 2 whole 512-byte rows).
     const int kx = tid >> 2, ky = 4 * (tid & 3);
-    const int xk = tid >> 5, xy = 4 * (tid & 31);
+    // XC: 4 wavefronts: k pair xk of 4 columns xy..xy+3; 8: of 2 columns
+    const int xk = NW == 8 ? tid >> 6 : tid >> 5;
+    const int xy = NW == 8 ? 2 * (tid & 63) : 4 * (tid & 31);
 
     float4 ra[2], rb[2];
     auto load_op = [&](float4 (&r)[2], bool kc, const float* X, int64_t ld,
@@ -1058,6 +1077,19 @@ __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g
           const int x = x0 + kx + 64 * p, k = k0 + ky;
           r[p] = fast ? ld4(X + (int64_t)x * ld + k) : load4(X, ld, x, k, X_extent, K, vec);
         }
+      } else if (NW == 8) {  // two columns of rows k, k + 1 in .x, .y
+        const int k = k0 + 2 * xk, x = x0 + xy;
+        float2 u0, u1;
+        if (fast) {
+          const float* q = X + (int64_t)k * ld + x;
+          u0 = *reinterpret_cast<const float2*>(q);
+          u1 = *reinterpret_cast<const float2*>(q + ld);
+        } else {
+          u0 = load2(X, ld, k, x, K, X_extent, vec);
+          u1 = load2(X, ld, k + 1, x, K, X_extent, vec);
+        }
+        r[0] = make_float4(u0.x, u0.y, 0.f, 0.f);
+        r[1] = make_float4(u1.x, u1.y, 0.f, 0.f);
       } else {
         const int k = k0 + 2 * xk, x = x0 + xy;
         if (fast) {
@@ -1092,6 +1124,14 @@ __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g
           *reinterpret_cast<uint2*>(&L[plane + w]) = m;
           *reinterpret_cast<uint2*>(&L[2 * plane + w]) = l;
         }
+      } else if (NW == 8) {  // k pair (rows 2kp, 2kp + 1) of 2 consecutive x
+        uint2 h, m, l;
+        split3(r[0].x, r[1].x, h.x, m.x, l.x);
+        split3(r[0].y, r[1].y, h.y, m.y, l.y);
+        const int w = xcs_word(xk, xy);
+        *reinterpret_cast<uint2*>(&L[w]) = h;
+        *reinterpret_cast<uint2*>(&L[plane + w]) = m;
+        *reinterpret_cast<uint2*>(&L[2 * plane + w]) = l;
       } else {   // k pair (rows 2kp, 2kp + 1) of 4 consecutive x
         uint4 h, m, l;
         split3(r[0].x, r[1].x, h.x, m.x, l.x);
@@ -1570,7 +1610,7 @@ hipError_t gemm_launch(const GemmBatch& b, void* workspace, size_t ws_bytes,
     else
       gemm_split_kernel<true, true, true><<<grid, 256, 0, s>>>(g, fx);
   } else if (!b.trans_a && !b.trans_b) {
-    gemm_split_kernel<false, false, false><<<grid, 256, 0, s>>>(g, fx);
+    gemm_split_kernel<false, false, false, 8><<<grid, 512, 0, s>>>(g, fx);
   } else if (b.trans_a && !b.trans_b) {
     gemm_split_kernel<true, false, false><<<grid, 256, 0, s>>>(g, fx);
   } else if (!b.trans_a && b.trans_b) {
