@@ -101,6 +101,8 @@ def parse():
     ap.add_argument("--no-floor", action="store_true",
                     help="skip the aggregation's gather floor (keeps a profile of the "
                          "step free of its standalone launches)")
+    ap.add_argument("--no-probe", action="store_true",
+                    help="skip the matrix cores' sustained-rate probe (gnn_mfma_rate_probe)")
     ap.add_argument("--no-rownorm", action="store_true",
                     help="skip the step with GNN_FLAG_ROW_NORMALIZED")
     ap.add_argument("--no-configs", action="store_true",
@@ -265,6 +267,17 @@ def main():
                 traffic["spmm"] / (kernels["spmm"]["avg_launch_us"] * 1e3), 1)
     if dom in gemm_names:
         roof["mfma_util_pct"] = measured_mfma_util(name, dtype).get(dom)
+        if not args.no_probe:
+            # what the bf16 matrix cores sustain on this GPU with nothing
+            # but MFMAs in the loop, and the shader clock under that load
+            pr = mfma_probe(torch, G, G.GNN_PROBE_MFMA_BF16)
+            ceil = pr["tflops"] / SPLIT_PRODUCTS
+            roof["mfma_probe"] = {"bf16_tflops": pr["tflops"], "shader_ghz": pr["shader_ghz"],
+                                  "frac_of_bf16_peak": round(pr["tflops"] / PEAK_TFLOPS["bf16"], 4),
+                                  "split_ceiling_tflops": round(ceil, 1),
+                                  "frac_of_split_ceiling": round(ach / ceil, 4)}
+            log("mfma probe: bf16 %.1f TFLOP/s at %.3f GHz; %s at %.3f of the split "
+                "ceiling it gives" % (pr["tflops"], pr["shader_ghz"], dom, ach / ceil))
 
     out = {
         "metric": METRIC,
@@ -310,6 +323,12 @@ def main():
             G.GNN_FLAG_F32_MFMA, "fp32 products on v_mfma_f32_32x32x2_f32, fp32 throughout",
             PEAK_TFLOPS["f32"])
         log("f32 MFMA variant: %.4f ms per step" % out["f32_mfma_variant"]["ms_per_step"])
+        vr = out["f32_mfma_variant"].get("roofline")
+        if not args.no_probe and vr and vr.get("unit") == "TFLOP/s":
+            pr = mfma_probe(torch, G, G.GNN_PROBE_MFMA_F32)
+            vr["mfma_probe"] = {"f32_tflops": pr["tflops"], "shader_ghz": pr["shader_ghz"],
+                                "frac_of_f32_peak": round(pr["tflops"] / PEAK_TFLOPS["f32"], 4),
+                                "frac_of_probe": round(vr["achieved"] / pr["tflops"], 4)}
         out["bf16_variant"] = bench_mode(
             G, runtime, torch, dg, params, wl, X, dY, args, want_dx_first, pad,
             G.GNN_FLAG_BF16, "bf16 GEMM operands, f32 accumulation and aggregation",
@@ -663,6 +682,38 @@ def bench_pipeline(G, runtime, synth, torch, np, args):
                          samp_ms, threads))
     del dev
     return res
+
+
+def mfma_probe(torch, G, kind, reps=3):
+    """The sustained rate of the matrix cores on this GPU: gnn_mfma_rate_probe
+    (register-operand MFMAs only, 512-thread workgroups, two per CU as in
+    the split-product GEMM), timed with events on the stream it runs on,
+    median of `reps` launches after one warm-up; and the shader clock that
+    its first wavefront counted (s_memtime cycles over 100 MHz ticks)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = 2 * cus
+    bf16 = kind == G.GNN_PROBE_MFMA_BF16
+    iters = 2000 if bf16 else 1000
+    flop = (32 * 32 * 16 * 2 if bf16 else 32 * 32 * 2 * 2) * 4.0 * iters * blocks * 8
+    sink = torch.empty(blocks * 512, device="cuda")
+    clocks = torch.zeros(2, dtype=torch.int64, device="cuda")
+    G.gnn_mfma_rate_probe(kind, blocks, iters, sink, clocks)
+    torch.cuda.synchronize()
+    us, ghz = [], []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        G.gnn_mfma_rate_probe(kind, blocks, iters, sink, clocks)
+        e1.record()
+        torch.cuda.synchronize()
+        us.append(1e3 * e0.elapsed_time(e1))
+        cyc, ticks = (int(v) for v in clocks.cpu())
+        ghz.append(0.1 * cyc / ticks if ticks > 0 else 0.0)
+    us.sort()
+    ghz.sort()
+    del sink, clocks
+    return {"tflops": round(flop / (us[len(us) // 2] * 1e6), 1),
+            "shader_ghz": round(ghz[len(ghz) // 2], 3)}
 
 
 def gather_floor(torch, G, dg, w, bytes_per_launch, reps=50):

@@ -506,6 +506,31 @@ gnn_status gnn_gemm(int32_t trans_a, int32_t trans_b, int32_t M, int32_t N,
                     void* workspace, size_t workspace_bytes,
                     hipStream_t stream);
 
+/* Measurement aid, not part of the method: the sustained rate of the
+ * device's matrix cores, against which the products' rates are read.
+ * Launches `blocks` workgroups of 512 threads (eight wavefronts, two
+ * workgroups per CU as in the split-product GEMM); every wavefront issues
+ * 4 x `iters` MFMAs on register operands into four independent accumulators,
+ * with no memory traffic in the loop:
+ *   GNN_PROBE_MFMA_BF16  v_mfma_f32_32x32x16_bf16, 32768 flop each
+ *   GNN_PROBE_MFMA_F32   v_mfma_f32_32x32x2_f32,    4096 flop each
+ * so one launch does blocks x 8 x 4 x iters x (flop each).  The caller times
+ * the launch (events on `stream`) for the rate.  `sink` (device, blocks x
+ * 512 floats, 4-byte aligned) receives each thread's accumulator sum.
+ * `clocks` (device, two 8-byte-aligned uint64) receives the shader-clock
+ * cycles (s_memtime) and the 100 MHz real-time ticks (s_memrealtime) that
+ * the first wavefront of workgroup 0 counted over its loop: cycles / ticks
+ * x 0.1 is the shader clock in GHz under this load.  Errors: an unknown
+ * kind GNN_ERR_UNSUPPORTED, blocks or iters outside [1, max]
+ * GNN_ERR_SHAPE, a NULL pointer GNN_ERR_NULL, misaligned pointers
+ * GNN_ERR_UNSUPPORTED, `sink` overlapping `clocks` GNN_ERR_ALIAS. */
+#define GNN_PROBE_MFMA_BF16 0
+#define GNN_PROBE_MFMA_F32 1
+#define GNN_PROBE_MAX_BLOCKS 65536
+#define GNN_PROBE_MAX_ITERS 100000
+gnn_status gnn_mfma_rate_probe(int32_t kind, int32_t blocks, int32_t iters,
+                               float* sink, uint64_t* clocks, hipStream_t stream);
+
 /* ----------------------------------------------------- kernel timing */
 
 /* Kernels timed by the optional event timer. */

@@ -32,6 +32,10 @@ KERNELS = {"spmm": 0, "spmm_reduce": 1, "gemm_nn": 2, "gemm_tn": 3,
            "induce": 13, "gather": 14, "sddmm": 15, "wsplit": 16}
 GNN_NORM_ROW = 0
 GNN_NORM_SYM = 1
+GNN_PROBE_MFMA_BF16 = 0
+GNN_PROBE_MFMA_F32 = 1
+GNN_PROBE_MAX_BLOCKS = 65536
+GNN_PROBE_MAX_ITERS = 100000
 
 _lib = None
 
@@ -91,6 +95,7 @@ EXPORTS = {
                                                ctypes.c_int64, ctypes.c_void_p,
                                                ctypes.c_int64, ctypes.c_void_p]),
     "gnn_gemm_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32] * 3),
+    "gnn_mfma_rate_probe": (ctypes.c_int32, [ctypes.c_int32] * 3 + [ctypes.c_void_p] * 3),
     "gnn_gemm": (ctypes.c_int32, [ctypes.c_int32] * 5 + [
         ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
         ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32, ctypes.c_void_p,
@@ -511,6 +516,11 @@ def gnn_gemm(trans_a: bool, trans_b: bool, M: int, N: int, K: int, A, lda: int,
                           _ptr(A), int(lda), _ptr(B), int(ldb), _ptr(C), int(ldc),
                           int(flags), _ptr(workspace), _nbytes(workspace),
                           _stream(stream)), "gnn_gemm")
+
+
+def gnn_mfma_rate_probe(kind: int, blocks: int, iters: int, sink, clocks, stream=None):
+    _check(lib().gnn_mfma_rate_probe(int(kind), int(blocks), int(iters), _ptr(sink),
+                                     _ptr(clocks), _stream(stream)), "gnn_mfma_rate_probe")
 
 
 def gnn_timer_enable(enable: bool = True):

@@ -311,3 +311,21 @@ def test_empty_problems_need_no_launch(lib):
     c = G.make_csr(0, 0, 0x1000, None, None, None, None)
     assert L.gnn_spmm(ctypes.byref(c), 0, 8, P(0x10), 8, P(0x20), 8, None, 0, None) == 0
     assert L.gnn_spmm_gather_floor(ctypes.byref(c), 0, 8, P(0x10), 8, P(0x20), 8, None) == 0
+
+
+def test_mfma_rate_probe_argument_errors(lib):
+    L = G.lib()
+    P = ctypes.c_void_p
+    bf, f32 = G.GNN_PROBE_MFMA_BF16, G.GNN_PROBE_MFMA_F32
+    assert L.gnn_mfma_rate_probe(2, 512, 100, P(0x1000), P(0x8000), None) == -4
+    assert L.gnn_mfma_rate_probe(-1, 512, 100, P(0x1000), P(0x8000), None) == -4
+    for blocks, iters in ((0, 100), (G.GNN_PROBE_MAX_BLOCKS + 1, 100), (512, 0),
+                          (512, G.GNN_PROBE_MAX_ITERS + 1), (-3, 100)):
+        assert L.gnn_mfma_rate_probe(bf, blocks, iters, P(0x1000), P(0x8000), None) == -2
+    assert L.gnn_mfma_rate_probe(f32, 512, 100, None, P(0x8000), None) == -1
+    assert L.gnn_mfma_rate_probe(f32, 512, 100, P(0x1000), None, None) == -1
+    assert L.gnn_mfma_rate_probe(bf, 512, 100, P(0x1002), P(0x100000), None) == -4
+    assert L.gnn_mfma_rate_probe(bf, 512, 100, P(0x1000), P(0x100004), None) == -4
+    # clocks inside sink (512 x 512 floats from 0x1000)
+    assert L.gnn_mfma_rate_probe(bf, 512, 100, P(0x1000), P(0x2000), None) == -7
+    assert G.GNN_PROBE_MAX_BLOCKS == 65536 and G.GNN_PROBE_MAX_ITERS == 100000
