@@ -61,7 +61,8 @@ constexpr int XC_STRIDE = 128 + 32; // floats per [k][x] row
 constexpr int KC_FLOATS = 128 * KC_STRIDE;
 constexpr int XC_FLOATS = BK * XC_STRIDE;
 constexpr int NUM_XCD = 8;
-constexpr int MAX_BLOCKS = 512;     // 2 resident blocks on each of 256 CUs
+constexpr int NUM_CU = 256;
+constexpr int MAX_BLOCKS = 2 * NUM_CU;  // 2 resident blocks on each CU
 
 struct GemmKArgs {
   GemmProblem p[2];
@@ -1017,6 +1018,15 @@ __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g
   __shared__ __attribute__((aligned(16))) uint32_t Bs0[B_WORDS];
   __shared__ __attribute__((aligned(16))) uint32_t Bs1[B_WORDS];
   static_assert(BD || NW == 8 || 3 * B_PLANE >= 2 * EPI_REGION, "epilogue regions");
+  // Two blocks share each CU, and the wavefront arbiter favours the older
+  // one: a block of the first dispatch round (every CU receives one before
+  // any receives a second) ran ahead of its CU-mate by ~16 us over a 64-stage
+  // tile, and the later block then finished alone at half occupancy.  The
+  // second-round block takes the higher priority instead: for all of its
+  // stages when B comes pre-split, for its first 60 % of stages otherwise
+  // (the settings that measured fastest; the two then end within ~2 us of
+  // each other).  Priority changes timing only, never results.
+  const bool second_round = blockIdx.x >= NUM_CU;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -1243,6 +1253,10 @@ __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g
         BFr b0, b1;
         auto step = [&](const uint32_t* as, uint32_t* as_n, int kl, BFr& bcur,
                         BFr& bnext, int kb) {
+          if (second_round)
+            __builtin_amdgcn_s_setprio(1);
+          else
+            __builtin_amdgcn_s_setprio(0);
           Frags f;
           read_a(f, as);
 #pragma unroll
@@ -1272,6 +1286,10 @@ __global__ __launch_bounds__(NW * 64, NW / 2) void gemm_split_kernel(GemmKArgs g
         // so that the next stage's LDS writes do not hold them up.
         auto step = [&](const uint32_t* as, const uint32_t* bs, uint32_t* as_n,
                         uint32_t* bs_n, int kl) {
+          if (second_round && (kl - kbeg) * 10 < (kf - kbeg) * 6)
+            __builtin_amdgcn_s_setprio(1);
+          else
+            __builtin_amdgcn_s_setprio(0);
           const Frags f = read_frags(as, bs);
           store_op(as_n, ra, A_KC, A_PLANE);
           store_op(bs_n, rb, B_KC, B_PLANE);
