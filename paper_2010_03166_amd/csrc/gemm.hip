@@ -568,6 +568,11 @@ __global__ __launch_bounds__(256, 2) void gemm_f32_kernel(GemmKArgs g, GemmKArgs
     // slice and the store fills the idle stage; neither is read again.
     auto step = [&](const float* as, const float* bs, float* as_n, float* bs_n,
                     int kl) {
+      // the second-round block of the CU first (see gemm_split_kernel)
+      if (blockIdx.x >= NUM_CU)
+        __builtin_amdgcn_s_setprio(1);
+      else
+        __builtin_amdgcn_s_setprio(0);
       store_slice(as_n, bs_n);
       load_full(kl);
       compute(as, bs);
@@ -900,6 +905,11 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmKArgs g, GemmKArg
       };
       auto step = [&](const uint32_t* as, const uint32_t* bs, uint32_t* as_n,
                       uint32_t* bs_n, int kl) {
+        // the second-round block of the CU first (see gemm_split_kernel)
+        if (blockIdx.x >= NUM_CU)
+          __builtin_amdgcn_s_setprio(1);
+        else
+          __builtin_amdgcn_s_setprio(0);
         store_op(as_n, ra, A_KC);
         store_op(bs_n, rb, B_KC);
         load_full(kl);
